@@ -1,0 +1,253 @@
+"""CPU oracle for the descriptor-ordered GEMM and row reduction.
+
+TEST INFRASTRUCTURE ONLY: the tests, the smoke check and the benchmark's CPU
+baseline load it; the product library never does.  It shares no code with the
+GPU path.  ``libdgo.so`` is compiled from ``dgo.c`` by :func:`build` (gcc,
+``-ffp-contract=off``, OpenMP).
+
+Descriptors are passed as plain dicts whose keys are the descriptor fields
+(see :func:`params`); this module maps them to the oracle's own C struct.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dgo.c")
+_HDR = os.path.join(_HERE, "dgo.h")
+_LIB = os.path.join(_HERE, "libdgo.so")
+
+# Group width of each gfx950 bf16 MFMA instruction (its K).
+INSTRUCTION_K = {"16x16x32": 32, "32x32x16": 16, "16x16x16": 16, "exact8": 8}
+MODEL_EXACT, MODEL_GFX950 = 0, 1
+CARRY, SEQ, TREE = 0, 1, 2
+EPI = {"none": 0, "bias": 1, "bias_silu": 2}
+COMBINE = {"carry": CARRY, "seq": SEQ, "tree": TREE}
+
+
+def build(force: bool = True) -> str:
+    """Compile libdgo.so from dgo.c (always, when force)."""
+    if not force and os.path.exists(_LIB) and os.path.getmtime(_LIB) >= max(
+            os.path.getmtime(_SRC), os.path.getmtime(_HDR)):
+        return _LIB
+    tmp = _LIB + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-std=gnu11", "-O2", "-fPIC", "-shared", "-fopenmp",
+           "-ffp-contract=off", "-fno-fast-math", "-Wall", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("model", "g", "tile_k", "split_k")] + [
+        ("k_cuts", ctypes.POINTER(ctypes.c_int64))] + [
+        (n, ctypes.c_int32) for n in (
+            "tile_combine", "split_combine", "tail_first", "fma", "partial_bf16",
+            "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq")]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        build(force=False)
+        _lib = _bind(_LIB)
+    return _lib
+
+
+def use_library(path):
+    """Route every call of this module to the oracle library at `path` (a
+    planted-mistake build in the power tests); returns the previous binding."""
+    global _lib
+    prev = _lib
+    _lib = _bind(path) if path else None
+    return prev
+
+
+def restore_library(prev):
+    global _lib
+    _lib = prev
+
+
+def _bind(path):
+    L = ctypes.CDLL(path)
+    vp, i64, i32, f32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float
+    P = ctypes.POINTER(_Params)
+    L.dgo_gemm.argtypes = [P, vp, vp, vp, vp, i64, i64, i64, i32]
+    L.dgo_gemm_at.argtypes = [P, vp, vp, vp, i64, i64, i64, vp, vp, i64, vp, i32]
+    L.dgo_rowsum.argtypes = [P, vp, vp, i64, i64, i32]
+    L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
+    L.dgo_group_update.restype = f32
+    L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
+    L.dgo_group_update_batch.restype = None
+    L.dgo_chunk8.argtypes = [f32, vp, vp, i32]
+    L.dgo_chunk8.restype = f32
+    L.dgo_exact_dot_rn32.argtypes = [f32, vp, vp, i32]
+    L.dgo_exact_dot_rn32.restype = f32
+    L.dgo_tree.argtypes = [vp, i32, i32]
+    L.dgo_tree.restype = f32
+    L.dgo_f32_to_bf16.argtypes = [f32]
+    L.dgo_f32_to_bf16.restype = ctypes.c_uint16
+    L.dgo_exp.argtypes = [f32]
+    L.dgo_exp.restype = f32
+    L.dgo_silu.argtypes = [f32]
+    L.dgo_silu.restype = f32
+    L.dgo_plan_cuts.argtypes = [P, i64, vp]
+    for f in ("dgo_gemm", "dgo_gemm_at", "dgo_rowsum", "dgo_plan_cuts"):
+        getattr(L, f).restype = i32
+    return L
+
+
+DEFAULTS = dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=1, k_cuts=None,
+                tile_combine="carry", split_combine="seq", tail="last", fma=1,
+                partial="f32", merge="f32", out="f32", epilogue="none",
+                epi_round="final", leaf_w=64, reduce="sum")
+
+
+def params(desc: dict):
+    """Map a descriptor dict to the oracle's C struct.  Returns (struct, keepalive)."""
+    d = dict(DEFAULTS)
+    d.update(desc)
+    cuts = None
+    if d["k_cuts"] is not None:
+        cuts = np.ascontiguousarray(np.asarray(d["k_cuts"], dtype=np.int64))
+    p = _Params()
+    p.model = MODEL_GFX950 if d["model"] == "gfx950" else MODEL_EXACT
+    p.g = int(d["g"]) if "g" in d else INSTRUCTION_K[d["mma"]]
+    p.tile_k = int(d["tile_k"])
+    p.split_k = int(d["split_k"])
+    p.k_cuts = cuts.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)) if cuts is not None else None
+    p.tile_combine = COMBINE[d["tile_combine"]]
+    p.split_combine = COMBINE[d["split_combine"]]
+    p.tail_first = 1 if d["tail"] == "first" else 0
+    p.fma = int(d["fma"])
+    p.partial_bf16 = 1 if d["partial"] == "bf16" else 0
+    p.merge_bf16 = 1 if d["merge"] == "bf16" else 0
+    p.out_bf16 = 1 if d["out"] == "bf16" else 0
+    p.epilogue = EPI[d["epilogue"]]
+    p.pre_act_round = 1 if d["epi_round"] == "pre_act" else 0
+    p.leaf_w = int(d["leaf_w"])
+    p.sumsq = 1 if d["reduce"] == "sumsq" else 0
+    return p, cuts
+
+
+class OracleError(RuntimeError):
+    pass
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _u16(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.uint16))
+
+
+def gemm(desc, A, B, bias=None, nthreads=None):
+    """Full GEMM.  A (M,K), B (K,N), bias (N,) as bf16 bit patterns (uint16).
+    Returns float32 (out f32) or uint16 bf16 bits (out bf16)."""
+    A, B = _u16(A), _u16(B)
+    bias = None if bias is None else _u16(bias)
+    M, K = A.shape
+    K2, N = B.shape
+    assert K == K2
+    p, keep = params(desc)
+    out = np.zeros((M, N), dtype=np.uint16 if p.out_bf16 else np.float32)
+    st = lib().dgo_gemm(ctypes.byref(p), _ptr(A), _ptr(B), _ptr(bias), out.ctypes.data,
+                        M, N, K, nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_gemm status %d" % st)
+    return out
+
+
+def gemm_at(desc, A, B, bias, ii, jj, M=None, nthreads=None):
+    """Outputs (ii[t], jj[t]) as float32 values.  A may hold only rows up to max(ii)."""
+    A, B = _u16(A), _u16(B)
+    bias = None if bias is None else _u16(bias)
+    K, N = B.shape
+    assert A.shape[1] == K
+    M = A.shape[0] if M is None else M
+    assert A.shape[0] >= int(np.max(ii)) + 1 if len(ii) else True
+    ii = np.ascontiguousarray(ii, dtype=np.int64)
+    jj = np.ascontiguousarray(jj, dtype=np.int64)
+    out = np.zeros(len(ii), dtype=np.float32)
+    p, keep = params(desc)
+    st = lib().dgo_gemm_at(ctypes.byref(p), _ptr(A), _ptr(B), _ptr(bias), M, N, K,
+                           ii.ctypes.data, jj.ctypes.data, len(ii), out.ctypes.data,
+                           nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_gemm_at status %d" % st)
+    return out
+
+
+def rowsum(desc, X, nthreads=None):
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    rows, cols = X.shape
+    out = np.zeros(rows, dtype=np.float32)
+    p, keep = params(desc)
+    st = lib().dgo_rowsum(ctypes.byref(p), X.ctypes.data, out.ctypes.data, rows, cols,
+                          nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_rowsum status %d" % st)
+    return out
+
+
+def plan_cuts(desc, K):
+    p, keep = params(desc)
+    cuts = np.zeros(p.split_k + 1, dtype=np.int64)
+    st = lib().dgo_plan_cuts(ctypes.byref(p), K, cuts.ctypes.data)
+    if st:
+        raise OracleError("dgo_plan_cuts status %d" % st)
+    return cuts
+
+
+def group_update(acc, a, b, g, fma, model="gfx950"):
+    a, b = _u16(a), _u16(b)
+    m = MODEL_GFX950 if model == "gfx950" else MODEL_EXACT
+    return np.float32(lib().dgo_group_update(m, float(acc), a.ctypes.data, b.ctypes.data,
+                                             len(a), g, fma))
+
+
+def group_update_batch(acc, a, b, g, fma, model="gfx950", nthreads=None):
+    """acc (count,), a and b (count, n) bf16 bits -> (count,) float32."""
+    acc = np.ascontiguousarray(acc, dtype=np.float32)
+    a, b = _u16(a), _u16(b)
+    count, n = a.shape
+    out = np.zeros(count, dtype=np.float32)
+    m = MODEL_GFX950 if model == "gfx950" else MODEL_EXACT
+    lib().dgo_group_update_batch(m, count, acc.ctypes.data, a.ctypes.data, b.ctypes.data,
+                                 n, g, fma, out.ctypes.data, nthreads or os.cpu_count())
+    return out
+
+
+def chunk8(acc, a, b):
+    a, b = _u16(a), _u16(b)
+    return np.float32(lib().dgo_chunk8(float(acc), a.ctypes.data, b.ctypes.data, len(a)))
+
+
+def exact_dot_rn32(c, a, b):
+    a, b = _u16(a), _u16(b)
+    return np.float32(lib().dgo_exact_dot_rn32(float(c), a.ctypes.data, b.ctypes.data, len(a)))
+
+
+def tree(v, bf16_round=False):
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    return np.float32(lib().dgo_tree(v.ctypes.data, len(v), int(bf16_round)))
+
+
+def f32_to_bf16(x):
+    return np.uint16(lib().dgo_f32_to_bf16(float(x)))
+
+
+def exp(x):
+    return np.float32(lib().dgo_exp(float(x)))
+
+
+def silu(x):
+    return np.float32(lib().dgo_silu(float(x)))

@@ -1,0 +1,126 @@
+/*
+ * dgo.h -- CPU oracle for the descriptor-ordered GEMM and row reduction.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, loads or
+ * calls this code; only the tests, the smoke check and the benchmark's CPU
+ * baseline do.  It shares no source with the GPU path.
+ *
+ * What it computes (paper: "Taming Bitwise Behavior in GPU Kernels with
+ * Tensor Core", Sec. 3 "Understand the bit behavior under GPU parallelism"):
+ *
+ *   A reduction is a dependence tree of binary32 additions; two kernels owe
+ *   each other the same bits when their trees are equivalent up to swapping
+ *   the children of a node (Sec. 3.1).  A matrix instruction folds
+ *   instruction_k products and (optionally) the incoming accumulator into ONE
+ *   rounding of their exact sum (Sec. 3.2.1).  A GEMM order is then fixed by
+ *   the group width, whether the accumulator joins that rounding
+ *   (use_fast_accum), where the short K turn falls (k_loop_step), the split-K
+ *   cut points, how tiles and parts are combined and at which precision
+ *   (partial_dtype / merge_dtype) (Sec. 3.2.2, "The algorithm families").
+ *
+ * The oracle evaluates exactly that order, one output at a time, with every
+ * rounding explicit: exact group sums in a wide fixed-point accumulator,
+ * binary32 round-to-nearest-even with gradual underflow, bfloat16 RNE.
+ *
+ * Storage: A is M x K bf16 row-major, B is K x N bf16 row-major, bias is N
+ * bf16, C is M x N (fp32 or bf16 bits) row-major.  X is rows x cols fp32.
+ */
+#ifndef DGO_H
+#define DGO_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { DGO_CARRY = 0, DGO_SEQ = 1, DGO_TREE = 2 };
+
+/* Arithmetic of one matrix-instruction accumulator update.
+ *  DGO_MODEL_EXACT  -- the paper's hypothesis (Sec. 3.2.1): the g products of
+ *                      a group and (fma = 1) the accumulator are summed
+ *                      exactly and rounded once.
+ *  DGO_MODEL_GFX950 -- what the gfx950 bf16 MFMA instructions compute, as
+ *                      read off the hardware with the paper's +L/-L/r
+ *                      numerical experiments (Sec. 4): the group is folded
+ *                      in chunks of 8 consecutive products; each chunk is
+ *                      aligned to a fixed-point grid set by its largest
+ *                      product, truncated, added to the accumulator and
+ *                      rounded once (see dgo_chunk8). */
+enum { DGO_MODEL_EXACT = 0, DGO_MODEL_GFX950 = 1 };
+enum { DGO_EPI_NONE = 0, DGO_EPI_BIAS = 1, DGO_EPI_BIAS_SILU = 2 };
+
+typedef struct {
+  int32_t model;          /* DGO_MODEL_* */
+  int32_t g;              /* products folded into one accumulator update (instruction_k) */
+  int32_t tile_k;         /* accumulator-closing tile length inside a part (inner k_cut) */
+  int32_t split_k;        /* number of parts S >= 1 (outer k_cut) */
+  const int64_t* k_cuts;  /* S-1 strictly increasing interior cut points, or NULL for the span rule */
+  int32_t tile_combine;   /* DGO_CARRY, DGO_SEQ or DGO_TREE */
+  int32_t split_combine;  /* DGO_SEQ or DGO_TREE */
+  int32_t tail_first;     /* 1: the short tile of a part comes first (k_loop_step) */
+  int32_t fma;            /* 1: the accumulator joins the group's single rounding */
+  int32_t partial_bf16;   /* 1: each part is rounded to bf16 before the merge */
+  int32_t merge_bf16;     /* 1: every merge addition is rounded to bf16 */
+  int32_t out_bf16;       /* 1: output stored as bf16 */
+  int32_t epilogue;       /* DGO_EPI_* */
+  int32_t pre_act_round;  /* 1: the pre-activation value is rounded to bf16 */
+  int32_t leaf_w;         /* row reduction: elements per sequential leaf */
+  int32_t sumsq;          /* row reduction: 1 = sum of squares */
+} dgo_params;
+
+/* Status: 0 ok, 1 invalid parameters, 3 shape inconsistent with the plan. */
+
+/* Full GEMM.  C receives M*N fp32 values (out_bf16 = 0) or bf16 bits. */
+int dgo_gemm(const dgo_params* p, const uint16_t* A, const uint16_t* B,
+             const uint16_t* bias, void* C, int64_t M, int64_t N, int64_t K,
+             int nthreads);
+
+/* Selected outputs (i[t], j[t]) of the same GEMM; out[t] is the output value
+ * widened to fp32 (a bf16 output is exactly representable in fp32).  Row i of
+ * A is read through A + i*K, so only the sampled rows need to exist. */
+int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
+                const uint16_t* bias, int64_t M, int64_t N, int64_t K,
+                const int64_t* ii, const int64_t* jj, int64_t n, float* out,
+                int nthreads);
+
+/* Row reduction: out[r] for each of `rows` rows of X (row stride = cols). */
+int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
+               int64_t cols, int nthreads);
+
+/* One accumulator update over n products a[t]*b[t] (n <= g; the rest of the
+ * group is zero padding) under the given model and fma rule.  Exposed for
+ * tests. */
+float dgo_group_update(int model, float acc, const uint16_t* a, const uint16_t* b,
+                       int n, int g, int fma);
+
+/* Batch of independent updates: out[t] = dgo_group_update(model, acc[t],
+ * a + t*n, b + t*n, n, g, fma) for t < count. */
+void dgo_group_update_batch(int model, int64_t count, const float* acc,
+                            const uint16_t* a, const uint16_t* b, int n, int g,
+                            int fma, float* out, int nthreads);
+
+/* One gfx950 bf16 MFMA chunk update: acc and n <= 8 products. */
+float dgo_chunk8(float acc, const uint16_t* a, const uint16_t* b, int n);
+
+/* Exact sum of n bf16 products plus c, rounded once to binary32 (RNE). */
+float dgo_exact_dot_rn32(float c, const uint16_t* a, const uint16_t* b, int n);
+
+/* Balanced tree over n binary32 values (level-wise pairing, odd last carried). */
+float dgo_tree(const float* v, int n, int bf16_round);
+
+/* Rounding helpers. */
+uint16_t dgo_f32_to_bf16(float x);
+float dgo_bf16_to_f32(uint16_t h);
+
+/* Epilogue functions: the exp and SiLU the descriptor's epilogue uses. */
+float dgo_exp(float x);
+float dgo_silu(float z);
+
+/* Cut plan for (K, params): writes S+1 cut points to cuts (caller provides
+ * split_k + 1 slots).  Returns 0 or a status. */
+int dgo_plan_cuts(const dgo_params* p, int64_t K, int64_t* cuts);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

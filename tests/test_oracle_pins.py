@@ -1,0 +1,548 @@
+"""Pins of the CPU oracle to facts other than itself (CPU only).
+
+Each test ties one part of the oracle to something it does not compute:
+values the paper prints for its worked examples (tests/golden), closed forms,
+library routines (numpy's correctly rounded conversions and sequential
+accumulation, torch's bf16 conversion, Python's exact rationals), textbook
+special cases, invariants, and error bounds against float64.
+"""
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2609_11356_amd import inputs
+from tests.exact import bf, f, rn32
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+ONE = np.uint16(0x3F80)
+
+
+def bits(x):
+    return inputs.f32_to_bf16_bits(np.asarray(x, dtype=np.float32))
+
+
+def exact_desc(g, **kw):
+    d = dict(model="exact", g=g, tile_k=kw.pop("tile_k", max(g, 64)))
+    d.update(kw)
+    return d
+
+
+# --------------------------------------------------------------- rounding
+
+
+def test_rn32_helper_matches_numpy_conversion():
+    """The exact-rational RN32 used by later pins agrees with numpy's
+    correctly rounded float64 -> float32 conversion, ties and subnormals
+    included."""
+    rng = np.random.default_rng(11)
+    d = rng.standard_normal(4000) * np.exp2(rng.integers(-160, 128, 4000))
+    # exact binary32 midpoints: x.5 ulp
+    mids = []
+    for _ in range(500):
+        v = np.float32(rng.standard_normal() * 2.0 ** rng.integers(-140, 100))
+        nxt = np.nextafter(v, np.float32(np.inf))
+        mids.append((float(v) + float(nxt)) / 2)
+    for x in list(d) + mids + [2.0 ** -150, 3 * 2.0 ** -151, 2.0 ** -149 * 1.5]:
+        assert rn32(Fraction(x)).view(np.uint32) == np.float32(x).view(np.uint32), x
+
+
+def test_bf16_rounding_matches_torch():
+    """Oracle bf16 RNE == torch's fp32 -> bf16 conversion over every high half
+    and the low halves that decide rounding."""
+    torch = pytest.importorskip("torch")
+    hi = np.arange(0, 1 << 16, dtype=np.uint32) << 16
+    lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF, 0x4000, 0xC000], dtype=np.uint32)
+    u = (hi[:, None] | lows[None, :]).reshape(-1)
+    x = u.view(np.float32)
+    ref = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    ours = np.array([oracle.f32_to_bf16(v) for v in x[::7]], dtype=np.uint16)
+    refs = ref[::7]
+    nan = np.isnan(x[::7])
+    assert np.array_equal(ours[~nan], refs[~nan])
+    assert np.all((ours[nan] & 0x7FFF) > 0x7F80)
+    # the input generator's packer agrees too
+    gen = inputs.f32_to_bf16_bits(x)
+    assert np.array_equal(gen[~np.isnan(x)], ref[~np.isnan(x)])
+
+
+# ------------------------------------------------------ exact group sums
+
+
+@pytest.mark.parametrize("mode", ["normal", "spread", "wide"])
+def test_exact_dot_matches_rationals(mode):
+    """One rounding of the exact sum of bf16 products plus an fp32 seed
+    (the paper's instruction hypothesis, Sec. 3.2.1) == Python's exact
+    rational sum rounded by the IEEE definition."""
+    rng = np.random.default_rng({"normal": 1, "spread": 2, "wide": 3}[mode])
+    for t in range(300):
+        n = int(rng.integers(1, 40))
+        if mode == "normal":
+            a, b = bits(rng.standard_normal(n)), bits(rng.standard_normal(n))
+        elif mode == "spread":
+            a = inputs.spread_bf16(1000 + t, n)
+            b = inputs.spread_bf16(5000 + t, n)
+        else:
+            a = inputs.spread_bf16(1000 + t, n, -120, 120)
+            b = inputs.spread_bf16(5000 + t, n, -10, 10)
+        c = np.float32(rng.standard_normal() * 2.0 ** rng.integers(-30, 30))
+        want = rn32(sum(bf(x) * bf(y) for x, y in zip(a, b)) + f(c))
+        got = oracle.exact_dot_rn32(c, a, b)
+        assert got.view(np.uint32) == want.view(np.uint32)
+        # fma = 0: the group rounds on its own, then a second rounding
+        got0 = oracle.group_update(c, a, b, g=64, fma=0, model="exact")
+        want0 = np.float32(c) + rn32(sum(bf(x) * bf(y) for x, y in zip(a, b)))
+        assert got0.view(np.uint32) == np.float32(want0).view(np.uint32)
+
+
+# ------------------------------------------------ order: textbook cases
+
+
+@pytest.mark.parametrize("fma", [0, 1])
+def test_group_of_one_is_sequential_fp32_dot(fma):
+    """g = 1, no split, carried accumulator: the descriptor's order is the
+    plain left-to-right binary32 dot product (a product of two bf16 values is
+    exact in binary32), i.e. numpy's sequential accumulation."""
+    rng = np.random.default_rng(5)
+    K, N = 300, 5
+    A = bits(rng.standard_normal((3, K)))
+    B = bits(rng.standard_normal((K, N)) * 0.1)
+    C = oracle.gemm(exact_desc(1, tile_k=8, fma=fma), A, B)
+    Af, Bf = inputs.bf16_bits_to_f32(A), inputs.bf16_bits_to_f32(B)
+    for i in range(3):
+        for j in range(N):
+            prods = (Af[i] * Bf[:, j]).astype(np.float32)
+            ref = np.add.accumulate(prods, dtype=np.float32)[-1]
+            assert C[i, j].view(np.uint32) == ref.view(np.uint32)
+
+
+DESCS = [
+    dict(model="gfx950", mma="16x16x32", tile_k=64),
+    dict(model="gfx950", mma="32x32x16", tile_k=64, fma=0),
+    dict(model="gfx950", mma="16x16x32", tile_k=32, split_k=2, tile_combine="tree", split_combine="tree"),
+    dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=3, tile_combine="seq", split_combine="seq"),
+    dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=9, split_combine="tree", tail="first"),
+    dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=4, partial="bf16", merge="bf16"),
+    dict(model="exact", g=16, tile_k=32, split_k=2, tile_combine="tree"),
+    dict(model="exact", g=1, tile_k=4, tile_combine="seq", fma=0),
+]
+
+
+@pytest.mark.parametrize("desc", DESCS)
+@pytest.mark.parametrize("K", [1, 7, 64, 257, 576, 8648])
+def test_all_ones_counts_terms(desc, K):
+    """All-ones A and B: every output is exactly K (binary32 holds every
+    integer below 2^24), so any dropped or doubled term shows (the paper's
+    App. D count test, including K = 8648 split nine ways)."""
+    S = desc.get("split_k", 1)
+    if desc.get("merge") == "bf16" and K > 256:
+        pytest.skip("bf16 merge cannot hold K > 256 exactly")
+    span = -(-K // S)
+    tk = desc["tile_k"]
+    span = -(-span // tk) * tk
+    if S > 1 and (S - 1) * span >= K:
+        with pytest.raises(oracle.OracleError):
+            oracle.gemm(desc, np.full((2, K), ONE), np.full((K, 3), ONE))
+        return
+    C = oracle.gemm(desc, np.full((2, K), ONE), np.full((K, 3), ONE))
+    assert np.all(C == K)
+
+
+@pytest.mark.parametrize("desc", DESCS)
+def test_small_integers_are_exact(desc):
+    """Integer operands whose partial sums stay below 2^24 make every order
+    exact: the oracle must return the integer matrix product."""
+    rng = np.random.default_rng(9)
+    K = 1152
+    Ai = rng.integers(-8, 9, (4, K))
+    Bi = rng.integers(-8, 9, (K, 6))
+    C = oracle.gemm(desc, bits(Ai), bits(Bi))
+    if desc.get("partial") == "bf16":
+        pytest.skip("bf16 partials round integers above 256")
+    assert np.array_equal(C.astype(np.int64), Ai @ Bi)
+
+
+# ---------------------------------------------- the paper's worked walks
+
+
+def _golden():
+    with open(os.path.join(GOLDEN, "paper_walks.json")) as fh:
+        return json.load(fh)
+
+
+def _splitk_zero_set(desc):
+    g = _golden()
+    w = g["splitk_walk"]
+    K, L, r = w["K"], g["L"], g["r"]
+    rows = []
+    for m in range(1, K - 1):
+        v = np.zeros(K, dtype=np.float32)
+        v[0], v[m], v[m + 1] = r, L, -L
+        rows.append(v)
+    A = bits(np.stack(rows))
+    B = np.full((K, 1), ONE)
+    C = oracle.gemm(desc, A, B)[:, 0]
+    assert set(np.unique(C)) <= {0.0, np.float32(r)}
+    return {m for m, v in zip(range(1, K - 1), C) if v == 0.0}
+
+
+def test_splitk_walk_gfx950_matches_paper():
+    """Sec. 4 split-K walk: r at k = 0, +L/-L at (m, m+1), K = 576 cut into
+    three parts of 192.  The paper reads zeros for m = 1..191 and at 383 only.
+    Under the gfx950 chunk arithmetic every placement inside r's part floors r
+    away, so the measured set is exactly the printed one, for either
+    instruction shape."""
+    w = _golden()["splitk_walk"]
+    want = set(range(w["zero_from"], w["zero_to"] + 1)) | set(w["zero_also"])
+    for mma in ("16x16x32", "32x32x16"):
+        desc = dict(model="gfx950", mma=mma, tile_k=64, split_k=w["parts"])
+        assert list(oracle.plan_cuts(desc, w["K"])) == [0, 192, 384, 576]
+        assert _splitk_zero_set(desc) == want
+
+
+@pytest.mark.parametrize("g", [1, 16, 32])
+def test_splitk_walk_exact_groups(g):
+    """The same walk under the paper's exact-group hypothesis (Sec. 3.2.1).
+    With g = 1 it reproduces the printed set.  With wider exact groups a pair
+    inside one group cancels before r is seen, so only placements whose +L
+    closes a group (m = g-1 mod g) or straddles a part boundary absorb r."""
+    w = _golden()["splitk_walk"]
+    desc = exact_desc(g, tile_k=64, split_k=w["parts"])
+    got = _splitk_zero_set(desc)
+    if g == 1:
+        want = set(range(1, 192)) | {383}
+    else:
+        want = {m for m in range(1, 191) if m % g == g - 1} | {191, 383}
+    assert got == want
+
+
+def test_contiguous_walk_matches_paper():
+    """Sec. 4 contiguous walk: eight terms summed in two groups of four, each
+    group a left fold; r at 0; the pair at (1,2), (2,3), (3,4) gives 0 and the
+    first placement returning r is (4,5)."""
+    g = _golden()
+    w = g["contiguous_walk"]
+    desc = exact_desc(1, tile_k=w["group"], tile_combine="seq")
+    for pair in w["pairs_zero"] + [w["first_pair_returning_r"]]:
+        v = np.zeros(w["terms"], dtype=np.float32)
+        v[w["r_at"]], v[pair[0]], v[pair[1]] = g["r"], g["L"], -g["L"]
+        c = oracle.gemm(desc, bits(v[None, :]), np.full((w["terms"], 1), ONE))[0, 0]
+        want = g["r"] if pair == w["first_pair_returning_r"] else 0.0
+        assert c == np.float32(want), pair
+
+
+# -------------------------------------------------------- trees and folds
+
+
+def test_nonassociativity_hand_examples():
+    """[2^24, 1, 1, -2^24]: chain 0, balanced tree 1, exact 2.
+    [2^24, 1, -2^24, 1]: the count-up (natural-order) tree gives 1 while the
+    count-down butterfly -- a tree over bit-reversed lanes (Sec. 3.2.2, GEMV)
+    -- gives 2; the pinned order is the first."""
+    v = np.array([2.0 ** 24, 1, 1, -2.0 ** 24], dtype=np.float32)
+    assert oracle.tree(v) == 1.0
+    X = v[None, :]
+    assert oracle.rowsum(dict(leaf_w=4), X)[0] == 0.0
+    assert oracle.rowsum(dict(leaf_w=1), X)[0] == 1.0
+    w = np.array([2.0 ** 24, 1, -2.0 ** 24, 1], dtype=np.float32)
+    assert oracle.tree(w) == 1.0
+    assert oracle.tree(w[[0, 2, 1, 3]]) == 2.0
+
+
+def _halving(v):
+    v = np.asarray(v, dtype=np.float32)
+    if len(v) == 1:
+        return v[0]
+    h = len(v) // 2
+    return np.float32(_halving(v[:h]) + _halving(v[h:]))
+
+
+def test_tree_is_recursive_halving_over_negzero_padding():
+    """The balanced tree equals textbook recursive halving for a power-of-two
+    count, and for any count equals it over the values padded on the right
+    with -0 (the exact identity of binary32 addition)."""
+    rng = np.random.default_rng(3)
+    for n in list(range(1, 70)) + [127, 128, 129, 1000]:
+        v = (rng.standard_normal(n) * np.exp2(rng.integers(-20, 20, n))).astype(np.float32)
+        p = 1 << (n - 1).bit_length()
+        padded = np.concatenate([v, np.full(p - n, -0.0, dtype=np.float32)])
+        assert oracle.tree(v).view(np.uint32) == _halving(padded).view(np.uint32), n
+
+
+def test_rowsum_special_cases():
+    rng = np.random.default_rng(4)
+    X = inputs.lognormal_f32(4, (6, 300))
+    # one leaf covering the row: plain sequential accumulation
+    seq = oracle.rowsum(dict(leaf_w=512), X)
+    for r in range(6):
+        assert seq[r] == np.add.accumulate(X[r], dtype=np.float32)[-1]
+    # leaves of one element: the balanced tree of the elements
+    tr = oracle.rowsum(dict(leaf_w=1), X)
+    for r in range(6):
+        assert tr[r] == oracle.tree(X[r])
+    # leaves of 64: tree over the sequential leaves (SUM)
+    lw = oracle.rowsum(dict(leaf_w=64), X)
+    for r in range(6):
+        leaves = [np.add.accumulate(X[r, i:i + 64], dtype=np.float32)[-1] for i in range(0, 300, 64)]
+        assert lw[r] == oracle.tree(np.array(leaves, dtype=np.float32))
+    # SUMSQ without fma: sequential sum of binary32 squares
+    sq = oracle.rowsum(dict(leaf_w=512, reduce="sumsq", fma=0), X)
+    for r in range(6):
+        assert sq[r] == np.add.accumulate((X[r] * X[r]).astype(np.float32), dtype=np.float32)[-1]
+    # SUMSQ with fma: s = RN32(x0^2), then s = RN32(x_i^2 + s) (one rounding)
+    Y = X[:, :40]
+    sf = oracle.rowsum(dict(leaf_w=64, reduce="sumsq", fma=1), Y)
+    for r in range(6):
+        s = rn32(f(Y[r, 0]) ** 2)
+        for x in Y[r, 1:]:
+            s = rn32(f(x) ** 2 + f(s))
+        assert sf[r].view(np.uint32) == s.view(np.uint32)
+    # comparable magnitudes, where one rounding and two roundings part ways
+    U = np.random.default_rng(41).uniform(1, 2, (4, 200)).astype(np.float32)
+    su = oracle.rowsum(dict(leaf_w=256, reduce="sumsq", fma=1), U)
+    sd = oracle.rowsum(dict(leaf_w=256, reduce="sumsq", fma=0), U)
+    for r in range(4):
+        s = rn32(f(U[r, 0]) ** 2)
+        for x in U[r, 1:]:
+            s = rn32(f(x) ** 2 + f(s))
+        assert su[r].view(np.uint32) == s.view(np.uint32)
+    assert not np.array_equal(su, sd)
+    # empty rows sum to +0
+    assert oracle.rowsum(dict(leaf_w=64), np.zeros((3, 0), np.float32)).tolist() == [0.0] * 3
+
+
+# ------------------------------------------- structural identities of order
+
+
+def _spread(seed, M=3, K=576, N=4):
+    return inputs.spread_bf16(seed, (M, K)), inputs.spread_bf16(seed + 1, (K, N))
+
+
+@pytest.mark.parametrize("model,g", [("exact", 16), ("gfx950", 32), ("gfx950", 16)])
+def test_tiles_of_one_group_seq_equals_carry_without_fma(model, g):
+    """Closing every tile after one group and chaining the tiles is the same
+    tree as carrying the accumulator with the group rounded on its own."""
+    A, B = _spread(21)
+    kw = dict(model=model, g=g) if model == "exact" else dict(model=model, mma={32: "16x16x32", 16: "32x32x16"}[g])
+    c1 = oracle.gemm(dict(kw, tile_k=g, tile_combine="seq", fma=1), A, B)
+    c2 = oracle.gemm(dict(kw, tile_k=g, tile_combine="carry", fma=0), A, B)
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_single_tile_tree_and_seq_equal_carry():
+    A, B = _spread(22)
+    base = oracle.gemm(dict(tile_k=576), A, B)
+    for tc in ("seq", "tree"):
+        assert np.array_equal(oracle.gemm(dict(tile_k=576, tile_combine=tc), A, B).view(np.uint32),
+                              base.view(np.uint32))
+
+
+def test_fma_on_ignores_instruction_shape_on_gfx950():
+    """With the accumulator carried through every chunk, the 16x16x32 and
+    32x32x16 instructions (groups of 32 and 16) fold the same 8-product chunks
+    in the same order."""
+    A, B = _spread(23)
+    for tc in ("carry", "tree"):
+        c1 = oracle.gemm(dict(mma="16x16x32", tile_k=64, tile_combine=tc), A, B)
+        c2 = oracle.gemm(dict(mma="32x32x16", tile_k=64, tile_combine=tc), A, B)
+        assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+    # ... but not with fma = 0, where the instruction's group is rounded alone
+    c1 = oracle.gemm(dict(mma="16x16x32", tile_k=64, fma=0), A, B)
+    c2 = oracle.gemm(dict(mma="32x32x16", tile_k=64, fma=0), A, B)
+    assert not np.array_equal(c1.view(np.uint32), c2.view(np.uint32))
+
+
+def test_explicit_cuts_equal_span_rule_and_tail_position():
+    A, B = _spread(24)
+    d = dict(tile_k=64, split_k=3)
+    assert np.array_equal(oracle.gemm(d, A, B).view(np.uint32),
+                          oracle.gemm(dict(d, k_cuts=[192, 384]), A, B).view(np.uint32))
+    # K a multiple of tile_k: the short-tile position is moot
+    assert np.array_equal(oracle.gemm(dict(d, tail="first"), A, B).view(np.uint32),
+                          oracle.gemm(d, A, B).view(np.uint32))
+    # a 40-element tail inside each tree-combined part changes the tree
+    A2, B2 = _spread(25, K=3 * 232)
+    d2 = dict(d, k_cuts=[232, 464], tile_combine="tree")
+    t1 = oracle.gemm(d2, A2, B2)
+    t2 = oracle.gemm(dict(d2, tail="first"), A2, B2)
+    assert not np.array_equal(t1.view(np.uint32), t2.view(np.uint32))
+
+
+def test_merge_trees_of_two_and_three_are_chains():
+    """A balanced tree over 2 or 3 parts is the sequential chain; over 4 it
+    is not."""
+    A, B = _spread(26, K=768, N=16)
+    for S in (2, 3):
+        seq = oracle.gemm(dict(tile_k=64, split_k=S), A, B)
+        tre = oracle.gemm(dict(tile_k=64, split_k=S, split_combine="tree"), A, B)
+        assert np.array_equal(seq.view(np.uint32), tre.view(np.uint32))
+    seq = oracle.gemm(dict(tile_k=64, split_k=4), A, B)
+    tre = oracle.gemm(dict(tile_k=64, split_k=4, split_combine="tree"), A, B)
+    assert not np.array_equal(seq.view(np.uint32), tre.view(np.uint32))
+
+
+def test_rows_do_not_depend_on_M():
+    """Each output follows its own order: the rows of a 7-row product equal
+    the first 7 rows of a 64-row product (batch invariance is structural)."""
+    A, B = _spread(27, M=64, K=256, N=8)
+    full = oracle.gemm(dict(tile_k=64, out="bf16"), A, B)
+    part = oracle.gemm(dict(tile_k=64, out="bf16"), A[:7], B)
+    assert np.array_equal(full[:7], part)
+    at = oracle.gemm_at(dict(tile_k=64, out="bf16"), A, B, None, [0, 5, 63], [1, 7, 3])
+    assert np.array_equal(inputs.f32_to_bf16_bits(at), full[[0, 5, 63], [1, 7, 3]])
+
+
+# ------------------------------------------------------------ error bounds
+
+
+def _bound_check(desc, A, B, bias=None, rel=2.0 ** -8):
+    C = oracle.gemm(desc, A, B, bias)
+    Af = inputs.bf16_bits_to_f32(A).astype(np.float64)
+    Bf = inputs.bf16_bits_to_f32(B).astype(np.float64)
+    ref = Af @ Bf
+    mag = np.abs(Af) @ np.abs(Bf)
+    Cf = inputs.bf16_bits_to_f32(C) if C.dtype == np.uint16 else C
+    err = np.abs(Cf.astype(np.float64) - ref)
+    assert np.all(err <= rel * mag), float(np.max(err / np.maximum(mag, 1e-300)))
+    return err, mag
+
+
+def test_error_bound_tiny_config():
+    """|C - C_fp64| <= 2^-8 * sum|a_ik b_kj| for the tiny descriptor, and the
+    fp32 result is far tighter: one rounding per chunk update and merge."""
+    A, B = inputs.tiny(0)
+    desc = dict(mma="16x16x32", tile_k=32, split_k=2, tile_combine="tree", split_combine="tree")
+    _bound_check(desc, A, B)
+    updates = 256 // 8 + 8 + 2
+    _bound_check(desc, A, B, rel=(2.0 ** -20 + updates * 2.0 ** -23))
+    As, Bs = inputs.tiny(0, spread=True)
+    _bound_check(desc, As, Bs, rel=(2.0 ** -20 + updates * 2.0 ** -23))
+
+
+def test_error_bound_bf16_output_sweep_rows():
+    A = inputs.sweep_activations(1, rows=4)[:, :1024]
+    B = inputs.sweep_weight(2)[:1024, :256]
+    _bound_check(dict(tile_k=64, out="bf16"), A, B)
+
+
+# ------------------------------------------------------------- epilogue
+
+
+def test_exp_accuracy_dense_sweep():
+    """Our binary32 exp stays within 2 ulp of the real exponential."""
+    xs = np.concatenate([np.linspace(-103.9, 88.7, 60001, dtype=np.float32),
+                         np.float32(np.random.default_rng(6).uniform(-20, 20, 20000))])
+    worst = 0.0
+    for x in xs:
+        y = oracle.exp(x)
+        t = math.exp(float(x))
+        if t < 2.0 ** -126:
+            ulp = 2.0 ** -149
+        else:
+            ulp = 2.0 ** (math.floor(math.log2(t)) - 23)
+        worst = max(worst, abs(float(y) - t) / ulp)
+    assert worst <= 2.0, worst
+    assert oracle.exp(-200.0) == 0.0 and oracle.exp(200.0) == np.inf
+    assert np.isnan(oracle.exp(np.nan))
+
+
+def test_silu_accuracy():
+    """z / (1 + exp(-z)) within 4 ulp of the real SiLU while exp(-z) is
+    finite in binary32 (z > -88.7); below that 1 + exp(-z) overflows and the
+    result is a zero whose distance to the true value is below 2^-120."""
+    rng = np.random.default_rng(7)
+    for z in np.concatenate([rng.standard_normal(5000) * 4, rng.uniform(-95, 90, 2000)]).astype(np.float32):
+        t = float(z) / (1.0 + math.exp(-float(z)))
+        y = float(oracle.silu(z))
+        if z > -88.7:
+            assert abs(y - t) <= 4 * 2.0 ** -24 * abs(t) + 2.0 ** -149, (z, y, t)
+        else:
+            assert y == 0.0 and abs(t) < 2.0 ** -120
+
+
+def test_epilogue_rounding_points():
+    """FINAL: one bf16 rounding of silu(y + bias).  PRE_ACT: the
+    pre-activation is rounded to bf16 first (an unfused Linear -> SiLU
+    pair).  Both equal the helpers applied to the fp32 GEMM result."""
+    A, B = inputs.tiny(0)
+    bias = inputs.normal_bf16(7, (64,), 0.5)
+    y = oracle.gemm(dict(tile_k=64), A, B)
+    fin = oracle.gemm(dict(tile_k=64, epilogue="bias_silu", out="bf16"), A, B, bias)
+    pre = oracle.gemm(dict(tile_k=64, epilogue="bias_silu", out="bf16", epi_round="pre_act"), A, B, bias)
+    bb = inputs.bf16_bits_to_f32(bias)
+    for i in range(0, 16, 5):
+        for j in range(0, 64, 9):
+            z = np.float32(y[i, j] + bb[j])
+            assert fin[i, j] == oracle.f32_to_bf16(oracle.silu(z))
+            zr = inputs.bf16_bits_to_f32(np.array([oracle.f32_to_bf16(z)]))[0]
+            assert pre[i, j] == oracle.f32_to_bf16(oracle.silu(zr))
+    plain = oracle.gemm(dict(tile_k=64, epilogue="bias"), A, B, bias)
+    assert np.array_equal(plain, (y + bb[None, :]).astype(np.float32))
+
+
+# --------------------------------------- the gfx950 chunk model by hand
+
+
+def _chunk(acc, prods):
+    a = bits([p[0] for p in prods])
+    b = bits([p[1] for p in prods])
+    return oracle.chunk8(np.float32(acc), a, b)
+
+
+def test_chunk_model_hand_examples():
+    """Worked cases of the gfx950 chunk arithmetic, each derived by hand from
+    its definition (anchor E = largest exponent sum, products truncated
+    toward zero onto 2^(E-24), T floored onto 2^max(E-24, x(T)-31, -157),
+    one RNE rounding)."""
+    # window: +2^e - 2^e + 1 keeps the 1 exactly when 2^0 >= 2^(e-24)
+    for e in range(0, 40):
+        got = _chunk(0, [(2.0 ** e, 1), (-(2.0 ** e), 1), (1, 1)])
+        assert got == (1.0 if e <= 24 else 0.0), e
+    # the Sec. 4 pair absorbs r inside one chunk ...
+    assert _chunk(0, [(2.0 ** -15, 1), (1024, 1), (-1024, 1)]) == 0.0
+    # ... and r survives when the pair cancels in an earlier chunk
+    a = bits([1024, -1024] + [0] * 6 + [2.0 ** -15] + [0] * 7)
+    assert oracle.group_update(0, a, np.full(16, ONE), 16, 1) == np.float32(2.0 ** -15)
+    # ties to even on the product sum, tail below the grid dropped
+    assert _chunk(0, [(1, 1), (2.0 ** -24, 1)]) == 1.0
+    assert _chunk(0, [(1, 1), (2.0 ** -23, 1), (2.0 ** -24, 1)]) == np.float32(1 + 2.0 ** -22)
+    assert _chunk(0, [(1, 1), (2.0 ** -24, 1), (2.0 ** -30, 1)]) == 1.0
+    # the result-relative grid 2^(x(T)-31) keeps a tail the product grid drops
+    assert _chunk(1.0, [(2.0 ** -24, 1), (2.0 ** -30, 1)]) == np.float32(1 + 2.0 ** -23)
+    assert _chunk(1.0, [(2.0 ** -24, 1), (2.0 ** -31, 1)]) == np.float32(1 + 2.0 ** -23)
+    assert _chunk(1.0, [(2.0 ** -24, 1), (2.0 ** -32, 1)]) == 1.0
+    # products truncate toward zero, the sum floors toward -inf
+    assert _chunk(0, [(1, 1), (-(2.0 ** -24), 1), (-(2.0 ** -30), 1)]) == np.float32(1 - 2.0 ** -24)
+    assert _chunk(-1.0, [(-(2.0 ** -24), 1), (-(2.0 ** -40), 1)]) == np.float32(-(1 + 2.0 ** -23))
+    # a small accumulator is floored onto the product grid
+    assert _chunk(-(2.0 ** -30), [(1, 1)]) == np.float32(1 - 2.0 ** -24)
+    assert _chunk(2.0 ** -30, [(1, 1)]) == 1.0
+    # exactly zero results are +0, even from -0 inputs
+    z = _chunk(-0.0, [(-0.0, 1), (0.0, -1)])
+    assert z == 0.0 and not np.signbit(z)
+    # products of 2^128 overflow to infinity before they can cancel
+    assert np.isnan(_chunk(0, [(2.0 ** 127, 2), (-(2.0 ** 127), 2), (1, 1)]))
+    assert _chunk(0, [(2.0 ** 127, 1.9921875), (-(2.0 ** 127), 1.9921875), (2.0 ** 103, 1)]) == np.float32(2.0 ** 103)
+    assert _chunk(0, [(2.0 ** 127, 1.9921875), (-(2.0 ** 127), 1.9921875), (2.0 ** 102, 1)]) == 0.0
+    # subnormal bf16 factors anchor at exponent -126
+    assert _chunk(0, [(2.0 ** -133, 2.0 ** 100), (1.5 * 2.0 ** -26, 2.0 ** -25)]) == np.float32(2.0 ** -33)
+    # the grid never goes below 2^-157
+    assert _chunk(0, [(2.0 ** -75, 2.0 ** -75), (2.0 ** -75, 2.0 ** -82)]) == np.float32(2.0 ** -149)
+    assert _chunk(0, [(2.0 ** -75, 2.0 ** -75), (2.0 ** -75, 2.0 ** -83)]) == 0.0
+    assert _chunk(0, [(-(2.0 ** -75), 2.0 ** -75), (-(2.0 ** -75), 2.0 ** -83)]) == np.float32(-(2.0 ** -149))
+
+
+def test_chunk_model_equals_exact_when_window_holds_everything():
+    """When every term of every chunk sits on the chunk's grid (integers with a
+    narrow spread), the chunk model is the exact-group hypothesis with groups
+    of 8."""
+    rng = np.random.default_rng(8)
+    A = bits(rng.integers(-64, 65, (4, 256)))
+    B = bits(rng.integers(-64, 65, (256, 5)))
+    c1 = oracle.gemm(dict(model="gfx950", tile_k=64), A, B)
+    c2 = oracle.gemm(dict(model="exact", g=8, tile_k=64), A, B)
+    assert np.array_equal(c1, c2)

@@ -1,0 +1,97 @@
+"""Power of the oracle's pins: plausible mistakes planted in a copy of the
+oracle's C source must each be caught by at least one pin (the paper checks
+its own byte comparisons against a deliberately broken kernel, App. E).
+CPU only; the planted copies live in a temporary directory."""
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import test_oracle_pins as pins
+
+HERE = os.path.dirname(os.path.abspath(oracle.__file__))
+
+MUTANTS = {
+    "drops the last group of a tile": (
+        "for (int64_t q = t0; q < t0 + tl; q += p->g) {",
+        "for (int64_t q = t0; q + p->g < t0 + tl; q += p->g) {"),
+    "merges the parts last to first": (
+        "  float s = v[0];\n  for (int k = 1; k < n; ++k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }",
+        "  float s = v[n - 1];\n  for (int k = n - 2; k >= 0; --k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }"),
+    "tree counts down (pairs k with k + n/2)": (
+        "float s = t[2 * k] + t[2 * k + 1];",
+        "float s = t[k] + t[k + h];"),
+    "products truncate toward -inf": (
+        "else m = (qe - e) >= 64 ? 0 : m >> (qe - e);",
+        "else m = (qe - e) >= 64 ? (neg ? 1 : 0) : (neg ? (m + ((uint64_t)1 << (qe - e)) - 1) >> (qe - e) : m >> (qe - e));"),
+    "product window one bit wider": ("#define CHUNK_W 24", "#define CHUNK_W 25"),
+    "result grid one bit coarser": ("#define CHUNK_F 31", "#define CHUNK_F 30"),
+    "accumulator left out of the chunk sum": (
+        "    split_f32(acc, &neg, &m, &e);\n    xacc_add_int(&x, neg, m, e);\n  }\n  /* leading bit",
+        "    split_f32(acc, &neg, &m, &e);\n    (void)m;\n  }\n  /* leading bit"),
+    "fma flag ignored": ("  s = fma ? acc : 0.0f;", "  s = acc; fma = 1;"),
+    "short tile always last": ("if (p->tail_first && len % tk)", "if (0 && len % tk)"),
+    "pre-activation rounding skipped": ("if (p->pre_act_round) z = rnbf(z);", "if (0) z = rnbf(z);"),
+    "B read transposed": ("bbuf[u] = bcol[(q + u) * c->ldb];", "bbuf[u] = bcol[(q + u)];"),
+    "bf16 conversion truncates": (
+        "return (uint16_t)((u + 0x7fffu + lsb) >> 16);", "(void)lsb; return (uint16_t)(u >> 16);"),
+    "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
+    "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
+    "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
+                               "int sign = 0;\n    if (bf16_isnan(a[t])"),
+}
+
+CHECKS = [
+    lambda: pins.test_bf16_rounding_matches_torch(),
+    lambda: pins.test_exact_dot_matches_rationals("spread"),
+    lambda: pins.test_group_of_one_is_sequential_fp32_dot(1),
+    lambda: [pins.test_all_ones_counts_terms(d, K) for d in pins.DESCS[:5] for K in (257, 576)],
+    lambda: pins.test_splitk_walk_gfx950_matches_paper(),
+    lambda: pins.test_nonassociativity_hand_examples(),
+    lambda: pins.test_tree_is_recursive_halving_over_negzero_padding(),
+    lambda: pins.test_rowsum_special_cases(),
+    lambda: pins.test_tiles_of_one_group_seq_equals_carry_without_fma("gfx950", 32),
+    lambda: pins.test_fma_on_ignores_instruction_shape_on_gfx950(),
+    lambda: pins.test_explicit_cuts_equal_span_rule_and_tail_position(),
+    lambda: pins.test_exp_accuracy_dense_sweep(),
+    lambda: pins.test_epilogue_rounding_points(),
+    lambda: pins.test_chunk_model_hand_examples(),
+]
+
+
+def _build_mutant(tmp, old, new):
+    src = open(os.path.join(HERE, "dgo.c")).read()
+    assert src.count(old) == 1, "mutation site not found exactly once: %r" % old[:60]
+    d = tmp / "m"
+    d.mkdir()
+    shutil.copy(os.path.join(HERE, "dgo.h"), d / "dgo.h")
+    (d / "dgo.c").write_text(src.replace(old, new))
+    lib = d / "libdgo.so"
+    subprocess.run(["gcc", "-std=gnu11", "-O2", "-fPIC", "-shared", "-fopenmp", "-ffp-contract=off",
+                    "-o", str(lib), str(d / "dgo.c"), "-lm"], check=True, capture_output=True)
+    return str(lib)
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_catch_planted_mistake(name, tmp_path):
+    lib = _build_mutant(tmp_path, *MUTANTS[name])
+    prev = oracle.use_library(lib)
+    caught = []
+    try:
+        for i, check in enumerate(CHECKS):
+            try:
+                check()
+            except (AssertionError, oracle.OracleError):
+                caught.append(i)
+                break
+    finally:
+        oracle.restore_library(prev)
+    assert caught, "no pin caught the planted mistake: " + name
+
+
+def test_unmutated_oracle_passes_every_check():
+    for check in CHECKS:
+        check()
