@@ -1,0 +1,169 @@
+/*
+ * dg.h -- descriptor-ordered bf16 GEMM and row reduction for MI355X (gfx950).
+ *
+ * C ABI of libdg.so.  Every floating-point reduction order the library
+ * computes is fixed by a descriptor, never by the tile shape, wave count or
+ * grid the library picks for speed, so the bits of every output depend only
+ * on the descriptor and the operands -- not on M, on other rows, or on the
+ * launch configuration.
+ *
+ * Paper: "Taming Bitwise Behavior in GPU Kernels with Tensor Core" --
+ *   Sec. 3.1  a reduction's order is its dependence tree; equal trees (up to
+ *             swapping children) give equal bits;
+ *   Sec. 3.2.1 a matrix instruction folds a group of products and the
+ *             accumulator with its own rounding rule;
+ *   Sec. 3.2.2 the GEMM descriptor: instruction_k, use_fast_accum,
+ *             k_loop_step, split-K span / k_cuts, partial_dtype, merge_dtype;
+ *   Sec. 5.1  the balanced (count-up) tree used for every tree combine.
+ *
+ * Conventions (all entry points):
+ *   - No exception crosses the ABI; every entry point returns a dg_status.
+ *   - Device pointers are caller-owned HIP device allocations; the library
+ *     never frees them.  Matrices are dense row-major: A is M x K (leading
+ *     dimension K), B is K x N (N), C is M x N (N), X is rows x cols (cols).
+ *     bf16 operands are raw IEEE bfloat16 bit patterns (uint16).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     and the call returns; results are ready when the stream reaches them.
+ *   - Validation happens before anything is enqueued: an error return means
+ *     nothing was launched and no output was written.
+ *   - A descriptor is immutable after dg_desc_create and may be used from any
+ *     number of host threads and streams at once.
+ */
+#ifndef DG_H
+#define DG_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DG_OK = 0,
+  DG_ERR_INVALID = 1,     /* a NULL handle/pointer or a field out of range */
+  DG_ERR_UNSUPPORTED = 2, /* a valid order this build cannot realise */
+  DG_ERR_SHAPE = 3,       /* sizes inconsistent with the descriptor's plan */
+  DG_ERR_ALIGN = 4,       /* a device pointer not aligned to its element size */
+  DG_ERR_NOMEM = 5,       /* split-K workspace allocation failed */
+  DG_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+} dg_status;
+
+/* Matrix instruction whose group the descriptor names (Sec. 3.2.1:
+ * instruction_k).  On gfx950 both bf16 instructions fold their products in
+ * chunks of 8 consecutive k; with fma = 1 they therefore give the same bits,
+ * and with fma = 0 the instruction's K (32 or 16) is the group rounded on its
+ * own before it meets the accumulator. */
+enum { DG_MMA_16X16X32_BF16 = 1, /* group of 32 */
+       DG_MMA_32X32X16_BF16 = 2  /* group of 16 */ };
+enum { DG_CARRY = 0, DG_SEQ = 1, DG_TREE = 2 };  /* combine rules */
+enum { DG_TAIL_LAST = 0, DG_TAIL_FIRST = 1 };     /* short K tile position (k_loop_step) */
+enum { DG_F32 = 0, DG_BF16 = 1 };                  /* storage/rounding types */
+enum { DG_EPI_NONE = 0, DG_EPI_BIAS = 1, DG_EPI_BIAS_SILU = 2 };
+enum { DG_ROUND_FINAL = 0, DG_ROUND_PRE_ACT = 1 };
+enum { DG_OP_SUM = 0, DG_OP_SUMSQ = 1 };
+
+#define DG_MAX_SPLIT 64
+
+/* The order fields, and nothing else (Sec. 3.2.2; Sec. 4: "a frozen record
+ * holding every one of those factors").  No speed knob appears here. */
+typedef struct {
+  uint32_t struct_size;   /* sizeof(dg_desc_params), for ABI versioning */
+  int32_t mma;            /* DG_MMA_*: the instruction group */
+  int32_t tile_k;         /* K tile: an accumulator may close every tile_k
+                             elements of a part; a multiple of the group */
+  int32_t split_k;        /* number of K parts S, 1..DG_MAX_SPLIT (Sec. 3.2.2 split-K) */
+  int32_t n_cuts;         /* 0: span rule; else S-1 explicit interior cuts */
+  const int64_t* k_cuts;  /* host array of n_cuts strictly increasing cut
+                             points in (0, K); copied at create time */
+  int32_t tile_combine;   /* DG_CARRY: one accumulator through the part;
+                             DG_SEQ / DG_TREE: each tile from +0, tiles
+                             chained / combined by the balanced tree */
+  int32_t split_combine;  /* DG_SEQ or DG_TREE over the S parts (second kernel) */
+  int32_t tail;           /* DG_TAIL_LAST / DG_TAIL_FIRST: where a part's short
+                             tile sits (k_loop_step) */
+  int32_t fma;            /* 1: the accumulator is the instruction's C operand
+                             (use_fast_accum off: one rounding per step);
+                             0: each group from +0, then a separate add */
+  int32_t partial_dtype;  /* DG_F32 / DG_BF16: type a finished part is written at */
+  int32_t merge_dtype;    /* DG_F32 / DG_BF16: type of the running merge sum
+                             (DG_BF16 requires partial_dtype DG_BF16) */
+  int32_t out_dtype;      /* DG_F32 / DG_BF16: C element type */
+  int32_t epilogue;       /* DG_EPI_*: z = y (+) bias_j, then SiLU */
+  int32_t epi_round;      /* DG_ROUND_FINAL: out = RN_out(silu(z));
+                             DG_ROUND_PRE_ACT: out = RN_bf16(silu(RN_bf16(z)))
+                             (requires DG_EPI_BIAS_SILU) */
+  int32_t leaf_w;         /* row reduction: elements folded in index order per
+                             leaf before the balanced tree over leaves (>= 1) */
+  int32_t reduce_op;      /* DG_OP_SUM or DG_OP_SUMSQ (fma: fused square-add) */
+} dg_desc_params;
+
+typedef struct dg_desc dg_desc; /* opaque, immutable */
+
+/* Validate `p` and build an immutable descriptor.  *out receives a handle
+ * owned by the caller (free with dg_desc_destroy).  Errors: DG_ERR_INVALID
+ * (NULL arguments, struct_size too small, a field out of range),
+ * DG_ERR_UNSUPPORTED (merge at bf16 over fp32 partials, pre-activation
+ * rounding without an activation). */
+dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out);
+
+/* Free a descriptor (NULL is ignored).  Calls already enqueued with it are
+ * unaffected: launches copy what they need. */
+void dg_desc_destroy(dg_desc* d);
+
+/* Canonical text of the order a descriptor fixes, NUL-terminated into buf
+ * (capacity n).  Descriptors with equal signatures give equal bits; fields
+ * that cannot change bits (the instruction shape when fma = 1) are
+ * normalised away.  DG_ERR_INVALID if buf is too small. */
+dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n);
+
+/* C = epilogue(A . B) in the descriptor's order.
+ *   A: device, M x K bf16 row-major;  B: device, K x N bf16 row-major;
+ *   bias: device, N bf16, required iff the epilogue uses it (else ignored);
+ *   C: device, M x N of out_dtype, row-major (written, never read).
+ * M = 0 or N = 0 is a no-op returning DG_OK.  K = 0 is allowed when
+ * split_k = 1 (every sum is +0).  DG_ERR_SHAPE if the plan for K leaves a
+ * part empty or an explicit cut lies outside (0, K); DG_ERR_ALIGN if A, B,
+ * bias or C is not aligned to its element size.  Split-K (S > 1) writes fp32
+ * or bf16 partials to a library-owned workspace cached per (device, stream)
+ * and merges them in a second kernel on the same stream (no atomics);
+ * DG_ERR_NOMEM if that workspace cannot grow. */
+dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias,
+                  void* C, int64_t M, int64_t N, int64_t K, void* stream);
+
+/* Speed knobs for dg_gemm_knobs.  Any value gives the same bits as
+ * dg_gemm; they exist so that this can be checked.  0 = the library's
+ * choice. */
+typedef struct {
+  int32_t kernel;  /* 0 auto, 1 generic chunk-ordered kernel, 2 tiled MFMA kernel */
+  int32_t tile_m;  /* tiled kernel rows per workgroup: 0, 16, 32, 64, 128, 256 */
+  int32_t tile_n;  /* tiled kernel columns per workgroup: 0, 64, 128, 256 */
+} dg_knobs;
+
+/* dg_gemm with explicit speed knobs (NULL = dg_gemm).  A knob combination
+ * the build lacks returns DG_ERR_UNSUPPORTED before any launch. */
+dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const void* bias,
+                        void* C, int64_t M, int64_t N, int64_t K,
+                        const dg_knobs* knobs, void* stream);
+
+/* out[r] = balanced-tree reduction of row r of X (Sec. 3.1, Sec. 5.1):
+ * leaves of leaf_w consecutive elements folded in index order (SUM: s = x0,
+ * s (+)= xi; SUMSQ: s = RN32(x0^2), then fma(xi, xi, s) if fma = 1 else
+ * s (+) RN32(xi^2)), then the leaves combined by the balanced tree (pairs of
+ * neighbours level by level, an odd last leaf carried up).
+ *   X: device, rows x cols fp32 row-major;  out: device, rows fp32.
+ * rows = 0 is a no-op; cols = 0 writes +0 to every out[r].  DG_ERR_ALIGN if
+ * X or out is not 4-byte aligned. */
+dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
+                    int64_t cols, void* stream);
+
+/* Static text for a status code. */
+const char* dg_strerror(dg_status s);
+
+/* Library version (major * 10000 + minor * 100 + patch). */
+int32_t dg_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DG_H */

@@ -1,0 +1,287 @@
+// dg_api.cpp -- host side of libdg: descriptor validation and plan, kernel
+// selection (speed only, never order), split-K workspace, error mapping.
+#include <hip/hip_runtime.h>
+
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <new>
+#include <utility>
+
+#include "dg_internal.h"
+
+namespace {
+
+bool in(int v, int lo, int hi) { return v >= lo && v <= hi; }
+
+// Cut points of the split for K (Sec. 3.2.2: contiguous parts, each started
+// at zero).  Explicit cuts must lie strictly inside (0, K) and increase.
+// Without them the span is ceil(K / S) rounded up to whole tiles and the last
+// part takes the rest; a part left empty is a shape error.
+dg_status plan_cuts(const dg_desc* d, int64_t K, int64_t* cuts) {
+  const int S = d->p.split_k;
+  cuts[0] = 0;
+  cuts[S] = K;
+  if (S == 1) return K >= 0 ? DG_OK : DG_ERR_SHAPE;
+  if (d->p.n_cuts) {
+    for (int s = 1; s < S; ++s) cuts[s] = d->cuts[s - 1];
+  } else {
+    int64_t span = (K + S - 1) / S;
+    span = (span + d->p.tile_k - 1) / d->p.tile_k * d->p.tile_k;
+    for (int s = 1; s < S; ++s) cuts[s] = (int64_t)s * span;
+  }
+  for (int s = 0; s < S; ++s)
+    if (!(cuts[s] < cuts[s + 1])) return DG_ERR_SHAPE;
+  return DG_OK;
+}
+
+void make_signature(dg_desc* d) {
+  const dg_desc_params& p = d->p;
+  // fma = 1 folds the same 8-k chunks whatever the instruction's K
+  char grp[32];
+  if (p.fma) std::snprintf(grp, sizeof grp, "chunk8");
+  else std::snprintf(grp, sizeof grp, "group%d", d->group);
+  int n = std::snprintf(d->sig, sizeof d->sig,
+                        "gfx950-bf16-mfma/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
+                        "out-%s/epi%d/%s/leaf%d/%s",
+                        grp, p.fma, p.tile_k,
+                        p.tile_combine == DG_CARRY ? "carry" : p.tile_combine == DG_SEQ ? "seq" : "tree",
+                        p.split_k, p.tail == DG_TAIL_FIRST ? "tail-first" : "tail-last",
+                        p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
+                        p.merge_dtype ? "bf16" : "f32", p.out_dtype ? "bf16" : "f32", p.epilogue,
+                        p.epi_round ? "pre-act" : "final", p.leaf_w, p.reduce_op ? "sumsq" : "sum");
+  if (p.n_cuts && n > 0 && n < (int)sizeof d->sig) {
+    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/cuts");
+    for (int i = 0; i < p.n_cuts && n > 0 && n < (int)sizeof d->sig; ++i)
+      n += std::snprintf(d->sig + n, sizeof d->sig - n, ":%lld", (long long)d->cuts[i]);
+  }
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+
+// ------------------------------------------------------------ workspace
+
+struct Workspace {
+  void* ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mutex;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
+
+// Workspace of at least `bytes` owned by (current device, stream).  Growth is
+// stream-ordered (hipMallocAsync / hipFreeAsync on that stream), so launches
+// already enqueued on the stream keep their buffer until they finish.
+dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return DG_ERR_HIP;
+  std::lock_guard<std::mutex> lock(g_ws_mutex);
+  Workspace& w = g_ws[{dev, st}];
+  if (w.bytes < bytes) {
+    size_t want = bytes + bytes / 4;
+    void* p = nullptr;
+    if (hipMallocAsync(&p, want, st) != hipSuccess) {
+      (void)hipGetLastError();
+      return DG_ERR_NOMEM;
+    }
+    if (w.ptr) (void)hipFreeAsync(w.ptr, st);
+    w.ptr = p;
+    w.bytes = want;
+  }
+  *out = w.ptr;
+  return DG_OK;
+}
+
+// Tile shape for the tiled kernel: a speed choice only.
+void pick_tiles(int64_t M, int64_t N, int S, int* tm, int* tn) {
+  (void)S;
+  if (M <= 16) { *tm = 16; *tn = (N >= 128 * 256) ? 128 : 64; return; }
+  if (M <= 32) { *tm = 32; *tn = 128; return; }
+  if (M <= 64) { *tm = 64; *tn = 128; return; }
+  *tm = 128;
+  *tn = 128;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t dg_version(void) { return 100; }
+
+const char* dg_strerror(dg_status s) {
+  switch (s) {
+    case DG_OK: return "ok";
+    case DG_ERR_INVALID: return "invalid argument";
+    case DG_ERR_UNSUPPORTED: return "unsupported descriptor or knob";
+    case DG_ERR_SHAPE: return "shape inconsistent with the descriptor's plan";
+    case DG_ERR_ALIGN: return "misaligned pointer";
+    case DG_ERR_NOMEM: return "workspace allocation failed";
+    case DG_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
+  if (!p || !out) return DG_ERR_INVALID;
+  *out = nullptr;
+  if (p->struct_size < sizeof(dg_desc_params)) return DG_ERR_INVALID;
+  int group;
+  if (p->mma == DG_MMA_16X16X32_BF16) group = 32;
+  else if (p->mma == DG_MMA_32X32X16_BF16) group = 16;
+  else return DG_ERR_INVALID;
+  if (p->tile_k < group || p->tile_k % group != 0 || p->tile_k > (1 << 30)) return DG_ERR_INVALID;
+  if (!in(p->split_k, 1, DG_MAX_SPLIT)) return DG_ERR_INVALID;
+  if (p->n_cuts != 0 && p->n_cuts != p->split_k - 1) return DG_ERR_INVALID;
+  if (p->n_cuts && !p->k_cuts) return DG_ERR_INVALID;
+  for (int i = 0; i < p->n_cuts; ++i)
+    if (p->k_cuts[i] <= 0 || (i && p->k_cuts[i] <= p->k_cuts[i - 1])) return DG_ERR_INVALID;
+  if (!in(p->tile_combine, DG_CARRY, DG_TREE)) return DG_ERR_INVALID;
+  if (p->split_combine != DG_SEQ && p->split_combine != DG_TREE) return DG_ERR_INVALID;
+  if (!in(p->tail, DG_TAIL_LAST, DG_TAIL_FIRST) || !in(p->fma, 0, 1)) return DG_ERR_INVALID;
+  if (!in(p->partial_dtype, DG_F32, DG_BF16) || !in(p->merge_dtype, DG_F32, DG_BF16) ||
+      !in(p->out_dtype, DG_F32, DG_BF16))
+    return DG_ERR_INVALID;
+  if (!in(p->epilogue, DG_EPI_NONE, DG_EPI_BIAS_SILU) || !in(p->epi_round, DG_ROUND_FINAL, DG_ROUND_PRE_ACT))
+    return DG_ERR_INVALID;
+  if (p->leaf_w < 1 || !in(p->reduce_op, DG_OP_SUM, DG_OP_SUMSQ)) return DG_ERR_INVALID;
+  if (p->merge_dtype == DG_BF16 && p->partial_dtype != DG_BF16) return DG_ERR_UNSUPPORTED;
+  if (p->epi_round == DG_ROUND_PRE_ACT && p->epilogue != DG_EPI_BIAS_SILU) return DG_ERR_UNSUPPORTED;
+  dg_desc* d = new (std::nothrow) dg_desc;
+  if (!d) return DG_ERR_NOMEM;
+  std::memset(d, 0, sizeof *d);
+  d->p = *p;
+  d->p.struct_size = sizeof(dg_desc_params);
+  for (int i = 0; i < p->n_cuts; ++i) d->cuts[i] = p->k_cuts[i];
+  d->p.k_cuts = p->n_cuts ? d->cuts : nullptr;
+  d->group = group;
+  make_signature(d);
+  *out = d;
+  return DG_OK;
+}
+
+void dg_desc_destroy(dg_desc* d) { delete d; }
+
+dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n) {
+  if (!d || !buf) return DG_ERR_INVALID;
+  size_t len = std::strlen(d->sig);
+  if (n < len + 1) return DG_ERR_INVALID;
+  std::memcpy(buf, d->sig, len + 1);
+  return DG_OK;
+}
+
+dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                        int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (M < 0 || N < 0 || K < 0) return DG_ERR_SHAPE;
+  const dg_desc_params& p = d->p;
+  const bool need_bias = p.epilogue != DG_EPI_NONE;
+  int kern = knobs ? knobs->kernel : 0;
+  int tm = knobs ? knobs->tile_m : 0, tn = knobs ? knobs->tile_n : 0;
+  if (!in(kern, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if ((tm || tn) && !(tm && tn && dg::tiled_supported(tm, tn))) return DG_ERR_UNSUPPORTED;
+  if (M == 0 || N == 0) return DG_OK;
+  if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
+  if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
+      (need_bias && !aligned(bias, 2)))
+    return DG_ERR_ALIGN;
+  if (K == 0 && p.split_k > 1) return DG_ERR_SHAPE;
+
+  dg::GemmArgs a;
+  std::memset(&a, 0, sizeof a);
+  if (K > 0) {
+    dg_status st = plan_cuts(d, K, a.cuts);
+    if (st != DG_OK) return st;
+  } else {
+    a.cuts[0] = a.cuts[1] = 0;
+  }
+  a.A = (const uint16_t*)A;
+  a.B = (const uint16_t*)B;
+  a.bias = (const uint16_t*)bias;
+  a.C = C;
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.S = p.split_k;
+  a.tile_k = p.tile_k;
+  a.group = d->group;
+  a.tile_combine = p.tile_combine;
+  a.tail_first = p.tail == DG_TAIL_FIRST;
+  a.fma = p.fma;
+  a.partial_bf16 = p.partial_dtype == DG_BF16;
+  a.out_bf16 = p.out_dtype == DG_BF16;
+  a.epilogue = p.epilogue;
+  a.pre_act = p.epi_round == DG_ROUND_PRE_ACT;
+  if ((M + 15) / 16 > 65535 || (N + 15) / 16 > (int64_t)1 << 31) return DG_ERR_SHAPE;
+
+  hipStream_t st = (hipStream_t)stream;
+  if (a.S > 1) {
+    void* ws = nullptr;
+    dg_status s = get_workspace(st, (size_t)a.S * (size_t)M * (size_t)N * sizeof(float), &ws);
+    if (s != DG_OK) return s;
+    a.ws = (float*)ws;
+  }
+
+  // The tiled kernel needs the chunk grid (8 k from every tile start) to sit
+  // on multiples of 8 from k = 0, a carried accumulator, and 16-byte rows.
+  bool tiled_ok = p.tile_combine == DG_CARRY && p.fma == 1 && K % 8 == 0 && N % 8 == 0 &&
+                  aligned(A, 16) && aligned(B, 16);
+  for (int s = 0; s < a.S && tiled_ok; ++s) {
+    if (a.cuts[s] % 8) tiled_ok = false;
+    int64_t len = a.cuts[s + 1] - a.cuts[s];
+    if (a.tail_first && (len % p.tile_k) % 8) tiled_ok = false;
+  }
+  if (kern == 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
+  hipError_t e;
+  if (kern != 1 && tiled_ok) {
+    if (!tm) pick_tiles(M, N, a.S, &tm, &tn);
+    if ((M + tm - 1) / tm > 65535) return DG_ERR_SHAPE;
+    e = dg::launch_gemm_tiled(a, tm, tn, st);
+  } else {
+    e = dg::launch_gemm_generic(a, st);
+  }
+  if (e != hipSuccess) return DG_ERR_HIP;
+  if (a.S > 1) {
+    dg::CombineArgs c;
+    c.ws = a.ws;
+    c.bias = a.bias;
+    c.C = C;
+    c.M = M;
+    c.N = N;
+    c.S = a.S;
+    c.split_combine = p.split_combine;
+    c.merge_bf16 = p.merge_dtype == DG_BF16;
+    c.out_bf16 = a.out_bf16;
+    c.epilogue = a.epilogue;
+    c.pre_act = a.pre_act;
+    if (dg::launch_splitk_combine(c, st) != hipSuccess) return DG_ERR_HIP;
+  }
+  return DG_OK;
+}
+
+dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                  int64_t M, int64_t N, int64_t K, void* stream) {
+  return dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
+}
+
+dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, int64_t cols,
+                    void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
+  if (rows == 0) return DG_OK;
+  if (!out || (cols > 0 && !X)) return DG_ERR_INVALID;
+  if (!aligned(out, 4) || (X && !aligned(X, 4))) return DG_ERR_ALIGN;
+  if ((rows + 3) / 4 > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  dg::RowsumArgs a;
+  a.X = X;
+  a.out = out;
+  a.rows = rows;
+  a.cols = cols;
+  a.leaf_w = d->p.leaf_w;
+  a.sumsq = d->p.reduce_op == DG_OP_SUMSQ;
+  a.fma = d->p.fma;
+  if (dg::launch_rowsum(a, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,55 @@
+// dg_internal.h -- library-internal types shared by the host API and kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/dg.h"
+
+struct dg_desc {
+  dg_desc_params p;            // validated copy; p.k_cuts points into cuts[]
+  int64_t cuts[DG_MAX_SPLIT];  // explicit interior cuts (n_cuts of them)
+  int group;                   // products per instruction group (32 or 16)
+  char sig[512];               // canonical order text
+};
+
+namespace dg {
+
+// Everything a GEMM launch needs, passed by value as the kernel argument.
+struct GemmArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  const uint16_t* bias;
+  void* C;
+  float* ws;                     // split-K partials [S][M][N] (fp32 storage)
+  int64_t M, N, K;
+  int64_t cuts[DG_MAX_SPLIT + 1];
+  int32_t S;
+  int32_t tile_k, group, tile_combine, tail_first, fma;
+  int32_t partial_bf16, out_bf16, epilogue, pre_act;
+};
+
+struct CombineArgs {
+  const float* ws;
+  const uint16_t* bias;
+  void* C;
+  int64_t M, N;
+  int32_t S;
+  int32_t split_combine, merge_bf16, out_bf16, epilogue, pre_act;
+};
+
+struct RowsumArgs {
+  const float* X;
+  float* out;
+  int64_t rows, cols;
+  int32_t leaf_w, sumsq, fma;
+};
+
+// launchers (return hipSuccess or the launch error)
+hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_tiled(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
+bool tiled_supported(int tile_m, int tile_n);
+hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
+hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
+
+}  // namespace dg

@@ -1,0 +1,125 @@
+// dg_rowsum.hip -- balanced-tree row reduction for gfx950 (paper Sec. 3.1,
+// Sec. 5.1).
+//
+// Order of row r: leaves of leaf_w consecutive elements, each folded in
+// index order; the leaves then meet in the balanced tree (neighbours pair
+// level by level, an odd last one carried up).  That tree equals the perfect
+// tree over the leaves padded on the right with -0 to a power of two (-0 is
+// the exact identity of binary32 addition), and the perfect tree over 64
+// lanes holding leaves 0..63 in lane order is the count-up xor butterfly
+// (offsets 1, 2, 4, .., 32).  So one wave reduces a row in passes of 64
+// leaves: every lane folds one leaf, the butterfly gives the pass root, and
+// the pass roots are combined by the same tree through a binary-counter
+// stack (lane k of the wave holds level k).
+//
+// Layout (free once the tree is pinned, Sec. 5.2): a pass's 64 leaves are
+// read from HBM with coalesced 16-byte loads and written to LDS with a
+// one-element skew per leaf (leaf stride leaf_w + 1), so that the lane-wise
+// sequential leaf reads are free of bank conflicts.  Leaves wider than 64
+// elements are folded straight from global memory.
+#include "dg_device.h"
+#include "dg_internal.h"
+
+namespace dg {
+
+constexpr int RS_WAVES = 4;            // rows per workgroup (one per wave)
+constexpr int RS_LDS = 64 * 65;        // floats per wave: 64 leaves x (64 + 1)
+
+__device__ __forceinline__ float leaf_step(float s, float x, int sumsq, int fma) {
+  if (!sumsq) return s + x;
+  if (fma) return __builtin_fmaf(x, x, s);
+  float q = x * x;
+  return s + q;
+}
+
+__device__ __forceinline__ float butterfly(float v) {
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
+  return v;
+}
+
+__global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
+  __shared__ float lds[RS_WAVES][RS_LDS];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * RS_WAVES + wave;
+  const bool live = row < a.rows;
+  const int lw = a.leaf_w;
+  const int64_t cols = a.cols;
+  const int64_t L = (cols + lw - 1) / lw;
+  const int64_t npass = (L + 63) / 64;
+  const float* x = a.X + (live ? row : 0) * cols;
+  const bool staged = lw <= 64;
+  const bool vec = ((((uintptr_t)a.X) & 15) == 0) && (cols % 4 == 0);
+  float* sl = lds[wave];
+
+  float stackv = 0.f;   // lane k: level k of the pass-root stack
+  uint32_t count = 0;
+  for (int64_t p = 0; p < npass; ++p) {
+    const int64_t base = p * 64 * lw;                   // first element of the pass
+    const int64_t nel = (cols - base < 64 * (int64_t)lw) ? cols - base : 64 * (int64_t)lw;
+    const int64_t leaf = p * 64 + lane;
+    float s = -0.0f;                                    // padding leaf
+    if (staged) {
+      if (live) {
+        if (vec) {
+          for (int64_t e = 4 * lane; e < nel; e += 256) {
+            const float4 v = *(const float4*)(x + base + e);
+            const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int64_t el = e + q;
+              if (el < nel) sl[(el / lw) * (lw + 1) + el % lw] = vv[q];
+            }
+          }
+        } else {
+          for (int64_t el = lane; el < nel; el += 64) sl[(el / lw) * (lw + 1) + el % lw] = x[base + el];
+        }
+      }
+      __syncthreads();
+      if (live && leaf < L) {
+        const int64_t n = (cols - leaf * lw < lw) ? cols - leaf * lw : lw;
+        const float* lp = sl + lane * (lw + 1);
+        float x0 = lp[0];
+        s = a.sumsq ? x0 * x0 : x0;
+        for (int64_t i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
+      }
+      __syncthreads();
+    } else if (live && leaf < L) {
+      const int64_t n = (cols - leaf * lw < lw) ? cols - leaf * lw : lw;
+      const float* lp = x + leaf * lw;
+      float x0 = lp[0];
+      s = a.sumsq ? x0 * x0 : x0;
+      for (int64_t i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
+    }
+    float v = butterfly(s);                             // root of this pass
+    // push onto the binary-counter stack (uniform across the wave)
+    uint32_t c = count;
+    int lvl = 0;
+    while (c & 1u) {
+      v = __shfl(stackv, lvl, 64) + v;
+      c >>= 1;
+      ++lvl;
+    }
+    if (lane == lvl) stackv = v;
+    ++count;
+  }
+  // flush low -> high
+  float r = 0.0f;
+  bool have = false;
+  for (int lvl = 0; lvl < 32; ++lvl) {
+    if ((count >> lvl) & 1u) {
+      const float sv = __shfl(stackv, lvl, 64);
+      r = have ? sv + r : sv;
+      have = true;
+    }
+  }
+  if (live && lane == 0) a.out[row] = have ? r : 0.0f;
+}
+
+hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t st) {
+  const int64_t blocks = (a.rows + RS_WAVES - 1) / RS_WAVES;
+  hipLaunchKernelGGL(rowsum_kernel, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace dg

@@ -1,0 +1,212 @@
+"""Thin ctypes binding of libdg.so (include/dg.h): argument marshalling only.
+
+Every step of the computation runs in the library's HIP kernels; this module
+checks shapes and dtypes, turns torch tensors into device pointers and the
+current HIP stream, and raises :class:`DgError` on a non-zero status.  It
+never computes a result itself: if libdg.so is missing it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdg.so")
+
+DG_OK, DG_ERR_INVALID, DG_ERR_UNSUPPORTED, DG_ERR_SHAPE, DG_ERR_ALIGN, DG_ERR_NOMEM, DG_ERR_HIP = range(7)
+MMA = {"16x16x32": 1, "32x32x16": 2}
+COMBINE = {"carry": 0, "seq": 1, "tree": 2}
+TAIL = {"last": 0, "first": 1}
+DTYPE = {"f32": 0, "bf16": 1}
+EPILOGUE = {"none": 0, "bias": 1, "bias_silu": 2}
+EPI_ROUND = {"final": 0, "pre_act": 1}
+REDUCE = {"sum": 0, "sumsq": 1}
+MAX_SPLIT = 64
+
+
+class DgError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, dg_strerror(status), status))
+
+
+class dg_desc_params(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32), ("mma", ctypes.c_int32), ("tile_k", ctypes.c_int32),
+                ("split_k", ctypes.c_int32), ("n_cuts", ctypes.c_int32),
+                ("k_cuts", ctypes.POINTER(ctypes.c_int64))] + [
+        (n, ctypes.c_int32) for n in ("tile_combine", "split_combine", "tail", "fma", "partial_dtype",
+                                      "merge_dtype", "out_dtype", "epilogue", "epi_round", "leaf_w",
+                                      "reduce_op")]
+
+
+class dg_knobs(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libdg.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libdg.so is not built (run __graft_entry__.build() or "
+                               "python -m paper_2609_11356_amd.build)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i64 = ctypes.c_void_p, ctypes.c_int64
+        L.dg_desc_create.argtypes = [ctypes.POINTER(dg_desc_params), ctypes.POINTER(vp)]
+        L.dg_desc_destroy.argtypes = [vp]
+        L.dg_desc_destroy.restype = None
+        L.dg_desc_signature.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
+        L.dg_gemm.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
+        L.dg_gemm_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
+        L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
+        L.dg_strerror.argtypes = [ctypes.c_int]
+        L.dg_strerror.restype = ctypes.c_char_p
+        L.dg_version.restype = ctypes.c_int32
+        for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum"):
+            getattr(L, f).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def dg_strerror(status: int) -> str:
+    return lib().dg_strerror(int(status)).decode()
+
+
+def dg_version() -> int:
+    return int(lib().dg_version())
+
+
+class Desc:
+    """An immutable descriptor (dg_desc_create / dg_desc_destroy).
+
+    Fields (strings as in the header's enums): mma ("16x16x32" | "32x32x16"),
+    tile_k, split_k, k_cuts (None or S-1 ints), tile_combine ("carry" |
+    "seq" | "tree"), split_combine ("seq" | "tree"), tail ("last" | "first"),
+    fma (0/1), partial / merge / out ("f32" | "bf16"), epilogue ("none" |
+    "bias" | "bias_silu"), epi_round ("final" | "pre_act"), leaf_w,
+    reduce ("sum" | "sumsq")."""
+
+    DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
+                    split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
+                    epilogue="none", epi_round="final", leaf_w=64, reduce="sum")
+
+    def __init__(self, **fields):
+        unknown = set(fields) - set(self.DEFAULTS) - {"model"}
+        if unknown:
+            raise ValueError("unknown descriptor fields: %s" % sorted(unknown))
+        if fields.get("model", "gfx950") != "gfx950":
+            raise ValueError("libdg realises the gfx950 MFMA arithmetic only")
+        f = dict(self.DEFAULTS)
+        f.update({k: v for k, v in fields.items() if k != "model"})
+        self.fields = f
+        p = dg_desc_params()
+        p.struct_size = ctypes.sizeof(dg_desc_params)
+        p.mma = MMA[f["mma"]]
+        p.tile_k = int(f["tile_k"])
+        p.split_k = int(f["split_k"])
+        cuts = f["k_cuts"]
+        self._cuts = None
+        if cuts is not None:
+            self._cuts = (ctypes.c_int64 * len(cuts))(*[int(c) for c in cuts])
+            p.n_cuts = len(cuts)
+            p.k_cuts = ctypes.cast(self._cuts, ctypes.POINTER(ctypes.c_int64))
+        p.tile_combine = COMBINE[f["tile_combine"]]
+        p.split_combine = COMBINE[f["split_combine"]]
+        p.tail = TAIL[f["tail"]]
+        p.fma = int(f["fma"])
+        p.partial_dtype = DTYPE[f["partial"]]
+        p.merge_dtype = DTYPE[f["merge"]]
+        p.out_dtype = DTYPE[f["out"]]
+        p.epilogue = EPILOGUE[f["epilogue"]]
+        p.epi_round = EPI_ROUND[f["epi_round"]]
+        p.leaf_w = int(f["leaf_w"])
+        p.reduce_op = REDUCE[f["reduce"]]
+        h = ctypes.c_void_p()
+        st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
+        if st != DG_OK:
+            raise DgError(st, "dg_desc_create")
+        self.handle = h
+
+    def signature(self) -> str:
+        buf = ctypes.create_string_buffer(1024)
+        st = lib().dg_desc_signature(self.handle, buf, len(buf))
+        if st != DG_OK:
+            raise DgError(st, "dg_desc_signature")
+        return buf.value.decode()
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h and _lib is not None:
+            _lib.dg_desc_destroy(h)
+            self.handle = None
+
+
+def dg_desc_create(**fields) -> Desc:
+    return Desc(**fields)
+
+
+def _stream(stream):
+    if stream is not None:
+        return int(stream)
+    import torch
+    return int(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return int(t.data_ptr())
+
+
+def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knobs=None):
+    """C = epilogue(A . B) in desc's order.  A (M,K) and B (K,N) bf16, bias (N,)
+    bf16 or None, C (M,N) of the descriptor's output type, all contiguous on
+    the GPU (or raw device addresses with M, N, K given)."""
+    import torch
+    if isinstance(A, torch.Tensor):
+        assert A.dtype == torch.bfloat16 and B.dtype == torch.bfloat16, "A and B must be bf16"
+        assert A.is_contiguous() and B.is_contiguous() and C.is_contiguous(), "row-major tensors"
+        assert A.is_cuda and B.is_cuda and C.is_cuda, "device tensors"
+        M, K = A.shape
+        K2, N = B.shape
+        assert K2 == K, "inner dimensions differ"
+        assert tuple(C.shape) == (M, N), "C shape"
+        want = torch.bfloat16 if desc.fields["out"] == "bf16" else torch.float32
+        assert C.dtype == want, "C dtype must match the descriptor's output type"
+        if bias is not None:
+            assert bias.dtype == torch.bfloat16 and bias.numel() == N and bias.is_contiguous()
+    kp = None
+    if knobs is not None:
+        kp = dg_knobs(int(knobs.get("kernel", 0)), int(knobs.get("tile_m", 0)), int(knobs.get("tile_n", 0)))
+        st = lib().dg_gemm_knobs(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K,
+                                 ctypes.byref(kp), _stream(stream))
+    else:
+        st = lib().dg_gemm(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_gemm")
+    return C
+
+
+def dg_rowsum(desc: Desc, X, out, rows=None, cols=None, stream=None):
+    """out[r] = balanced-tree reduction of row r of X (fp32, row-major)."""
+    import torch
+    if isinstance(X, torch.Tensor):
+        assert X.dtype == torch.float32 and out.dtype == torch.float32
+        assert X.is_contiguous() and out.is_contiguous() and X.is_cuda and out.is_cuda
+        rows, cols = X.shape
+        assert out.numel() == rows
+    st = lib().dg_rowsum(desc.handle, _ptr(X), _ptr(out), rows, cols, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_rowsum")
+    return out
+
+
+def exported_symbols():
+    """Names of the entry points include/dg.h declares."""
+    return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs",
+            "dg_rowsum", "dg_strerror", "dg_version"]

@@ -1,0 +1,98 @@
+"""The C ABI on the host: the library loads, exports every entry point
+include/dg.h declares, and validates descriptors and arguments before any
+launch (CPU only: no call here reaches a kernel)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def dg():
+    from paper_2609_11356_amd import dg as _dg
+    if not os.path.exists(_dg.LIB_PATH):
+        from paper_2609_11356_amd import build
+        build.build()
+    return _dg
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "dg.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dg_[a-z_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(dg):
+    lib = dg.lib()
+    names = declared_functions()
+    assert set(names) == set(dg.exported_symbols())
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strerror(dg):
+    assert dg.dg_version() == 100
+    for s in range(7):
+        assert dg.dg_strerror(s)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(tile_k=24), dict(tile_k=0), dict(mma="8x8"), dict(split_k=0), dict(split_k=65),
+    dict(split_k=3, k_cuts=[5]), dict(split_k=3, k_cuts=[10, 5]), dict(split_k=2, k_cuts=[0]),
+    dict(leaf_w=0), dict(fma=2)])
+def test_invalid_descriptors_rejected(dg, bad):
+    with pytest.raises((dg.DgError, KeyError)):
+        dg.Desc(**bad)
+
+
+def test_unsupported_combinations(dg):
+    with pytest.raises(dg.DgError) as e:
+        dg.Desc(merge="bf16", partial="f32")
+    assert e.value.status == dg.DG_ERR_UNSUPPORTED
+    with pytest.raises(dg.DgError) as e:
+        dg.Desc(epi_round="pre_act", epilogue="bias")
+    assert e.value.status == dg.DG_ERR_UNSUPPORTED
+
+
+def test_signature_canonical(dg):
+    a = dg.Desc(mma="16x16x32", tile_k=64).signature()
+    b = dg.Desc(mma="32x32x16", tile_k=64).signature()
+    assert a == b  # fma = 1: the same 8-k chunks
+    c = dg.Desc(mma="16x16x32", tile_k=64, fma=0).signature()
+    d = dg.Desc(mma="32x32x16", tile_k=64, fma=0).signature()
+    assert c != d and c != a
+    assert dg.Desc(split_k=3, k_cuts=[100, 200]).signature().endswith("cuts:100:200")
+
+
+def test_argument_errors_need_no_gpu(dg):
+    d = dg.Desc()
+    lib = dg.lib()
+    # M = 0 / N = 0: no-op, no launch
+    assert lib.dg_gemm(d.handle, 16, 16, None, 16, 0, 8, 8, None) == dg.DG_OK
+    assert lib.dg_gemm(d.handle, 16, 16, None, 16, 8, 0, 8, None) == dg.DG_OK
+    # negative sizes, NULL operands, misalignment, missing bias: rejected first
+    assert lib.dg_gemm(d.handle, 16, 16, None, 16, -1, 8, 8, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_gemm(d.handle, None, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_INVALID
+    assert lib.dg_gemm(d.handle, 17, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_gemm(d.handle, 16, 16, None, 18, 8, 8, 8, None) == dg.DG_ERR_ALIGN  # fp32 C
+    assert lib.dg_gemm(None, 16, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_INVALID
+    e = dg.Desc(epilogue="bias")
+    assert lib.dg_gemm(e.handle, 16, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_INVALID
+    # a plan that leaves a part empty
+    s = dg.Desc(split_k=8, tile_k=64)
+    assert lib.dg_gemm(s.handle, 16, 16, None, 16, 8, 8, 100, None) == dg.DG_ERR_SHAPE
+    c = dg.Desc(split_k=2, k_cuts=[300])
+    assert lib.dg_gemm(c.handle, 16, 16, None, 16, 8, 8, 256, None) == dg.DG_ERR_SHAPE
+    k0 = dg.Desc(split_k=2)
+    assert lib.dg_gemm(k0.handle, 16, 16, None, 16, 8, 8, 0, None) == dg.DG_ERR_SHAPE
+    # knobs the build lacks
+    kn = dg.dg_knobs(2, 48, 128)
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    # row reduction
+    assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK
+    assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_rowsum(d.handle, 16, None, 4, 5, None) == dg.DG_ERR_INVALID
+    assert lib.dg_rowsum(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
