@@ -135,9 +135,18 @@ dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bi
  * dg_gemm; they exist so that this can be checked.  0 = the library's
  * choice. */
 typedef struct {
-  int32_t kernel;  /* 0 auto, 1 generic chunk-ordered kernel, 2 tiled MFMA kernel */
-  int32_t tile_m;  /* tiled kernel rows per workgroup: 0, 16, 32, 64, 128, 256 */
-  int32_t tile_n;  /* tiled kernel columns per workgroup: 0, 64, 128, 256 */
+  int32_t kernel;  /* 0 auto, 1 generic chunk-ordered kernel, 2 tiled MFMA kernel,
+                      3 tiled MFMA kernel with transposing LDS reads and a
+                      two-slab prefetch, 4 few-row kernel (tile_m <= 64,
+                      tile_n 16/32/64) with a deep load ring */
+  int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
+  int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
+  int32_t order;   /* kernel 3 block order: 0 library's choice, 1 row-major
+                      (consecutive workgroups share an A panel), 2 groups of
+                      eight block rows walked column by column, 3 as 2 with
+                      each of the eight XCDs given a contiguous range */
+  int32_t occupancy; /* kernel 3: 0 library's choice, 1 or 2 workgroups per CU */
+  int32_t depth;   /* kernel 4: slabs of loads kept in flight, 0, 4, 8 or 12 */
 } dg_knobs;
 
 /* dg_gemm with explicit speed knobs (NULL = dg_gemm).  A knob combination

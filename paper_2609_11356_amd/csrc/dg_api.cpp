@@ -93,13 +93,24 @@ dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
 }
 
 // Tile shape for the tiled kernel: a speed choice only.
-void pick_tiles(int64_t M, int64_t N, int S, int* tm, int* tn) {
-  (void)S;
-  if (M <= 16) { *tm = 16; *tn = (N >= 128 * 256) ? 128 : 64; return; }
-  if (M <= 32) { *tm = 32; *tn = 128; return; }
-  if (M <= 64) { *tm = 64; *tn = 128; return; }
-  *tm = 128;
-  *tn = 128;
+// The library's choice of kernel and tiles for the chunk-grid kernels
+// (speed only; every choice gives the same bits).  Measured on MI355X at
+// N = K = 4096 and at the decode and MLP shapes: few rows stream B through
+// the deep-ring kernel (whole 128-byte B rows per workgroup once the grid
+// is wide enough), larger M uses the transposing-read kernel at two
+// workgroups per CU with XCD-contiguous grouped block order.
+struct AutoConfig {
+  int kern, tm, tn, order, occ, depth;
+};
+
+AutoConfig auto_config(int64_t M, int64_t N, int S) {
+  if (M <= 32) {
+    const int64_t wide = S * ((N + 63) / 64);
+    return {4, 16, wide >= 256 ? 64 : 32, 0, 0, 4};
+  }
+  if (M <= 128) return {4, 64, 32, 0, 0, 4};
+  if (M <= 1536) return {3, 64, 128, 3, 2, 0};
+  return {3, 128, 128, 3, 2, 0};
 }
 
 }  // namespace
@@ -177,8 +188,15 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   const bool need_bias = p.epilogue != DG_EPI_NONE;
   int kern = knobs ? knobs->kernel : 0;
   int tm = knobs ? knobs->tile_m : 0, tn = knobs ? knobs->tile_n : 0;
-  if (!in(kern, 0, 2)) return DG_ERR_UNSUPPORTED;
-  if ((tm || tn) && !(tm && tn && dg::tiled_supported(tm, tn))) return DG_ERR_UNSUPPORTED;
+  int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
+  int depth = knobs ? knobs->depth : 0;
+  if (!in(kern, 0, 4) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && (order || occ)) return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && depth) return DG_ERR_UNSUPPORTED;
+  if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth)) return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && (tm || tn) &&
+      !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
+    return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
   if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
   if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
@@ -224,17 +242,33 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   // The tiled kernel needs the chunk grid (8 k from every tile start) to sit
   // on multiples of 8 from k = 0, a carried accumulator, and 16-byte rows.
   bool tiled_ok = p.tile_combine == DG_CARRY && p.fma == 1 && K % 8 == 0 && N % 8 == 0 &&
-                  aligned(A, 16) && aligned(B, 16);
+                  aligned(A, 16) && aligned(B, 16) && aligned(C, 16) && (!need_bias || aligned(bias, 16));
   for (int s = 0; s < a.S && tiled_ok; ++s) {
     if (a.cuts[s] % 8) tiled_ok = false;
     int64_t len = a.cuts[s + 1] - a.cuts[s];
     if (a.tail_first && (len % p.tile_k) % 8) tiled_ok = false;
   }
-  if (kern == 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern >= 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
+  if (kern == 0 && tiled_ok) {
+    const AutoConfig c = auto_config(M, N, a.S);
+    kern = c.kern;
+    tm = c.tm;
+    tn = c.tn;
+    order = c.order;
+    occ = c.occ;
+    depth = c.depth;
+  }
   hipError_t e;
-  if (kern != 1 && tiled_ok) {
-    if (!tm) pick_tiles(M, N, a.S, &tm, &tn);
+  if (kern == 4) {
+    e = dg::launch_gemm_skinny(a, tm ? tm : 16, tn ? tn : 64, depth, st);
+  } else if (kern == 3) {
+    if (!tm) { tm = 128; tn = 128; }
+    if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = order ? order : 1;
+    e = dg::launch_gemm_v3(a, tm, tn, occ == 2 ? 2 : 1, st);
+  } else if (kern == 2) {
+    if (!tm) { tm = 128; tn = 128; }
     if ((M + tm - 1) / tm > 65535) return DG_ERR_SHAPE;
     e = dg::launch_gemm_tiled(a, tm, tn, st);
   } else {

@@ -26,6 +26,8 @@
 //   splitk_combine   S fp32 partials -> chain or balanced tree at the merge
 //                    precision -> epilogue (no atomics: the second kernel on
 //                    the same stream).
+#include <type_traits>
+
 #include "dg_device.h"
 #include "dg_internal.h"
 
@@ -34,6 +36,27 @@ namespace dg {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short shortx8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Sixteen zero bytes (device globals start zeroed).  A load that falls
+// outside the matrix or past the part end reads this instead, so that no
+// instruction touches a loaded value before it is stored -- a select on the
+// loaded value would make the load wait at once.
+__device__ u32x4 g_zero16[1];
+
+__device__ __forceinline__ const u32x4* chunk_or_zero(bool ok, const uint16_t* p) {
+  return ok ? reinterpret_cast<const u32x4*>(p) : &g_zero16[0];
+}
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
+// that register arrays indexed by I stay in registers.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
 
 __device__ __forceinline__ floatx4 mfma16(shortx8 a, shortx8 b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
@@ -57,6 +80,41 @@ __device__ __forceinline__ void finish(const GemmArgs& a, int s, int64_t i, int6
   }
   if (a.out_bf16) ((uint16_t*)a.C)[i * a.N + j] = f32_bf16(z);
   else ((float*)a.C)[i * a.N + j] = z;
+}
+
+// finish() for four consecutive columns j..j+3 (all < N: the tiled path
+// requires N % 8 == 0 and 16-byte aligned C), with one vector store.
+__device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4) {
+  float y[4] = {y4.x, y4.y, y4.z, y4.w};
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (a.partial_bf16) y[e] = round_bf16(y[e]);
+  if (a.S > 1) {
+    *(float4*)&a.ws[((int64_t)s * a.M + i) * a.N + j] = float4{y[0], y[1], y[2], y[3]};
+    return;
+  }
+  if (a.epilogue != DG_EPI_NONE) {
+    const uint2 bb = *(const uint2*)&a.bias[j];
+    const float b[4] = {bits_f32(bb.x << 16), bits_f32(bb.x & 0xffff0000u), bits_f32(bb.y << 16),
+                        bits_f32(bb.y & 0xffff0000u)};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) y[e] = y[e] + b[e];
+  }
+  if (a.epilogue == DG_EPI_BIAS_SILU) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      float z = y[e];
+      if (a.pre_act) z = round_bf16(z);
+      y[e] = silu_f32(z);
+    }
+  }
+  if (a.out_bf16) {
+    const uint32_t lo = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+    const uint32_t hi = (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16);
+    *(uint2*)&((uint16_t*)a.C)[i * a.N + j] = uint2{lo, hi};
+  } else {
+    *(float4*)&((float*)a.C)[i * a.N + j] = float4{y[0], y[1], y[2], y[3]};
+  }
 }
 
 // ------------------------------------------------------------- generic
@@ -138,27 +196,20 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
 constexpr int BK = 64;
 constexpr int LDS_PITCH = BK + 8;  // bf16 elements per LDS row (16 B pad)
 
-// A 16-byte vector of A row `row` at k..k+7, zero past M or past the part end.
-__device__ __forceinline__ uint4 load_a_vec(const GemmArgs& a, int64_t row, int64_t k, int64_t k1) {
-  uint4 r = {0u, 0u, 0u, 0u};
-  if (row >= a.M || k >= k1) return r;
-  const uint16_t* p = a.A + row * a.K + k;
-  if (k + 8 <= k1) return *(const uint4*)p;
-  uint16_t t[8];
-#pragma unroll
-  for (int e = 0; e < 8; ++e) t[e] = (k + e < k1) ? p[e] : (uint16_t)0;
-  return __builtin_bit_cast(uint4, t);
+// A 16-byte vector of A row `row` at k..k+7, zero past M or past the part
+// end (the tiled paths run only where part ends are multiples of 8, so a
+// vector is wholly inside or wholly outside).
+__device__ __forceinline__ u32x4 load_a_vec(const GemmArgs& a, int64_t row, int64_t k, int64_t k1) {
+  return *chunk_or_zero(row < a.M && k < k1, a.A + row * a.K + k);
 }
 
 // A 16-byte vector of B row k at columns n..n+7 (N % 8 == 0: all or none).
-__device__ __forceinline__ uint4 load_b_vec(const GemmArgs& a, int64_t k, int64_t n, int64_t k1) {
-  uint4 r = {0u, 0u, 0u, 0u};
-  if (k >= k1 || n >= a.N) return r;
-  return *(const uint4*)(a.B + k * a.N + n);
+__device__ __forceinline__ u32x4 load_b_vec(const GemmArgs& a, int64_t k, int64_t n, int64_t k1) {
+  return *chunk_or_zero(k < k1 && n < a.N, a.B + k * a.N + n);
 }
 
 template <int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
+__device__ __forceinline__ void tiled_body(const GemmArgs& a, int64_t i0, int64_t j0) {
   static_assert(WM * WN == 4, "four waves");
   constexpr int WTM = BM / WM, WTN = BN / WN;  // rows / cols per wave
   constexpr int TM = WTM / 16, TN = WTN / 16;  // 16x16 MFMA blocks per wave
@@ -167,12 +218,12 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
   constexpr int BB = (BK / 4) * (BN / 8);      // 4x8 blocks in a B slab
   constexpr int AV_T = (AV + 255) / 256, BB_T = (BB + 255) / 256;
 
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM][LDS_PITCH];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN][LDS_PITCH];
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM + BN) * LDS_PITCH];
+  uint16_t (*As)[BM][LDS_PITCH] = reinterpret_cast<uint16_t (*)[BM][LDS_PITCH]>(smem);
+  uint16_t (*Bs)[BN][LDS_PITCH] = reinterpret_cast<uint16_t (*)[BN][LDS_PITCH]>(smem + 2 * BM * LDS_PITCH);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
-  const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
@@ -183,8 +234,8 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  uint4 ra[AV_T];
-  uint4 rb[BB_T][4];
+  u32x4 ra[AV_T];
+  u32x4 rb[BB_T][4];
 
   auto gload = [&](int64_t ks) {
 #pragma unroll
@@ -207,7 +258,7 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
     for (int t = 0; t < AV_T; ++t) {
       const int v = tid + 256 * t;
       if (AV % 256 == 0 || v < AV)
-        *(uint4*)&As[buf][v / (BK / 8)][8 * (v % (BK / 8))] = ra[t];
+        *(u32x4*)&As[buf][v / (BK / 8)][8 * (v % (BK / 8))] = ra[t];
     }
 #pragma unroll
     for (int t = 0; t < BB_T; ++t) {
@@ -262,17 +313,347 @@ __global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
     __syncthreads();
   }
 
+  // Epilogue through LDS, one 16-row strip of every wave at a time: the
+  // accumulators are parked as fp32, then each lane finishes 4 consecutive
+  // columns (bias, SiLU, rounding) and stores them with one vector store.
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
+  static_assert(4 * 16 * WTN * 4 <= (int)sizeof(smem), "epilogue staging fits");
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+    __syncthreads();
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * WTN + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+    __syncthreads();
+#pragma unroll 1
+    for (int q = lane; q < 16 * WTN / 4; q += 64) {
+      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+      const int64_t i = i0 + wm * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
+      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * WTN + cc]);
+    }
+  }
+}
+
+// Blocks of up to 128x128: several workgroups per CU.
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256) void gemm_tiled(GemmArgs a) {
+  tiled_body<BM, BN, WM, WN>(a, (int64_t)blockIdx.y * BM, (int64_t)blockIdx.x * BN);
+}
+
+// 256-wide blocks: one workgroup per CU, one wave per SIMD, so that a wave
+// may hold its 128x128 (or 128x64) accumulator tile in the AGPR file next to
+// the staging registers.  Tiles are visited in groups of eight block rows,
+// column by column, so concurrently running workgroups share B panels.
+template <int BM, int BN, int WM, int WN>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_big(GemmArgs a) {
+  const int tiles_m = (int)((a.M + BM - 1) / BM);
+  const int w = blockIdx.x;
+  constexpr int GROUP = 8;
+  const int tiles_n = gridDim.x / tiles_m;
+  const int group = w / (GROUP * tiles_n);
+  const int first = group * GROUP;
+  const int rows = (tiles_m - first < GROUP) ? tiles_m - first : GROUP;
+  const int in_group = w - group * GROUP * tiles_n;
+  const int ty = first + in_group % rows, tx = in_group / rows;
+  tiled_body<BM, BN, WM, WN>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+}
+
+// ------------------------------------------------------------ tiled v3
+//
+// Same order as gemm_tiled (16x16x32 MFMA chain, 8-k chunks from k = 0), with
+// a deeper, branch-free pipeline:
+//   * A and B live in LDS in their global row-major layouts ([m][k], [k][n]),
+//     16-byte chunks XOR-swizzled per row so that fragment reads spread over
+//     the banks; B fragments come out of LDS already transposed through
+//     ds_read_b64_tr_b16 (a 16-lane group reading rows k0..k0+3, 4 columns
+//     per lane, hands lane j column j of those 4 rows);
+//   * every chunk is either wholly inside the part and the matrix or wholly
+//     outside (part ends and N are multiples of 8), so a load is a select
+//     between a 16-byte load and zero, with no branches;
+//   * global loads run two 64-k slabs ahead through a ring of two register
+//     sets, into an LDS double buffer, one barrier per slab.
+typedef short shortx4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) shortx4* lds_s4;
+
+template <int BM, int BN, int WM, int WN, int V3_BK>
+__device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j0) {
+  static_assert(WM * WN == 4, "four waves");
+  constexpr int WTM = BM / WM, WTN = BN / WN;
+  constexpr int TM = WTM / 16, TN = WTN / 16;
+  constexpr int ACH = BM * (V3_BK / 8);        // 16-byte chunks per A slab
+  constexpr int BCH = V3_BK * (BN / 8);        // 16-byte chunks per B slab
+  constexpr int ACH_T = ACH / 256, BCH_T = BCH / 256;
+  static_assert(ACH % 256 == 0 && BCH % 256 == 0, "whole chunks per thread");
+  constexpr int A_ELEMS = BM * V3_BK, B_ELEMS = V3_BK * BN;   // bf16 per stage
+  constexpr int BROW = BN / 8;                 // chunks per B row
+
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (A_ELEMS + B_ELEMS)];
+  uint16_t* As0 = smem;
+  uint16_t* Bs0 = smem + 2 * A_ELEMS;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + V3_BK - 1) / V3_BK);
+
+  // A chunk (row, c): LDS chunk row*CPR + (c ^ ((row / (16/CPR)) % CPR)), CPR = chunks per
+  // row -- sixteen consecutive rows at one logical chunk land on sixteen
+  // different 16-byte bank groups.
+  // B chunk (k, c): LDS chunk k*BROW + (c ^ ((k & 3) << 1)) -- the four rows a
+  // transpose read touches land on four different 32-byte bank groups.
+  constexpr int CPR = V3_BK / 8;
+  static_assert(CPR == 4 || CPR == 8, "BK 32 or 64");
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / (16 / CPR)) % CPR)); };
+  auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1)); };
+
+  u32x4 r0a[ACH_T], r0b[BCH_T], r1a[ACH_T], r1b[BCH_T];
+  auto gload = [&](int sl, u32x4* ra, u32x4* rb) {
+    const int64_t ks = k0 + (int64_t)sl * V3_BK;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t, row = q / (V3_BK / 8), c = q % (V3_BK / 8);
+      const int64_t gi = i0 + row, gk = ks + 8 * c;
+      ra[t] = *chunk_or_zero((gi < a.M) && (gk < k1), a.A + gi * a.K + gk);
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t, kr = q / BROW, c = q % BROW;
+      const int64_t gk = ks + kr, gn = j0 + 8 * c;
+      rb[t] = *chunk_or_zero((gk < k1) && (gn < a.N), a.B + gk * a.N + gn);
+    }
+  };
+  auto lstore = [&](int buf, const u32x4* ra, const u32x4* rb) {
+    uint16_t* As = As0 + buf * A_ELEMS;
+    uint16_t* Bs = Bs0 + buf * B_ELEMS;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t;
+      *(u32x4*)&As[8 * ldsA(q / (V3_BK / 8), q % (V3_BK / 8))] = ra[t];
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t;
+      *(u32x4*)&Bs[8 * ldsB(q / BROW, q % BROW)] = rb[t];
+    }
+  };
+
+  floatx4 acc[TM][TN];
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-      const int64_t j = j0 + wn * WTN + 16 * ni + (lane & 15);
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf) {
+    const uint16_t* As = As0 + buf * A_ELEMS;
+    const uint16_t* Bs = Bs0 + buf * B_ELEMS;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t i = i0 + wm * WTM + 16 * mi + 4 * (lane >> 4) + r;
-        if (i < a.M && j < a.N) finish(a, s, i, j, acc[mi][ni][r]);
+    for (int kk = 0; kk < V3_BK; kk += 32) {
+      shortx8 af[TM], bfr[TN];
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi) {
+        const int row = wm * WTM + 16 * mi + (lane & 15);
+        af[mi] = *(const shortx8*)&As[8 * ldsA(row, kk / 8 + (lane >> 4))];
+      }
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) {
+        const int i = lane & 15, g = lane >> 4;
+        const int n = wn * WTN + 16 * ni + 4 * (i & 3);
+        const int kr0 = kk + 8 * g + (i >> 2), kr1 = kr0 + 4;
+        const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+        const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+        bfr[ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bfr[ni], acc[mi][ni]);
+    }
+  };
+
+  // prologue: slabs 0 and 1 in flight, slab 0 in LDS.  Loads and LDS
+  // stores are unconditional (past the part end they read the zero chunk) so
+  // that the store of a slab waits only for that slab's loads.
+  gload(0, r0a, r0b);
+  gload(1, r1a, r1b);
+  lstore(0, r0a, r0b);
+  __syncthreads();
+  for (int sl = 0; sl < nslab; sl += 2) {
+    // even slab sl in buffer 0, its successor's registers in set 1
+    gload(sl + 2, r0a, r0b);
+    compute(0);
+    lstore(1, r1a, r1b);
+    __syncthreads();
+    gload(sl + 3, r1a, r1b);
+    if (sl + 1 < nslab) compute(1);
+    lstore(0, r0a, r0b);
+    __syncthreads();
+  }
+
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
+  static_assert(4 * 16 * WTN * 4 <= (int)sizeof(smem), "epilogue staging fits");
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+    __syncthreads();
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * WTN + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+    __syncthreads();
+#pragma unroll 1
+    for (int q = lane; q < 16 * WTN / 4; q += 64) {
+      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+      const int64_t i = i0 + wm * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
+      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * WTN + cc]);
+    }
+  }
+}
+
+// Block order (speed only).  order 1: row-major, consecutive workgroups share
+// an A panel.  order 2: groups of eight block rows walked column by column.
+// order 3: as 2, after giving each XCD (workgroup w runs on XCD w % 8) a
+// contiguous range of blocks, so that one XCD's L2 sees neighbouring panels.
+__device__ __forceinline__ void grouped_tile(int w, int tiles_m, int tiles_n, int order, int* ty, int* tx) {
+  if (order <= 1) {
+    *ty = w / tiles_n;
+    *tx = w % tiles_n;
+    return;
+  }
+  const int nwg = tiles_m * tiles_n;
+  if (order == 3 && nwg % 8 == 0) w = (w % 8) * (nwg / 8) + w / 8;
+  constexpr int GROUP = 8;
+  const int group = w / (GROUP * tiles_n);
+  const int first = group * GROUP;
+  const int rows = (tiles_m - first < GROUP) ? tiles_m - first : GROUP;
+  const int in_group = w - group * GROUP * tiles_n;
+  *ty = first + in_group % rows;
+  *tx = in_group / rows;
+}
+
+template <int BM, int BN, int WM, int WN, int BK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_v3(GemmArgs a) {
+  const int tiles_m = (int)((a.M + BM - 1) / BM);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  v3_body<BM, BN, WM, WN, BK>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+}
+
+template <int BM, int BN, int WM, int WN, int BK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_v3x2(GemmArgs a) {
+  const int tiles_m = (int)((a.M + BM - 1) / BM);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  v3_body<BM, BN, WM, WN, BK>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+}
+
+// ---------------------------------------------------------- skinny (M <= 64)
+//
+// Few rows: the GEMM streams B from HBM and the MFMA work per slab is small,
+// so the time goes to memory latency.  Each workgroup owns BN columns (one
+// 16-column MFMA tile per computing wave, all four waves loading) and keeps
+// D 64-k slabs of loads in flight through a ring of D register sets, staged
+// through an LDS double buffer in the layouts of the v3 kernel (A [m][k], B
+// [k][n], transposing reads for B).  Same chunk order as every other path.
+template <int TMS, int BN, int D>
+__global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
+  constexpr int BK = 64, CPR = BK / 8, BM = 16 * TMS, NWC = BN / 16;
+  constexpr int ACH = BM * CPR, BCH = BK * (BN / 8), BROW = BN / 8;
+  constexpr int ACH_T = (ACH + 255) / 256, BCH_T = (BCH + 255) / 256;
+  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
+  static_assert(BN % 64 == 0 || BN == 16 || BN == 32, "B rows of whole swizzle blocks");
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (A_ELEMS + B_ELEMS)];
+  uint16_t* As0 = smem;
+  uint16_t* Bs0 = smem + 2 * A_ELEMS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); };
+  // rows of fewer than 8 chunks (BN < 64) are swizzled within the row
+  auto ldsB = [](int k, int c) { return k * BROW + ((c ^ ((k & 3) << 1)) & (BROW - 1)); };
+
+  u32x4 ra[D][ACH_T], rb[D][BCH_T];
+  auto gload = [&](int sl, u32x4* xa, u32x4* xb) {
+    const int64_t ks = k0 + (int64_t)sl * BK;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t, row = q / CPR, c = q % CPR;
+      const int64_t gi = i0 + row, gk = ks + 8 * c;
+      xa[t] = *chunk_or_zero((q < ACH) && (gi < a.M) && (gk < k1), a.A + gi * a.K + gk);
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t, kr = q / BROW, c = q % BROW;
+      const int64_t gk = ks + kr, gn = j0 + 8 * c;
+      xb[t] = *chunk_or_zero((q < BCH) && (gk < k1) && (gn < a.N), a.B + gk * a.N + gn);
+    }
+  };
+  auto lstore = [&](int buf, const u32x4* xa, const u32x4* xb) {
+    uint16_t* As = As0 + buf * A_ELEMS;
+    uint16_t* Bs = Bs0 + buf * B_ELEMS;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t;
+      if (q < ACH) *(u32x4*)&As[8 * ldsA(q / CPR, q % CPR)] = xa[t];
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t;
+      if (q < BCH) *(u32x4*)&Bs[8 * ldsB(q / BROW, q % BROW)] = xb[t];
+    }
+  };
+  floatx4 acc[TMS];
+#pragma unroll
+  for (int mi = 0; mi < TMS; ++mi) acc[mi] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](int buf) {
+    if (wave >= NWC) return;
+    const uint16_t* As = As0 + buf * A_ELEMS;
+    const uint16_t* Bs = Bs0 + buf * B_ELEMS;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      const int i = lane & 15, g = lane >> 4;
+      const int n = 16 * wave + 4 * (i & 3);
+      const int kr0 = kk + 8 * g + (i >> 2), kr1 = kr0 + 4;
+      const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+      const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+      const shortx8 bfr = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+      for (int mi = 0; mi < TMS; ++mi) {
+        const shortx8 af = *(const shortx8*)&As[8 * ldsA(16 * mi + (lane & 15), kk / 8 + (lane >> 4))];
+        acc[mi] = mfma16(af, bfr, acc[mi]);
       }
     }
+  };
+
+  // Loads and LDS stores are issued unconditionally (a slab past the part
+  // end reads the zero chunk), so that every path holds the same number of
+  // loads in flight and the LDS store of slab s+1 waits only for its own
+  // loads, not for the D-1 slabs behind it.  Only the MFMA work is skipped.
+  static_for<0, D>([&](auto j) { gload(j, ra[j], rb[j]); });
+  lstore(0, ra[0], rb[0]);
+  __syncthreads();
+  for (int base = 0; base < nslab; base += D) {
+    static_for<0, D>([&](auto u) {
+      const int sl = base + u;
+      if (sl < nslab) compute(sl & 1);
+      gload(sl + D, ra[u], rb[u]);
+      lstore((sl + 1) & 1, ra[(u + 1) % D], rb[(u + 1) % D]);
+      __syncthreads();
+    });
+  }
+  if (wave < NWC) {
+#pragma unroll
+    for (int mi = 0; mi < TMS; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t i = i0 + 16 * mi + 4 * (lane >> 4) + r, j = j0 + 16 * wave + (lane & 15);
+        if (i < a.M && j < a.N) finish(a, s, i, j, acc[mi][r]);
+      }
+  }
 }
 
 // ------------------------------------------------------- split-K merge
@@ -346,9 +727,79 @@ static hipError_t launch_tiled_t(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int BM, int BN, int WM, int WN>
+static hipError_t launch_big_t(const GemmArgs& a, hipStream_t st) {
+  const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
+  hipLaunchKernelGGL((gemm_big<BM, BN, WM, WN>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int BM, int BN, int WM, int WN, int BK, bool TWO>
+static hipError_t launch_v3_t(const GemmArgs& a, hipStream_t st) {
+  const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
+  dim3 grid((unsigned)(tm * tn), 1, (unsigned)a.S);
+  if constexpr (TWO) hipLaunchKernelGGL((gemm_v3x2<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gemm_v3<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+template <int TMS, int BN, int D>
+static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t st) {
+  dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
+  hipLaunchKernelGGL((gemm_skinny<TMS, BN, D>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+bool skinny_supported(int tm, int tn, int depth) {
+  return (tm == 16 || tm == 32 || tm == 64) && (tn == 16 || tn == 32 || tn == 64) &&
+         (depth == 0 || depth == 4 || depth == 8 || depth == 12);
+}
+
+hipError_t launch_gemm_skinny(const GemmArgs& a, int tm, int tn, int depth, hipStream_t st) {
+#define DG_SKINNY(TM_, TN_, D_) \
+  if (tm == TM_ && tn == TN_ && depth == D_) return launch_skinny_t<TM_ / 16, TN_, D_>(a, st);
+  if (depth == 0) depth = 8;
+  DG_SKINNY(16, 16, 4) DG_SKINNY(16, 16, 8) DG_SKINNY(16, 16, 12)
+  DG_SKINNY(16, 32, 4) DG_SKINNY(16, 32, 8) DG_SKINNY(16, 32, 12)
+  DG_SKINNY(16, 64, 4) DG_SKINNY(16, 64, 8) DG_SKINNY(16, 64, 12)
+  DG_SKINNY(32, 16, 4) DG_SKINNY(32, 16, 8) DG_SKINNY(32, 16, 12)
+  DG_SKINNY(32, 32, 4) DG_SKINNY(32, 32, 8) DG_SKINNY(32, 32, 12)
+  DG_SKINNY(32, 64, 4) DG_SKINNY(32, 64, 8) DG_SKINNY(32, 64, 12)
+  DG_SKINNY(64, 16, 4) DG_SKINNY(64, 16, 8) DG_SKINNY(64, 16, 12)
+  DG_SKINNY(64, 32, 4) DG_SKINNY(64, 32, 8) DG_SKINNY(64, 32, 12)
+  DG_SKINNY(64, 64, 4) DG_SKINNY(64, 64, 8) DG_SKINNY(64, 64, 12)
+#undef DG_SKINNY
+  return hipErrorInvalidValue;
+}
+
+bool v3_supported(int tm, int tn, int occ) {
+  if (occ == 2) return (tm == 128 && tn == 128) || (tm == 64 && tn == 128) || (tm == 32 && tn == 128);
+  return (tm == 256 && tn == 256) || (tm == 256 && tn == 128) || (tm == 128 && tn == 256) ||
+         (tm == 128 && tn == 128) || (tm == 64 && tn == 128) || (tm == 32 && tn == 256) ||
+         (tm == 32 && tn == 128);
+}
+
+hipError_t launch_gemm_v3(const GemmArgs& a, int tm, int tn, int occ, hipStream_t st) {
+  if (occ == 2) {
+    if (tm == 128 && tn == 128) return launch_v3_t<128, 128, 2, 2, 32, true>(a, st);
+    if (tm == 64 && tn == 128) return launch_v3_t<64, 128, 2, 2, 64, true>(a, st);
+    if (tm == 32 && tn == 128) return launch_v3_t<32, 128, 1, 4, 64, true>(a, st);
+    return hipErrorInvalidValue;
+  }
+  if (tm == 256 && tn == 256) return launch_v3_t<256, 256, 2, 2, 32, false>(a, st);
+  if (tm == 256 && tn == 128) return launch_v3_t<256, 128, 2, 2, 32, false>(a, st);
+  if (tm == 128 && tn == 256) return launch_v3_t<128, 256, 2, 2, 32, false>(a, st);
+  if (tm == 128 && tn == 128) return launch_v3_t<128, 128, 2, 2, 64, false>(a, st);
+  if (tm == 64 && tn == 128) return launch_v3_t<64, 128, 2, 2, 64, false>(a, st);
+  if (tm == 32 && tn == 256) return launch_v3_t<32, 256, 1, 4, 64, false>(a, st);
+  if (tm == 32 && tn == 128) return launch_v3_t<32, 128, 1, 4, 64, false>(a, st);
+  return hipErrorInvalidValue;
+}
+
 bool tiled_supported(int tm, int tn) {
   return (tm == 16 && (tn == 64 || tn == 128)) || (tm == 32 && tn == 128) ||
-         (tm == 64 && tn == 128) || (tm == 128 && tn == 128);
+         (tm == 64 && tn == 128) || (tm == 128 && tn == 128) || (tm == 256 && tn == 256) ||
+         (tm == 256 && tn == 128) || (tm == 128 && tn == 256);
 }
 
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) {
@@ -357,6 +808,9 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) 
   if (tm == 32 && tn == 128) return launch_tiled_t<32, 128, 1, 4>(a, st);
   if (tm == 64 && tn == 128) return launch_tiled_t<64, 128, 2, 2>(a, st);
   if (tm == 128 && tn == 128) return launch_tiled_t<128, 128, 2, 2>(a, st);
+  if (tm == 256 && tn == 256) return launch_big_t<256, 256, 2, 2>(a, st);
+  if (tm == 256 && tn == 128) return launch_big_t<256, 128, 2, 2>(a, st);
+  if (tm == 128 && tn == 256) return launch_big_t<128, 256, 2, 2>(a, st);
   return hipErrorInvalidValue;
 }
 

@@ -27,6 +27,7 @@ struct GemmArgs {
   int32_t S;
   int32_t tile_k, group, tile_combine, tail_first, fma;
   int32_t partial_bf16, out_bf16, epilogue, pre_act;
+  int32_t order;                 // block order of the v3 kernels (speed only)
 };
 
 struct CombineArgs {
@@ -49,6 +50,10 @@ struct RowsumArgs {
 hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool tiled_supported(int tile_m, int tile_n);
+hipError_t launch_gemm_v3(const GemmArgs& a, int tile_m, int tile_n, int occupancy, hipStream_t s);
+bool v3_supported(int tile_m, int tile_n, int occupancy);
+hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, hipStream_t s);
+bool skinny_supported(int tile_m, int tile_n, int depth);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
 

@@ -38,6 +38,11 @@ __device__ __forceinline__ float butterfly(float v) {
   return v;
 }
 
+// Staged path (leaf_w <= 64, 16-byte aligned rows): a pass's 64 leaves are
+// fetched with all of the pass's 16-byte loads in flight at once (a lane
+// holds leaf_w floats of the pass in registers), the next pass's loads are
+// issued before the current pass is folded, and LDS is only the transpose.
+template <bool VEC>
 __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
   __shared__ float lds[RS_WAVES][RS_LDS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -49,39 +54,53 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
   const int64_t npass = (L + 63) / 64;
   const float* x = a.X + (live ? row : 0) * cols;
   const bool staged = lw <= 64;
-  const bool vec = ((((uintptr_t)a.X) & 15) == 0) && (cols % 4 == 0);
   float* sl = lds[wave];
+
+  float4 cur[16];
+  // pass p holds elements [p*64*lw, p*64*lw + nel); lane takes elements
+  // 4*lane + 256*i (i < 16) of it
+  auto fetch = [&](int64_t p, float4* r) {
+    const int64_t base = p * 64 * lw;
+    const int nel = (int)((cols - base < 64 * (int64_t)lw) ? cols - base : 64 * (int64_t)lw);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int e = 4 * lane + 256 * i;
+      r[i] = (live && e < nel) ? *(const float4*)(x + base + e) : float4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  if (VEC && staged && npass > 0) fetch(0, cur);
 
   float stackv = 0.f;   // lane k: level k of the pass-root stack
   uint32_t count = 0;
   for (int64_t p = 0; p < npass; ++p) {
     const int64_t base = p * 64 * lw;                   // first element of the pass
-    const int64_t nel = (cols - base < 64 * (int64_t)lw) ? cols - base : 64 * (int64_t)lw;
+    const int nel = (int)((cols - base < 64 * (int64_t)lw) ? cols - base : 64 * (int64_t)lw);
     const int64_t leaf = p * 64 + lane;
     float s = -0.0f;                                    // padding leaf
     if (staged) {
-      if (live) {
-        if (vec) {
-          for (int64_t e = 4 * lane; e < nel; e += 256) {
-            const float4 v = *(const float4*)(x + base + e);
-            const float vv[4] = {v.x, v.y, v.z, v.w};
+      if (VEC) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const int64_t el = e + q;
-              if (el < nel) sl[(el / lw) * (lw + 1) + el % lw] = vv[q];
-            }
+        for (int i = 0; i < 16; ++i) {
+          const int e = 4 * lane + 256 * i;
+          if (e < nel) {
+            const float vv[4] = {cur[i].x, cur[i].y, cur[i].z, cur[i].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) sl[((e + q) / lw) * (lw + 1) + (e + q) % lw] = vv[q];
           }
-        } else {
-          for (int64_t el = lane; el < nel; el += 64) sl[(el / lw) * (lw + 1) + el % lw] = x[base + el];
         }
+      } else if (live) {
+        for (int el = lane; el < nel; el += 64) sl[(el / lw) * (lw + 1) + el % lw] = x[base + el];
       }
       __syncthreads();
+      // cur has been written to LDS: reuse it for the next pass's loads,
+      // which stay in flight while this pass is folded
+      if (VEC && p + 1 < npass) fetch(p + 1, cur);
       if (live && leaf < L) {
-        const int64_t n = (cols - leaf * lw < lw) ? cols - leaf * lw : lw;
+        const int n = (int)((cols - leaf * lw < lw) ? cols - leaf * lw : lw);
         const float* lp = sl + lane * (lw + 1);
         float x0 = lp[0];
         s = a.sumsq ? x0 * x0 : x0;
-        for (int64_t i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
+        for (int i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
       }
       __syncthreads();
     } else if (live && leaf < L) {
@@ -118,7 +137,11 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
 
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t st) {
   const int64_t blocks = (a.rows + RS_WAVES - 1) / RS_WAVES;
-  hipLaunchKernelGGL(rowsum_kernel, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
+  const bool vec = ((((uintptr_t)a.X) & 15) == 0) && (a.cols % 4 == 0);
+  if (vec)
+    hipLaunchKernelGGL(rowsum_kernel<true>, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
+  else
+    hipLaunchKernelGGL(rowsum_kernel<false>, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
   return hipGetLastError();
 }
 

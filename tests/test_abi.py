@@ -89,7 +89,9 @@ def test_argument_errors_need_no_gpu(dg):
     k0 = dg.Desc(split_k=2)
     assert lib.dg_gemm(k0.handle, 16, 16, None, 16, 8, 8, 0, None) == dg.DG_ERR_SHAPE
     # knobs the build lacks
-    kn = dg.dg_knobs(2, 48, 128)
+    kn = dg.dg_knobs(2, 48, 128, 0, 0, 0)
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(4, 16, 64, 0, 0, 5)
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     # row reduction
     assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK

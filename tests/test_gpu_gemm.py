@@ -131,14 +131,23 @@ def test_k_zero_gives_epilogue_of_zero(dg):
 
 KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, tile_m=16, tile_n=128),
          dict(kernel=2, tile_m=32, tile_n=128), dict(kernel=2, tile_m=64, tile_n=128),
-         dict(kernel=2, tile_m=128, tile_n=128), None]
+         dict(kernel=2, tile_m=128, tile_n=128), dict(kernel=2, tile_m=256, tile_n=256),
+         dict(kernel=2, tile_m=256, tile_n=128), dict(kernel=2, tile_m=128, tile_n=256),
+         dict(kernel=3, tile_m=256, tile_n=256), dict(kernel=3, tile_m=256, tile_n=128),
+         dict(kernel=3, tile_m=128, tile_n=256), dict(kernel=3, tile_m=128, tile_n=128),
+         dict(kernel=3, tile_m=64, tile_n=128), dict(kernel=3, tile_m=32, tile_n=256),
+         dict(kernel=3, tile_m=32, tile_n=128), dict(kernel=3, tile_m=128, tile_n=128, occupancy=2, order=2),
+         dict(kernel=3, tile_m=64, tile_n=128, occupancy=2, order=3), dict(kernel=3, tile_m=256, tile_n=128, order=3),
+         dict(kernel=4, tile_m=16, tile_n=16, depth=4), dict(kernel=4, tile_m=32, tile_n=32, depth=8),
+         dict(kernel=4, tile_m=64, tile_n=64, depth=12), dict(kernel=4, tile_m=16, tile_n=64, depth=12),
+         None]
 
 
 @pytest.mark.parametrize("desc", [dict(tile_k=64, out="bf16"), dict(tile_k=64, split_k=4, split_combine="tree"),
                                   dict(tile_k=64, out="bf16", epilogue="bias_silu")])
 def test_speed_knobs_do_not_change_bits(dg, desc):
     """Kernel choice and block shape are speed knobs: identical bytes."""
-    M, N, K = 100, 256, 1024
+    M, N, K = 300, 520, 1032
     A = inputs.spread_bf16(7, (M, K))
     B = inputs.spread_bf16(8, (K, N))
     bias = inputs.normal_bf16(9, (N,), 0.5)
