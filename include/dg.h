@@ -138,10 +138,12 @@ typedef struct {
   int32_t kernel;  /* 0 auto, 1 generic chunk-ordered kernel, 2 tiled MFMA kernel,
                       3 tiled MFMA kernel with transposing LDS reads and a
                       two-slab prefetch, 4 few-row kernel (tile_m <= 64,
-                      tile_n 16/32/64) with a deep load ring */
+                      tile_n 16/32/64) with a deep load ring, 5 eight-wave
+                      kernel for large M and N (256x128, 128x256; 256x256 runs
+                      two groups of four waves one phase apart) */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
-  int32_t order;   /* kernel 3 block order: 0 library's choice, 1 row-major
+  int32_t order;   /* kernels 3 and 5: block order: 0 library's choice, 1 row-major
                       (consecutive workgroups share an A panel), 2 groups of
                       eight block rows walked column by column, 3 as 2 with
                       each of the eight XCDs given a contiguous range */

@@ -97,8 +97,9 @@ dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
 // (speed only; every choice gives the same bits).  Measured on MI355X at
 // N = K = 4096 and at the decode and MLP shapes: few rows stream B through
 // the deep-ring kernel (whole 128-byte B rows per workgroup once the grid
-// is wide enough), larger M uses the transposing-read kernel at two
-// workgroups per CU with XCD-contiguous grouped block order.
+// is wide enough); when 256 x 256 blocks fill most of the chip the
+// ping-pong kernel takes them, otherwise the transposing-read kernel runs at
+// two workgroups per CU with XCD-contiguous grouped block order.
 struct AutoConfig {
   int kern, tm, tn, order, occ, depth;
 };
@@ -109,6 +110,8 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
     return {4, 16, wide >= 256 ? 64 : 32, 0, 0, 4};
   }
   if (M <= 128) return {4, 64, 32, 0, 0, 4};
+  const int64_t big_tiles = S * ((M + 255) / 256) * ((N + 255) / 256);
+  if (big_tiles >= 192) return {5, 256, 256, 1, 0, 0};
   if (M <= 1536) return {3, 64, 128, 3, 2, 0};
   return {3, 128, 128, 3, 2, 0};
 }
@@ -190,11 +193,13 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int tm = knobs ? knobs->tile_m : 0, tn = knobs ? knobs->tile_n : 0;
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0;
-  if (!in(kern, 0, 4) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
-  if (kern != 3 && (order || occ)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 5) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && kern != 5 && order) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
+  if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && depth) return DG_ERR_UNSUPPORTED;
   if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && (tm || tn) &&
+  if (kern != 4 && kern != 5 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
@@ -267,6 +272,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = order ? order : 1;
     e = dg::launch_gemm_v3(a, tm, tn, occ == 2 ? 2 : 1, st);
+  } else if (kern == 5) {
+    if (!tm) { tm = 256; tn = 128; }
+    if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = order ? order : 3;
+    e = dg::launch_gemm_wide(a, tm, tn, st);
   } else if (kern == 2) {
     if (!tm) { tm = 128; tn = 128; }
     if ((M + tm - 1) / tm > 65535) return DG_ERR_SHAPE;
