@@ -104,6 +104,16 @@ struct AutoConfig {
   int kern, tm, tn, order, occ, depth;
 };
 
+// The 256 x 256 ping-pong kernel addresses its operands with 31-bit byte
+// offsets from the block's first A row and the part's first B row.
+bool pp_fits(const dg::GemmArgs& a) {
+  const int64_t lim = 0x7fffffff;
+  if (256 * a.K * 2 + 64 > lim || 66 * a.N * 2 > lim) return false;
+  for (int s = 0; s < a.S; ++s)
+    if ((a.cuts[s + 1] - a.cuts[s] + 4 * 32) * a.N * 2 > lim) return false;
+  return true;
+}
+
 AutoConfig auto_config(int64_t M, int64_t N, int S) {
   if (M <= 32) {
     const int64_t wide = S * ((N + 63) / 64);
@@ -256,7 +266,8 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   if (kern >= 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && tiled_ok) {
-    const AutoConfig c = auto_config(M, N, a.S);
+    AutoConfig c = auto_config(M, N, a.S);
+    if (c.kern == 5 && !pp_fits(a)) c = {3, 128, 128, 3, 2, 0};
     kern = c.kern;
     tm = c.tm;
     tn = c.tn;
@@ -276,6 +287,7 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     if (!tm) { tm = 256; tn = 128; }
     if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = order ? order : 3;
+    if (tm == 256 && tn == 256 && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
     e = dg::launch_gemm_wide(a, tm, tn, st);
   } else if (kern == 2) {
     if (!tm) { tm = 128; tn = 128; }

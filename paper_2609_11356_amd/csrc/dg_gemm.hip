@@ -705,15 +705,18 @@ __global__ __launch_bounds__(512) void gemm_wide(GemmArgs a) {
 // rows [128 g, 128 g + 128) of the block; each wave a 128 x 64 sub-tile.
 // The groups run the same sequence of phases one phase apart, a barrier
 // closing every phase, so that on each SIMD one wave issues MFMAs while the
-// other does memory work:
-//   memory phase of slab s: write the group's half of slab s+1 (loaded two
-//     memory phases earlier, through a ring of two register sets) to LDS,
-//     issue the loads of its half of slab s+3, read the fragments of slab s;
-//   compute phase of slab s: the MFMAs of slab s.
+// other works on LDS:
+//   memory phase of slab s: write the group's half of slab s+1 to LDS from
+//     registers, read the wave's fragments of slab s;
+//   compute phase of slab s: the MFMAs of slab s, with the loads of the
+//     group's half of slab s+3 issued among them (into the register set
+//     just written to LDS; two sets alternate).
 // Slab s+1's halves are written in phases 2s and 2s+1 and first read in
 // phase 2s+2; its buffer last held slab s-1, last read in phase 2s-1.  The
 // group that starts late and the group that ends early each take one barrier
-// on their own, so every wave takes the same number of barriers.
+// on their own, so every wave takes the same number of barriers.  Slabs past
+// the part end are all zero chunks, whose MFMAs leave the accumulators' bits
+// unchanged.
 template <int BM, int BN>
 __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   constexpr int BK = 32, CPR = BK / 8, WTM = BM / 2, WTN = BN / 4, TM = WTM / 16, TN = WTN / 16;
@@ -737,21 +740,48 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 2) & 3)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
-  // the group's half of a slab: A rows [grp BM/2, +BM/2), B rows [grp BK/2, +BK/2)
+  // The group's half of a slab: A rows [grp BM/2, +BM/2), B rows
+  // [grp BK/2, +BK/2), through buffer resources.  A thread's byte offsets
+  // inside the block are fixed (computed once; a row past M or a column past
+  // N gets an offset past the resource's end, which reads zero), the slab
+  // moves a scalar offset, and only a slab that reaches the part end checks
+  // chunks against it.  The host guarantees that every offset fits 31 bits.
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = (a.K - k0) * a.N * 2;
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.B + k0 * a.N), (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
+  uint32_t offA[ACH_T], offB[BCH_T];
+  int kcA[ACH_T], kcB[BCH_T];   // the chunk's k within the slab
+#pragma unroll
+  for (int t = 0; t < ACH_T; ++t) {
+    const int q = tg + 256 * t, row = grp * (BM / 2) + q / CPR, c = q % CPR;
+    offA[t] = (i0 + row < a.M) ? (uint32_t)((row * a.K + 8 * c) * 2) : OOB;
+    kcA[t] = 8 * c;
+  }
+#pragma unroll
+  for (int t = 0; t < BCH_T; ++t) {
+    const int q = tg + 256 * t, kr = grp * (BK / 2) + q / BROW, c = q % BROW;
+    offB[t] = (j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
+    kcB[t] = kr;
+  }
   u32x4 ga2[2][ACH_T], gb2[2][BCH_T];
   auto gload = [&](int sl, u32x4* ga, u32x4* gb) {
-    const int64_t ks = k0 + (int64_t)sl * BK;
+    const int64_t ks = k0 + (int64_t)sl * BK, lim = k1 - ks;
+    const int soA = (int)(ks * 2), soB = (int)((ks - k0) * a.N * 2);
+    if (lim >= BK) {
 #pragma unroll
-    for (int t = 0; t < ACH_T; ++t) {
-      const int q = tg + 256 * t, row = grp * (BM / 2) + q / CPR, c = q % CPR;
-      const int64_t gi = i0 + row, gk = ks + 8 * c;
-      ga[t] = *chunk_or_zero((gi < a.M) && (gk < k1), a.A + gi * a.K + gk);
-    }
+      for (int t = 0; t < ACH_T; ++t) ga[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, offA[t], soA, 0));
 #pragma unroll
-    for (int t = 0; t < BCH_T; ++t) {
-      const int q = tg + 256 * t, kr = grp * (BK / 2) + q / BROW, c = q % BROW;
-      const int64_t gk = ks + kr, gn = j0 + 8 * c;
-      gb[t] = *chunk_or_zero((gk < k1) && (gn < a.N), a.B + gk * a.N + gn);
+      for (int t = 0; t < BCH_T; ++t) gb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, offB[t], soB, 0));
+    } else {
+#pragma unroll
+      for (int t = 0; t < ACH_T; ++t)
+        ga[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, kcA[t] < lim ? offA[t] : OOB, soA, 0));
+#pragma unroll
+      for (int t = 0; t < BCH_T; ++t)
+        gb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, kcB[t] < lim ? offB[t] : OOB, soB, 0));
     }
   };
   auto lstore = [&](int buf, const u32x4* ga, const u32x4* gb) {
@@ -795,6 +825,13 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
     }
   };
 
+  auto mm = [&](int m0, int m1) {
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi)
+      if (mi >= m0 && mi < m1)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bf[ni], acc[mi][ni]);
+  };
   // prologue: slab 0 in buffer 0, slabs 1 and 2 in the two register sets
   gload(0, ga2[0], gb2[0]);
   lstore(0, ga2[0], gb2[0]);
@@ -803,23 +840,23 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   __syncthreads();
   if (grp == 1) __syncthreads();
   auto step = [&](int sl, u32x4* ga, u32x4* gb) {
-    // memory phase: ga/gb hold slab sl+1 and are refilled with slab sl+3
+    // memory phase: ga/gb hold slab sl+1
     __builtin_amdgcn_sched_barrier(0);
     lstore((sl + 1) & 1, ga, gb);
-    gload(sl + 3, ga, gb);
     rd(sl & 1);
     __syncthreads();
-    // compute phase
+    // compute phase; ga/gb are refilled with slab sl+3
     __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bf[ni], acc[mi][ni]);
+    __builtin_amdgcn_s_setprio(2);
+    mm(0, 2);
     __builtin_amdgcn_sched_barrier(0);
+    gload(sl + 3, ga, gb);
+    __builtin_amdgcn_sched_barrier(0);
+    mm(2, TM);
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   };
-  // slab sl+1 sits in set (sl+1) % 2; a slab past the part end is all zero
-  // chunks, whose MFMAs leave the accumulators' bits unchanged
   for (int sl = 0; sl < nslab; sl += 2) {
     step(sl, ga2[1], gb2[1]);
     step(sl + 1, ga2[0], gb2[0]);
