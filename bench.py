@@ -32,6 +32,61 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 MALL_BYTES = 256 << 20
 
 
+# The kernel the library picks for the fused MLP row (2048 x 14336 x 4096):
+# 256 x 256 blocks, 448 of them, so the ping-pong kernel.
+MLP_KERNEL = "dg::gemm_pp<256, 256> (eight-wave ping-pong, fused bias+SiLU epilogue, 448 blocks)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_pp_mlp_hbm_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_11356_amd", "csrc", "dg_gemm.hip")
+
+
+def mlp_traffic():
+    """HBM bytes per MLP launch from the committed counter summary, or None if
+    the GEMM source has changed since those counters were taken."""
+    import hashlib
+    try:
+        fields = {}
+        for line in open(TRAFFIC_FILE):
+            if line.startswith("- ") and ": " in line:
+                k, v = line[2:].strip().split(": ", 1)
+                fields[k] = v.strip("` ")
+        sha = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
+        if fields.get("dg_gemm.hip sha256") != sha:
+            return None
+        return float(fields["HBM bytes per launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def profile_only(args, torch, dg, inputs, d_bf16):
+    """Launch one workload only (for rocprofv3 runs) and print its time."""
+    dev = torch.device("cuda")
+    stream = torch.cuda.current_stream()
+    sptr = int(stream.cuda_stream)
+    if args.only == "mlp":
+        A, B, bias = inputs.mlp()
+        dA, dB, db = d_bf16(A), d_bf16(B), d_bf16(bias)
+        C = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
+        D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", epi_round="final")
+        run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr)
+        what = "fused MLP GEMM 2048x14336x4096"
+    else:
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)   # 1 GiB
+        dst = torch.empty_like(src)
+        run = lambda: dst.copy_(src)
+        what = "device copy of 1 GiB (reads 1 GiB, writes 1 GiB)"
+    for _ in range(args.warmup):
+        run()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(args.steps):
+        run()
+    b.record(stream)
+    torch.cuda.synchronize()
+    print(json.dumps({"only": args.only, "what": what, "launches": args.steps,
+                      "ms_per_launch": round(a.elapsed_time(b) / args.steps, 4)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -40,6 +95,9 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
+    ap.add_argument("--only", choices=("mlp", "copy"), default=None,
+                    help="profiling runs: launch only the fused MLP GEMM, or only a plain "
+                         "1 GiB device copy (the calibration kernel for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -61,6 +119,10 @@ def main():
     def copies(t, nbytes_each):
         n = max(1, -(-2 * MALL_BYTES // nbytes_each))
         return [t] + [t.clone() for _ in range(n - 1)]
+
+    if args.only:
+        profile_only(args, torch, dg, inputs, d_bf16)
+        return
 
     # ---------------------------------------------------------------- inputs
     B_sw = inputs.sweep_weight(2)
@@ -257,9 +319,9 @@ def main():
         "rows_ms": {k: round(v, 4) for k, v in row_ms.items()},
         "rows_tflops": {k: round(flops[k] / (row_ms[k] * 1e-3) / 1e12, 2) for k in row_ms},
         "decode_GB/s": round(2 * (B_dec.nbytes + A_dec.nbytes) / (row_ms["decode"] * 1e-3) / 1e9, 1),
-        "roofline": {"bound": "mfma", "kernel": "gemm_tiled 128x128 (fused MLP, bias+SiLU epilogue)",
+        "roofline": {"bound": "mfma", "kernel": MLP_KERNEL,
                      "achieved": round(mlp_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(mlp_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "frac": round(mlp_tflops / PEAK_BF16_TFLOPS, 4), "traffic": mlp_traffic()},
         "rowsum": rs,
         "free_order": free,
         "bit_match": {"checked": checked, "matched": matched,

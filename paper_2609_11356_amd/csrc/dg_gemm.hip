@@ -767,22 +767,21 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
     kcB[t] = kr;
   }
   u32x4 ga2[2][ACH_T], gb2[2][BCH_T];
-  auto gload = [&](int sl, u32x4* ga, u32x4* gb) {
+  // load number t of the thread's share of slab sl (A chunks first)
+  auto gload1 = [&](int sl, int t, u32x4* ga, u32x4* gb) {
     const int64_t ks = k0 + (int64_t)sl * BK, lim = k1 - ks;
-    const int soA = (int)(ks * 2), soB = (int)((ks - k0) * a.N * 2);
-    if (lim >= BK) {
-#pragma unroll
-      for (int t = 0; t < ACH_T; ++t) ga[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, offA[t], soA, 0));
-#pragma unroll
-      for (int t = 0; t < BCH_T; ++t) gb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, offB[t], soB, 0));
+    if (t < ACH_T) {
+      const uint32_t off = kcA[t] < lim ? offA[t] : OOB;
+      ga[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, off, (int)(ks * 2), 0));
     } else {
-#pragma unroll
-      for (int t = 0; t < ACH_T; ++t)
-        ga[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, kcA[t] < lim ? offA[t] : OOB, soA, 0));
-#pragma unroll
-      for (int t = 0; t < BCH_T; ++t)
-        gb[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, kcB[t] < lim ? offB[t] : OOB, soB, 0));
+      const int u = t - ACH_T;
+      const uint32_t off = kcB[u] < lim ? offB[u] : OOB;
+      gb[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, off, (int)((ks - k0) * a.N * 2), 0));
     }
+  };
+  auto gload = [&](int sl, u32x4* ga, u32x4* gb) {
+#pragma unroll
+    for (int t = 0; t < ACH_T + BCH_T; ++t) gload1(sl, t, ga, gb);
   };
   auto lstore = [&](int buf, const u32x4* ga, const u32x4* gb) {
     uint16_t* As = As0 + buf * A_ELEMS;
@@ -848,12 +847,14 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
     // compute phase; ga/gb are refilled with slab sl+3
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(2);
-    mm(0, 2);
-    __builtin_amdgcn_sched_barrier(0);
-    gload(sl + 3, ga, gb);
-    __builtin_amdgcn_sched_barrier(0);
-    mm(2, TM);
-    __builtin_amdgcn_sched_barrier(0);
+    static_assert(ACH_T + BCH_T == 4 && TM == 8, "one load after each quarter of the MFMAs");
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      mm(2 * q, 2 * q + 2);
+      __builtin_amdgcn_sched_barrier(0);
+      gload1(sl + 3, q, ga, gb);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   };
