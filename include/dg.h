@@ -139,8 +139,8 @@ typedef struct {
                       3 tiled MFMA kernel with transposing LDS reads and a
                       two-slab prefetch, 4 few-row kernel (tile_m <= 64,
                       tile_n 16/32/64) with a deep load ring, 5 eight-wave
-                      kernel for large M and N (256x128, 128x256; 256x256 runs
-                      two groups of four waves one phase apart) */
+                      ping-pong kernel (tile_m, tile_n each 128 or 256): two
+                      groups of four waves one phase apart */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
   int32_t order;   /* kernels 3 and 5: block order: 0 library's choice, 1 row-major

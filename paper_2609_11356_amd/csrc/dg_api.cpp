@@ -97,20 +97,21 @@ dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
 // (speed only; every choice gives the same bits).  Measured on MI355X at
 // N = K = 4096 and at the decode and MLP shapes: few rows stream B through
 // the deep-ring kernel (whole 128-byte B rows per workgroup once the grid
-// is wide enough); when 256 x 256 blocks fill most of the chip the
-// ping-pong kernel takes them, otherwise the transposing-read kernel runs at
-// two workgroups per CU with XCD-contiguous grouped block order.
+// is wide enough); larger M goes to the ping-pong kernel with 256 x 256
+// blocks when they fill most of the chip, else with 128 x 128 blocks, and
+// to the transposing-read kernel (two workgroups per CU, XCD-contiguous
+// grouped order) when even those are too few.
 struct AutoConfig {
   int kern, tm, tn, order, occ, depth;
 };
 
-// The 256 x 256 ping-pong kernel addresses its operands with 31-bit byte
-// offsets from the block's first A row and the part's first B row.
+// The ping-pong kernels address their operands with 31-bit byte offsets from
+// the block's first A row and the part's first B row.
 bool pp_fits(const dg::GemmArgs& a) {
   const int64_t lim = 0x7fffffff;
   if (256 * a.K * 2 + 64 > lim || 66 * a.N * 2 > lim) return false;
   for (int s = 0; s < a.S; ++s)
-    if ((a.cuts[s + 1] - a.cuts[s] + 4 * 32) * a.N * 2 > lim) return false;
+    if ((a.cuts[s + 1] - a.cuts[s] + 4 * 64) * a.N * 2 > lim) return false;
   return true;
 }
 
@@ -120,10 +121,11 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
     return {4, 16, wide >= 256 ? 64 : 32, 0, 0, 4};
   }
   if (M <= 128) return {4, 64, 32, 0, 0, 4};
-  const int64_t big_tiles = S * ((M + 255) / 256) * ((N + 255) / 256);
-  if (big_tiles >= 192) return {5, 256, 256, 1, 0, 0};
-  if (M <= 1536) return {3, 64, 128, 3, 2, 0};
-  return {3, 128, 128, 3, 2, 0};
+  const int64_t tiles256 = S * ((M + 255) / 256) * ((N + 255) / 256);
+  const int64_t tiles128 = S * ((M + 127) / 128) * ((N + 127) / 128);
+  if (tiles256 >= 192) return {5, 256, 256, 1, 0, 0};
+  if (tiles128 >= 128) return {5, 128, 128, 3, 0, 0};
+  return {3, 64, 128, 3, 2, 0};
 }
 
 }  // namespace
@@ -267,7 +269,7 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && tiled_ok) {
     AutoConfig c = auto_config(M, N, a.S);
-    if (c.kern == 5 && !pp_fits(a)) c = {3, 128, 128, 3, 2, 0};
+    if (c.kern == 5 && !pp_fits(a)) c = {3, 64, 128, 3, 2, 0};
     kern = c.kern;
     tm = c.tm;
     tn = c.tn;
@@ -287,7 +289,7 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     if (!tm) { tm = 256; tn = 128; }
     if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = order ? order : 3;
-    if (tm == 256 && tn == 256 && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
+    if (dg::wide_is_pp(tm, tn) && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
     e = dg::launch_gemm_wide(a, tm, tn, st);
   } else if (kern == 2) {
     if (!tm) { tm = 128; tn = 128; }

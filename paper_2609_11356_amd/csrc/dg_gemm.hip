@@ -549,180 +549,40 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   v3_body<BM, BN, WM, WN, BK>(a, (int64_t)ty * BM, (int64_t)tx * BN);
 }
 
-// ------------------------------------------------- wide (eight waves)
-//
-// Large M and N: a BM x BN block per workgroup of WM x WN waves, each wave
-// owning a (BM/WM) x (BN/WN) sub-tile, 64-k slabs in an LDS double buffer.
-// Eight waves (2 x 4, two per SIMD) or four waves (2 x 2, one per SIMD with
-// the accumulators in the AGPR half of the register file).  A step (one slab) runs:
-//   read the fragments of the slab's second 32-k half,
-//   MFMAs of the first half (while those reads are in flight),
-//   write slab s+1 (loaded during the previous step) to the other buffer,
-//   issue the loads of slab s+2, barrier,
-//   read the fragments of slab s+1's first half,
-//   MFMAs of slab s's second half (while those reads are in flight).
-// So every LDS read overlaps MFMA work, and global loads have a whole step
-// to land.  Per output the MFMAs still meet the k chunks in increasing
-// order: the chunk order of every other path.
-//
-// LDS: A [row][64 k] with the 16-byte chunk c of row r at c ^ ((r/2) % 8);
-// B [k][BN] with chunk c of row k at c ^ (2 (k % 4)) ^ (8 ((k/8) % 2)), so
-// that the sixteen lanes of a transposing read touch 32 distinct banks and
-// the lane groups reading rows k and k+8 use the other half of the banks.
-template <int BM, int BN, int WM, int WN>
-__device__ __forceinline__ void wide_body(const GemmArgs& a) {
-  constexpr int NT = 64 * WM * WN, BK = 64, CPR = BK / 8;
-  constexpr int WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
-  constexpr int ACH = BM * CPR, BCH = BK * (BN / 8), BROW = BN / 8;
-  constexpr int ACH_T = ACH / NT, BCH_T = BCH / NT;
-  static_assert(ACH % NT == 0 && BCH % NT == 0 && BROW >= 16, "whole chunks per thread");
-  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (A_ELEMS + B_ELEMS)];
-  uint16_t* As0 = smem;
-  uint16_t* Bs0 = smem + 2 * A_ELEMS;
-
-  const int tiles_m = (int)((a.M + BM - 1) / BM);
-  int ty, tx;
-  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  const int64_t i0 = (int64_t)ty * BM, j0 = (int64_t)tx * BN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int s = blockIdx.z;
-  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
-  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); };
-  auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
-
-  u32x4 ga[ACH_T], gb[BCH_T];
-  auto gload = [&](int sl) {
-    const int64_t ks = k0 + (int64_t)sl * BK;
-#pragma unroll
-    for (int t = 0; t < ACH_T; ++t) {
-      const int q = tid + NT * t, row = q / CPR, c = q % CPR;
-      const int64_t gi = i0 + row, gk = ks + 8 * c;
-      ga[t] = *chunk_or_zero((gi < a.M) && (gk < k1), a.A + gi * a.K + gk);
-    }
-#pragma unroll
-    for (int t = 0; t < BCH_T; ++t) {
-      const int q = tid + NT * t, kr = q / BROW, c = q % BROW;
-      const int64_t gk = ks + kr, gn = j0 + 8 * c;
-      gb[t] = *chunk_or_zero((gk < k1) && (gn < a.N), a.B + gk * a.N + gn);
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint16_t* As = As0 + buf * A_ELEMS;
-    uint16_t* Bs = Bs0 + buf * B_ELEMS;
-#pragma unroll
-    for (int t = 0; t < ACH_T; ++t) {
-      const int q = tid + NT * t;
-      *(u32x4*)&As[8 * ldsA(q / CPR, q % CPR)] = ga[t];
-    }
-#pragma unroll
-    for (int t = 0; t < BCH_T; ++t) {
-      const int q = tid + NT * t;
-      *(u32x4*)&Bs[8 * ldsB(q / BROW, q % BROW)] = gb[t];
-    }
-  };
-
-  floatx4 acc[TM][TN];
-#pragma unroll
-  for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  // fragments of one 32-k half of a slab
-  auto rd = [&](int buf, int kk, shortx8* af, shortx8* bf) {
-    const uint16_t* As = As0 + buf * A_ELEMS;
-    const uint16_t* Bs = Bs0 + buf * B_ELEMS;
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-      const int i = lane & 15, g = lane >> 4;
-      const int n = wn * WTN + 16 * ni + 4 * (i & 3);
-      const int kr0 = kk + 8 * g + (i >> 2), kr1 = kr0 + 4;
-      const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
-      const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
-      bf[ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
-#pragma unroll
-    for (int mi = 0; mi < TM; ++mi) {
-      const int row = wm * WTM + 16 * mi + (lane & 15);
-      af[mi] = *(const shortx8*)&As[8 * ldsA(row, kk / 8 + (lane >> 4))];
-    }
-  };
-  auto mm = [&](const shortx8* af, const shortx8* bf) {
-#pragma unroll
-    for (int mi = 0; mi < TM; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bf[ni], acc[mi][ni]);
-  };
-
-  shortx8 a0[TM], b0[TN], a1[TM], b1[TN];
-  // Loads, LDS stores and fragment reads are unconditional (past the part
-  // end they read the zero chunk), so the loop body has no branch.
-  gload(0);
-  lstore(0);
-  gload(1);
-  __syncthreads();
-  rd(0, 0, a0, b0);
-  for (int sl = 0; sl < nslab; ++sl) {
-    const int cur = sl & 1;
-    rd(cur, 32, a1, b1);
-    mm(a0, b0);
-    lstore(cur ^ 1);
-    gload(sl + 2);
-    __syncthreads();
-    rd(cur ^ 1, 0, a0, b0);
-    mm(a1, b1);
-  }
-
-  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
-  static_assert(WM * WN * 16 * WTN * 4 <= (int)sizeof(smem), "epilogue staging fits");
-#pragma unroll
-  for (int mi = 0; mi < TM; ++mi) {
-    __syncthreads();
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * WTN + 16 * ni + (lane & 15)] = acc[mi][ni][r];
-    __syncthreads();
-#pragma unroll 1
-    for (int q = lane; q < 16 * WTN / 4; q += 64) {
-      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
-      const int64_t i = i0 + wm * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
-      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * WTN + cc]);
-    }
-  }
-}
-
-template <int BM, int BN>
-__global__ __launch_bounds__(512) void gemm_wide(GemmArgs a) {
-  wide_body<BM, BN, 2, 4>(a);
-}
-
-// ------------------------------------------- ping-pong (eight waves, 256 x 256)
+// ------------------------------------------------- ping-pong (eight waves)
 //
 // Two groups of four waves (one wave of each group per SIMD).  Group g owns
-// rows [128 g, 128 g + 128) of the block; each wave a 128 x 64 sub-tile.
-// The groups run the same sequence of phases one phase apart, a barrier
-// closing every phase, so that on each SIMD one wave issues MFMAs while the
-// other works on LDS:
+// rows [g BM/2, (g+1) BM/2) of the BM x BN block; each wave a (BM/2) x (BN/4)
+// sub-tile.  The groups run the same sequence of phases one phase apart, a
+// barrier closing every phase, so that on each SIMD one wave issues MFMAs
+// while the other works on LDS:
 //   memory phase of slab s: write the group's half of slab s+1 to LDS from
 //     registers, read the wave's fragments of slab s;
-//   compute phase of slab s: the MFMAs of slab s, with the loads of the
-//     group's half of slab s+3 issued among them (into the register set
-//     just written to LDS; two sets alternate).
+//   compute phase of slab s: the MFMAs of slab s (its 32-k halves in order),
+//     with the loads of the group's half of slab s+3 spread among them (into
+//     the register set just written to LDS; two sets alternate).
 // Slab s+1's halves are written in phases 2s and 2s+1 and first read in
 // phase 2s+2; its buffer last held slab s-1, last read in phase 2s-1.  The
 // group that starts late and the group that ends early each take one barrier
 // on their own, so every wave takes the same number of barriers.  Slabs past
 // the part end are all zero chunks, whose MFMAs leave the accumulators' bits
 // unchanged.
-template <int BM, int BN>
+//
+// Global loads go through buffer resources: a thread's byte offsets inside
+// the block are fixed for the launch (a row past M or a column past N gets
+// an offset past the resource's end, which reads zero), the slab moves a
+// scalar offset, and chunks are checked against the part end only through a
+// compare with the elements left.  The host guarantees every offset fits 31
+// bits.
+template <int BM, int BN, int BK>
 __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
-  constexpr int BK = 32, CPR = BK / 8, WTM = BM / 2, WTN = BN / 4, TM = WTM / 16, TN = WTN / 16;
-  constexpr int ACH = BM * CPR, BCH = BK * (BN / 8), BROW = BN / 8;
-  constexpr int ACH_T = ACH / 512, BCH_T = BCH / 512;     // per thread, own group's half
-  static_assert(ACH % 512 == 0 && BCH % 512 == 0 && BROW >= 16, "whole chunks per thread");
+  constexpr int CPR = BK / 8, KK = BK / 32, WTM = BM / 2, WTN = BN / 4, TM = WTM / 16, TN = WTN / 16;
+  constexpr int BROW = BN / 8;
+  constexpr int ACH_T = (BM / 2) * CPR / 256, BCH_T = (BK / 2) * BROW / 256;   // per thread
+  constexpr int NLOAD = ACH_T + BCH_T, NPAIR = KK * TM;
+  static_assert((BM / 2) * CPR % 256 == 0 && (BK / 2) * BROW % 256 == 0 && BROW >= 16, "whole chunks");
+  static_assert(CPR == 4 || CPR == 8, "32- or 64-k slabs");
+  static_assert(NPAIR >= NLOAD, "at most one load per MFMA group");
   constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (A_ELEMS + B_ELEMS)];
   uint16_t* As0 = smem;
@@ -737,34 +597,34 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 2) & 3)); };
+  // A: chunk c of row r at c ^ ((r / (16 / CPR)) % CPR); B: chunk c of
+  // k-row k at c ^ 2 (k % 4) ^ 8 ((k / 8) % 2)
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / (16 / CPR)) % CPR)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
-  // The group's half of a slab: A rows [grp BM/2, +BM/2), B rows
-  // [grp BK/2, +BK/2), through buffer resources.  A thread's byte offsets
-  // inside the block are fixed (computed once; a row past M or a column past
-  // N gets an offset past the resource's end, which reads zero), the slab
-  // moves a scalar offset, and only a slab that reaches the part end checks
-  // chunks against it.  The host guarantees that every offset fits 31 bits.
   constexpr uint32_t OOB = 0x80000000u;
   const int64_t recA = (a.M - i0) * a.K * 2, recB = (a.K - k0) * a.N * 2;
   const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
   const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.B + k0 * a.N), (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
+  // the group's half of a slab: A rows [grp BM/2, +BM/2), B k-rows [grp BK/2, +BK/2)
   uint32_t offA[ACH_T], offB[BCH_T];
   int kcA[ACH_T], kcB[BCH_T];   // the chunk's k within the slab
+  int ldA[ACH_T], ldB[BCH_T];   // its LDS chunk
 #pragma unroll
   for (int t = 0; t < ACH_T; ++t) {
     const int q = tg + 256 * t, row = grp * (BM / 2) + q / CPR, c = q % CPR;
     offA[t] = (i0 + row < a.M) ? (uint32_t)((row * a.K + 8 * c) * 2) : OOB;
     kcA[t] = 8 * c;
+    ldA[t] = ldsA(row, c);
   }
 #pragma unroll
   for (int t = 0; t < BCH_T; ++t) {
     const int q = tg + 256 * t, kr = grp * (BK / 2) + q / BROW, c = q % BROW;
     offB[t] = (j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
     kcB[t] = kr;
+    ldB[t] = ldsB(kr, c);
   }
   u32x4 ga2[2][ACH_T], gb2[2][BCH_T];
   // load number t of the thread's share of slab sl (A chunks first)
@@ -781,21 +641,15 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   };
   auto gload = [&](int sl, u32x4* ga, u32x4* gb) {
 #pragma unroll
-    for (int t = 0; t < ACH_T + BCH_T; ++t) gload1(sl, t, ga, gb);
+    for (int t = 0; t < NLOAD; ++t) gload1(sl, t, ga, gb);
   };
   auto lstore = [&](int buf, const u32x4* ga, const u32x4* gb) {
     uint16_t* As = As0 + buf * A_ELEMS;
     uint16_t* Bs = Bs0 + buf * B_ELEMS;
 #pragma unroll
-    for (int t = 0; t < ACH_T; ++t) {
-      const int q = tg + 256 * t, row = grp * (BM / 2) + q / CPR;
-      *(u32x4*)&As[8 * ldsA(row, q % CPR)] = ga[t];
-    }
+    for (int t = 0; t < ACH_T; ++t) *(u32x4*)&As[8 * ldA[t]] = ga[t];
 #pragma unroll
-    for (int t = 0; t < BCH_T; ++t) {
-      const int q = tg + 256 * t, kr = grp * (BK / 2) + q / BROW;
-      *(u32x4*)&Bs[8 * ldsB(kr, q % BROW)] = gb[t];
-    }
+    for (int t = 0; t < BCH_T; ++t) *(u32x4*)&Bs[8 * ldB[t]] = gb[t];
   };
 
   floatx4 acc[TM][TN];
@@ -804,33 +658,35 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  shortx8 af[TM], bf[TN];
+  shortx8 af[KK][TM], bf[KK][TN];
   auto rd = [&](int buf) {
     const uint16_t* As = As0 + buf * A_ELEMS;
     const uint16_t* Bs = Bs0 + buf * B_ELEMS;
 #pragma unroll
-    for (int ni = 0; ni < TN; ++ni) {
-      const int i = lane & 15, g = lane >> 4;
-      const int n = wn * WTN + 16 * ni + 4 * (i & 3);
-      const int kr0 = 8 * g + (i >> 2), kr1 = kr0 + 4;
-      const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
-      const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
-      bf[ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
+    for (int h = 0; h < KK; ++h) {
 #pragma unroll
-    for (int mi = 0; mi < TM; ++mi) {
-      const int row = grp * WTM + 16 * mi + (lane & 15);
-      af[mi] = *(const shortx8*)&As[8 * ldsA(row, lane >> 4)];
+      for (int ni = 0; ni < TN; ++ni) {
+        const int i = lane & 15, g = lane >> 4;
+        const int n = wn * WTN + 16 * ni + 4 * (i & 3);
+        const int kr0 = 32 * h + 8 * g + (i >> 2), kr1 = kr0 + 4;
+        const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+        const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+        bf[h][ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi) {
+        const int row = grp * WTM + 16 * mi + (lane & 15);
+        af[h][mi] = *(const shortx8*)&As[8 * ldsA(row, 4 * h + (lane >> 4))];
+      }
     }
+  };
+  // MFMAs of pair p: 32-k half p / TM, fragment row p % TM (halves in order)
+  auto mm_pair = [&](int p) {
+    const int h = p / TM, mi = p % TM;
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[h][mi], bf[h][ni], acc[mi][ni]);
   };
 
-  auto mm = [&](int m0, int m1) {
-#pragma unroll
-    for (int mi = 0; mi < TM; ++mi)
-      if (mi >= m0 && mi < m1)
-#pragma unroll
-        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bf[ni], acc[mi][ni]);
-  };
   // prologue: slab 0 in buffer 0, slabs 1 and 2 in the two register sets
   gload(0, ga2[0], gb2[0]);
   lstore(0, ga2[0], gb2[0]);
@@ -847,14 +703,17 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
     // compute phase; ga/gb are refilled with slab sl+3
     __builtin_amdgcn_sched_barrier(0);
     __builtin_amdgcn_s_setprio(2);
-    static_assert(ACH_T + BCH_T == 4 && TM == 8, "one load after each quarter of the MFMAs");
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      mm(2 * q, 2 * q + 2);
-      __builtin_amdgcn_sched_barrier(0);
-      gload1(sl + 3, q, ga, gb);
-      __builtin_amdgcn_sched_barrier(0);
-    }
+    // load l goes after MFMA group (l + 1) NPAIR / NLOAD - 1
+    static_for<0, NPAIR>([&](auto p) {
+      mm_pair(p);
+      static_for<0, NLOAD>([&](auto l) {
+        if constexpr ((l + 1) * NPAIR / NLOAD - 1 == p) {
+          __builtin_amdgcn_sched_barrier(0);
+          gload1(sl + 3, l, ga, gb);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    });
     __builtin_amdgcn_s_setprio(0);
     __syncthreads();
   };
@@ -1078,23 +937,24 @@ static hipError_t launch_v3_t(const GemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, bool PP>
-static hipError_t launch_wide_t(const GemmArgs& a, hipStream_t st) {
+template <int BM, int BN, int BK>
+static hipError_t launch_pp_t(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  const dim3 grid((unsigned)(tm * tn), 1, (unsigned)a.S);
-  if constexpr (PP) hipLaunchKernelGGL((gemm_pp<BM, BN>), grid, dim3(512), 0, st, a);
-  else hipLaunchKernelGGL((gemm_wide<BM, BN>), grid, dim3(512), 0, st, a);
+  hipLaunchKernelGGL((gemm_pp<BM, BN, BK>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 
 bool wide_supported(int tm, int tn) {
-  return (tm == 256 && tn == 128) || (tm == 128 && tn == 256) || (tm == 256 && tn == 256);
+  return (tm == 256 || tm == 128) && (tn == 256 || tn == 128);
 }
 
+bool wide_is_pp(int tm, int tn) { return wide_supported(tm, tn); }
+
 hipError_t launch_gemm_wide(const GemmArgs& a, int tm, int tn, hipStream_t st) {
-  if (tm == 256 && tn == 128) return launch_wide_t<256, 128, false>(a, st);
-  if (tm == 128 && tn == 256) return launch_wide_t<128, 256, false>(a, st);
-  if (tm == 256 && tn == 256) return launch_wide_t<256, 256, true>(a, st);
+  if (tm == 256 && tn == 256) return launch_pp_t<256, 256, 32>(a, st);
+  if (tm == 256 && tn == 128) return launch_pp_t<256, 128, 64>(a, st);
+  if (tm == 128 && tn == 256) return launch_pp_t<128, 256, 64>(a, st);
+  if (tm == 128 && tn == 128) return launch_pp_t<128, 128, 64>(a, st);
   return hipErrorInvalidValue;
 }
 

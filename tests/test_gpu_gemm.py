@@ -141,6 +141,7 @@ KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, ti
          dict(kernel=4, tile_m=16, tile_n=16, depth=4), dict(kernel=4, tile_m=32, tile_n=32, depth=8),
          dict(kernel=4, tile_m=64, tile_n=64, depth=12), dict(kernel=4, tile_m=16, tile_n=64, depth=12),
          dict(kernel=5, tile_m=256, tile_n=128, order=1), dict(kernel=5, tile_m=256, tile_n=256),
+         dict(kernel=5, tile_m=128, tile_n=128, order=2),
          dict(kernel=5, tile_m=128, tile_n=256, order=2), None]
 
 
