@@ -148,7 +148,10 @@ typedef struct {
                       eight block rows walked column by column, 3 as 2 with
                       each of the eight XCDs given a contiguous range */
   int32_t occupancy; /* kernel 3: 0 library's choice, 1 or 2 workgroups per CU */
-  int32_t depth;   /* kernel 4: slabs of loads kept in flight, 0, 4, 8 or 12 */
+  int32_t depth;   /* kernel 4: slabs of loads kept in flight (0 = 4; 2, 4 or 8) */
+  int32_t slab_k;  /* kernel 4: k per slab (0 = 64; 64, 128 or 256).  Kernel 4
+                      builds a fixed list of (tile_m, tile_n, depth, slab_k);
+                      others return DG_ERR_UNSUPPORTED */
 } dg_knobs;
 
 /* dg_gemm with explicit speed knobs (NULL = dg_gemm).  A knob combination

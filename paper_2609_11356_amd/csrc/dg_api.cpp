@@ -102,7 +102,7 @@ dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
 // to the transposing-read kernel (two workgroups per CU, XCD-contiguous
 // grouped order) when even those are too few.
 struct AutoConfig {
-  int kern, tm, tn, order, occ, depth;
+  int kern, tm, tn, order, occ, depth, slab_k;
 };
 
 // The ping-pong kernels address their operands with 31-bit byte offsets from
@@ -117,15 +117,15 @@ bool pp_fits(const dg::GemmArgs& a) {
 
 AutoConfig auto_config(int64_t M, int64_t N, int S) {
   if (M <= 32) {
-    const int64_t wide = S * ((N + 63) / 64);
-    return {4, 16, wide >= 256 ? 64 : 32, 0, 0, 4};
+    if (S * ((N + 63) / 64) >= 256) return {4, 16, 64, 0, 0, 4, 64};
+    return {4, 16, M <= 16 ? 16 : 32, 0, 0, 2, 256};
   }
-  if (M <= 128) return {4, 64, 32, 0, 0, 4};
+  if (M <= 128) return {4, 64, 32, 0, 0, 2, 128};
   const int64_t tiles256 = S * ((M + 255) / 256) * ((N + 255) / 256);
   const int64_t tiles128 = S * ((M + 127) / 128) * ((N + 127) / 128);
-  if (tiles256 >= 192) return {5, 256, 256, 1, 0, 0};
-  if (tiles128 >= 128) return {5, 128, 128, 3, 0, 0};
-  return {3, 64, 128, 3, 2, 0};
+  if (tiles256 >= 192) return {5, 256, 256, 1, 0, 0, 0};
+  if (tiles128 >= 128) return {5, 128, 128, 3, 0, 0, 0};
+  return {3, 64, 128, 3, 2, 0, 0};
 }
 
 }  // namespace
@@ -204,13 +204,13 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int kern = knobs ? knobs->kernel : 0;
   int tm = knobs ? knobs->tile_m : 0, tn = knobs ? knobs->tile_n : 0;
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
-  int depth = knobs ? knobs->depth : 0;
+  int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   if (!in(kern, 0, 5) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && order) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && depth) return DG_ERR_UNSUPPORTED;
-  if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth)) return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
+  if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth, slab_k)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && kern != 5 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
@@ -269,17 +269,18 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && tiled_ok) {
     AutoConfig c = auto_config(M, N, a.S);
-    if (c.kern == 5 && !pp_fits(a)) c = {3, 64, 128, 3, 2, 0};
+    if (c.kern == 5 && !pp_fits(a)) c = {3, 64, 128, 3, 2, 0, 0};
     kern = c.kern;
     tm = c.tm;
     tn = c.tn;
     order = c.order;
     occ = c.occ;
     depth = c.depth;
+    slab_k = c.slab_k;
   }
   hipError_t e;
   if (kern == 4) {
-    e = dg::launch_gemm_skinny(a, tm ? tm : 16, tn ? tn : 64, depth, st);
+    e = dg::launch_gemm_skinny(a, tm ? tm : 16, tn ? tn : 64, depth, slab_k, st);
   } else if (kern == 3) {
     if (!tm) { tm = 128; tn = 128; }
     if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;

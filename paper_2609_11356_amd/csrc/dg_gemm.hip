@@ -748,12 +748,15 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 // Few rows: the GEMM streams B from HBM and the MFMA work per slab is small,
 // so the time goes to memory latency.  Each workgroup owns BN columns (one
 // 16-column MFMA tile per computing wave, all four waves loading) and keeps
-// D 64-k slabs of loads in flight through a ring of D register sets, staged
+// D BK-k slabs of loads in flight through a ring of D register sets, staged
 // through an LDS double buffer in the layouts of the v3 kernel (A [m][k], B
 // [k][n], transposing reads for B).  Same chunk order as every other path.
-template <int TMS, int BN, int D>
+// When the column tiles split evenly over the eight XCDs (workgroup w runs
+// on XCD w mod 8), each XCD takes a contiguous range of them, so that tiles
+// sharing 128-byte B lines share an L2.
+template <int TMS, int BN, int D, int BK>
 __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
-  constexpr int BK = 64, CPR = BK / 8, BM = 16 * TMS, NWC = BN / 16;
+  constexpr int CPR = BK / 8, BM = 16 * TMS, NWC = BN / 16;
   constexpr int ACH = BM * CPR, BCH = BK * (BN / 8), BROW = BN / 8;
   constexpr int ACH_T = (ACH + 255) / 256, BCH_T = (BCH + 255) / 256;
   constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
@@ -762,10 +765,13 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   uint16_t* As0 = smem;
   uint16_t* Bs0 = smem + 2 * A_ELEMS;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)blockIdx.x * BN;
+  const int nt = gridDim.x, x = blockIdx.x;
+  const int tile = (nt % 8 == 0) ? (x % 8) * (nt / 8) + x / 8 : x;
+  const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)tile * BN;
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  static_assert(CPR >= 8, "A rows of whole swizzle blocks");
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); };
   // rows of fewer than 8 chunks (BN < 64) are swizzled within the row
   auto ldsB = [](int k, int c) { return k * BROW + ((c ^ ((k & 3) << 1)) & (BROW - 1)); };
@@ -958,32 +964,39 @@ hipError_t launch_gemm_wide(const GemmArgs& a, int tm, int tn, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
-template <int TMS, int BN, int D>
+template <int TMS, int BN, int D, int BK>
 static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
-  hipLaunchKernelGGL((gemm_skinny<TMS, BN, D>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((gemm_skinny<TMS, BN, D, BK>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
-bool skinny_supported(int tm, int tn, int depth) {
-  return (tm == 16 || tm == 32 || tm == 64) && (tn == 16 || tn == 32 || tn == 64) &&
-         (depth == 0 || depth == 4 || depth == 8 || depth == 12);
+// (tile_m, tile_n, depth, slab_k) combinations built; slab_k 0 means 64
+#define DG_SKINNY_LIST(X)                                                                   \
+  X(16, 16, 4, 64) X(16, 16, 8, 64) X(16, 32, 4, 64) X(16, 32, 8, 64) X(16, 64, 4, 64)      \
+  X(16, 64, 8, 64) X(32, 16, 4, 64) X(32, 32, 4, 64) X(32, 32, 8, 64) X(32, 64, 4, 64)      \
+  X(64, 16, 4, 64) X(64, 32, 4, 64) X(64, 32, 8, 64) X(64, 64, 4, 64)                       \
+  X(16, 16, 2, 256) X(16, 16, 4, 256) X(16, 32, 2, 256) X(16, 32, 4, 256) X(16, 64, 2, 256) \
+  X(16, 64, 4, 256) X(32, 32, 2, 256) X(32, 64, 2, 256) X(64, 32, 2, 128) X(64, 32, 4, 128) \
+  X(64, 64, 2, 128)
+
+bool skinny_supported(int tm, int tn, int depth, int slab_k) {
+  if (depth == 0) depth = 4;
+  if (slab_k == 0) slab_k = 64;
+#define DG_SKINNY_HAS(TM_, TN_, D_, BK_) \
+  if (tm == TM_ && tn == TN_ && depth == D_ && slab_k == BK_) return true;
+  DG_SKINNY_LIST(DG_SKINNY_HAS)
+#undef DG_SKINNY_HAS
+  return false;
 }
 
-hipError_t launch_gemm_skinny(const GemmArgs& a, int tm, int tn, int depth, hipStream_t st) {
-#define DG_SKINNY(TM_, TN_, D_) \
-  if (tm == TM_ && tn == TN_ && depth == D_) return launch_skinny_t<TM_ / 16, TN_, D_>(a, st);
-  if (depth == 0) depth = 8;
-  DG_SKINNY(16, 16, 4) DG_SKINNY(16, 16, 8) DG_SKINNY(16, 16, 12)
-  DG_SKINNY(16, 32, 4) DG_SKINNY(16, 32, 8) DG_SKINNY(16, 32, 12)
-  DG_SKINNY(16, 64, 4) DG_SKINNY(16, 64, 8) DG_SKINNY(16, 64, 12)
-  DG_SKINNY(32, 16, 4) DG_SKINNY(32, 16, 8) DG_SKINNY(32, 16, 12)
-  DG_SKINNY(32, 32, 4) DG_SKINNY(32, 32, 8) DG_SKINNY(32, 32, 12)
-  DG_SKINNY(32, 64, 4) DG_SKINNY(32, 64, 8) DG_SKINNY(32, 64, 12)
-  DG_SKINNY(64, 16, 4) DG_SKINNY(64, 16, 8) DG_SKINNY(64, 16, 12)
-  DG_SKINNY(64, 32, 4) DG_SKINNY(64, 32, 8) DG_SKINNY(64, 32, 12)
-  DG_SKINNY(64, 64, 4) DG_SKINNY(64, 64, 8) DG_SKINNY(64, 64, 12)
-#undef DG_SKINNY
+hipError_t launch_gemm_skinny(const GemmArgs& a, int tm, int tn, int depth, int slab_k, hipStream_t st) {
+  if (depth == 0) depth = 4;
+  if (slab_k == 0) slab_k = 64;
+#define DG_SKINNY_RUN(TM_, TN_, D_, BK_) \
+  if (tm == TM_ && tn == TN_ && depth == D_ && slab_k == BK_) return launch_skinny_t<TM_ / 16, TN_, D_, BK_>(a, st);
+  DG_SKINNY_LIST(DG_SKINNY_RUN)
+#undef DG_SKINNY_RUN
   return hipErrorInvalidValue;
 }
 

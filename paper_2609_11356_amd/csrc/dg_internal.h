@@ -55,8 +55,8 @@ bool v3_supported(int tile_m, int tile_n, int occupancy);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)
-hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, hipStream_t s);
-bool skinny_supported(int tile_m, int tile_n, int depth);
+hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, int slab_k, hipStream_t s);
+bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
 

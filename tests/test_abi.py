@@ -93,6 +93,10 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(4, 16, 64, 0, 0, 5)
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(4, 64, 64, 0, 0, 4, 256)      # a combination the build lacks
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(3, 0, 0, 0, 0, 0, 128)        # slab_k is a kernel-4 knob
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     # row reduction
     assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN

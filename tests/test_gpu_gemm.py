@@ -139,7 +139,9 @@ KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, ti
          dict(kernel=3, tile_m=32, tile_n=128), dict(kernel=3, tile_m=128, tile_n=128, occupancy=2, order=2),
          dict(kernel=3, tile_m=64, tile_n=128, occupancy=2, order=3), dict(kernel=3, tile_m=256, tile_n=128, order=3),
          dict(kernel=4, tile_m=16, tile_n=16, depth=4), dict(kernel=4, tile_m=32, tile_n=32, depth=8),
-         dict(kernel=4, tile_m=64, tile_n=64, depth=12), dict(kernel=4, tile_m=16, tile_n=64, depth=12),
+         dict(kernel=4, tile_m=64, tile_n=64, depth=4), dict(kernel=4, tile_m=16, tile_n=64, depth=8),
+         dict(kernel=4, tile_m=16, tile_n=32, depth=4, slab_k=256), dict(kernel=4, tile_m=32, tile_n=64, depth=2, slab_k=256),
+         dict(kernel=4, tile_m=64, tile_n=32, depth=4, slab_k=128),
          dict(kernel=5, tile_m=256, tile_n=128, order=1), dict(kernel=5, tile_m=256, tile_n=256),
          dict(kernel=5, tile_m=128, tile_n=128, order=2),
          dict(kernel=5, tile_m=128, tile_n=256, order=2), None]
