@@ -57,6 +57,19 @@ def mlp_traffic():
         return None
 
 
+def gpu_clock():
+    """The current shader clock as rocm-smi reports it (None if unavailable)."""
+    import subprocess
+    try:
+        out = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True, timeout=20).stdout
+    except (OSError, subprocess.SubprocessError):
+        return None
+    for ln in out.splitlines():
+        if "sclk" in ln.lower():
+            return ln.split(":", 1)[-1].strip() if ":" in ln else ln.strip()
+    return None
+
+
 def profile_only(args, torch, dg, inputs, d_bf16):
     """Launch one workload only (for rocprofv3 runs) and print its time."""
     dev = torch.device("cuda")
@@ -164,23 +177,32 @@ def main():
     def ev():
         return torch.cuda.Event(enable_timing=True)
 
-    row_ms = {"sweep": 0.0, "decode": 0.0, "mlp": 0.0}
+    # one entry per launch of a step, in launch order: (row, name, flops, algorithmic bytes)
+    launches = [("sweep", "sweep_M%d" % M, 2 * M * 4096 * 4096, 2 * (M * 4096 + 4096 * 4096 + M * 4096))
+                for M in inputs.SWEEP_M]
+    launches += [("decode", "decode_" + c, 2 * 8 * 4096 * 14336,
+                  2 * (8 * 14336 + 14336 * 4096 + 8 * 4096) + 2 * 4 * 8 * 8 * 4096) for c in ("seq", "tree")]
+    launches += [("mlp", "mlp", 2 * 2048 * 14336 * 4096, 2 * (2048 * 4096 + 4096 * 14336 + 14336 + 2048 * 14336))]
 
     def step(i, record):
-        e = [ev() for _ in range(4)] if record else None
+        e = [ev() for _ in range(len(launches) + 1)] if record else None
         if record:
             e[0].record(stream)
+        n = 0
         for M in inputs.SWEEP_M:
             dg.dg_gemm(D_sw, dA_sw_M[M], dB_sw[i % len(dB_sw)], None, C_sw[M], stream=sptr)
-        if record:
-            e[1].record(stream)
-        for c in ("seq", "tree"):
-            dg.dg_gemm(D_dec[c], dA_dec, dB_dec[i % len(dB_dec)], None, C_dec[c], stream=sptr)
-        if record:
-            e[2].record(stream)
+            n += 1
+            if record:
+                e[n].record(stream)
+        for u, c in enumerate(("seq", "tree")):
+            dg.dg_gemm(D_dec[c], dA_dec, dB_dec[(2 * i + u) % len(dB_dec)], None, C_dec[c], stream=sptr)
+            n += 1
+            if record:
+                e[n].record(stream)
         dg.dg_gemm(D_mlp, dA_mlp, dB_mlp[i % len(dB_mlp)], dbias, C_mlp, stream=sptr)
+        n += 1
         if record:
-            e[3].record(stream)
+            e[n].record(stream)
         return e
 
     # ------------------------------------------------------------- warmup
@@ -196,13 +218,18 @@ def main():
     t1.record(stream)
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
-    for e in evs:
-        row_ms["sweep"] += e[0].elapsed_time(e[1])
-        row_ms["decode"] += e[1].elapsed_time(e[2])
-        row_ms["mlp"] += e[2].elapsed_time(e[3])
+    per_launch = [[e[n].elapsed_time(e[n + 1]) for e in evs] for n in range(len(launches))]
+    row_ms = {"sweep": 0.0, "decode": 0.0, "mlp": 0.0}
+    shapes = {}
+    for (row, name, fl, by), ts in zip(launches, per_launch):
+        row_ms[row] += sum(ts) / len(ts)
+        med = float(np.median(ts))
+        shapes[name] = {"us_mean": round(1e3 * sum(ts) / len(ts), 2), "us_median": round(1e3 * med, 2),
+                        "TFLOP/s": round(fl / (med * 1e-3) / 1e12, 2),
+                        "frac_mfma_peak": round(fl / (med * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                        "GB/s": round(by / (med * 1e-3) / 1e9, 1),
+                        "frac_hbm": round(by / (med * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
     ms_per_step = total_ms / args.steps
-    for k in row_ms:
-        row_ms[k] /= args.steps
     value = step_flops / (ms_per_step * 1e-3) / 1e12
 
     # ------------------------------------------------------ row reduction
@@ -245,12 +272,20 @@ def main():
         t_mlp = timeit(lambda i: torch.nn.functional.silu(torch.matmul(dA_mlp, dB_mlp[i % len(dB_mlp)]) + dbias),
                        args.steps)
         t_rs = timeit(lambda i: torch.sum(dX, 1), args.steps)
+        t_rs2 = timeit(lambda i: torch.sum(dX * dX, 1), args.steps)
+        t_sw_m = {M: timeit(lambda i, M=M: torch.matmul(dA_sw_M[M], dB_sw[i % len(dB_sw)]), args.steps)
+                  for M in inputs.SWEEP_M}
         free = {"sweep_ms": round(t_sw, 4), "decode_ms_per_launch": round(t_dec, 4), "mlp_ms": round(t_mlp, 4),
                 "rowsum_ms": round(t_rs, 4),
                 "cost_sweep": round(row_ms["sweep"] / t_sw, 3),
                 "cost_decode": round(row_ms["decode"] / 2 / t_dec, 3),
                 "cost_mlp": round(row_ms["mlp"] / t_mlp, 3),
                 "cost_rowsum": round(rs["sum"]["ms"] / t_rs, 3),
+                "rowsum_sumsq_ms": round(t_rs2, 4),
+                "cost_rowsum_sumsq": round(rs["sumsq"]["ms"] / t_rs2, 3),
+                "sweep_ms_by_M": {str(M): round(t, 4) for M, t in t_sw_m.items()},
+                "cost_sweep_by_M": {str(M): round(shapes["sweep_M%d" % M]["us_mean"] * 1e-3 / t, 3)
+                                    for M, t in t_sw_m.items()},
                 "what": "torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum on the same shapes; cost = t_dg / t_free"}
     except Exception as exc:  # the library under test never depends on this
         free = {"error": repr(exc)}
@@ -296,6 +331,18 @@ def main():
     oracle.gemm_at(desc_mlp, A_mlp, B_mlp, bias_mlp, ii, jj, nthreads=ncpu)
     tc = time.perf_counter() - tc
     cpu_tflops = 2 * 4096 * n_s / tc / 1e12
+    n_1 = max(1000, n_s // (4 * ncpu))
+    t1c = time.perf_counter()
+    oracle.gemm_at(desc_mlp, A_mlp, B_mlp, bias_mlp, ii[:n_1], jj[:n_1], nthreads=1)
+    t1c = time.perf_counter() - t1c
+    cpu_model = ""
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                cpu_model = ln.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
 
     mlp_tflops = flops["mlp"] / (row_ms["mlp"] * 1e-3) / 1e12
     line = {
@@ -319,6 +366,8 @@ def main():
         "rows_ms": {k: round(v, 4) for k, v in row_ms.items()},
         "rows_tflops": {k: round(flops[k] / (row_ms[k] * 1e-3) / 1e12, 2) for k in row_ms},
         "decode_GB/s": round(2 * (B_dec.nbytes + A_dec.nbytes) / (row_ms["decode"] * 1e-3) / 1e9, 1),
+        "shapes": shapes,
+        "gpu_clock": gpu_clock(),
         "roofline": {"bound": "mfma", "kernel": MLP_KERNEL,
                      "achieved": round(mlp_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(mlp_tflops / PEAK_BF16_TFLOPS, 4), "traffic": mlp_traffic()},
@@ -329,7 +378,8 @@ def main():
                       "batch_invariant_row0": inv_ok},
         "cpu_baseline": {"value": round(cpu_tflops, 6), "unit": "TFLOP/s", "cores": ncpu, "kind": "oracle",
                          "sample": "%d random outputs of the fused MLP (K=4096, bias+SiLU, bf16), %.1f s"
-                                   % (n_s, tc)},
+                                   % (n_s, tc),
+                         "one_thread_TFLOP/s": round(2 * 4096 * n_1 / t1c / 1e12, 7), "cpu_model": cpu_model},
     }
     print(json.dumps(line), flush=True)
 
