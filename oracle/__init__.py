@@ -47,7 +47,8 @@ class _Params(ctypes.Structure):
         ("k_cuts", ctypes.POINTER(ctypes.c_int64))] + [
         (n, ctypes.c_int32) for n in (
             "tile_combine", "split_combine", "tail_first", "fma", "partial_bf16",
-            "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq")]
+            "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq",
+            "split_strided", "split_tile")]
 
 
 _lib = None
@@ -107,7 +108,7 @@ def _bind(path):
 DEFAULTS = dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=1, k_cuts=None,
                 tile_combine="carry", split_combine="seq", tail="last", fma=1,
                 partial="f32", merge="f32", out="f32", epilogue="none",
-                epi_round="final", leaf_w=64, reduce="sum")
+                epi_round="final", leaf_w=64, reduce="sum", split_layout="contiguous", split_tile=0)
 
 
 def params(desc: dict):
@@ -134,6 +135,8 @@ def params(desc: dict):
     p.pre_act_round = 1 if d["epi_round"] == "pre_act" else 0
     p.leaf_w = int(d["leaf_w"])
     p.sumsq = 1 if d["reduce"] == "sumsq" else 0
+    p.split_strided = 1 if d["split_layout"] == "strided" else 0
+    p.split_tile = int(d["split_tile"])
     return p, cuts
 
 

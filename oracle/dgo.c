@@ -404,6 +404,12 @@ static int check_params(const dgo_params* p) {
   if (p->merge_bf16 && !p->partial_bf16) return 1;
   if (p->epilogue < DGO_EPI_NONE || p->epilogue > DGO_EPI_BIAS_SILU) return 1;
   if (p->pre_act_round && p->epilogue != DGO_EPI_BIAS_SILU) return 1;
+  if (p->split_strided) {
+    /* dealt tiles hold whole accumulator tiles; no explicit cuts, no
+     * leading short tile */
+    if (p->split_tile < 1 || p->split_tile % p->tile_k != 0) return 1;
+    if (p->k_cuts || p->tail_first) return 1;
+  }
   return 0;
 }
 
@@ -449,30 +455,40 @@ float dgo_silu(float z) {
 /* ------------------------------------------------------------- GEMM */
 
 /* One output (i, j) of the descriptor's order.  a = row i of A (K values),
- * B column j read with stride ldb.  Scratch: g + 2 tile/part buffers. */
+ * B column j read with stride ldb.  A part is a sequence of k indices:
+ * contiguous parts are the ranges between cut points; in the strided layout
+ * (Sec. 3.2.2, GEMV: each lane takes every S-th tile of the axis) part s is
+ * every k whose tile index floor(k / split_tile) is s mod S, in increasing
+ * order.  Accumulator tiles, groups and the leading short tile are cut from
+ * the start of the part's sequence. */
 typedef struct {
   const dgo_params* p;
-  const int64_t* cuts;
+  const int64_t* idx;      /* the parts' k indices, part after part */
+  const int64_t* start;    /* part s is idx[start[s] .. start[s+1]) */
   int64_t K, ldb;
 } gemm_ctx;
 
 static float part_value(const gemm_ctx* c, const uint16_t* a, const uint16_t* bcol,
-                        int64_t k0, int64_t k1, uint16_t* bbuf, float* tvals) {
+                        const int64_t* idx, int64_t len, uint16_t* abuf, uint16_t* bbuf,
+                        float* tvals) {
   const dgo_params* p = c->p;
-  int64_t len = k1 - k0, tk = p->tile_k;
+  int64_t tk = p->tile_k;
   int64_t ntiles = (len + tk - 1) / tk;
   int64_t first = tk; /* length of the first tile */
   if (p->tail_first && len % tk) first = len % tk;
   float acc = 0.0f;
-  int64_t t0 = k0;
+  int64_t t0 = 0;
   for (int64_t t = 0; t < ntiles; ++t) {
     int64_t tl = (t == 0) ? (first < len ? first : len) : tk;
-    if (t0 + tl > k1) tl = k1 - t0;
+    if (t0 + tl > len) tl = len - t0;
     if (p->tile_combine != DGO_CARRY) acc = 0.0f; /* each tile starts at zero */
     for (int64_t q = t0; q < t0 + tl; q += p->g) {
       int n = (int)((t0 + tl - q) < p->g ? (t0 + tl - q) : p->g);
-      for (int u = 0; u < n; ++u) bbuf[u] = bcol[(q + u) * c->ldb];
-      acc = dgo_group_update(p->model, acc, a + q, bbuf, n, p->g, p->fma);
+      for (int u = 0; u < n; ++u) {
+        abuf[u] = a[idx[q + u]];
+        bbuf[u] = bcol[idx[q + u] * c->ldb];
+      }
+      acc = dgo_group_update(p->model, acc, abuf, bbuf, n, p->g, p->fma);
     }
     if (p->tile_combine != DGO_CARRY) tvals[t] = acc;
     t0 += tl;
@@ -484,13 +500,14 @@ static float part_value(const gemm_ctx* c, const uint16_t* a, const uint16_t* bc
 }
 
 static float gemm_one(const gemm_ctx* c, const uint16_t* a, const uint16_t* B,
-                      const uint16_t* bias, int64_t j, uint16_t* bbuf,
+                      const uint16_t* bias, int64_t j, uint16_t* abuf, uint16_t* bbuf,
                       float* tvals, float* pvals) {
   const dgo_params* p = c->p;
   const uint16_t* bcol = B + j;
   int S = p->split_k;
   for (int s = 0; s < S; ++s) {
-    float v = part_value(c, a, bcol, c->cuts[s], c->cuts[s + 1], bbuf, tvals);
+    float v = part_value(c, a, bcol, c->idx + c->start[s], c->start[s + 1] - c->start[s],
+                         abuf, bbuf, tvals);
     pvals[s] = p->partial_bf16 ? rnbf(v) : v;
   }
   float y = (S == 1) ? pvals[0]
@@ -505,24 +522,41 @@ static float gemm_one(const gemm_ctx* c, const uint16_t* a, const uint16_t* B,
   return p->out_bf16 ? rnbf(z) : z;
 }
 
+/* Validate and lay out the parts: idx (K entries) and start (S+1). */
 static int gemm_setup(const dgo_params* p, const uint16_t* bias, int64_t K,
-                      int64_t** cuts_out) {
+                      int64_t** idx_out, int64_t** start_out) {
   int st = check_params(p);
   if (st) return st;
   if (p->epilogue != DGO_EPI_NONE && !bias) return 1;
   if (K < 0) return 3;
   if (K == 0 && p->split_k > 1) return 3;
-  int64_t* cuts = (int64_t*)malloc(sizeof(int64_t) * (size_t)(p->split_k + 1));
-  if (K == 0) { cuts[0] = 0; cuts[1] = 0; }
-  else if ((st = dgo_plan_cuts(p, K, cuts))) { free(cuts); return st; }
-  *cuts_out = cuts;
+  const int S = p->split_k;
+  int64_t* start = (int64_t*)malloc(sizeof(int64_t) * (size_t)(S + 1));
+  int64_t* idx = (int64_t*)malloc(sizeof(int64_t) * (size_t)(K > 0 ? K : 1));
+  if (!p->split_strided) {
+    int64_t* cuts = start;  /* contiguous: part s is [cuts[s], cuts[s+1]) */
+    if (K == 0) { cuts[0] = 0; cuts[1] = 0; }
+    else if ((st = dgo_plan_cuts(p, K, cuts))) { free(start); free(idx); return st; }
+    for (int64_t k = 0; k < K; ++k) idx[k] = k;
+  } else {
+    const int64_t w = p->split_tile;
+    int64_t n = 0;
+    for (int s = 0; s < S; ++s) {
+      start[s] = n;
+      for (int64_t u = s; u * w < K; u += S)
+        for (int64_t k = u * w; k < (u + 1) * w && k < K; ++k) idx[n++] = k;
+    }
+    start[S] = n;
+  }
+  *idx_out = idx;
+  *start_out = start;
   return 0;
 }
 
-static int64_t max_tiles(const dgo_params* p, const int64_t* cuts) {
+static int64_t max_tiles(const dgo_params* p, const int64_t* start) {
   int64_t m = 1;
   for (int s = 0; s < p->split_k; ++s) {
-    int64_t n = (cuts[s + 1] - cuts[s] + p->tile_k - 1) / p->tile_k;
+    int64_t n = (start[s + 1] - start[s] + p->tile_k - 1) / p->tile_k;
     if (n > m) m = n;
   }
   return m;
@@ -531,28 +565,29 @@ static int64_t max_tiles(const dgo_params* p, const int64_t* cuts) {
 int dgo_gemm(const dgo_params* p, const uint16_t* A, const uint16_t* B,
              const uint16_t* bias, void* C, int64_t M, int64_t N, int64_t K,
              int nthreads) {
-  int64_t* cuts = NULL;
-  int st = gemm_setup(p, bias, K, &cuts);
+  int64_t *idx = NULL, *start = NULL;
+  int st = gemm_setup(p, bias, K, &idx, &start);
   if (st) return st;
-  gemm_ctx c = {p, cuts, K, N};
-  int64_t nt = max_tiles(p, cuts);
+  gemm_ctx c = {p, idx, start, K, N};
+  int64_t nt = max_tiles(p, start);
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel num_threads(nthreads)
   {
+    uint16_t* abuf = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)p->g);
     uint16_t* bbuf = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)p->g);
     float* tvals = (float*)malloc(sizeof(float) * (size_t)nt);
     float* pvals = (float*)malloc(sizeof(float) * (size_t)p->split_k);
 #pragma omp for schedule(dynamic, 1)
     for (int64_t i = 0; i < M; ++i) {
       for (int64_t j = 0; j < N; ++j) {
-        float v = gemm_one(&c, A + i * K, B, bias, j, bbuf, tvals, pvals);
+        float v = gemm_one(&c, A + i * K, B, bias, j, abuf, bbuf, tvals, pvals);
         if (p->out_bf16) ((uint16_t*)C)[i * N + j] = dgo_f32_to_bf16(v);
         else ((float*)C)[i * N + j] = v;
       }
     }
-    free(bbuf); free(tvals); free(pvals);
+    free(abuf); free(bbuf); free(tvals); free(pvals);
   }
-  free(cuts);
+  free(idx); free(start);
   return 0;
 }
 
@@ -560,25 +595,26 @@ int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
                 const uint16_t* bias, int64_t M, int64_t N, int64_t K,
                 const int64_t* ii, const int64_t* jj, int64_t n, float* out,
                 int nthreads) {
-  int64_t* cuts = NULL;
-  int st = gemm_setup(p, bias, K, &cuts);
+  int64_t *idx = NULL, *start = NULL;
+  int st = gemm_setup(p, bias, K, &idx, &start);
   if (st) return st;
   for (int64_t t = 0; t < n; ++t)
-    if (ii[t] < 0 || ii[t] >= M || jj[t] < 0 || jj[t] >= N) { free(cuts); return 3; }
-  gemm_ctx c = {p, cuts, K, N};
-  int64_t nt = max_tiles(p, cuts);
+    if (ii[t] < 0 || ii[t] >= M || jj[t] < 0 || jj[t] >= N) { free(idx); free(start); return 3; }
+  gemm_ctx c = {p, idx, start, K, N};
+  int64_t nt = max_tiles(p, start);
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel num_threads(nthreads)
   {
+    uint16_t* abuf = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)p->g);
     uint16_t* bbuf = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)p->g);
     float* tvals = (float*)malloc(sizeof(float) * (size_t)nt);
     float* pvals = (float*)malloc(sizeof(float) * (size_t)p->split_k);
 #pragma omp for schedule(dynamic, 16)
     for (int64_t t = 0; t < n; ++t)
-      out[t] = gemm_one(&c, A + ii[t] * K, B, bias, jj[t], bbuf, tvals, pvals);
-    free(bbuf); free(tvals); free(pvals);
+      out[t] = gemm_one(&c, A + ii[t] * K, B, bias, jj[t], abuf, bbuf, tvals, pvals);
+    free(abuf); free(bbuf); free(tvals); free(pvals);
   }
-  free(cuts);
+  free(idx); free(start);
   return 0;
 }
 

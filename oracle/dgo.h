@@ -66,6 +66,10 @@ typedef struct {
   int32_t pre_act_round;  /* 1: the pre-activation value is rounded to bf16 */
   int32_t leaf_w;         /* row reduction: elements per sequential leaf */
   int32_t sumsq;          /* row reduction: 1 = sum of squares */
+  int32_t split_strided;  /* outer cut layout (Sec. 3.2.2, GEMV: layout): 0 contiguous
+                             parts; 1 the axis is dealt in tiles of split_tile,
+                             tile u going to part u mod S */
+  int32_t split_tile;     /* width of a dealt tile (strided layout only) */
 } dgo_params;
 
 /* Status: 0 ok, 1 invalid parameters, 3 shape inconsistent with the plan. */

@@ -546,3 +546,87 @@ def test_chunk_model_equals_exact_when_window_holds_everything():
     c1 = oracle.gemm(dict(model="gfx950", tile_k=64), A, B)
     c2 = oracle.gemm(dict(model="exact", g=8, tile_k=64), A, B)
     assert np.array_equal(c1, c2)
+
+
+# ------------------------------------------------ strided layout of the split
+#
+# Sec. 3.2.2 (GEMV): a cut may deal the axis to its parts in tiles, part s
+# taking every S-th tile, instead of giving each part a contiguous slice; the
+# descriptor records which (layout).  Part s is then every k whose tile index
+# floor(k / split_tile) is s mod S, in increasing k.
+
+
+def _walk_operands(vals, K=32):
+    """Row vector a with the given {k: value} entries (zero elsewhere) and an
+    all-ones column: the products are the a entries themselves."""
+    a = np.zeros((1, K), np.float32)
+    for k, v in vals.items():
+        a[0, k] = v
+    return bits(a), np.full((K, 1), ONE)
+
+
+@pytest.mark.parametrize("model", ["exact", "gfx950"])
+def test_strided_layout_hand_walk(model):
+    """A cancelling pair L, -L and a small r: which partial each lands in
+    decides whether r survives (worked by hand; L = 2^30, r = 1, so that
+    L + r rounds back to L in binary32)."""
+    L = 2.0 ** 30
+    base = dict(model=model, g=8, tile_k=8)
+    a, b = _walk_operands({0: L, 16: -L, 8: 1.0})
+    # contiguous halves [0,16) [16,32): (L (+) 1) = L, then L (+) -L = 0
+    assert oracle.gemm(dict(base, split_k=2), a, b)[0, 0] == 0.0
+    # strided, tiles of 8: part 0 = k 0-7, 16-23 (L then -L: exact 0),
+    # part 1 = k 8-15, 24-31 (= 1): 0 (+) 1 = 1
+    st = dict(base, split_k=2, split_layout="strided", split_tile=8)
+    assert oracle.gemm(st, a, b)[0, 0] == 1.0
+    # four parts, one tile each: L, 1, -L, 1.  Chain: ((L (+) 1) (+) -L) (+) 1
+    # = 0 (+) 1 = 1; tree: (L (+) 1) (+) (-L (+) 1) = L (+) -L = 0
+    a, b = _walk_operands({0: L, 8: 1.0, 16: -L, 24: 1.0})
+    st4 = dict(base, split_k=4, split_layout="strided", split_tile=8)
+    assert oracle.gemm(dict(st4, split_combine="seq"), a, b)[0, 0] == 1.0
+    assert oracle.gemm(dict(st4, split_combine="tree"), a, b)[0, 0] == 0.0
+
+
+@pytest.mark.parametrize("S,w,tile_k,K", [(2, 64, 64, 1032), (4, 64, 32, 4096), (4, 128, 64, 4160),
+                                          (3, 32, 32, 1000), (4, 64, 64, 100), (8, 32, 32, 40)])
+def test_strided_small_integers_are_exact(S, w, tile_k, K):
+    """Integer operands keep every order exact, so a dropped, repeated or
+    misplaced k shows as a wrong integer -- including ragged K and parts
+    left empty (K < S w), whose value is +0."""
+    rng = np.random.default_rng(S * 1000 + K)
+    Ai = rng.integers(-8, 9, (3, K))
+    Bi = rng.integers(-8, 9, (K, 5))
+    for comb in ("seq", "tree"):
+        d = dict(tile_k=tile_k, split_k=S, split_layout="strided", split_tile=w, split_combine=comb)
+        C = oracle.gemm(d, bits(Ai), bits(Bi))
+        assert np.array_equal(C.astype(np.int64), Ai @ Bi)
+
+
+def test_strided_parts_are_gathered_chains():
+    """Each strided part equals the one-part product over its own k, taken in
+    increasing order; the split's merge chains those parts in part order."""
+    A, B = _spread(21, M=2, K=1100, N=3)
+    S, w = 4, 64
+    ks = np.arange(1100)
+    parts = []
+    for s in range(S):
+        idx = ks[(ks // w) % S == s]
+        parts.append(oracle.gemm(dict(tile_k=64), np.ascontiguousarray(A[:, idx]),
+                                 np.ascontiguousarray(B[idx])))
+    y = parts[0]
+    for p in parts[1:]:
+        y = (y + p).astype(np.float32)
+    got = oracle.gemm(dict(tile_k=64, split_k=S, split_layout="strided", split_tile=w), A, B)
+    assert np.array_equal(got.view(np.uint32), y.view(np.uint32))
+    one = oracle.gemm(dict(tile_k=64, split_layout="strided", split_tile=w), A, B)
+    assert np.array_equal(one.view(np.uint32), oracle.gemm(dict(tile_k=64), A, B).view(np.uint32))
+
+
+def test_strided_layout_rejects_what_it_cannot_express():
+    A, B = np.full((1, 64), ONE), np.full((64, 1), ONE)
+    for bad in (dict(split_tile=48, tile_k=32), dict(split_tile=0), dict(k_cuts=[32], split_tile=32),
+                dict(tail="first", split_tile=32)):
+        d = dict(tile_k=32, split_k=2, split_layout="strided")
+        d.update(bad)
+        with pytest.raises(oracle.OracleError):
+            oracle.gemm(d, A, B)

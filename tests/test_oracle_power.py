@@ -35,7 +35,10 @@ MUTANTS = {
     "fma flag ignored": ("  s = fma ? acc : 0.0f;", "  s = acc; fma = 1;"),
     "short tile always last": ("if (p->tail_first && len % tk)", "if (0 && len % tk)"),
     "pre-activation rounding skipped": ("if (p->pre_act_round) z = rnbf(z);", "if (0) z = rnbf(z);"),
-    "B read transposed": ("bbuf[u] = bcol[(q + u) * c->ldb];", "bbuf[u] = bcol[(q + u)];"),
+    "B read transposed": ("bbuf[u] = bcol[idx[q + u] * c->ldb];", "bbuf[u] = bcol[idx[q + u]];"),
+    "strided tiles dealt to the next part": ("for (int64_t u = s; u * w < K; u += S)",
+                                             "for (int64_t u = (s + 1) % S; u * w < K; u += S)"),
+    "strided tile width halved": ("const int64_t w = p->split_tile;", "const int64_t w = p->split_tile / 2;"),
     "bf16 conversion truncates": (
         "return (uint16_t)((u + 0x7fffu + lsb) >> 16);", "(void)lsb; return (uint16_t)(u >> 16);"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
@@ -59,6 +62,8 @@ CHECKS = [
     lambda: pins.test_exp_accuracy_dense_sweep(),
     lambda: pins.test_epilogue_rounding_points(),
     lambda: pins.test_chunk_model_hand_examples(),
+    lambda: pins.test_strided_layout_hand_walk("gfx950"),
+    lambda: pins.test_strided_small_integers_are_exact(4, 64, 32, 4096),
 ]
 
 
