@@ -62,6 +62,7 @@ enum { DG_F32 = 0, DG_BF16 = 1 };                  /* storage/rounding types */
 enum { DG_EPI_NONE = 0, DG_EPI_BIAS = 1, DG_EPI_BIAS_SILU = 2 };
 enum { DG_ROUND_FINAL = 0, DG_ROUND_PRE_ACT = 1 };
 enum { DG_OP_SUM = 0, DG_OP_SUMSQ = 1 };
+enum { DG_SPLIT_CONTIGUOUS = 0, DG_SPLIT_STRIDED = 1 };  /* layout of the split (Sec. 3.2.2) */
 
 #define DG_MAX_SPLIT 64
 
@@ -96,6 +97,15 @@ typedef struct {
   int32_t leaf_w;         /* row reduction: elements folded in index order per
                              leaf before the balanced tree over leaves (>= 1) */
   int32_t reduce_op;      /* DG_OP_SUM or DG_OP_SUMSQ (fma: fused square-add) */
+  int32_t split_layout;   /* DG_SPLIT_CONTIGUOUS: part s is the k range between
+                             cuts s and s+1; DG_SPLIT_STRIDED: the K axis is
+                             dealt in tiles of split_tile, tile u (k in
+                             [u w, u w + w)) going to part u mod S, each part
+                             walking its tiles in increasing k (Sec. 3.2.2, the
+                             cut's layout).  A part may be empty (K < S w): its
+                             value is +0.  Requires n_cuts = 0, tail =
+                             DG_TAIL_LAST and split_tile a multiple of tile_k */
+  int32_t split_tile;     /* w, the dealt tile (strided layout; else 0) */
 } dg_desc_params;
 
 typedef struct dg_desc dg_desc; /* opaque, immutable */

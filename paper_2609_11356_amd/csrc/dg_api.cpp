@@ -51,6 +51,9 @@ void make_signature(dg_desc* d) {
                         p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
                         p.merge_dtype ? "bf16" : "f32", p.out_dtype ? "bf16" : "f32", p.epilogue,
                         p.epi_round ? "pre-act" : "final", p.leaf_w, p.reduce_op ? "sumsq" : "sum");
+  // one strided part is the whole axis, as one contiguous part is
+  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && n > 0 && n < (int)sizeof d->sig)
+    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/strided:%d", p.split_tile);
   if (p.n_cuts && n > 0 && n < (int)sizeof d->sig) {
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/cuts");
     for (int i = 0; i < p.n_cuts && n > 0 && n < (int)sizeof d->sig; ++i)
@@ -170,6 +173,14 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   if (!in(p->epilogue, DG_EPI_NONE, DG_EPI_BIAS_SILU) || !in(p->epi_round, DG_ROUND_FINAL, DG_ROUND_PRE_ACT))
     return DG_ERR_INVALID;
   if (p->leaf_w < 1 || !in(p->reduce_op, DG_OP_SUM, DG_OP_SUMSQ)) return DG_ERR_INVALID;
+  if (!in(p->split_layout, DG_SPLIT_CONTIGUOUS, DG_SPLIT_STRIDED)) return DG_ERR_INVALID;
+  if (p->split_layout == DG_SPLIT_STRIDED) {
+    if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
+      return DG_ERR_INVALID;
+    if (p->n_cuts != 0 || p->tail != DG_TAIL_LAST) return DG_ERR_INVALID;
+  } else if (p->split_tile != 0) {
+    return DG_ERR_INVALID;
+  }
   if (p->merge_dtype == DG_BF16 && p->partial_dtype != DG_BF16) return DG_ERR_UNSUPPORTED;
   if (p->epi_round == DG_ROUND_PRE_ACT && p->epilogue != DG_EPI_BIAS_SILU) return DG_ERR_UNSUPPORTED;
   dg_desc* d = new (std::nothrow) dg_desc;
@@ -214,6 +225,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   if (kern != 4 && kern != 5 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
+  // A strided split runs on the generic kernel or on the few-row kernel with
+  // one dealt tile per slab.
+  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 &&
+      !(kern == 4 && slab_k == p.split_tile))
+    return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
   if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
   if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
@@ -223,7 +239,13 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
 
   dg::GemmArgs a;
   std::memset(&a, 0, sizeof a);
-  if (K > 0) {
+  const bool strided = p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1;
+  if (strided) {
+    // parts are dealt tiles, not ranges: the kernels read split_w instead
+    a.split_w = p.split_tile;
+    a.cuts[0] = 0;
+    for (int s = 1; s <= p.split_k; ++s) a.cuts[s] = K;
+  } else if (K > 0) {
     dg_status st = plan_cuts(d, K, a.cuts);
     if (st != DG_OK) return st;
   } else {
@@ -266,6 +288,19 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     if (a.tail_first && (len % p.tile_k) % 8) tiled_ok = false;
   }
   if (kern >= 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (strided && kern == 0) {
+    const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
+    const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
+    if (tiled_ok && M <= 64 && dg::skinny_supported(tmc, tnc, 4, p.split_tile)) {
+      kern = 4;
+      tm = tmc;
+      tn = tnc;
+      depth = 4;
+      slab_k = p.split_tile;
+    } else {
+      kern = 1;
+    }
+  }
   if (kern == 1 && (tm || tn)) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && tiled_ok) {
     AutoConfig c = auto_config(M, N, a.S);

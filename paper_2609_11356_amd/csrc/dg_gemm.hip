@@ -124,22 +124,16 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
   const int lane = threadIdx.x;
   const int64_t i0 = (int64_t)blockIdx.y * 16, j0 = (int64_t)blockIdx.x * 16;
   const int s = blockIdx.z;
-  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
-  const int64_t len = k1 - k0, tk = a.tile_k;
-  const int64_t ntiles = (len + tk - 1) / tk;
-  int64_t first = tk;
-  if (a.tail_first && (len % tk)) first = len % tk;
+  const int64_t tk = a.tile_k;
   const int64_t arow = i0 + (lane & 15), bcol = j0 + (lane & 15);
   const int kb = 8 * (lane >> 4);
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   const int64_t step = a.fma ? 32 : a.group;  // one instruction per step
   floatx4 acc = zero;
   uint32_t count = 0;
-  int64_t ts = k0;
-  for (int64_t t = 0; t < ntiles; ++t) {
-    int64_t tl = (t == 0) ? (first < len ? first : len) : tk;
-    if (ts + tl > k1) tl = k1 - ts;
-    const int64_t te = ts + tl;
+  int64_t t = 0;  // tiles of the part so far
+  // one accumulator tile [ts, te) of the part
+  auto tile = [&](int64_t ts, int64_t te) {
     floatx4 v = (a.tile_combine == DG_CARRY) ? acc : zero;
     for (int64_t gs = ts; gs < te; gs += step) {
       const int64_t ge = (gs + step < te) ? gs + step : te;
@@ -173,7 +167,31 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
       stk[lvl][lane] = v;
       ++count;
     }
-    ts = te;
+    ++t;
+  };
+  if (a.split_w == 0) {
+    // contiguous part [cuts[s], cuts[s+1]): tiles of tile_k from its start,
+    // the short one first or last
+    const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+    const int64_t len = k1 - k0;
+    const int64_t ntiles = (len + tk - 1) / tk;
+    int64_t first = tk;
+    if (a.tail_first && (len % tk)) first = len % tk;
+    int64_t ts = k0;
+    for (int64_t u = 0; u < ntiles; ++u) {
+      int64_t tl = (u == 0) ? (first < len ? first : len) : tk;
+      if (ts + tl > k1) tl = k1 - ts;
+      tile(ts, ts + tl);
+      ts += tl;
+    }
+  } else {
+    // strided part: dealt tiles u = s, s + S, ... of width w, each cut into
+    // accumulator tiles of tile_k (w is a multiple of tile_k)
+    const int64_t w = a.split_w;
+    for (int64_t u = s; u * w < a.K; u += a.S) {
+      const int64_t ue = (u * w + w < a.K) ? u * w + w : a.K;
+      for (int64_t ts = u * w; ts < ue; ts += tk) tile(ts, (ts + tk < ue) ? ts + tk : ue);
+    }
   }
   if (a.tile_combine == DG_TREE && count) {
     bool have = false;
@@ -769,8 +787,14 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   const int tile = (nt % 8 == 0) ? (x % 8) * (nt / 8) + x / 8 : x;
   const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)tile * BN;
   const int s = blockIdx.z;
-  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
-  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  // slab sl of the part covers [k0 + sl kstep, + BK), loads stop at k1: a
+  // contiguous part steps by BK through [cuts[s], cuts[s+1]); a strided part
+  // (dealt tiles of width BK) steps by S BK from s BK up to K
+  const bool strided = a.split_w != 0;
+  const int64_t k0 = strided ? (int64_t)s * BK : a.cuts[s];
+  const int64_t k1 = strided ? a.K : a.cuts[s + 1];
+  const int64_t kstep = strided ? (int64_t)a.S * BK : BK;
+  const int nslab = (k1 > k0) ? (int)((k1 - k0 + kstep - 1) / kstep) : 0;
   static_assert(CPR >= 8, "A rows of whole swizzle blocks");
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); };
   // rows of fewer than 8 chunks (BN < 64) are swizzled within the row
@@ -778,7 +802,7 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 
   u32x4 ra[D][ACH_T], rb[D][BCH_T];
   auto gload = [&](int sl, u32x4* xa, u32x4* xb) {
-    const int64_t ks = k0 + (int64_t)sl * BK;
+    const int64_t ks = k0 + (int64_t)sl * kstep;
 #pragma unroll
     for (int t = 0; t < ACH_T; ++t) {
       const int q = tid + 256 * t, row = q / CPR, c = q % CPR;
@@ -978,7 +1002,8 @@ static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t st) {
   X(64, 16, 4, 64) X(64, 32, 4, 64) X(64, 32, 8, 64) X(64, 64, 4, 64)                       \
   X(16, 16, 2, 256) X(16, 16, 4, 256) X(16, 32, 2, 256) X(16, 32, 4, 256) X(16, 64, 2, 256) \
   X(16, 64, 4, 256) X(32, 32, 2, 256) X(32, 64, 2, 256) X(64, 32, 2, 128) X(64, 32, 4, 128) \
-  X(64, 64, 2, 128)
+  X(64, 64, 2, 128) X(16, 16, 4, 128) X(16, 32, 4, 128) X(16, 64, 4, 128) X(32, 32, 4, 128) \
+  X(32, 64, 4, 128)
 
 bool skinny_supported(int tm, int tn, int depth, int slab_k) {
   if (depth == 0) depth = 4;

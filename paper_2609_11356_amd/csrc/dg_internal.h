@@ -28,6 +28,7 @@ struct GemmArgs {
   int32_t tile_k, group, tile_combine, tail_first, fma;
   int32_t partial_bf16, out_bf16, epilogue, pre_act;
   int32_t order;                 // block order of the v3 kernels (speed only)
+  int64_t split_w;               // strided split: dealt tile width (0: contiguous parts)
 };
 
 struct CombineArgs {

@@ -36,7 +36,7 @@ class dg_desc_params(ctypes.Structure):
                 ("k_cuts", ctypes.POINTER(ctypes.c_int64))] + [
         (n, ctypes.c_int32) for n in ("tile_combine", "split_combine", "tail", "fma", "partial_dtype",
                                       "merge_dtype", "out_dtype", "epilogue", "epi_round", "leaf_w",
-                                      "reduce_op")]
+                                      "reduce_op", "split_layout", "split_tile")]
 
 
 class dg_knobs(ctypes.Structure):
@@ -89,11 +89,13 @@ class Desc:
     "seq" | "tree"), split_combine ("seq" | "tree"), tail ("last" | "first"),
     fma (0/1), partial / merge / out ("f32" | "bf16"), epilogue ("none" |
     "bias" | "bias_silu"), epi_round ("final" | "pre_act"), leaf_w,
-    reduce ("sum" | "sumsq")."""
+    reduce ("sum" | "sumsq"), split_layout ("contiguous" | "strided"),
+    split_tile (the dealt tile of a strided split)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
-                    epilogue="none", epi_round="final", leaf_w=64, reduce="sum")
+                    epilogue="none", epi_round="final", leaf_w=64, reduce="sum",
+                    split_layout="contiguous", split_tile=0)
 
     def __init__(self, **fields):
         unknown = set(fields) - set(self.DEFAULTS) - {"model"}
@@ -126,6 +128,8 @@ class Desc:
         p.epi_round = EPI_ROUND[f["epi_round"]]
         p.leaf_w = int(f["leaf_w"])
         p.reduce_op = REDUCE[f["reduce"]]
+        p.split_layout = {"contiguous": 0, "strided": 1}[f["split_layout"]]
+        p.split_tile = int(f["split_tile"])
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:

@@ -42,7 +42,12 @@ def test_version_and_strerror(dg):
 @pytest.mark.parametrize("bad", [
     dict(tile_k=24), dict(tile_k=0), dict(mma="8x8"), dict(split_k=0), dict(split_k=65),
     dict(split_k=3, k_cuts=[5]), dict(split_k=3, k_cuts=[10, 5]), dict(split_k=2, k_cuts=[0]),
-    dict(leaf_w=0), dict(fma=2)])
+    dict(leaf_w=0), dict(fma=2),
+    dict(split_k=4, split_layout="strided", split_tile=48),              # not whole accumulator tiles
+    dict(split_k=4, split_layout="strided", split_tile=0),
+    dict(split_k=3, split_layout="strided", split_tile=64, k_cuts=[64, 128]),
+    dict(split_k=4, split_layout="strided", split_tile=64, tail="first"),
+    dict(split_k=4, split_tile=64)])                                     # a tile without the layout
 def test_invalid_descriptors_rejected(dg, bad):
     with pytest.raises((dg.DgError, KeyError)):
         dg.Desc(**bad)
@@ -65,6 +70,10 @@ def test_signature_canonical(dg):
     d = dg.Desc(mma="32x32x16", tile_k=64, fma=0).signature()
     assert c != d and c != a
     assert dg.Desc(split_k=3, k_cuts=[100, 200]).signature().endswith("cuts:100:200")
+    st = dg.Desc(split_k=4, split_layout="strided", split_tile=64).signature()
+    assert st.endswith("strided:64") and st != dg.Desc(split_k=4).signature()
+    # one strided part is the whole axis: the same order as one contiguous part
+    assert dg.Desc(split_layout="strided", split_tile=64).signature() == dg.Desc().signature()
 
 
 def test_argument_errors_need_no_gpu(dg):
@@ -97,6 +106,12 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(3, 0, 0, 0, 0, 0, 128)        # slab_k is a kernel-4 knob
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    # a strided split runs on the generic kernel or on kernel 4 with one dealt tile per slab
+    sd = dg.Desc(split_k=4, split_layout="strided", split_tile=64)
+    for kn in (dg.dg_knobs(3, 0, 0, 0, 0, 0, 0), dg.dg_knobs(5, 0, 0, 0, 0, 0, 0),
+               dg.dg_knobs(4, 16, 32, 0, 0, 4, 128)):
+        assert lib.dg_gemm_knobs(sd.handle, 16, 16, None, 16, 8, 8, 64, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED
     # row reduction
     assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
