@@ -32,6 +32,14 @@ __device__ __forceinline__ float leaf_step(float s, float x, int sumsq, int fma)
   return s + q;
 }
 
+// The waves of a workgroup reduce different rows in disjoint LDS regions, so
+// no workgroup barrier is needed: a wave waits for its own LDS operations
+// (lgkmcnt(0)) before the next phase touches the same locations.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_s_waitcnt(0xc07f);
+  __builtin_amdgcn_wave_barrier();
+}
+
 __device__ __forceinline__ float butterfly(float v) {
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
@@ -42,13 +50,16 @@ __device__ __forceinline__ float butterfly(float v) {
 // fetched with all of the pass's 16-byte loads in flight at once (a lane
 // holds leaf_w floats of the pass in registers), the next pass's loads are
 // issued before the current pass is folded, and LDS is only the transpose.
-template <bool VEC>
+// LW: the leaf width when fixed at compile time, else 0.  OP: 0 SUM, 1 SUMSQ
+// with fused square-add, 2 SUMSQ with a rounded square, -1 read from a.
+template <bool VEC, int LW, int OP>
 __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
+  const int sumsq = OP < 0 ? a.sumsq : OP > 0, fma = OP < 0 ? a.fma : OP == 1;
   __shared__ float lds[RS_WAVES][RS_LDS];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t row = (int64_t)blockIdx.x * RS_WAVES + wave;
   const bool live = row < a.rows;
-  const int lw = a.leaf_w;
+  const int lw = LW ? LW : a.leaf_w;
   const int64_t cols = a.cols;
   const int64_t L = (cols + lw - 1) / lw;
   const int64_t npass = (L + 63) / 64;
@@ -91,7 +102,7 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
       } else if (live) {
         for (int el = lane; el < nel; el += 64) sl[(el / lw) * (lw + 1) + el % lw] = x[base + el];
       }
-      __syncthreads();
+      wave_lds_sync();
       // cur has been written to LDS: reuse it for the next pass's loads,
       // which stay in flight while this pass is folded
       if (VEC && p + 1 < npass) fetch(p + 1, cur);
@@ -99,16 +110,16 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
         const int n = (int)((cols - leaf * lw < lw) ? cols - leaf * lw : lw);
         const float* lp = sl + lane * (lw + 1);
         float x0 = lp[0];
-        s = a.sumsq ? x0 * x0 : x0;
-        for (int i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
+        s = sumsq ? x0 * x0 : x0;
+        for (int i = 1; i < n; ++i) s = leaf_step(s, lp[i], sumsq, fma);
       }
-      __syncthreads();
+      wave_lds_sync();
     } else if (live && leaf < L) {
       const int64_t n = (cols - leaf * lw < lw) ? cols - leaf * lw : lw;
       const float* lp = x + leaf * lw;
       float x0 = lp[0];
-      s = a.sumsq ? x0 * x0 : x0;
-      for (int64_t i = 1; i < n; ++i) s = leaf_step(s, lp[i], a.sumsq, a.fma);
+      s = sumsq ? x0 * x0 : x0;
+      for (int64_t i = 1; i < n; ++i) s = leaf_step(s, lp[i], sumsq, fma);
     }
     float v = butterfly(s);                             // root of this pass
     // push onto the binary-counter stack (uniform across the wave)
@@ -138,10 +149,17 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t st) {
   const int64_t blocks = (a.rows + RS_WAVES - 1) / RS_WAVES;
   const bool vec = ((((uintptr_t)a.X) & 15) == 0) && (a.cols % 4 == 0);
-  if (vec)
-    hipLaunchKernelGGL(rowsum_kernel<true>, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
-  else
-    hipLaunchKernelGGL(rowsum_kernel<false>, dim3((unsigned)blocks), dim3(64 * RS_WAVES), 0, st, a);
+  const dim3 grid((unsigned)blocks), block(64 * RS_WAVES);
+  const int op = !a.sumsq ? 0 : a.fma ? 1 : 2;
+  if (vec && a.leaf_w == 64) {
+    if (op == 0) hipLaunchKernelGGL((rowsum_kernel<true, 64, 0>), grid, block, 0, st, a);
+    else if (op == 1) hipLaunchKernelGGL((rowsum_kernel<true, 64, 1>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((rowsum_kernel<true, 64, 2>), grid, block, 0, st, a);
+  } else if (vec) {
+    hipLaunchKernelGGL((rowsum_kernel<true, 0, -1>), grid, block, 0, st, a);
+  } else {
+    hipLaunchKernelGGL((rowsum_kernel<false, 0, -1>), grid, block, 0, st, a);
+  }
   return hipGetLastError();
 }
 
