@@ -34,7 +34,8 @@ MALL_BYTES = 256 << 20
 
 # The kernel the library picks for the fused MLP row (2048 x 14336 x 4096):
 # 256 x 256 blocks, 448 of them, so the ping-pong kernel.
-MLP_KERNEL = "dg::gemm_pp<256, 256> (eight-wave ping-pong, fused bias+SiLU epilogue, 448 blocks)"
+MLP_KERNEL = ("dg::gemm_pp_mixed<32> (eight-wave ping-pong, fused bias+SiLU epilogue; 256 blocks of 256x256 "
+              "then 256 of 256x192)")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_pp_mlp_hbm_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_11356_amd", "csrc", "dg_gemm.hip")
 

@@ -101,7 +101,9 @@ dg_status get_workspace(hipStream_t st, size_t bytes, void** out) {
 // N = K = 4096 and at the decode and MLP shapes: few rows stream B through
 // the deep-ring kernel (whole 128-byte B rows per workgroup once the grid
 // is wide enough); larger M goes to the ping-pong kernel with 256 x 256
-// blocks when they fill most of the chip, else with 128 x 128 blocks, and
+// blocks when they fill most of the chip (mixed with 256 x 192 blocks when
+// that makes the last round over the chip fuller), else with 128 x 128
+// blocks, and
 // to the transposing-read kernel (two workgroups per CU, XCD-contiguous
 // grouped order) when even those are too few.
 struct AutoConfig {
@@ -116,6 +118,41 @@ bool pp_fits(const dg::GemmArgs& a) {
   for (int s = 0; s < a.S; ++s)
     if ((a.cuts[s + 1] - a.cuts[s] + 4 * 64) * a.N * 2 > lim) return false;
   return true;
+}
+
+// Compute units of the current device (cached per device; 256 on MI355X).
+int cu_count() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (!cached[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+// Columns for 256-wide blocks in the mixed-width ping-pong launch, or -1
+// when 256-wide blocks alone are as good.  One block runs per CU; the
+// estimate counts rounds of blocks over the chip, a 192-wide block taking
+// 7/8 of the time of a 256-wide one (measured on MI355X: 117 us for 256
+// blocks of 256 x 192 against 131 us for 256 of 256 x 256 at K = 4096;
+// the A side of the block's LDS and load traffic does not shrink).
+int64_t mixed_split(int64_t M, int64_t N, int S, int ncu) {
+  const int64_t tm = S * ((M + 255) / 256);
+  auto rounds = [&](int64_t blocks) { return (double)((blocks + ncu - 1) / ncu); };
+  const double plain = rounds(tm * ((N + 255) / 256));
+  double best = 0.97 * plain;
+  int64_t split = -1;
+  for (int64_t c = 0; 256 * c <= N; ++c) {
+    const double est = rounds(tm * c) + 0.875 * rounds(tm * ((N - 256 * c + 191) / 192));
+    if (est < best) {
+      best = est;
+      split = 256 * c;
+    }
+  }
+  return split;
 }
 
 AutoConfig auto_config(int64_t M, int64_t N, int S) {
@@ -216,8 +253,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int tm = knobs ? knobs->tile_m : 0, tn = knobs ? knobs->tile_n : 0;
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
-  if (!in(kern, 0, 5) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
-  if (kern != 3 && kern != 5 && order) return DG_ERR_UNSUPPORTED;
+  int64_t split_n = knobs ? knobs->split_n : 0;
+  if (!in(kern, 0, 6) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && kern != 5 && kern != 6 && order) return DG_ERR_UNSUPPORTED;
+  if (kern == 6 && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
+  if (kern != 6 && split_n) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
@@ -305,6 +345,14 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   if (kern == 0 && tiled_ok) {
     AutoConfig c = auto_config(M, N, a.S);
     if (c.kern == 5 && !pp_fits(a)) c = {3, 64, 128, 3, 2, 0, 0};
+    if (c.kern == 5 && c.tm == 256 && c.tn == 256) {
+      const int64_t sp = mixed_split(M, N, a.S, cu_count());
+      if (sp >= 0) {
+        c.kern = 6;
+        c.tm = c.tn = 0;
+        split_n = sp;
+      }
+    }
     kern = c.kern;
     tm = c.tm;
     tn = c.tn;
@@ -327,6 +375,16 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     a.order = order ? order : 3;
     if (dg::wide_is_pp(tm, tn) && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
     e = dg::launch_gemm_wide(a, tm, tn, st);
+  } else if (kern == 6) {
+    if (!pp_fits(a)) return DG_ERR_UNSUPPORTED;
+    if (knobs && knobs->kernel == 6 && split_n == 0) {
+      const int64_t sp = mixed_split(M, N, a.S, cu_count());
+      split_n = sp > 0 ? sp : 0;
+    }
+    if (((M + 255) / 256) * (split_n / 256 + (N - split_n + 191) / 192) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = order ? order : 1;
+    a.n_split = split_n;
+    e = dg::launch_gemm_pp_mixed(a, st);
   } else if (kern == 2) {
     if (!tm) { tm = 128; tn = 128; }
     if ((M + tm - 1) / tm > 65535) return DG_ERR_SHAPE;

@@ -592,24 +592,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // scalar offset, and chunks are checked against the part end only through a
 // compare with the elements left.  The host guarantees every offset fits 31
 // bits.
-template <int BM, int BN, int BK>
-__global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
-  constexpr int CPR = BK / 8, KK = BK / 32, WTM = BM / 2, WTN = BN / 4, TM = WTM / 16, TN = WTN / 16;
+// BNC <= BN is the number of columns the block computes; the B slab keeps
+// the BN-wide LDS layout and load mapping, and its chunks past BNC are
+// neither loaded nor stored.
+template <int BM, int BN, int BK, int BNC>
+__device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j0, uint16_t* smem) {
+  constexpr int CPR = BK / 8, KK = BK / 32, WTM = BM / 2, WTN = BNC / 4, TM = WTM / 16, TN = WTN / 16;
   constexpr int BROW = BN / 8;
   constexpr int ACH_T = (BM / 2) * CPR / 256, BCH_T = (BK / 2) * BROW / 256;   // per thread
   constexpr int NLOAD = ACH_T + BCH_T, NPAIR = KK * TM;
   static_assert((BM / 2) * CPR % 256 == 0 && (BK / 2) * BROW % 256 == 0 && BROW >= 16, "whole chunks");
   static_assert(CPR == 4 || CPR == 8, "32- or 64-k slabs");
   static_assert(NPAIR >= NLOAD, "at most one load per MFMA group");
+  static_assert(BNC <= BN && BNC % 64 == 0, "whole 16-column fragments per wave");
   constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (A_ELEMS + B_ELEMS)];
   uint16_t* As0 = smem;
   uint16_t* Bs0 = smem + 2 * A_ELEMS;
 
-  const int tiles_m = (int)((a.M + BM - 1) / BM);
-  int ty, tx;
-  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  const int64_t i0 = (int64_t)ty * BM, j0 = (int64_t)tx * BN;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int grp = wave >> 2, wn = wave & 3, tg = tid & 255;
   const int s = blockIdx.z;
@@ -640,9 +639,9 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 #pragma unroll
   for (int t = 0; t < BCH_T; ++t) {
     const int q = tg + 256 * t, kr = grp * (BK / 2) + q / BROW, c = q % BROW;
-    offB[t] = (j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
+    offB[t] = (8 * c < BNC && j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
     kcB[t] = kr;
-    ldB[t] = ldsB(kr, c);
+    ldB[t] = 8 * c < BNC ? ldsB(kr, c) : -1;
   }
   u32x4 ga2[2][ACH_T], gb2[2][BCH_T];
   // load number t of the thread's share of slab sl (A chunks first)
@@ -667,7 +666,8 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 #pragma unroll
     for (int t = 0; t < ACH_T; ++t) *(u32x4*)&As[8 * ldA[t]] = ga[t];
 #pragma unroll
-    for (int t = 0; t < BCH_T; ++t) *(u32x4*)&Bs[8 * ldB[t]] = gb[t];
+    for (int t = 0; t < BCH_T; ++t)
+      if (BNC == BN || ldB[t] >= 0) *(u32x4*)&Bs[8 * ldB[t]] = gb[t];
   };
 
   floatx4 acc[TM][TN];
@@ -743,7 +743,7 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 
   constexpr int CSP = WTN + 4;   // staging pitch: rows 4 apart start 16 banks apart
   float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
-  static_assert(8 * 16 * CSP * 4 <= (int)sizeof(smem), "epilogue staging fits");
+  static_assert(8 * 16 * CSP * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
     __syncthreads();
@@ -758,6 +758,37 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
       const int64_t i = i0 + grp * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
       if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
     }
+  }
+}
+
+template <int BM, int BN, int BK>
+__global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM * BK + BK * BN)];
+  const int tiles_m = (int)((a.M + BM - 1) / BM);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  pp_body<BM, BN, BK, BN>(a, (int64_t)ty * BM, (int64_t)tx * BN, smem);
+}
+
+// Two column widths in one launch: columns [0, n_split) in 256 x 256 blocks
+// (the first workgroups), the rest in 256 x 192 blocks.  With one block per
+// CU, a width mix can make the work a whole number of rounds over the chip
+// where 256-wide blocks alone leave the last round partly idle (2048 x 14336:
+// 448 blocks of 256 x 256 take two rounds on 256 CUs; 256 blocks of
+// 256 x 256 and 256 of 256 x 192 take 1.75 rounds of work).
+template <int BK>
+__global__ __launch_bounds__(512) void gemm_pp_mixed(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (256 * BK + BK * 256)];
+  const int tiles_m = (int)((a.M + 255) / 256);
+  const int tn1 = (int)(a.n_split / 256), nb1 = tiles_m * tn1;
+  int ty, tx;
+  if ((int)blockIdx.x < nb1) {
+    grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
+    pp_body<256, 256, BK, 256>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
+  } else {
+    const int tn2 = (int)((a.N - a.n_split + 191) / 192);
+    grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
+    pp_body<256, 256, BK, 192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
   }
 }
 
@@ -971,6 +1002,12 @@ template <int BM, int BN, int BK>
 static hipError_t launch_pp_t(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   hipLaunchKernelGGL((gemm_pp<BM, BN, BK>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t st) {
+  const int64_t tm = (a.M + 255) / 256, tn = a.n_split / 256 + (a.N - a.n_split + 191) / 192;
+  hipLaunchKernelGGL((gemm_pp_mixed<32>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 

@@ -29,6 +29,7 @@ struct GemmArgs {
   int32_t partial_bf16, out_bf16, epilogue, pre_act;
   int32_t order;                 // block order of the v3 kernels (speed only)
   int64_t split_w;               // strided split: dealt tile width (0: contiguous parts)
+  int64_t n_split;               // mixed-width ping-pong: first column of the 192-wide blocks
 };
 
 struct CombineArgs {
@@ -56,6 +57,7 @@ bool v3_supported(int tile_m, int tile_n, int occupancy);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)
+hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t s);   // n_split set
 hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, int slab_k, hipStream_t s);
 bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);

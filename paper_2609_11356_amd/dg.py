@@ -42,7 +42,7 @@ class dg_desc_params(ctypes.Structure):
 class dg_knobs(ctypes.Structure):
     _fields_ = [("kernel", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
                 ("order", ctypes.c_int32), ("occupancy", ctypes.c_int32), ("depth", ctypes.c_int32),
-                ("slab_k", ctypes.c_int32)]
+                ("slab_k", ctypes.c_int32), ("split_n", ctypes.c_int32)]
 
 
 _lib = None
@@ -190,7 +190,7 @@ def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knob
     if knobs is not None:
         kp = dg_knobs(int(knobs.get("kernel", 0)), int(knobs.get("tile_m", 0)), int(knobs.get("tile_n", 0)),
                       int(knobs.get("order", 0)), int(knobs.get("occupancy", 0)), int(knobs.get("depth", 0)),
-                      int(knobs.get("slab_k", 0)))
+                      int(knobs.get("slab_k", 0)), int(knobs.get("split_n", 0)))
         st = lib().dg_gemm_knobs(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K,
                                  ctypes.byref(kp), _stream(stream))
     else:
