@@ -33,7 +33,8 @@ MALL_BYTES = 256 << 20
 
 
 # The kernel the library picks for the fused MLP row (2048 x 14336 x 4096):
-# 256 x 256 blocks, 448 of them, so the ping-pong kernel.
+# the ping-pong kernel in one launch of 512 blocks (columns 0..8191 in
+# 256 x 256 blocks, the rest in 256 x 192 blocks).
 MLP_KERNEL = ("dg::gemm_pp_mixed<32> (eight-wave ping-pong, fused bias+SiLU epilogue; 256 blocks of 256x256 "
               "then 256 of 256x192)")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_pp_mlp_hbm_traffic.md")
