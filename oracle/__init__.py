@@ -48,7 +48,7 @@ class _Params(ctypes.Structure):
         (n, ctypes.c_int32) for n in (
             "tile_combine", "split_combine", "tail_first", "fma", "partial_bf16",
             "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq",
-            "split_strided", "split_tile")]
+            "split_strided", "split_tile", "leaf_strided", "fold_down")]
 
 
 _lib = None
@@ -93,6 +93,8 @@ def _bind(path):
     L.dgo_exact_dot_rn32.restype = f32
     L.dgo_tree.argtypes = [vp, i32, i32]
     L.dgo_tree.restype = f32
+    L.dgo_tree_bitrev.argtypes = [vp, i32, i32]
+    L.dgo_tree_bitrev.restype = f32
     L.dgo_f32_to_bf16.argtypes = [f32]
     L.dgo_f32_to_bf16.restype = ctypes.c_uint16
     L.dgo_exp.argtypes = [f32]
@@ -108,7 +110,8 @@ def _bind(path):
 DEFAULTS = dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=1, k_cuts=None,
                 tile_combine="carry", split_combine="seq", tail="last", fma=1,
                 partial="f32", merge="f32", out="f32", epilogue="none",
-                epi_round="final", leaf_w=64, reduce="sum", split_layout="contiguous", split_tile=0)
+                epi_round="final", leaf_w=64, reduce="sum", split_layout="contiguous", split_tile=0,
+                leaf_layout="contiguous", lane_fold="up")
 
 
 def params(desc: dict):
@@ -137,6 +140,8 @@ def params(desc: dict):
     p.sumsq = 1 if d["reduce"] == "sumsq" else 0
     p.split_strided = 1 if d["split_layout"] == "strided" else 0
     p.split_tile = int(d["split_tile"])
+    p.leaf_strided = {"contiguous": 0, "strided": 1}[d["leaf_layout"]]
+    p.fold_down = {"up": 0, "down": 1}[d["lane_fold"]]
     return p, cuts
 
 
@@ -242,6 +247,13 @@ def exact_dot_rn32(c, a, b):
 def tree(v, bf16_round=False):
     v = np.ascontiguousarray(v, dtype=np.float32)
     return np.float32(lib().dgo_tree(v.ctypes.data, len(v), int(bf16_round)))
+
+
+def tree_bitrev(v, lanes=None):
+    """The count-down butterfly's tree over `lanes` lanes (default len(v)),
+    lane j holding v[j] and lanes past len(v) empty."""
+    v = np.ascontiguousarray(v, dtype=np.float32)
+    return np.float32(lib().dgo_tree_bitrev(v.ctypes.data, len(v), int(lanes or len(v))))
 
 
 def f32_to_bf16(x):

@@ -16,7 +16,10 @@
  *                        lane exchange = perfect tree over lanes in natural order
  *   merge                Sec. 3.2.2 partial_dtype / merge_dtype
  *   rowsum               Sec. 3.1 three-level tree: in-thread index-order fold,
- *                        then lane and cross-warp stages pinned to the balanced tree
+ *                        then lane and cross-warp stages pinned to the balanced tree;
+ *                        Sec. 3.2.2 GEMV: leaves dealt every count-th element
+ *                        (strided layout), lanes folded by a butterfly whose
+ *                        offsets count up or down
  *   epilogue             Sec. 1: the rounding points of a fused epilogue are part
  *                        of the order; exp is our own (Cody-Waite + Taylor)
  */
@@ -364,6 +367,43 @@ float dgo_tree(const float* v, int n, int bf16_round) {
   return r;
 }
 
+/* A butterfly over P = 2^b lanes whose offsets count down (P/2, .., 2, 1)
+ * (Sec. 3.2.2 GEMV): its first step pairs lanes P/2 apart, so the tree it
+ * builds is the perfect tree over the lanes taken in bit-reversed order.
+ * Lane j < n holds v[j]; lanes j >= n hold nothing, and a node with one
+ * empty child passes the other child up unchanged (no addition). */
+static unsigned bitrev(unsigned i, int b) {
+  unsigned r = 0;
+  for (int k = 0; k < b; ++k) r |= ((i >> k) & 1u) << (b - 1 - k);
+  return r;
+}
+
+float dgo_tree_bitrev(const float* v, int n, int P) {
+  if (n <= 0) return 0.0f;
+  int b = 0;
+  while ((1 << b) < P) ++b;
+  P = 1 << b;
+  float* t = (float*)malloc(sizeof(float) * (size_t)P);
+  unsigned char* has = (unsigned char*)malloc((size_t)P);
+  for (int i = 0; i < P; ++i) {
+    unsigned j = bitrev((unsigned)i, b);
+    has[i] = (int)j < n;
+    t[i] = has[i] ? v[j] : 0.0f;
+  }
+  for (int w = P; w > 1; w /= 2) {
+    for (int k = 0; k < w / 2; ++k) {
+      float l = t[2 * k], r = t[2 * k + 1];
+      int hl = has[2 * k], hr = has[2 * k + 1];
+      t[k] = (hl && hr) ? l + r : (hl ? l : r);
+      has[k] = (unsigned char)(hl | hr);
+    }
+  }
+  float r = t[0];
+  free(t);
+  free(has);
+  return r;
+}
+
 static float chain(const float* v, int n, int bf16_round) {
   float s = v[0];
   for (int k = 1; k < n; ++k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }
@@ -620,15 +660,24 @@ int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
 
 /* -------------------------------------------------------- row reduction */
 
-/* Leaves of leaf_w contiguous elements, each folded in index order (the
- * in-thread level of Sec. 3.1); the leaves then meet in the balanced tree
- * (the lane and cross-warp levels, pinned to count-up order, Sec. 5.1).
+/* Leaves folded in index order (the in-thread level of Sec. 3.1): leaf j is
+ * elements [j leaf_w, (j+1) leaf_w) (contiguous layout), or, in the strided
+ * layout of Sec. 3.2.2 (GEMV: lanes take every count-th element), one of
+ * leaf_w lanes taking elements j, j + leaf_w, j + 2 leaf_w, ...  The leaves
+ * then meet in the balanced tree: in leaf order (the pinned count-up lane and
+ * cross-warp levels of Sec. 5.1) or, with fold_down, over the leaves in
+ * bit-reversed order (a butterfly counting its offsets down, over leaf_w
+ * lanes when strided, else over the leaf count rounded up to a power of two).
  * SUM: s = x0, s = s (+) xi.  SUMSQ: s = RN32(x0^2), then s = fma(xi, xi, s)
  * when fma = 1, else s (+) RN32(xi^2).  An empty row sums to +0. */
 int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
                int64_t cols, int nthreads) {
   if (p->leaf_w < 1 || rows < 0 || cols < 0) return 1;
-  int64_t L = (cols + p->leaf_w - 1) / p->leaf_w;
+  const int strided = p->leaf_strided != 0;
+  const int64_t W = p->leaf_w;
+  /* leaves holding at least one element */
+  const int64_t L = strided ? (cols < W ? cols : W) : (cols + W - 1) / W;
+  const int64_t lanes = strided ? W : L;
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel num_threads(nthreads)
   {
@@ -637,16 +686,21 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
     for (int64_t r = 0; r < rows; ++r) {
       const float* x = X + r * cols;
       for (int64_t l = 0; l < L; ++l) {
-        int64_t b = l * p->leaf_w, e = b + p->leaf_w < cols ? b + p->leaf_w : cols;
+        /* elements of leaf l: first b, then every step-th while < e */
+        int64_t b = strided ? l : l * W;
+        int64_t step = strided ? W : 1;
+        int64_t e = strided ? cols : (b + W < cols ? b + W : cols);
         float s = p->sumsq ? x[b] * x[b] : x[b];
-        for (int64_t k = b + 1; k < e; ++k) {
+        for (int64_t k = b + step; k < e; k += step) {
           if (!p->sumsq) s = s + x[k];
           else if (p->fma) s = fmaf(x[k], x[k], s);
           else { float q = x[k] * x[k]; s = s + q; }
         }
         leaves[l] = s;
       }
-      out[r] = (L == 0) ? 0.0f : dgo_tree(leaves, (int)L, 0);
+      if (L == 0) out[r] = 0.0f;
+      else if (p->fold_down) out[r] = dgo_tree_bitrev(leaves, (int)L, (int)lanes);
+      else out[r] = dgo_tree(leaves, (int)L, 0);
     }
     free(leaves);
   }

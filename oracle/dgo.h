@@ -70,6 +70,14 @@ typedef struct {
                              parts; 1 the axis is dealt in tiles of split_tile,
                              tile u going to part u mod S */
   int32_t split_tile;     /* width of a dealt tile (strided layout only) */
+  int32_t leaf_strided;   /* row reduction leaf layout (Sec. 3.2.2, GEMV: layout):
+                             0: leaf j holds elements [j leaf_w, (j+1) leaf_w);
+                             1: leaf_w leaves (lanes), leaf j holding elements
+                             j, j + leaf_w, j + 2 leaf_w, ... */
+  int32_t fold_down;      /* how the leaves meet (Sec. 3.2.2 GEMV, Sec. 5.1):
+                             0: balanced tree in leaf order (butterfly counting
+                             its offsets up); 1: balanced tree over the leaves in
+                             bit-reversed order (offsets counting down) */
 } dgo_params;
 
 /* Status: 0 ok, 1 invalid parameters, 3 shape inconsistent with the plan. */
@@ -90,6 +98,10 @@ int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
 /* Row reduction: out[r] for each of `rows` rows of X (row stride = cols). */
 int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
                int64_t cols, int nthreads);
+
+/* The count-down butterfly's tree over lanes 0..P-1 (P rounded up to a power
+ * of two), lane j < n holding v[j], lanes from n on empty.  Exposed for tests. */
+float dgo_tree_bitrev(const float* v, int n, int P);
 
 /* One accumulator update over n products a[t]*b[t] (n <= g; the rest of the
  * group is zero padding) under the given model and fma rule.  Exposed for

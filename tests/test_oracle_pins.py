@@ -315,6 +315,90 @@ def test_rowsum_special_cases():
     assert oracle.rowsum(dict(leaf_w=64), np.zeros((3, 0), np.float32)).tolist() == [0.0] * 3
 
 
+# ------------------------------------- strided leaves and the count-down fold
+
+
+def _butterfly(lanes, down):
+    """An xor butterfly simulated lane by lane in binary32 over len(lanes) (a
+    power of two) lanes: at each step every lane adds its partner's value, a
+    lane holding nothing (None) taking its partner's value as it is.  Offsets
+    run 1, 2, 4, .. (up) or in the reverse order (down).  Returns lane 0."""
+    P = len(lanes)
+    v = list(lanes)
+    offs = [1 << k for k in range(P.bit_length() - 1)]
+    for d in (offs[::-1] if down else offs):
+        nv = []
+        for lane in range(P):
+            a, b = v[lane], v[lane ^ d]
+            nv.append(b if a is None else a if b is None else np.float32(np.float32(a) + np.float32(b)))
+        v = nv
+    return v[0]
+
+
+def test_fold_down_hand_example():
+    """[2^24, 1, -2^24, 1] as four lanes: the count-up butterfly pairs 0-1
+    and 2-3 and gives 1; the count-down butterfly pairs 0-2 and 1-3 (a tree
+    over the lanes in bit-reversed order, Sec. 3.2.2 GEMV) and gives 2."""
+    X = np.array([[2.0 ** 24, 1, -2.0 ** 24, 1]], dtype=np.float32)
+    for layout, w in (("strided", 4), ("contiguous", 1)):
+        assert oracle.rowsum(dict(leaf_w=w, leaf_layout=layout), X)[0] == 1.0
+        assert oracle.rowsum(dict(leaf_w=w, leaf_layout=layout, lane_fold="down"), X)[0] == 2.0
+
+
+def test_folds_match_simulated_butterflies():
+    """The oracle's two trees equal the two butterflies simulated lane by lane,
+    for every lane count up to 256 and every number of occupied lanes (a -0
+    lane next to an empty one keeps its sign: nothing is added to it)."""
+    rng = np.random.default_rng(17)
+    for P in (1, 2, 4, 8, 16, 32, 64, 128, 256):
+        for n in sorted({1, 2, 3, P // 2 + 1, P - 1, P} - {0}):
+            if n > P:
+                continue
+            v = (rng.standard_normal(n) * np.exp2(rng.integers(-30, 30, n))).astype(np.float32)
+            lanes = list(v) + [None] * (P - n)
+            assert oracle.tree_bitrev(v, P).view(np.uint32) == _butterfly(lanes, True).view(np.uint32), (P, n)
+            assert oracle.tree(v).view(np.uint32) == _butterfly(lanes, False).view(np.uint32), (P, n)
+    negz = np.array([-0.0], dtype=np.float32)
+    assert oracle.tree_bitrev(negz, 4).view(np.uint32) == np.float32(-0.0).view(np.uint32)
+
+
+def test_strided_leaves_take_every_count_th_element():
+    """Two lanes over six elements: lane 0 folds x0, x2, x4 = 2^24, 1, 1 (each
+    1 lost to rounding) and lane 1 folds -2^24, 0, 0, so the row sums to 0;
+    contiguous leaves of three give (2^24 - 2^24 + 1) + (0 + 1 + 0) = 2."""
+    X = np.array([[2.0 ** 24, -2.0 ** 24, 1, 0, 1, 0]], dtype=np.float32)
+    for fold in ("up", "down"):
+        assert oracle.rowsum(dict(leaf_w=2, leaf_layout="strided", lane_fold=fold), X)[0] == 0.0
+    assert oracle.rowsum(dict(leaf_w=3), X)[0] == 2.0
+
+
+def test_strided_special_cases():
+    """One lane is plain sequential accumulation; as many lanes as elements is
+    the butterfly over the elements; small integers are exact in every order."""
+    X = inputs.lognormal_f32(5, (5, 300))
+    for fold in ("up", "down"):
+        one = oracle.rowsum(dict(leaf_w=1, leaf_layout="strided", lane_fold=fold), X)
+        for r in range(5):
+            assert one[r] == np.add.accumulate(X[r], dtype=np.float32)[-1]
+    Y = X[:, :200]
+    for fold, down in (("up", False), ("down", True)):
+        got = oracle.rowsum(dict(leaf_w=256, leaf_layout="strided", lane_fold=fold), Y)
+        for r in range(5):
+            assert got[r].view(np.uint32) == _butterfly(list(Y[r]) + [None] * 56, down).view(np.uint32)
+    # each lane a sequential chain over its own elements, then the butterfly
+    for W in (2, 8, 64):
+        for fold, down in (("up", False), ("down", True)):
+            got = oracle.rowsum(dict(leaf_w=W, leaf_layout="strided", lane_fold=fold), X)
+            for r in range(5):
+                lanes = [np.add.accumulate(X[r, j::W], dtype=np.float32)[-1] for j in range(W)]
+                assert got[r].view(np.uint32) == _butterfly(lanes, down).view(np.uint32), (W, fold)
+    Z = np.random.default_rng(6).integers(-1000, 1000, (4, 777)).astype(np.float32)
+    for W in (1, 4, 32, 64, 256):
+        for fold in ("up", "down"):
+            got = oracle.rowsum(dict(leaf_w=W, leaf_layout="strided", lane_fold=fold), Z)
+            assert got.tolist() == Z.sum(1, dtype=np.float64).tolist()
+
+
 # ------------------------------------------- structural identities of order
 
 

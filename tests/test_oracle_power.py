@@ -41,6 +41,11 @@ MUTANTS = {
     "strided tile width halved": ("const int64_t w = p->split_tile;", "const int64_t w = p->split_tile / 2;"),
     "bf16 conversion truncates": (
         "return (uint16_t)((u + 0x7fffu + lsb) >> 16);", "(void)lsb; return (uint16_t)(u >> 16);"),
+    "strided leaves take consecutive elements": ("int64_t step = strided ? W : 1;", "int64_t step = 1;"),
+    "count-down fold taken in leaf order": ("else if (p->fold_down) out[r] = dgo_tree_bitrev(leaves, (int)L, (int)lanes);",
+                                            "else if (p->fold_down) out[r] = dgo_tree(leaves, (int)L, 0);"),
+    "bit reversal one bit short": ("while ((1 << b) < P) ++b;", "while ((2 << b) < P) ++b;"),
+    "empty lane adds zero": ("t[k] = (hl && hr) ? l + r : (hl ? l : r);", "t[k] = l + r;"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
     "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
@@ -64,6 +69,10 @@ CHECKS = [
     lambda: pins.test_chunk_model_hand_examples(),
     lambda: pins.test_strided_layout_hand_walk("gfx950"),
     lambda: pins.test_strided_small_integers_are_exact(4, 64, 32, 4096),
+    lambda: pins.test_fold_down_hand_example(),
+    lambda: pins.test_folds_match_simulated_butterflies(),
+    lambda: pins.test_strided_leaves_take_every_count_th_element(),
+    lambda: pins.test_strided_special_cases(),
 ]
 
 
