@@ -162,12 +162,15 @@ def main():
     D_sw, D_dec, D_mlp = dg.Desc(**desc_sw), {c: dg.Desc(**v) for c, v in desc_dec.items()}, dg.Desc(**desc_mlp)
     D_sum = dg.Desc(leaf_w=64, reduce="sum")
     D_sq = dg.Desc(leaf_w=64, reduce="sumsq", fma=1)
+    # 256 strided lanes folded by the count-down butterfly (the GEMV lane tree)
+    D_st = dg.Desc(leaf_w=256, leaf_layout="strided", lane_fold="down")
 
     C_sw = {M: torch.empty((M, 4096), dtype=torch.bfloat16, device=dev) for M in inputs.SWEEP_M}
     C_dec = {c: torch.empty((8, 4096), dtype=torch.bfloat16, device=dev) for c in ("seq", "tree")}
     C_mlp = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
     out_sum = torch.empty(X.shape[0], dtype=torch.float32, device=dev)
     out_sq = torch.empty(X.shape[0], dtype=torch.float32, device=dev)
+    out_st = torch.empty(X.shape[0], dtype=torch.float32, device=dev)
 
     stream = torch.cuda.current_stream()
     sptr = int(stream.cuda_stream)
@@ -237,7 +240,7 @@ def main():
     # ------------------------------------------------------ row reduction
     rs_bytes = X.nbytes + X.shape[0] * 4
     rs = {}
-    for name, D, o in (("sum", D_sum, out_sum), ("sumsq", D_sq, out_sq)):
+    for name, D, o in (("sum", D_sum, out_sum), ("sumsq", D_sq, out_sq), ("sum_strided256_down", D_st, out_st)):
         for _ in range(args.warmup):
             dg.dg_rowsum(D, dX, o, stream=sptr)
         a, b = ev(), ev()
@@ -258,6 +261,11 @@ def main():
         for _ in range(3):
             torch.matmul(dA_sw, Bs_f)
             torch.nn.functional.silu(torch.matmul(dA_mlp, Bm_f) + dbias)
+            torch.matmul(dA_dec, Bd_f)
+            torch.sum(dX, 1)
+            torch.sum(dX * dX, 1)
+            for M in inputs.SWEEP_M:
+                torch.matmul(dA_sw_M[M], Bs_f)
         torch.cuda.synchronize()
 
         def timeit(fn, reps):
@@ -358,6 +366,10 @@ def main():
     got_rs = out_sum.cpu().numpy()[rows]
     checked += rows.size
     matched += int(np.sum(got_rs.view(np.uint32) == want_rs.view(np.uint32)))
+    want_st = oracle.rowsum(dict(leaf_w=256, leaf_layout="strided", lane_fold="down"), X[rows])
+    got_st = out_st.cpu().numpy()[rows]
+    checked += rows.size
+    matched += int(np.sum(got_st.view(np.uint32) == want_st.view(np.uint32)))
 
     # ------------------------------------------------------- CPU baseline
     ncpu = os.cpu_count() or 1

@@ -63,6 +63,8 @@ enum { DG_EPI_NONE = 0, DG_EPI_BIAS = 1, DG_EPI_BIAS_SILU = 2 };
 enum { DG_ROUND_FINAL = 0, DG_ROUND_PRE_ACT = 1 };
 enum { DG_OP_SUM = 0, DG_OP_SUMSQ = 1 };
 enum { DG_SPLIT_CONTIGUOUS = 0, DG_SPLIT_STRIDED = 1 };  /* layout of the split (Sec. 3.2.2) */
+enum { DG_LEAF_CONTIGUOUS = 0, DG_LEAF_STRIDED = 1 };    /* row-reduction leaf layout */
+enum { DG_FOLD_UP = 0, DG_FOLD_DOWN = 1 };               /* how the leaves meet */
 
 #define DG_MAX_SPLIT 64
 
@@ -106,6 +108,20 @@ typedef struct {
                              value is +0.  Requires n_cuts = 0, tail =
                              DG_TAIL_LAST and split_tile a multiple of tile_k */
   int32_t split_tile;     /* w, the dealt tile (strided layout; else 0) */
+  int32_t leaf_layout;    /* row reduction.  DG_LEAF_CONTIGUOUS: leaf j is the
+                             elements [j leaf_w, (j+1) leaf_w).  DG_LEAF_STRIDED:
+                             leaf_w leaves (lanes), leaf j folding elements j,
+                             j + leaf_w, j + 2 leaf_w, ... in index order (Sec.
+                             3.2.2 GEMV: lanes take every count-th element);
+                             this build realises leaf_w a power of two <= 256 */
+  int32_t lane_fold;      /* row reduction.  DG_FOLD_UP: the leaves meet in the
+                             balanced tree in leaf order (a butterfly whose
+                             offsets count up: the order Sec. 5.1 pins).
+                             DG_FOLD_DOWN: the balanced tree over the leaf_w
+                             lanes in bit-reversed order (a butterfly counting
+                             its offsets down, the default of common kernels,
+                             Sec. 3.2.2 GEMV); strided layout only.  An empty
+                             lane (leaf_w > cols) joins no addition */
 } dg_desc_params;
 
 typedef struct dg_desc dg_desc; /* opaque, immutable */
@@ -189,7 +205,9 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
 /* Static text for a status code. */
 const char* dg_strerror(dg_status s);
 
-/* Library version (major * 10000 + minor * 100 + patch). */
+/* Library version (major * 10000 + minor * 100 + patch).  0.2.0 (200) added
+ * dg_desc_params.leaf_layout / lane_fold and dg_knobs.split_n: a caller
+ * built against an earlier header must not pass its dg_knobs to this one. */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

@@ -51,6 +51,11 @@ void make_signature(dg_desc* d) {
                         p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
                         p.merge_dtype ? "bf16" : "f32", p.out_dtype ? "bf16" : "f32", p.epilogue,
                         p.epi_round ? "pre-act" : "final", p.leaf_w, p.reduce_op ? "sumsq" : "sum");
+  // the row reduction's leaf layout and lane fold, when not the defaults (one
+  // lane has nothing to fold)
+  if (p.leaf_layout == DG_LEAF_STRIDED && n > 0 && n < (int)sizeof d->sig)
+    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/leaf-strided%s",
+                       p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
   // one strided part is the whole axis, as one contiguous part is
   if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && n > 0 && n < (int)sizeof d->sig)
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/strided:%d", p.split_tile);
@@ -172,7 +177,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 100; }
+int32_t dg_version(void) { return 200; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {
@@ -211,6 +216,8 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
     return DG_ERR_INVALID;
   if (p->leaf_w < 1 || !in(p->reduce_op, DG_OP_SUM, DG_OP_SUMSQ)) return DG_ERR_INVALID;
   if (!in(p->split_layout, DG_SPLIT_CONTIGUOUS, DG_SPLIT_STRIDED)) return DG_ERR_INVALID;
+  if (!in(p->leaf_layout, DG_LEAF_CONTIGUOUS, DG_LEAF_STRIDED) || !in(p->lane_fold, DG_FOLD_UP, DG_FOLD_DOWN))
+    return DG_ERR_INVALID;
   if (p->split_layout == DG_SPLIT_STRIDED) {
     if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
       return DG_ERR_INVALID;
@@ -220,6 +227,11 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   }
   if (p->merge_dtype == DG_BF16 && p->partial_dtype != DG_BF16) return DG_ERR_UNSUPPORTED;
   if (p->epi_round == DG_ROUND_PRE_ACT && p->epilogue != DG_EPI_BIAS_SILU) return DG_ERR_UNSUPPORTED;
+  // strided leaves: up to 256 lanes, a power of two; the count-down fold only
+  // over strided lanes
+  if (p->leaf_layout == DG_LEAF_STRIDED && (p->leaf_w > 256 || (p->leaf_w & (p->leaf_w - 1))))
+    return DG_ERR_UNSUPPORTED;
+  if (p->lane_fold == DG_FOLD_DOWN && p->leaf_layout != DG_LEAF_STRIDED) return DG_ERR_UNSUPPORTED;
   dg_desc* d = new (std::nothrow) dg_desc;
   if (!d) return DG_ERR_NOMEM;
   std::memset(d, 0, sizeof *d);
@@ -432,6 +444,9 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, 
   a.leaf_w = d->p.leaf_w;
   a.sumsq = d->p.reduce_op == DG_OP_SUMSQ;
   a.fma = d->p.fma;
+  a.strided = d->p.leaf_layout == DG_LEAF_STRIDED;
+  a.down = d->p.lane_fold == DG_FOLD_DOWN;
+  if (a.strided && (rows + 3) / 4 > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
   if (dg::launch_rowsum(a, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
   return DG_OK;
 }

@@ -46,6 +46,7 @@ struct RowsumArgs {
   float* out;
   int64_t rows, cols;
   int32_t leaf_w, sumsq, fma;
+  int32_t strided, down;         // leaf layout and lane fold
 };
 
 // launchers (return hipSuccess or the launch error)

@@ -146,7 +146,149 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
   if (live && lane == 0) a.out[row] = have ? r : 0.0f;
 }
 
+// --------------------------------------------------------- strided leaves
+//
+// W lanes per row, W a power of two <= 256, lane j folding elements j, j + W,
+// j + 2W, ... in index order (Sec. 3.2.2, GEMV: lanes take every count-th
+// element).  A row belongs to G = min(W, 64) lanes of one wave (64 / G rows
+// per wave); lane q of the group holds the LPL = W / G leaves q LPL ..
+// q LPL + LPL - 1, whose elements at step t are the LPL consecutive floats
+// from t W + q LPL (one vector load when the row allows it), so every load
+// instruction of a wave reads whole contiguous runs.  A leaf without an
+// element holds -0, the exact identity of binary32 addition: it joins the
+// tree without changing a bit, as an elided addition would.  The tree is
+// the perfect tree over the W leaves: in leaf order (DOWN false) the
+// in-lane levels (the low leaf bits) come first and then the xor butterfly
+// with offsets 1, 2, .., G/2; in bit-reversed order (DOWN true) the
+// butterfly runs with offsets G/2, .., 1 first, then the in-lane levels
+// from the highest leaf bit down.
+template <int W, int OP, bool DOWN, bool VEC>
+__global__ __launch_bounds__(256) void rowsum_strided(RowsumArgs a) {
+  constexpr int G = W < 64 ? W : 64, LPL = W / G, R = 64 / G;
+  constexpr int U = LPL == 4 ? 8 : 16;   // steps whose loads are in flight together
+  constexpr int sumsq = OP > 0, fma = OP == 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = lane / G, q = lane % G;
+  const int64_t row = ((int64_t)blockIdx.x * RS_WAVES + wave) * R + g;
+  const bool live = row < a.rows;
+  const int64_t cols = a.cols, nfull = cols / W;
+  const float* x = a.X + (live ? row : 0) * cols + q * LPL;
+
+  auto load = [&](int64_t t, float* v) {
+    const float* p = x + t * W;
+    if constexpr (VEC && LPL == 4) {
+      const float4 f = *(const float4*)p;
+      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    } else if constexpr (VEC && LPL == 2) {
+      const float2 f = *(const float2*)p;
+      v[0] = f.x; v[1] = f.y;
+    } else {
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) v[u] = p[u];
+    }
+  };
+  float s[LPL];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) s[u] = -0.0f;
+  if (live && nfull > 0) {
+    float v0[LPL];
+    load(0, v0);
+#pragma unroll
+    for (int u = 0; u < LPL; ++u) s[u] = sumsq ? v0[u] * v0[u] : v0[u];
+    int64_t t = 1;
+    for (; t + U <= nfull; t += U) {
+      float v[U][LPL];
+#pragma unroll
+      for (int i = 0; i < U; ++i) load(t + i, v[i]);
+#pragma unroll
+      for (int i = 0; i < U; ++i)
+#pragma unroll
+        for (int u = 0; u < LPL; ++u) s[u] = leaf_step(s[u], v[i][u], sumsq, fma);
+    }
+    for (; t < nfull; ++t) {
+      float v[LPL];
+      load(t, v);
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = leaf_step(s[u], v[u], sumsq, fma);
+    }
+  }
+  // the short last step: elements nfull W + q LPL + u below cols
+  if (live) {
+#pragma unroll
+    for (int u = 0; u < LPL; ++u) {
+      if (nfull * W + q * LPL + u < cols) {
+        const float xv = x[nfull * W + u];
+        s[u] = nfull ? leaf_step(s[u], xv, sumsq, fma) : (sumsq ? xv * xv : xv);
+      }
+    }
+  }
+  float r;
+  if constexpr (!DOWN) {
+#pragma unroll
+    for (int h = 1; h < LPL; h <<= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
+    r = s[0];
+#pragma unroll
+    for (int m = 1; m < G; m <<= 1) r = r + __shfl_xor(r, m, 64);
+  } else {
+#pragma unroll
+    for (int m = G / 2; m >= 1; m >>= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], m, 64);
+#pragma unroll
+    for (int h = LPL / 2; h >= 1; h >>= 1)
+#pragma unroll
+      for (int u = 0; u < h; ++u) s[u] = s[u] + s[u + h];
+    r = s[0];
+  }
+  if (live && q == 0) a.out[row] = cols ? r : 0.0f;
+}
+
+template <int W, bool DOWN, bool VEC>
+static void launch_strided_t(const RowsumArgs& a, int op, hipStream_t st) {
+  constexpr int R = 64 / (W < 64 ? W : 64);
+  const int64_t per_block = (int64_t)RS_WAVES * R;
+  const dim3 grid((unsigned)((a.rows + per_block - 1) / per_block)), block(64 * RS_WAVES);
+  if (op == 0) hipLaunchKernelGGL((rowsum_strided<W, 0, DOWN, VEC>), grid, block, 0, st, a);
+  else if (op == 1) hipLaunchKernelGGL((rowsum_strided<W, 1, DOWN, VEC>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((rowsum_strided<W, 2, DOWN, VEC>), grid, block, 0, st, a);
+}
+
+template <int W, bool DOWN>
+static void launch_strided_w(const RowsumArgs& a, int op, hipStream_t st) {
+  constexpr int LPL = W > 64 ? W / 64 : 1;
+  if constexpr (LPL > 1) {
+    if ((((uintptr_t)a.X) % (4 * LPL) == 0) && (a.cols % LPL == 0)) {
+      launch_strided_t<W, DOWN, true>(a, op, st);
+      return;
+    }
+  }
+  launch_strided_t<W, DOWN, false>(a, op, st);
+}
+
+template <bool DOWN>
+static hipError_t launch_strided(const RowsumArgs& a, int op, hipStream_t st) {
+  switch (a.leaf_w) {
+    case 1: launch_strided_w<1, DOWN>(a, op, st); break;
+    case 2: launch_strided_w<2, DOWN>(a, op, st); break;
+    case 4: launch_strided_w<4, DOWN>(a, op, st); break;
+    case 8: launch_strided_w<8, DOWN>(a, op, st); break;
+    case 16: launch_strided_w<16, DOWN>(a, op, st); break;
+    case 32: launch_strided_w<32, DOWN>(a, op, st); break;
+    case 64: launch_strided_w<64, DOWN>(a, op, st); break;
+    case 128: launch_strided_w<128, DOWN>(a, op, st); break;
+    case 256: launch_strided_w<256, DOWN>(a, op, st); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t st) {
+  if (a.strided) {
+    const int op = !a.sumsq ? 0 : a.fma ? 1 : 2;
+    return a.down ? launch_strided<true>(a, op, st) : launch_strided<false>(a, op, st);
+  }
   const int64_t blocks = (a.rows + RS_WAVES - 1) / RS_WAVES;
   const bool vec = ((((uintptr_t)a.X) & 15) == 0) && (a.cols % 4 == 0);
   const dim3 grid((unsigned)blocks), block(64 * RS_WAVES);

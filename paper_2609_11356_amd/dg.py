@@ -36,7 +36,8 @@ class dg_desc_params(ctypes.Structure):
                 ("k_cuts", ctypes.POINTER(ctypes.c_int64))] + [
         (n, ctypes.c_int32) for n in ("tile_combine", "split_combine", "tail", "fma", "partial_dtype",
                                       "merge_dtype", "out_dtype", "epilogue", "epi_round", "leaf_w",
-                                      "reduce_op", "split_layout", "split_tile")]
+                                      "reduce_op", "split_layout", "split_tile", "leaf_layout",
+                                      "lane_fold")]
 
 
 class dg_knobs(ctypes.Structure):
@@ -90,12 +91,14 @@ class Desc:
     fma (0/1), partial / merge / out ("f32" | "bf16"), epilogue ("none" |
     "bias" | "bias_silu"), epi_round ("final" | "pre_act"), leaf_w,
     reduce ("sum" | "sumsq"), split_layout ("contiguous" | "strided"),
-    split_tile (the dealt tile of a strided split)."""
+    split_tile (the dealt tile of a strided split), leaf_layout ("contiguous" |
+    "strided": leaf_w lanes each taking every leaf_w-th element), lane_fold
+    ("up" | "down": the butterfly's offsets counting up or down)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
                     epilogue="none", epi_round="final", leaf_w=64, reduce="sum",
-                    split_layout="contiguous", split_tile=0)
+                    split_layout="contiguous", split_tile=0, leaf_layout="contiguous", lane_fold="up")
 
     def __init__(self, **fields):
         unknown = set(fields) - set(self.DEFAULTS) - {"model"}
@@ -130,6 +133,8 @@ class Desc:
         p.reduce_op = REDUCE[f["reduce"]]
         p.split_layout = {"contiguous": 0, "strided": 1}[f["split_layout"]]
         p.split_tile = int(f["split_tile"])
+        p.leaf_layout = {"contiguous": 0, "strided": 1}[f["leaf_layout"]]
+        p.lane_fold = {"up": 0, "down": 1}[f["lane_fold"]]
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:

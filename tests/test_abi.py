@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 100
+    assert dg.dg_version() == 200
     for s in range(7):
         assert dg.dg_strerror(s)
 
@@ -47,10 +47,37 @@ def test_version_and_strerror(dg):
     dict(split_k=4, split_layout="strided", split_tile=0),
     dict(split_k=3, split_layout="strided", split_tile=64, k_cuts=[64, 128]),
     dict(split_k=4, split_layout="strided", split_tile=64, tail="first"),
-    dict(split_k=4, split_tile=64)])                                     # a tile without the layout
+    dict(split_k=4, split_tile=64),                                      # a tile without the layout
+    dict(leaf_layout="diagonal"), dict(lane_fold="sideways")])
 def test_invalid_descriptors_rejected(dg, bad):
     with pytest.raises((dg.DgError, KeyError)):
         dg.Desc(**bad)
+
+
+def test_raw_field_values_checked(dg):
+    """Out-of-range enum values of the new fields are rejected at create."""
+    lib = dg.lib()
+    for field, value in (("leaf_layout", 2), ("lane_fold", -1)):
+        p = dg.dg_desc_params()
+        p.struct_size = ctypes.sizeof(p)
+        p.mma, p.tile_k, p.split_k, p.leaf_w = 1, 64, 1, 64
+        setattr(p, field, value)
+        h = ctypes.c_void_p()
+        assert lib.dg_desc_create(ctypes.byref(p), ctypes.byref(h)) == dg.DG_ERR_INVALID
+
+
+def test_strided_leaf_limits(dg):
+    """Strided leaves: a power of two up to 256 lanes; the count-down fold
+    needs strided lanes."""
+    for w in (3, 48, 512):
+        with pytest.raises(dg.DgError) as e:
+            dg.Desc(leaf_w=w, leaf_layout="strided")
+        assert e.value.status == dg.DG_ERR_UNSUPPORTED
+    with pytest.raises(dg.DgError) as e:
+        dg.Desc(leaf_w=64, lane_fold="down")
+    assert e.value.status == dg.DG_ERR_UNSUPPORTED
+    for w in (1, 2, 32, 64, 256):
+        dg.Desc(leaf_w=w, leaf_layout="strided", lane_fold="down")
 
 
 def test_unsupported_combinations(dg):
@@ -74,6 +101,13 @@ def test_signature_canonical(dg):
     assert st.endswith("strided:64") and st != dg.Desc(split_k=4).signature()
     # one strided part is the whole axis: the same order as one contiguous part
     assert dg.Desc(split_layout="strided", split_tile=64).signature() == dg.Desc().signature()
+    # leaf layout and fold appear when they are not the defaults; one lane has no fold
+    up = dg.Desc(leaf_w=256, leaf_layout="strided").signature()
+    down = dg.Desc(leaf_w=256, leaf_layout="strided", lane_fold="down").signature()
+    assert up.endswith("leaf-strided") and down.endswith("leaf-strided/fold-down")
+    assert dg.Desc(leaf_w=1, leaf_layout="strided", lane_fold="down").signature() == \
+        dg.Desc(leaf_w=1, leaf_layout="strided").signature()
+    assert up != dg.Desc(leaf_w=256).signature()
 
 
 def test_argument_errors_need_no_gpu(dg):

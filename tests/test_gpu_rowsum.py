@@ -65,3 +65,64 @@ def test_rowsum_independent_of_row_count(dg):
     a = run(dg, dict(leaf_w=64), X)
     b = run(dg, dict(leaf_w=64), X[:37].copy())
     assert np.array_equal(a[:37].view(np.uint32), b.view(np.uint32))
+
+
+# ------------------------------------- strided leaves, count-up / count-down fold
+
+STRIDED_W = [1, 2, 4, 8, 16, 32, 64, 128, 256]
+
+
+@pytest.mark.parametrize("W", STRIDED_W)
+@pytest.mark.parametrize("fold", ["up", "down"])
+def test_rowsum_strided_ragged(dg, W, fold):
+    """W lanes each taking every W-th element, folded by the count-up or the
+    count-down butterfly: fewer elements than lanes, partial last steps,
+    widths that defeat the vector loads (cols % 4 != 0), row counts that
+    leave a wave's row groups partly idle; SUM and both SUMSQ rules."""
+    for cols in (0, 1, 3, 5, W - 1, W, W + 1, 3 * W + 7, 1000, 4099):
+        if cols < 0:
+            continue
+        rows = 37
+        X = inputs.lognormal_f32(cols * 17 + W, (rows, cols))
+        for extra in (dict(), dict(reduce="sumsq", fma=1), dict(reduce="sumsq", fma=0)):
+            desc = dict(leaf_w=W, leaf_layout="strided", lane_fold=fold, **extra)
+            assert_bits_equal(run(dg, desc, X), oracle.rowsum(desc, X), "%s cols %d" % (desc, cols))
+
+
+@pytest.mark.parametrize("fold", ["up", "down"])
+def test_rowsum_strided_full_config(dg, fold):
+    """The 16384 x 8192 reduction with 256 strided lanes (the vector path),
+    every row against the oracle, and the count-down order differing from
+    the count-up one on this data."""
+    X = inputs.rowsum_input(8)
+    desc = dict(leaf_w=256, leaf_layout="strided", lane_fold=fold)
+    got = run(dg, desc, X)
+    assert_bits_equal(got, oracle.rowsum(desc, X), "rowsum %s" % desc)
+    if fold == "down":
+        up = oracle.rowsum(dict(desc, lane_fold="up"), X)
+        assert not np.array_equal(got.view(np.uint32), up.view(np.uint32))
+
+
+def test_rowsum_strided_unaligned_rows(dg):
+    """A row base 4 bytes past a 16-byte boundary takes the scalar loads and
+    gives the same bits."""
+    import torch
+    X = inputs.lognormal_f32(77, (9, 1024))
+    desc = dict(leaf_w=256, leaf_layout="strided", lane_fold="down")
+    want = oracle.rowsum(desc, X)
+    buf = torch.empty(X.size + 1, dtype=torch.float32, device="cuda")
+    buf[1:] = torch.from_numpy(X.reshape(-1)).cuda()
+    out = torch.full((9,), float("nan"), dtype=torch.float32, device="cuda")
+    d = dg.Desc(**desc)
+    dg.dg_rowsum(d, buf[1:].data_ptr(), out.data_ptr(), 9, 1024)
+    torch.cuda.synchronize()
+    assert_bits_equal(out.cpu().numpy(), want)
+
+
+def test_rowsum_strided_independent_of_row_count(dg):
+    X = inputs.rowsum_input(9, rows=1000, cols=2048)
+    for W in (32, 256):
+        desc = dict(leaf_w=W, leaf_layout="strided", lane_fold="down")
+        a = run(dg, desc, X)
+        b = run(dg, desc, X[:37].copy())
+        assert np.array_equal(a[:37].view(np.uint32), b.view(np.uint32)), W
