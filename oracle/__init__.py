@@ -48,7 +48,7 @@ class _Params(ctypes.Structure):
         (n, ctypes.c_int32) for n in (
             "tile_combine", "split_combine", "tail_first", "fma", "partial_bf16",
             "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq",
-            "split_strided", "split_tile", "leaf_strided", "fold_down")]
+            "split_strided", "split_tile", "leaf_strided", "fold_down", "norm_pre_round")]
 
 
 _lib = None
@@ -83,6 +83,7 @@ def _bind(path):
     L.dgo_gemm.argtypes = [P, vp, vp, vp, vp, i64, i64, i64, i32]
     L.dgo_gemm_at.argtypes = [P, vp, vp, vp, i64, i64, i64, vp, vp, i64, vp, i32]
     L.dgo_rowsum.argtypes = [P, vp, vp, i64, i64, i32]
+    L.dgo_rmsnorm.argtypes = [P, vp, vp, f32, vp, vp, i64, i64, i32]
     L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
     L.dgo_group_update.restype = f32
     L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
@@ -111,7 +112,7 @@ DEFAULTS = dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=1, k_cuts=Non
                 tile_combine="carry", split_combine="seq", tail="last", fma=1,
                 partial="f32", merge="f32", out="f32", epilogue="none",
                 epi_round="final", leaf_w=64, reduce="sum", split_layout="contiguous", split_tile=0,
-                leaf_layout="contiguous", lane_fold="up")
+                leaf_layout="contiguous", lane_fold="up", norm_round="final")
 
 
 def params(desc: dict):
@@ -142,6 +143,7 @@ def params(desc: dict):
     p.split_tile = int(d["split_tile"])
     p.leaf_strided = {"contiguous": 0, "strided": 1}[d["leaf_layout"]]
     p.fold_down = {"up": 0, "down": 1}[d["lane_fold"]]
+    p.norm_pre_round = {"final": 0, "pre_weight": 1}[d["norm_round"]]
     return p, cuts
 
 
@@ -204,6 +206,27 @@ def rowsum(desc, X, nthreads=None):
     if st:
         raise OracleError("dgo_rowsum status %d" % st)
     return out
+
+
+def rmsnorm(desc, X, w=None, eps=0.0, nthreads=None, with_rinv=False):
+    """RMS normalisation of each row of X (fp32) by its sum of squares in the
+    descriptor's order, scaled by w (bf16 bits, or None).  Returns fp32
+    values (out f32) or bf16 bits (out bf16); with_rinv adds each row's
+    reciprocal root."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    rows, cols = X.shape
+    d = dict(desc)
+    d["reduce"] = "sumsq"
+    p, keep = params(d)
+    w = None if w is None else _u16(w)
+    assert w is None or w.shape == (cols,)
+    Y = np.zeros((rows, cols), dtype=np.uint16 if p.out_bf16 else np.float32)
+    rinv = np.zeros(rows, dtype=np.float32)
+    st = lib().dgo_rmsnorm(ctypes.byref(p), X.ctypes.data, _ptr(w), float(np.float32(eps)), Y.ctypes.data,
+                           rinv.ctypes.data, rows, cols, nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_rmsnorm status %d" % st)
+    return (Y, rinv) if with_rinv else Y
 
 
 def plan_cuts(desc, K):

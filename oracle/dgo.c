@@ -670,14 +670,59 @@ int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
  * lanes when strided, else over the leaf count rounded up to a power of two).
  * SUM: s = x0, s = s (+) xi.  SUMSQ: s = RN32(x0^2), then s = fma(xi, xi, s)
  * when fma = 1, else s (+) RN32(xi^2).  An empty row sums to +0. */
-int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
-               int64_t cols, int nthreads) {
-  if (p->leaf_w < 1 || rows < 0 || cols < 0) return 1;
+static float row_reduce(const dgo_params* p, const float* x, int64_t cols, float* leaves) {
   const int strided = p->leaf_strided != 0;
   const int64_t W = p->leaf_w;
   /* leaves holding at least one element */
   const int64_t L = strided ? (cols < W ? cols : W) : (cols + W - 1) / W;
   const int64_t lanes = strided ? W : L;
+  for (int64_t l = 0; l < L; ++l) {
+    /* elements of leaf l: first b, then every step-th while < e */
+    int64_t b = strided ? l : l * W;
+    int64_t step = strided ? W : 1;
+    int64_t e = strided ? cols : (b + W < cols ? b + W : cols);
+    float s = p->sumsq ? x[b] * x[b] : x[b];
+    for (int64_t k = b + step; k < e; k += step) {
+      if (!p->sumsq) s = s + x[k];
+      else if (p->fma) s = fmaf(x[k], x[k], s);
+      else { float q = x[k] * x[k]; s = s + q; }
+    }
+    leaves[l] = s;
+  }
+  if (L == 0) return 0.0f;
+  if (p->fold_down) return dgo_tree_bitrev(leaves, (int)L, (int)lanes);
+  return dgo_tree(leaves, (int)L, 0);
+}
+
+static int64_t leaf_count(const dgo_params* p, int64_t cols) {
+  return p->leaf_strided ? (cols < p->leaf_w ? cols : p->leaf_w) : (cols + p->leaf_w - 1) / p->leaf_w;
+}
+
+int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
+               int64_t cols, int nthreads) {
+  if (p->leaf_w < 1 || rows < 0 || cols < 0) return 1;
+  const int64_t L = leaf_count(p, cols);
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    float* leaves = (float*)malloc(sizeof(float) * (size_t)(L > 0 ? L : 1));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t r = 0; r < rows; ++r) out[r] = row_reduce(p, X + r * cols, cols, leaves);
+    free(leaves);
+  }
+  return 0;
+}
+
+/* -------------------------------------------------- RMS normalisation */
+
+/* The step after the row's sum of squares (Sec. 3.1 tree; the normalisation
+ * kernels of the paper's evaluation): every rounding is one binary32
+ * operation, sqrt and division correctly rounded as IEEE 754 requires. */
+int dgo_rmsnorm(const dgo_params* p, const float* X, const uint16_t* w, float eps,
+                void* Y, float* rinv_out, int64_t rows, int64_t cols, int nthreads) {
+  if (p->leaf_w < 1 || rows < 0 || cols < 0 || !p->sumsq) return 1;
+  const int64_t L = leaf_count(p, cols);
+  const float n = (float)cols;
   if (nthreads < 1) nthreads = 1;
 #pragma omp parallel num_threads(nthreads)
   {
@@ -685,22 +730,19 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
 #pragma omp for schedule(dynamic, 16)
     for (int64_t r = 0; r < rows; ++r) {
       const float* x = X + r * cols;
-      for (int64_t l = 0; l < L; ++l) {
-        /* elements of leaf l: first b, then every step-th while < e */
-        int64_t b = strided ? l : l * W;
-        int64_t step = strided ? W : 1;
-        int64_t e = strided ? cols : (b + W < cols ? b + W : cols);
-        float s = p->sumsq ? x[b] * x[b] : x[b];
-        for (int64_t k = b + step; k < e; k += step) {
-          if (!p->sumsq) s = s + x[k];
-          else if (p->fma) s = fmaf(x[k], x[k], s);
-          else { float q = x[k] * x[k]; s = s + q; }
-        }
-        leaves[l] = s;
+      float s = row_reduce(p, x, cols, leaves);
+      float ms = s / n;
+      float v = ms + eps;
+      float q = sqrtf(v);
+      float rinv = 1.0f / q;
+      if (rinv_out) rinv_out[r] = rinv;
+      for (int64_t j = 0; j < cols; ++j) {
+        float y = x[j] * rinv;
+        if (p->norm_pre_round) y = rnbf(y);
+        if (w) y = y * dgo_bf16_to_f32(w[j]);
+        if (p->out_bf16) ((uint16_t*)Y)[r * cols + j] = dgo_f32_to_bf16(y);
+        else ((float*)Y)[r * cols + j] = y;
       }
-      if (L == 0) out[r] = 0.0f;
-      else if (p->fold_down) out[r] = dgo_tree_bitrev(leaves, (int)L, (int)lanes);
-      else out[r] = dgo_tree(leaves, (int)L, 0);
     }
     free(leaves);
   }

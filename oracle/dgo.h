@@ -78,6 +78,8 @@ typedef struct {
                              0: balanced tree in leaf order (butterfly counting
                              its offsets up); 1: balanced tree over the leaves in
                              bit-reversed order (offsets counting down) */
+  int32_t norm_pre_round; /* RMS normalisation: 1 = the normalised value is
+                             rounded to bf16 before the weight multiplies it */
 } dgo_params;
 
 /* Status: 0 ok, 1 invalid parameters, 3 shape inconsistent with the plan. */
@@ -98,6 +100,17 @@ int dgo_gemm_at(const dgo_params* p, const uint16_t* A, const uint16_t* B,
 /* Row reduction: out[r] for each of `rows` rows of X (row stride = cols). */
 int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
                int64_t cols, int nthreads);
+
+/* RMS normalisation of each row, on the row's sum of squares s taken in the
+ * descriptor's order (as dgo_rowsum with sumsq = 1):
+ *   ms = RN32(s / n)  (n = cols as binary32),  v = RN32(ms + eps),
+ *   q = RN32(sqrt(v)),  rinv = RN32(1 / q),  y_j = RN32(x_j * rinv),
+ *   out_j = RN_out(RN32(y'_j * w_j)) with y'_j = y_j, or RN_bf16(y_j) when
+ *   norm_pre_round;  without w (NULL), out_j = RN_out(y'_j).
+ * w holds cols bf16 values; Y receives rows*cols fp32 values (out_bf16 = 0)
+ * or bf16 bits.  rinv (if not NULL) receives each row's rinv. */
+int dgo_rmsnorm(const dgo_params* p, const float* X, const uint16_t* w, float eps,
+                void* Y, float* rinv, int64_t rows, int64_t cols, int nthreads);
 
 /* The count-down butterfly's tree over lanes 0..P-1 (P rounded up to a power
  * of two), lane j < n holding v[j], lanes from n on empty.  Exposed for tests. */

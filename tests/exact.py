@@ -47,3 +47,24 @@ def f(x) -> Fraction:
 
 def bf(h) -> Fraction:
     return Fraction(float((np.uint32(int(h)) << np.uint32(16)).view(np.float32)))
+
+
+def rn32_sqrt(q: Fraction) -> np.float32:
+    """RN32 of the exact square root of q >= 0: a binary32 candidate from the
+    float64 root, then moved while a neighbour is nearer, each comparison made
+    exactly on squares (an exact square root is never halfway between two
+    binary32 values, so no tie can occur)."""
+    import math
+    assert q >= 0
+    if q == 0:
+        return np.float32(0.0)
+    c = np.float32(math.sqrt(float(q)))
+    while True:
+        up = np.nextafter(c, np.float32(np.inf))
+        dn = np.nextafter(c, np.float32(0))
+        if ((f(c) + f(up)) / 2) ** 2 < q:
+            c = up
+        elif ((f(c) + f(dn)) / 2) ** 2 > q:
+            c = dn
+        else:
+            return c

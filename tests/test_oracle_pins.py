@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from paper_2609_11356_amd import inputs
-from tests.exact import bf, f, rn32
+from tests.exact import bf, f, rn32, rn32_sqrt
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 ONE = np.uint16(0x3F80)
@@ -714,3 +714,92 @@ def test_strided_layout_rejects_what_it_cannot_express():
         d.update(bad)
         with pytest.raises(oracle.OracleError):
             oracle.gemm(d, A, B)
+
+
+# ------------------------------------------------------ RMS normalisation
+
+
+def test_rn32_sqrt_helper_matches_numpy():
+    """The exact-comparison root used below against numpy's binary32 sqrt
+    (correctly rounded) over values of every exponent."""
+    rng = np.random.default_rng(29)
+    v = (rng.uniform(1, 2, 3000) * np.exp2(rng.integers(-140, 120, 3000))).astype(np.float32)
+    for x in v:
+        assert rn32_sqrt(f(x)).view(np.uint32) == np.sqrt(x).view(np.uint32), x
+
+
+def test_rmsnorm_hand_example():
+    """Row [3, 4]: s = 9 + 16 = 25 and the mean 12.5 are exact; the root and
+    the reciprocal are each the exact value rounded once (exact rationals);
+    eps joins before the root."""
+    X = np.array([[3.0, 4.0]], dtype=np.float32)
+    for eps, v in ((0.0, Fraction(25, 2)), (0.5, Fraction(13))):
+        Y, rinv = oracle.rmsnorm(dict(leaf_w=64), X, eps=eps, with_rinv=True)
+        q = rn32_sqrt(v)
+        r = rn32(1 / f(q))
+        assert rinv[0].view(np.uint32) == r.view(np.uint32), eps
+        assert Y[0, 0] == rn32(3 * f(r)) and Y[0, 1] == rn32(4 * f(r))
+
+
+def test_rmsnorm_closed_forms():
+    """Rows of +-2^e over a power-of-two width: mean square 4^e, root 2^e,
+    so the normalised values are +-1 exactly and the output is +-w; with
+    eps = 3 * 4^e the root doubles and the output is +-w/2."""
+    rng = np.random.default_rng(23)
+    for cols in (1, 2, 64, 256, 4096):
+        for e in (-20, -3, 0, 7, 20):
+            sign = rng.choice([-1.0, 1.0], (3, cols)).astype(np.float32)
+            X = (sign * np.float32(2.0 ** e)).astype(np.float32)
+            w = inputs.normal_bf16(cols + e + 100, (cols,), 1.0)
+            wf = (w.astype(np.uint32) << 16).view(np.float32)
+            for layout, lw in (("contiguous", 64), ("strided", 256), ("strided", 1)):
+                d = dict(leaf_w=lw, leaf_layout=layout)
+                assert np.array_equal(oracle.rmsnorm(d, X), sign), (cols, e, layout)
+                assert np.array_equal(oracle.rmsnorm(d, X, w), sign * wf)
+                assert np.array_equal(oracle.rmsnorm(d, X, w, eps=3 * 4.0 ** e), sign * wf / 2)
+                assert np.array_equal(oracle.rmsnorm(dict(d, out="bf16"), X, w),
+                                      np.where(sign > 0, w, w ^ 0x8000).astype(np.uint16))
+
+
+def test_rmsnorm_within_fp64_bound():
+    """Log-normal rows against float64: the sum of squares of positive terms
+    carries a relative error below 70 * 2^-24 (leaf of 64 plus the tree over
+    128 leaves), the mean, root and reciprocal three more roundings, the two
+    products two more: everything well inside 2^-17 relative."""
+    X = inputs.lognormal_f32(31, (64, 8192))
+    w = inputs.normal_bf16(32, (8192,), 1.0)
+    wf = (w.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    eps = 1e-6
+    X64 = X.astype(np.float64)
+    ref = X64 / np.sqrt((X64 ** 2).mean(1, keepdims=True) + np.float64(np.float32(eps))) * wf
+    for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down"),
+              dict(leaf_w=64, fma=0)):
+        got = oracle.rmsnorm(d, X, w, eps=eps).astype(np.float64)
+        assert np.all(np.abs(got - ref) <= 2.0 ** -17 * np.abs(ref) + 1e-38), d
+
+
+def test_rmsnorm_follows_the_rowsum_order_and_rounding_points():
+    """The reciprocal root is taken from exactly the row sum of squares the
+    descriptor fixes (dg_rowsum's order), and the bf16 rounding sits before
+    the weight multiply only when asked (norm_round = pre_weight); the
+    element step recomputed with numpy binary32 products and torch's bf16
+    conversion."""
+    import torch
+    X = inputs.lognormal_f32(33, (16, 1000))
+    w = inputs.normal_bf16(34, (1000,), 1.0)
+    wf = (w.astype(np.uint32) << 16).view(np.float32)
+    d = dict(leaf_w=128, leaf_layout="strided", lane_fold="down", fma=0)
+    s = oracle.rowsum(dict(d, reduce="sumsq"), X)
+    Y, rinv = oracle.rmsnorm(d, X, w, eps=1e-5, with_rinv=True)
+    for r in range(16):
+        v = rn32(f(rn32(f(s[r]) / 1000)) + f(np.float32(1e-5)))
+        assert rinv[r] == rn32(1 / f(rn32_sqrt(f(v))))
+    y = (X * rinv[:, None]).astype(np.float32)
+    assert np.array_equal(Y, (y * wf).astype(np.float32))
+    bf = lambda a: torch.from_numpy(a).to(torch.bfloat16).float().numpy()
+    P = oracle.rmsnorm(dict(d, norm_round="pre_weight"), X, w, eps=1e-5)
+    assert np.array_equal(P, (bf(y) * wf).astype(np.float32))
+    assert not np.array_equal(P, Y)
+    Pb = oracle.rmsnorm(dict(d, norm_round="pre_weight", out="bf16"), X, w, eps=1e-5)
+    want = torch.from_numpy((bf(y) * wf).astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy()
+    assert np.array_equal(Pb.view(np.int16), want)

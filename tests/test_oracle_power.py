@@ -42,10 +42,18 @@ MUTANTS = {
     "bf16 conversion truncates": (
         "return (uint16_t)((u + 0x7fffu + lsb) >> 16);", "(void)lsb; return (uint16_t)(u >> 16);"),
     "strided leaves take consecutive elements": ("int64_t step = strided ? W : 1;", "int64_t step = 1;"),
-    "count-down fold taken in leaf order": ("else if (p->fold_down) out[r] = dgo_tree_bitrev(leaves, (int)L, (int)lanes);",
-                                            "else if (p->fold_down) out[r] = dgo_tree(leaves, (int)L, 0);"),
+    "count-down fold taken in leaf order": ("if (p->fold_down) return dgo_tree_bitrev(leaves, (int)L, (int)lanes);",
+                                            "if (p->fold_down) return dgo_tree(leaves, (int)L, 0);"),
     "bit reversal one bit short": ("while ((1 << b) < P) ++b;", "while ((2 << b) < P) ++b;"),
     "empty lane adds zero": ("t[k] = (hl && hr) ? l + r : (hl ? l : r);", "t[k] = l + r;"),
+    "mean over cols - 1": ("const float n = (float)cols;", "const float n = (float)(cols - 1);"),
+    "eps added after the root": ("float v = ms + eps;\n      float q = sqrtf(v);",
+                                 "float v = ms;\n      float q = sqrtf(v) + eps;"),
+    "weight before the bf16 rounding": (
+        "if (p->norm_pre_round) y = rnbf(y);\n        if (w) y = y * dgo_bf16_to_f32(w[j]);",
+        "if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (p->norm_pre_round) y = rnbf(y);"),
+    "rmsnorm sums the row in index order": ("float s = row_reduce(p, x, cols, leaves);",
+                                            "float s = 0.0f;\n      for (int64_t k = 0; k < cols; ++k) s = fmaf(x[k], x[k], s);"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
     "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
@@ -73,6 +81,9 @@ CHECKS = [
     lambda: pins.test_folds_match_simulated_butterflies(),
     lambda: pins.test_strided_leaves_take_every_count_th_element(),
     lambda: pins.test_strided_special_cases(),
+    lambda: pins.test_rmsnorm_hand_example(),
+    lambda: pins.test_rmsnorm_closed_forms(),
+    lambda: pins.test_rmsnorm_follows_the_rowsum_order_and_rounding_points(),
 ]
 
 
