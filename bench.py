@@ -164,6 +164,13 @@ def main():
     D_sq = dg.Desc(leaf_w=64, reduce="sumsq", fma=1)
     # 256 strided lanes folded by the count-down butterfly (the GEMV lane tree)
     D_st = dg.Desc(leaf_w=256, leaf_layout="strided", lane_fold="down")
+    # RMS normalisation on that order, bf16 weight and output, bf16 rounding before the weight
+    desc_rms = dict(leaf_w=256, leaf_layout="strided", lane_fold="down", reduce="sumsq", out="bf16",
+                    norm_round="pre_weight")
+    D_rms = dg.Desc(**desc_rms)
+    w_rms = inputs.normal_bf16(10, (X.shape[1],), 1.0)
+    dw_rms = d_bf16(w_rms)
+    Y_rms = torch.empty(X.shape, dtype=torch.bfloat16, device=dev)
 
     C_sw = {M: torch.empty((M, 4096), dtype=torch.bfloat16, device=dev) for M in inputs.SWEEP_M}
     C_dec = {c: torch.empty((8, 4096), dtype=torch.bfloat16, device=dev) for c in ("seq", "tree")}
@@ -253,6 +260,22 @@ def main():
         ms = a.elapsed_time(b) / args.steps
         rs[name] = {"ms": round(ms, 4), "GB/s": round(rs_bytes / ms / 1e6, 1),
                     "frac_hbm": round(rs_bytes / ms / 1e6 / PEAK_HBM_GBS, 4)}
+    # RMS normalisation: X read and Y written once (algorithmic), two launches
+    rms_bytes = X.nbytes + X.size * 2 + X.shape[1] * 2
+    for _ in range(args.warmup):
+        dg.dg_rmsnorm(D_rms, dX, dw_rms, 1e-5, Y_rms, stream=sptr)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(args.steps):
+        dg.dg_rmsnorm(D_rms, dX, dw_rms, 1e-5, Y_rms, stream=sptr)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / args.steps
+    rs["rmsnorm_bf16"] = {"ms": round(ms, 4), "GB/s": round(rms_bytes / ms / 1e6, 1),
+                          "frac_hbm": round(rms_bytes / ms / 1e6 / PEAK_HBM_GBS, 4),
+                          "what": "sum of squares over 256 strided lanes (count-down fold), then "
+                                  "y = x / sqrt(mean + 1e-5), bf16, times the bf16 weight; bytes = X + Y once"}
 
     # ---------------------------------------------- free-order references
     free = {}
@@ -264,6 +287,7 @@ def main():
             torch.matmul(dA_dec, Bd_f)
             torch.sum(dX, 1)
             torch.sum(dX * dX, 1)
+            (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16) * dw_rms
             for M in inputs.SWEEP_M:
                 torch.matmul(dA_sw_M[M], Bs_f)
         torch.cuda.synchronize()
@@ -283,6 +307,8 @@ def main():
                        args.steps)
         t_rs = timeit(lambda i: torch.sum(dX, 1), args.steps)
         t_rs2 = timeit(lambda i: torch.sum(dX * dX, 1), args.steps)
+        t_rms = timeit(lambda i: (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16)
+                       * dw_rms, args.steps)
         t_sw_m = {M: timeit(lambda i, M=M: torch.matmul(dA_sw_M[M], dB_sw[i % len(dB_sw)]), args.steps)
                   for M in inputs.SWEEP_M}
         free = {"sweep_ms": round(t_sw, 4), "decode_ms_per_launch": round(t_dec, 4), "mlp_ms": round(t_mlp, 4),
@@ -293,10 +319,13 @@ def main():
                 "cost_rowsum": round(rs["sum"]["ms"] / t_rs, 3),
                 "rowsum_sumsq_ms": round(t_rs2, 4),
                 "cost_rowsum_sumsq": round(rs["sumsq"]["ms"] / t_rs2, 3),
+                "rmsnorm_ms": round(t_rms, 4),
+                "cost_rmsnorm": round(rs["rmsnorm_bf16"]["ms"] / t_rms, 3),
                 "sweep_ms_by_M": {str(M): round(t, 4) for M, t in t_sw_m.items()},
                 "cost_sweep_by_M": {str(M): round(shapes["sweep_M%d" % M]["us_mean"] * 1e-3 / t, 3)
                                     for M, t in t_sw_m.items()},
-                "what": "torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum on the same shapes; cost = t_dg / t_free"}
+                "what": ("torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum / x * rsqrt(mean(x^2) + eps) "
+                         "-> bf16 * w on the same shapes; cost = t_dg / t_free")}
     except Exception as exc:  # the library under test never depends on this
         free = {"error": repr(exc)}
 
@@ -370,6 +399,11 @@ def main():
     got_st = out_st.cpu().numpy()[rows]
     checked += rows.size
     matched += int(np.sum(got_st.view(np.uint32) == want_st.view(np.uint32)))
+    rr = rows[:64]
+    want_rms = oracle.rmsnorm(desc_rms, X[rr], w_rms, eps=1e-5)
+    got_rms = host(Y_rms)[rr]
+    checked += want_rms.size
+    matched += int(np.sum(got_rms == want_rms))
 
     # ------------------------------------------------------- CPU baseline
     ncpu = os.cpu_count() or 1

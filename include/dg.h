@@ -65,6 +65,7 @@ enum { DG_OP_SUM = 0, DG_OP_SUMSQ = 1 };
 enum { DG_SPLIT_CONTIGUOUS = 0, DG_SPLIT_STRIDED = 1 };  /* layout of the split (Sec. 3.2.2) */
 enum { DG_LEAF_CONTIGUOUS = 0, DG_LEAF_STRIDED = 1 };    /* row-reduction leaf layout */
 enum { DG_FOLD_UP = 0, DG_FOLD_DOWN = 1 };               /* how the leaves meet */
+enum { DG_NORM_FINAL = 0, DG_NORM_PRE_WEIGHT = 1 };      /* RMS-norm rounding point */
 
 #define DG_MAX_SPLIT 64
 
@@ -122,6 +123,11 @@ typedef struct {
                              its offsets down, the default of common kernels,
                              Sec. 3.2.2 GEMV); strided layout only.  An empty
                              lane (leaf_w > cols) joins no addition */
+  int32_t norm_round;     /* dg_rmsnorm.  DG_NORM_FINAL: the normalised value
+                             meets the weight at binary32; DG_NORM_PRE_WEIGHT:
+                             it is rounded to bf16 first (an unfused "normalise
+                             in fp32, cast to bf16, scale by the bf16 weight"
+                             pair) */
 } dg_desc_params;
 
 typedef struct dg_desc dg_desc; /* opaque, immutable */
@@ -203,6 +209,26 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
                     int64_t cols, void* stream);
 
 /* Static text for a status code. */
+/* Root-mean-square normalisation of each row, on the row's sum of squares
+ * in the descriptor's order (exactly the value dg_rowsum returns for the
+ * descriptor with reduce_op DG_OP_SUMSQ: leaf_w, leaf_layout, lane_fold and
+ * fma apply; the descriptor's reduce_op must be DG_OP_SUMSQ).  Then, each
+ * step one IEEE binary32 operation (sqrt and division correctly rounded):
+ *   ms = s / n (n = cols as binary32),  v = ms + eps,  q = sqrt(v),
+ *   rinv = 1 / q,  y_j = x_j * rinv,
+ *   y'_j = y_j (DG_NORM_FINAL) or RN_bf16(y_j) (DG_NORM_PRE_WEIGHT),
+ *   out_j = RN_out(y'_j * w_j), or RN_out(y'_j) when w is NULL.
+ * These are the steps around the pinned reduction that normalisation kernels
+ * run (the paper's evaluation, Sec. 7: rmsnorm).
+ *   X: device, rows x cols fp32 row-major;  w: device, cols bf16 or NULL;
+ *   Y: device, rows x cols of out_dtype (written, never read; may not
+ *   overlap X).  rows = 0 or cols = 0 is a no-op.  Uses a library-owned
+ *   workspace of rows fp32 values per (device, stream) (DG_ERR_NOMEM if it
+ *   cannot grow); two launches on `stream`.  Errors as dg_rowsum, plus
+ *   DG_ERR_INVALID for a descriptor whose reduce_op is not DG_OP_SUMSQ. */
+dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
+                     int64_t rows, int64_t cols, void* stream);
+
 const char* dg_strerror(dg_status s);
 
 /* Library version (major * 10000 + minor * 100 + patch).  0.2.0 (200) added

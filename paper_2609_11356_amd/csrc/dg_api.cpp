@@ -56,6 +56,8 @@ void make_signature(dg_desc* d) {
   if (p.leaf_layout == DG_LEAF_STRIDED && n > 0 && n < (int)sizeof d->sig)
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/leaf-strided%s",
                        p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
+  if (p.norm_round == DG_NORM_PRE_WEIGHT && n > 0 && n < (int)sizeof d->sig)
+    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/norm-pre-weight");
   // one strided part is the whole axis, as one contiguous part is
   if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && n > 0 && n < (int)sizeof d->sig)
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/strided:%d", p.split_tile);
@@ -218,6 +220,7 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   if (!in(p->split_layout, DG_SPLIT_CONTIGUOUS, DG_SPLIT_STRIDED)) return DG_ERR_INVALID;
   if (!in(p->leaf_layout, DG_LEAF_CONTIGUOUS, DG_LEAF_STRIDED) || !in(p->lane_fold, DG_FOLD_UP, DG_FOLD_DOWN))
     return DG_ERR_INVALID;
+  if (!in(p->norm_round, DG_NORM_FINAL, DG_NORM_PRE_WEIGHT)) return DG_ERR_INVALID;
   if (p->split_layout == DG_SPLIT_STRIDED) {
     if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
       return DG_ERR_INVALID;
@@ -428,15 +431,9 @@ dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bi
   return dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
 }
 
-dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, int64_t cols,
-                    void* stream) {
-  if (!d) return DG_ERR_INVALID;
-  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
-  if (rows == 0) return DG_OK;
-  if (!out || (cols > 0 && !X)) return DG_ERR_INVALID;
-  if (!aligned(out, 4) || (X && !aligned(X, 4))) return DG_ERR_ALIGN;
-  if ((rows + 3) / 4 > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+static dg::RowsumArgs rowsum_args(const dg_desc* d, const float* X, float* out, int64_t rows, int64_t cols) {
   dg::RowsumArgs a;
+  std::memset(&a, 0, sizeof a);
   a.X = X;
   a.out = out;
   a.rows = rows;
@@ -446,8 +443,57 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, 
   a.fma = d->p.fma;
   a.strided = d->p.leaf_layout == DG_LEAF_STRIDED;
   a.down = d->p.lane_fold == DG_FOLD_DOWN;
-  if (a.strided && (rows + 3) / 4 > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  return a;
+}
+
+dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, int64_t cols,
+                    void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
+  if (rows == 0) return DG_OK;
+  if (!out || (cols > 0 && !X)) return DG_ERR_INVALID;
+  if (!aligned(out, 4) || (X && !aligned(X, 4))) return DG_ERR_ALIGN;
+  if ((rows + 3) / 4 > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  dg::RowsumArgs a = rowsum_args(d, X, out, rows, cols);
   if (dg::launch_rowsum(a, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
+dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
+                     int64_t rows, int64_t cols, void* stream) {
+  if (!d || d->p.reduce_op != DG_OP_SUMSQ) return DG_ERR_INVALID;
+  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
+  if (rows == 0 || cols == 0) return DG_OK;
+  if (!X || !Y) return DG_ERR_INVALID;
+  const bool out_bf16 = d->p.out_dtype == DG_BF16;
+  if (!aligned(X, 4) || !aligned(Y, out_bf16 ? 2 : 4) || (w && !aligned(w, 2))) return DG_ERR_ALIGN;
+  if (rows > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  hipStream_t st = (hipStream_t)stream;
+  dg::RowsumArgs a = rowsum_args(d, X, nullptr, rows, cols);
+  a.rms = 1;
+  a.eps = eps;
+  dg::NormArgs n;
+  n.X = X;
+  n.rinv = nullptr;
+  n.w = (const uint16_t*)w;
+  n.Y = Y;
+  n.rows = rows;
+  n.cols = cols;
+  n.out_bf16 = out_bf16;
+  n.pre_round = d->p.norm_round == DG_NORM_PRE_WEIGHT;
+  // one pass when the row fits in registers, else the reciprocal roots to a
+  // workspace and a scaling pass
+  if (dg::rmsnorm_fused_ok(a, n)) {
+    if (dg::launch_rmsnorm_fused(a, n, st) != hipSuccess) return DG_ERR_HIP;
+    return DG_OK;
+  }
+  void* ws = nullptr;
+  dg_status s = get_workspace(st, (size_t)rows * sizeof(float), &ws);
+  if (s != DG_OK) return s;
+  a.out = (float*)ws;
+  n.rinv = (const float*)ws;
+  if (dg::launch_rowsum(a, st) != hipSuccess) return DG_ERR_HIP;
+  if (dg::launch_rmsnorm_scale(n, st) != hipSuccess) return DG_ERR_HIP;
   return DG_OK;
 }
 

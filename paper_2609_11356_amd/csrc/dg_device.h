@@ -66,4 +66,14 @@ __device__ __forceinline__ float silu_f32(float z) {
   return z / (1.0f + e);
 }
 
+// RMS-norm reciprocal root of a row's sum of squares s over n = cols
+// elements: ms = s / n, v = ms + eps, q = sqrt(v), 1 / q, each one correctly
+// rounded binary32 operation (the build keeps IEEE division and sqrt).
+__device__ __forceinline__ float rms_inv(float s, int64_t cols, float eps) {
+  const float ms = s / (float)cols;
+  const float v = ms + eps;
+  const float q = __builtin_sqrtf(v);
+  return 1.0f / q;
+}
+
 }  // namespace dg

@@ -47,6 +47,17 @@ struct RowsumArgs {
   int64_t rows, cols;
   int32_t leaf_w, sumsq, fma;
   int32_t strided, down;         // leaf layout and lane fold
+  int32_t rms;                   // 1: out[row] = the RMS-norm reciprocal root of the sum
+  float eps;
+};
+
+struct NormArgs {
+  const float* X;
+  const float* rinv;             // per row
+  const uint16_t* w;             // bf16 weight or null
+  void* Y;
+  int64_t rows, cols;
+  int32_t out_bf16, pre_round;
 };
 
 // launchers (return hipSuccess or the launch error)
@@ -63,5 +74,8 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int dep
 bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
+hipError_t launch_rmsnorm_scale(const NormArgs& a, hipStream_t s);
+bool rmsnorm_fused_ok(const RowsumArgs& r, const NormArgs& a);
+hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
 
 }  // namespace dg

@@ -143,7 +143,10 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
       have = true;
     }
   }
-  if (live && lane == 0) a.out[row] = have ? r : 0.0f;
+  if (live && lane == 0) {
+    const float v = have ? r : 0.0f;
+    a.out[row] = a.rms ? rms_inv(v, cols, a.eps) : v;
+  }
 }
 
 // --------------------------------------------------------- strided leaves
@@ -242,7 +245,10 @@ __global__ __launch_bounds__(256) void rowsum_strided(RowsumArgs a) {
       for (int u = 0; u < h; ++u) s[u] = s[u] + s[u + h];
     r = s[0];
   }
-  if (live && q == 0) a.out[row] = cols ? r : 0.0f;
+  if (live && q == 0) {
+    const float v = cols ? r : 0.0f;
+    a.out[row] = a.rms ? rms_inv(v, cols, a.eps) : v;
+  }
 }
 
 template <int W, bool DOWN, bool VEC>
@@ -281,6 +287,251 @@ static hipError_t launch_strided(const RowsumArgs& a, int op, hipStream_t st) {
     case 256: launch_strided_w<256, DOWN>(a, op, st); break;
     default: return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ RMS-norm scaling
+//
+// out_j = RN_out(y'_j * w_j), y_j = x_j * rinv[row], y'_j = y_j or its bf16
+// rounding: elementwise once the row's reciprocal root is known.  One
+// workgroup per row; with VEC every thread takes 4 consecutive columns per
+// step (16-byte loads of X, 8- or 16-byte stores of Y).
+template <bool VEC>
+__global__ __launch_bounds__(256) void rmsnorm_scale(NormArgs a) {
+  const int64_t row = blockIdx.x, cols = a.cols;
+  const float r = a.rinv[row];
+  const float* x = a.X + row * cols;
+  auto one = [&](float xv, int64_t j) {
+    float y = xv * r;
+    if (a.pre_round) y = round_bf16(y);
+    if (a.w) y = y * bf16_f32(a.w[j]);
+    return y;
+  };
+  if (VEC) {
+    // U steps of 16-byte loads in flight before any is used
+    constexpr int U = 8;
+    for (int64_t j0 = 4 * (int64_t)threadIdx.x; j0 < cols; j0 += 1024 * U) {
+      float4 xv[U];
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        const int64_t j = j0 + 1024 * i;
+        xv[i] = j < cols ? *(const float4*)(x + j) : float4{0.f, 0.f, 0.f, 0.f};
+      }
+#pragma unroll
+      for (int i = 0; i < U; ++i) {
+        const int64_t j = j0 + 1024 * i;
+        if (j >= cols) break;
+        float y0, y1, y2, y3;
+        if (a.w && ((uintptr_t)a.w) % 8 == 0) {
+          // the four weights in one 8-byte load
+          const uint2 q = *(const uint2*)&a.w[j];
+          const float xs[4] = {xv[i].x, xv[i].y, xv[i].z, xv[i].w};
+          const uint32_t wb[4] = {q.x << 16, q.x & 0xffff0000u, q.y << 16, q.y & 0xffff0000u};
+          float ys[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            float y = xs[u] * r;
+            if (a.pre_round) y = round_bf16(y);
+            ys[u] = y * bits_f32(wb[u]);
+          }
+          y0 = ys[0]; y1 = ys[1]; y2 = ys[2]; y3 = ys[3];
+        } else {
+          y0 = one(xv[i].x, j); y1 = one(xv[i].y, j + 1); y2 = one(xv[i].z, j + 2); y3 = one(xv[i].w, j + 3);
+        }
+        if (a.out_bf16) {
+          const uint32_t lo = (uint32_t)f32_bf16(y0) | ((uint32_t)f32_bf16(y1) << 16);
+          const uint32_t hi = (uint32_t)f32_bf16(y2) | ((uint32_t)f32_bf16(y3) << 16);
+          *(uint2*)&((uint16_t*)a.Y)[row * cols + j] = uint2{lo, hi};
+        } else {
+          *(float4*)&((float*)a.Y)[row * cols + j] = float4{y0, y1, y2, y3};
+        }
+      }
+    }
+  } else {
+    for (int64_t j = threadIdx.x; j < cols; j += 256) {
+      const float y = one(x[j], j);
+      if (a.out_bf16) ((uint16_t*)a.Y)[row * cols + j] = f32_bf16(y);
+      else ((float*)a.Y)[row * cols + j] = y;
+    }
+  }
+}
+
+// One pass for strided lanes (W = 64, 128, 256) and rows of at most 8192
+// elements: one wave per row loads the whole row into registers (lane q
+// holds the LPL = W / 64 consecutive floats of every step, at most 128 per
+// lane), folds its leaves and meets the other lanes exactly as
+// rowsum_strided does, so every lane ends with the row's sum of squares;
+// then it scales the values it holds and stores them.  X is read once; the
+// weight is staged in LDS once per workgroup.
+template <int W, int OP, bool DOWN>
+__global__ __launch_bounds__(256) void rmsnorm_strided_fused(RowsumArgs ra, NormArgs a) {
+  constexpr int LPL = W / 64, NST = 128 / LPL;
+  constexpr int fma = OP == 1;
+  __shared__ __attribute__((aligned(16))) uint16_t wl[8192];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * RS_WAVES + wave;
+  const bool live = row < a.rows;
+  const int64_t cols = a.cols, nfull = live ? cols / W : 0;
+  const float* x = a.X + (live ? row : 0) * cols + lane * LPL;
+  if (a.w) {
+    if (((uintptr_t)a.w) % 16 == 0 && cols % 8 == 0) {
+      for (int64_t j = 8 * (int64_t)threadIdx.x; j < cols; j += 8 * 256) *(uint4*)&wl[j] = *(const uint4*)&a.w[j];
+    } else {
+      for (int64_t j = threadIdx.x; j < cols; j += 256) wl[j] = a.w[j];
+    }
+  }
+  __syncthreads();
+  float v[NST + 1][LPL];
+#pragma unroll
+  for (int t = 0; t < NST; ++t) {
+    if (t < nfull) {
+      if constexpr (LPL == 4) {
+        const float4 f = *(const float4*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y; v[t][2] = f.z; v[t][3] = f.w;
+      } else if constexpr (LPL == 2) {
+        const float2 f = *(const float2*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y;
+      } else {
+        v[t][0] = x[(int64_t)t * W];
+      }
+    }
+  }
+  // the short last step
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    v[NST][u] = (live && nfull * W + lane * LPL + u < cols) ? x[nfull * W + u] : 0.0f;
+  float s[LPL];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) s[u] = -0.0f;
+  if (nfull > 0) {
+#pragma unroll
+    for (int u = 0; u < LPL; ++u) s[u] = v[0][u] * v[0][u];
+  }
+#pragma unroll
+  for (int t = 1; t < NST; ++t)
+    if (t < nfull) {
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = leaf_step(s[u], v[t][u], 1, fma);
+    }
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (live && nfull * W + lane * LPL + u < cols)
+      s[u] = nfull ? leaf_step(s[u], v[NST][u], 1, fma) : v[NST][u] * v[NST][u];
+  float r;
+  if constexpr (!DOWN) {
+#pragma unroll
+    for (int h = 1; h < LPL; h <<= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
+    r = s[0];
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) r = r + __shfl_xor(r, m, 64);
+  } else {
+#pragma unroll
+    for (int m = 32; m >= 1; m >>= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], m, 64);
+#pragma unroll
+    for (int h = LPL / 2; h >= 1; h >>= 1)
+#pragma unroll
+      for (int u = 0; u < h; ++u) s[u] = s[u] + s[u + h];
+    r = s[0];
+  }
+  if (!live) return;
+  const float rinv = rms_inv(r, cols, ra.eps);
+  auto one = [&](float xv, int64_t j) {
+    float y = xv * rinv;
+    if (a.pre_round) y = round_bf16(y);
+    if (a.w) y = y * bf16_f32(wl[j]);
+    return y;
+  };
+  auto put = [&](int64_t j, const float* y, int n) {
+    if (a.out_bf16) {
+      uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
+      if (n == 4) {
+        *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
+                            (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+      } else if (n == 2) {
+        *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+      } else {
+        for (int u = 0; u < n; ++u) yp[u] = f32_bf16(y[u]);
+      }
+    } else {
+      float* yp = (float*)a.Y + row * cols + j;
+      if (n == 4) *(float4*)yp = float4{y[0], y[1], y[2], y[3]};
+      else if (n == 2) *(float2*)yp = float2{y[0], y[1]};
+      else for (int u = 0; u < n; ++u) yp[u] = y[u];
+    }
+  };
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull) {
+      const int64_t j = (int64_t)t * W + lane * LPL;
+      float y[LPL];
+      if (a.w) {
+        // the step's LPL weights in one LDS read
+        uint16_t wv[LPL];
+        if constexpr (LPL == 4) {
+          const uint2 q = *(const uint2*)&wl[j];
+          wv[0] = (uint16_t)q.x; wv[1] = (uint16_t)(q.x >> 16); wv[2] = (uint16_t)q.y; wv[3] = (uint16_t)(q.y >> 16);
+        } else if constexpr (LPL == 2) {
+          const uint32_t q = *(const uint32_t*)&wl[j];
+          wv[0] = (uint16_t)q; wv[1] = (uint16_t)(q >> 16);
+        } else {
+          wv[0] = wl[j];
+        }
+#pragma unroll
+        for (int u = 0; u < LPL; ++u) {
+          float yy = v[t][u] * rinv;
+          if (a.pre_round) yy = round_bf16(yy);
+          y[u] = yy * bf16_f32(wv[u]);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < LPL; ++u) y[u] = one(v[t][u], j + u);
+      }
+      put(j, y, LPL);
+    }
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) {
+    const int64_t j = nfull * W + lane * LPL + u;
+    if (j < cols) {
+      const float y = one(v[NST][u], j);
+      put(j, &y, 1);
+    }
+  }
+}
+
+// The fused pass applies when the row fits the registers and every vector
+// access is aligned.
+bool rmsnorm_fused_ok(const RowsumArgs& r, const NormArgs& a) {
+  const int W = r.leaf_w, LPL = W / 64;
+  if (!r.strided || (W != 64 && W != 128 && W != 256) || a.cols > 8192 || a.cols % LPL) return false;
+  const int ybytes = a.out_bf16 ? 2 : 4;
+  return ((uintptr_t)a.X) % (4 * LPL) == 0 && ((uintptr_t)a.Y) % (ybytes * LPL) == 0;
+}
+
+template <int W, bool DOWN>
+static void launch_fused_w(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)((a.rows + RS_WAVES - 1) / RS_WAVES)), block(64 * RS_WAVES);
+  if (r.fma) hipLaunchKernelGGL((rmsnorm_strided_fused<W, 1, DOWN>), grid, block, 0, st, r, a);
+  else hipLaunchKernelGGL((rmsnorm_strided_fused<W, 2, DOWN>), grid, block, 0, st, r, a);
+}
+
+hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  if (r.leaf_w == 64) r.down ? launch_fused_w<64, true>(r, a, st) : launch_fused_w<64, false>(r, a, st);
+  else if (r.leaf_w == 128) r.down ? launch_fused_w<128, true>(r, a, st) : launch_fused_w<128, false>(r, a, st);
+  else if (r.leaf_w == 256) r.down ? launch_fused_w<256, true>(r, a, st) : launch_fused_w<256, false>(r, a, st);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t launch_rmsnorm_scale(const NormArgs& a, hipStream_t st) {
+  const bool vec = a.cols % 4 == 0 && ((uintptr_t)a.X) % 16 == 0 &&
+                   ((uintptr_t)a.Y) % (a.out_bf16 ? 8 : 16) == 0;
+  const dim3 grid((unsigned)a.rows), block(256);
+  if (vec) hipLaunchKernelGGL((rmsnorm_scale<true>), grid, block, 0, st, a);
+  else hipLaunchKernelGGL((rmsnorm_scale<false>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 

@@ -37,7 +37,7 @@ class dg_desc_params(ctypes.Structure):
         (n, ctypes.c_int32) for n in ("tile_combine", "split_combine", "tail", "fma", "partial_dtype",
                                       "merge_dtype", "out_dtype", "epilogue", "epi_round", "leaf_w",
                                       "reduce_op", "split_layout", "split_tile", "leaf_layout",
-                                      "lane_fold")]
+                                      "lane_fold", "norm_round")]
 
 
 class dg_knobs(ctypes.Structure):
@@ -65,10 +65,11 @@ def lib():
         L.dg_gemm.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_gemm_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
         L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
+        L.dg_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_strerror.argtypes = [ctypes.c_int]
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
-        for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum"):
+        for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -93,12 +94,15 @@ class Desc:
     reduce ("sum" | "sumsq"), split_layout ("contiguous" | "strided"),
     split_tile (the dealt tile of a strided split), leaf_layout ("contiguous" |
     "strided": leaf_w lanes each taking every leaf_w-th element), lane_fold
-    ("up" | "down": the butterfly's offsets counting up or down)."""
+    ("up" | "down": the butterfly's offsets counting up or down), norm_round
+    ("final" | "pre_weight": dg_rmsnorm rounds the normalised value to bf16
+    before the weight)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
                     epilogue="none", epi_round="final", leaf_w=64, reduce="sum",
-                    split_layout="contiguous", split_tile=0, leaf_layout="contiguous", lane_fold="up")
+                    split_layout="contiguous", split_tile=0, leaf_layout="contiguous", lane_fold="up",
+                    norm_round="final")
 
     def __init__(self, **fields):
         unknown = set(fields) - set(self.DEFAULTS) - {"model"}
@@ -135,6 +139,7 @@ class Desc:
         p.split_tile = int(f["split_tile"])
         p.leaf_layout = {"contiguous": 0, "strided": 1}[f["leaf_layout"]]
         p.lane_fold = {"up": 0, "down": 1}[f["lane_fold"]]
+        p.norm_round = {"final": 0, "pre_weight": 1}[f["norm_round"]]
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:
@@ -219,7 +224,22 @@ def dg_rowsum(desc: Desc, X, out, rows=None, cols=None, stream=None):
     return out
 
 
+def dg_rmsnorm(desc: Desc, X, w, eps, Y, rows=None, cols=None, stream=None):
+    """Y = RMS normalisation of the rows of X (fp32) scaled by w (bf16 or
+    None), in the descriptor's order (its reduce must be "sumsq")."""
+    import torch
+    if isinstance(X, torch.Tensor):
+        assert X.dtype == torch.float32 and X.is_contiguous() and X.is_cuda
+        assert Y.is_contiguous() and Y.is_cuda and Y.shape == X.shape
+        assert w is None or (w.dtype == torch.bfloat16 and w.is_contiguous() and w.numel() == X.shape[1])
+        rows, cols = X.shape
+    st = lib().dg_rmsnorm(desc.handle, _ptr(X), _ptr(w), ctypes.c_float(eps), _ptr(Y), rows, cols, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_rmsnorm")
+    return Y
+
+
 def exported_symbols():
     """Names of the entry points include/dg.h declares."""
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs",
-            "dg_rowsum", "dg_strerror", "dg_version"]
+            "dg_rowsum", "dg_rmsnorm", "dg_strerror", "dg_version"]

@@ -48,7 +48,7 @@ def test_version_and_strerror(dg):
     dict(split_k=3, split_layout="strided", split_tile=64, k_cuts=[64, 128]),
     dict(split_k=4, split_layout="strided", split_tile=64, tail="first"),
     dict(split_k=4, split_tile=64),                                      # a tile without the layout
-    dict(leaf_layout="diagonal"), dict(lane_fold="sideways")])
+    dict(leaf_layout="diagonal"), dict(lane_fold="sideways"), dict(norm_round="never")])
 def test_invalid_descriptors_rejected(dg, bad):
     with pytest.raises((dg.DgError, KeyError)):
         dg.Desc(**bad)
@@ -57,7 +57,7 @@ def test_invalid_descriptors_rejected(dg, bad):
 def test_raw_field_values_checked(dg):
     """Out-of-range enum values of the new fields are rejected at create."""
     lib = dg.lib()
-    for field, value in (("leaf_layout", 2), ("lane_fold", -1)):
+    for field, value in (("leaf_layout", 2), ("lane_fold", -1), ("norm_round", 5)):
         p = dg.dg_desc_params()
         p.struct_size = ctypes.sizeof(p)
         p.mma, p.tile_k, p.split_k, p.leaf_w = 1, 64, 1, 64
@@ -108,6 +108,7 @@ def test_signature_canonical(dg):
     assert dg.Desc(leaf_w=1, leaf_layout="strided", lane_fold="down").signature() == \
         dg.Desc(leaf_w=1, leaf_layout="strided").signature()
     assert up != dg.Desc(leaf_w=256).signature()
+    assert dg.Desc(norm_round="pre_weight").signature().endswith("norm-pre-weight")
 
 
 def test_argument_errors_need_no_gpu(dg):
@@ -152,6 +153,16 @@ def test_argument_errors_need_no_gpu(dg):
                dg.dg_knobs(4, 16, 32, 0, 0, 4, 128)):
         assert lib.dg_gemm_knobs(sd.handle, 16, 16, None, 16, 8, 8, 64, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
+    # RMS normalisation: the descriptor must name the sum of squares
+    q = dg.Desc(reduce="sumsq")
+    assert lib.dg_rmsnorm(d.handle, 16, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_INVALID
+    assert lib.dg_rmsnorm(q.handle, 16, None, 0.0, 16, 0, 5, None) == dg.DG_OK
+    assert lib.dg_rmsnorm(q.handle, 16, None, 0.0, 16, 4, 0, None) == dg.DG_OK
+    assert lib.dg_rmsnorm(q.handle, 16, None, 0.0, 16, -1, 5, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_rmsnorm(q.handle, None, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_INVALID
+    assert lib.dg_rmsnorm(q.handle, 18, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_rmsnorm(q.handle, 16, 17, 0.0, 16, 4, 5, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_rmsnorm(None, 16, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_INVALID
     # row reduction
     assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
