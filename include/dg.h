@@ -174,7 +174,9 @@ typedef struct {
                       ping-pong kernel (tile_m, tile_n each 128 or 256): two
                       groups of four waves one phase apart, 6 the kernel-5
                       256 x 256 blocks on the first split_n columns and
-                      256 x 192 blocks on the rest, in one launch */
+                      256 x 192 blocks on the rest, in one launch, 7 as 6 (or
+                      256 x 256 blocks alone when split_n is 0 and no split
+                      helps) with direct-to-LDS loads */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
   int32_t order;   /* kernels 3 and 5: block order: 0 library's choice, 1 row-major
@@ -186,7 +188,7 @@ typedef struct {
   int32_t slab_k;  /* kernel 4: k per slab (0 = 64; 64, 128 or 256).  Kernel 4
                       builds a fixed list of (tile_m, tile_n, depth, slab_k);
                       others return DG_ERR_UNSUPPORTED */
-  int32_t split_n; /* kernel 6: columns computed in 256-wide blocks, a multiple of
+  int32_t split_n; /* kernels 6, 7: columns computed in 256-wide blocks, a multiple of
                       256 in [0, N] (0 = library's choice, which may be 0: all
                       blocks 192 wide); tile_m, tile_n must be 0 */
 } dg_knobs;

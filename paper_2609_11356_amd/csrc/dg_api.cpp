@@ -269,10 +269,10 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 6) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
-  if (kern != 3 && kern != 5 && kern != 6 && order) return DG_ERR_UNSUPPORTED;
-  if (kern == 6 && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
-  if (kern != 6 && split_n) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 7) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && order) return DG_ERR_UNSUPPORTED;
+  if ((kern == 6 || kern == 7) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
+  if (kern != 6 && kern != 7 && split_n) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
@@ -390,6 +390,20 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     a.order = order ? order : 3;
     if (dg::wide_is_pp(tm, tn) && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
     e = dg::launch_gemm_wide(a, tm, tn, st);
+  } else if (kern == 7) {
+    if (!pp_fits(a)) return DG_ERR_UNSUPPORTED;
+    // split_n 0: the library's split, or 256-wide blocks alone when no split helps
+    bool mixed = true;
+    if (split_n == 0) {
+      const int64_t sp = mixed_split(M, N, a.S, cu_count());
+      if (sp < 0) mixed = false;
+      else split_n = sp;
+    }
+    if (((M + 255) / 256) * (split_n / 256 + (N - split_n + 191) / 192 + (N + 255) / 256) > INT32_MAX)
+      return DG_ERR_SHAPE;
+    a.order = order ? order : 1;
+    a.n_split = split_n;
+    e = dg::launch_gemm_ppd(a, mixed, st);
   } else if (kern == 6) {
     if (!pp_fits(a)) return DG_ERR_UNSUPPORTED;
     if (knobs && knobs->kernel == 6 && split_n == 0) {

@@ -761,6 +761,223 @@ __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j
   }
 }
 
+// ------------------------------------- ping-pong with direct-to-LDS loads
+//
+// The same eight-wave schedule and LDS layouts as pp_body for 256 x BNC
+// blocks and 32-k slabs, but the loads go from memory straight into LDS
+// (buffer_load ... lds: lane l's 16 bytes land at the instruction's LDS base
+// + 16 l), so no staging registers and no LDS write instructions remain:
+// VGPR->LDS writes run at under 100 B/clk per CU on MI355X against ~230 for
+// reads, and they were the largest single cost of the register-staged
+// schedule.  Each lane fetches the chunk that belongs at its LDS slot under
+// the swizzle (the XOR maps are involutions), so the layouts are unchanged.
+//
+// A ring of four slots (one slab each, in four separate LDS arrays so that
+// the compiler tells them apart and waits only for the slot it reads): the
+// loads of slab s+3 are issued during the compute phase of slab s into the
+// slot that slab s-1 left.  A group's loads are complete once its own
+// outstanding count allows it, and visible to the other group after the
+// next barrier:
+//   group 0 ends each compute phase with at most two slabs of its loads in
+//   flight (s+2, s+3), group 1 ends each memory phase with at most one
+//   (s+2), so slab s+1 is in LDS, from both groups, at the barrier that
+//   precedes group 0's memory phase of s+1.
+constexpr int PPD_SLOT = 256 * 32 + 32 * 256;   // bf16 elements per slot
+__shared__ __attribute__((aligned(1024))) uint16_t ppd_s0[PPD_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t ppd_s1[PPD_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t ppd_s2[PPD_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t ppd_s3[PPD_SLOT];
+
+template <int S>
+__device__ __forceinline__ uint16_t* ppd_slot() {
+  if constexpr (S == 0) return ppd_s0;
+  else if constexpr (S == 1) return ppd_s1;
+  else if constexpr (S == 2) return ppd_s2;
+  else return ppd_s3;
+}
+
+typedef __attribute__((address_space(3))) void* lds_void;
+
+// s_waitcnt immediate waiting for at most n outstanding vector-memory
+// operations (gfx9 encoding: vmcnt[3:0] in bits 3:0, vmcnt[5:4] in bits
+// 15:14; expcnt 7 and lgkmcnt 15 mean no wait on those counters).
+constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Workgroup barrier without the memory fence of __syncthreads: the fence
+// would make every wave wait for all of its direct-to-LDS loads.  The loads
+// a phase needs are waited for explicitly (vmcnt) before it.
+__device__ __forceinline__ void barrier_nofence() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int BNC>
+__device__ __forceinline__ void ppd_body(const GemmArgs& a, int64_t i0, int64_t j0) {
+  constexpr int BM = 256, BN = 256, BK = 32, CPR = 4, WTM = 128, WTN = BNC / 4, TM = 8, TN = WTN / 16;
+  constexpr int A_ELEMS = BM * BK;
+  constexpr int NL = 4;                     // loads per thread per slab: 2 of A, 2 of B
+  constexpr int NPAIR = TM;                 // MFMA groups per compute phase
+  static_assert(BNC <= BN && BNC % 64 == 0, "whole 16-column fragments per wave");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2, wn = wave & 3;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / 4) % CPR)); };
+  auto ldsB = [](int k, int c) { return k * (BN / 8) + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
+
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = (a.K - k0) * a.N * 2;
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.B + k0 * a.N), (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
+  // Load i of the thread's share, i = 0, 1: A rows grp*128 + (wn*2+i)*16 +
+  // lane/4 (physical chunk lane%4), then B k-rows grp*16 + (wn*2+i)*2 +
+  // lane/32 (physical chunk lane%32).  Each instruction fills 1 KB of LDS.
+  uint32_t offA[2], offB[2];
+  int kcA[2], kcB[2], dA[2], dB[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int r = grp * 128 + (wn * 2 + i) * 16 + lane / 4, pc = lane & 3;
+    const int c = pc ^ ((r / 4) % CPR);
+    offA[i] = (i0 + r < a.M) ? (uint32_t)((r * a.K + 8 * c) * 2) : OOB;
+    kcA[i] = 8 * c;
+    dA[i] = (grp * 128 + (wn * 2 + i) * 16) * BK;           // element offset of the 1 KB run
+    const int kr = grp * 16 + (wn * 2 + i) * 2 + lane / 32, pb = lane & 31;
+    const int cb = pb ^ ((kr & 3) << 1) ^ (((kr >> 3) & 1) << 3);
+    offB[i] = (8 * cb < BNC && j0 + 8 * cb < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * cb) * 2) : OOB;
+    kcB[i] = kr;
+    dB[i] = A_ELEMS + (grp * 16 + (wn * 2 + i) * 2) * BN;
+  }
+  // load l (0, 1: A; 2, 3: B) of slab sl into slot S
+  auto dma1 = [&](auto S, int sl, int l) {
+    uint16_t* base = ppd_slot<decltype(S)::value>();
+    const int64_t ks = k0 + (int64_t)sl * BK, lim = k1 - ks;
+    if (l < 2) {
+      const uint32_t off = kcA[l] < lim ? offA[l] : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(base + dA[l]), 16, off, (int)(ks * 2), 0, 0);
+    } else {
+      const int i = l - 2;
+      const uint32_t off = kcB[i] < lim ? offB[i] : OOB;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(base + dB[i]), 16, off, (int)((ks - k0) * a.N * 2), 0, 0);
+    }
+  };
+
+  floatx4 acc[TM][TN];
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
+  shortx8 af[TM], bf[TN];
+  auto rd = [&](auto S) {
+    const uint16_t* As = ppd_slot<decltype(S)::value>();
+    const uint16_t* Bs = As + A_ELEMS;
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      const int i = lane & 15, g = lane >> 4;
+      const int n = wn * WTN + 16 * ni + 4 * (i & 3);
+      const int kr0 = 8 * g + (i >> 2), kr1 = kr0 + 4;
+      const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+      const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+      bf[ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi) {
+      const int row = grp * WTM + 16 * mi + (lane & 15);
+      af[mi] = *(const shortx8*)&As[8 * ldsA(row, lane >> 4)];
+    }
+  };
+
+  // prologue: slabs 0, 1, 2 into slots 0, 1, 2; slab 0 complete everywhere
+  static_for<0, NL>([&](auto l) { dma1(std::integral_constant<int, 0>{}, 0, l); });
+  static_for<0, NL>([&](auto l) { dma1(std::integral_constant<int, 1>{}, 1, l); });
+  static_for<0, NL>([&](auto l) { dma1(std::integral_constant<int, 2>{}, 2, l); });
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * NL));
+  barrier_nofence();
+  if (grp == 1) barrier_nofence();
+  auto step = [&](auto S, int sl) {
+    constexpr int SL = decltype(S)::value;
+    // memory phase: fragments of slab sl
+    __builtin_amdgcn_sched_barrier(0);
+    rd(S);
+    if (grp == 1) __builtin_amdgcn_s_waitcnt(vmcnt_only(NL));   // slab sl+1 landed
+    barrier_nofence();
+    // compute phase: the MFMAs of slab sl, the loads of slab sl+3 spread among them
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(2);
+    static_for<0, NPAIR>([&](auto p) {
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) acc[p][ni] = mfma16(af[p], bf[ni], acc[p][ni]);
+      static_for<0, NL>([&](auto l) {
+        if constexpr ((l + 1) * NPAIR / NL - 1 == p) {
+          __builtin_amdgcn_sched_barrier(0);
+          dma1(std::integral_constant<int, (SL + 3) % 4>{}, sl + 3, l);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      });
+    });
+    __builtin_amdgcn_s_setprio(0);
+    if (grp == 0) __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * NL));   // slab sl+1 landed
+    barrier_nofence();
+  };
+  for (int sl = 0; sl < nslab; sl += 4) {
+    step(std::integral_constant<int, 0>{}, sl);
+    step(std::integral_constant<int, 1>{}, sl + 1);
+    step(std::integral_constant<int, 2>{}, sl + 2);
+    step(std::integral_constant<int, 3>{}, sl + 3);
+  }
+  if (grp == 0) barrier_nofence();
+  // loads of slabs past the end (zeros) may still be landing in the slots
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+  __syncthreads();
+
+  // epilogue: wave w stages through slot w % 4, at (w / 4) * 16 rows of pitch CSP
+  constexpr int CSP = WTN + 4;
+  static_assert(2 * 16 * CSP * 4 <= PPD_SLOT * 2, "epilogue staging fits");
+  uint16_t* sb = (wave & 3) == 0 ? ppd_s0 : (wave & 3) == 1 ? ppd_s1 : (wave & 3) == 2 ? ppd_s2 : ppd_s3;
+  float* cs = reinterpret_cast<float*>(sb) + (wave >> 2) * 16 * CSP;
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+    __syncthreads();
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+    __syncthreads();
+#pragma unroll 1
+    for (int q = lane; q < 16 * WTN / 4; q += 64) {
+      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+      const int64_t i = i0 + grp * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
+      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
+    }
+  }
+}
+
+__global__ __launch_bounds__(512) void gemm_ppd(GemmArgs a) {
+  const int tiles_m = (int)((a.M + 255) / 256);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  ppd_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256);
+}
+
+__global__ __launch_bounds__(512) void gemm_ppd_mixed(GemmArgs a) {
+  const int tiles_m = (int)((a.M + 255) / 256);
+  const int tn1 = (int)(a.n_split / 256), nb1 = tiles_m * tn1;
+  int ty, tx;
+  if ((int)blockIdx.x < nb1) {
+    grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
+    ppd_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256);
+  } else {
+    const int tn2 = (int)((a.N - a.n_split + 191) / 192);
+    grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
+    ppd_body<192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192);
+  }
+}
+
 template <int BM, int BN, int BK>
 __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM * BK + BK * BN)];
@@ -1008,6 +1225,18 @@ static hipError_t launch_pp_t(const GemmArgs& a, hipStream_t st) {
 hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + 255) / 256, tn = a.n_split / 256 + (a.N - a.n_split + 191) / 192;
   hipLaunchKernelGGL((gemm_pp_mixed<32>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_ppd(const GemmArgs& a, bool mixed, hipStream_t st) {
+  const int64_t tm = (a.M + 255) / 256;
+  if (mixed) {
+    const int64_t tn = a.n_split / 256 + (a.N - a.n_split + 191) / 192;
+    hipLaunchKernelGGL(gemm_ppd_mixed, dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  } else {
+    const int64_t tn = (a.N + 255) / 256;
+    hipLaunchKernelGGL(gemm_ppd, dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  }
   return hipGetLastError();
 }
 

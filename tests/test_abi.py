@@ -141,11 +141,14 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(3, 0, 0, 0, 0, 0, 128)        # slab_k is a kernel-4 knob
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
-    # kernel 6 takes no tile shape; split_n is a multiple of 256 within N, and only for kernel 6
-    for kn in (dg.dg_knobs(6, 256, 256, 0, 0, 0, 0, 0), dg.dg_knobs(6, 0, 0, 0, 0, 0, 0, 100),
-               dg.dg_knobs(6, 0, 0, 0, 0, 0, 0, 512), dg.dg_knobs(6, 0, 0, 0, 0, 0, 0, -256),
-               dg.dg_knobs(5, 256, 256, 0, 0, 0, 0, 256), dg.dg_knobs(7, 0, 0, 0, 0, 0, 0, 0)):
-        assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 300, 8, ctypes.byref(kn), None) == \
+    # kernels 6 and 7 take no tile shape; split_n is a multiple of 256 within N, and only for them
+    for k in (6, 7):
+        for kn in (dg.dg_knobs(k, 256, 256, 0, 0, 0, 0, 0), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 100),
+                   dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 512), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, -256)):
+            assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
+                dg.DG_ERR_UNSUPPORTED
+    for kn in (dg.dg_knobs(5, 256, 256, 0, 0, 0, 0, 256), dg.dg_knobs(8, 0, 0, 0, 0, 0, 0, 0)):
+        assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
     # a strided split runs on the generic kernel or on kernel 4 with one dealt tile per slab
     sd = dg.Desc(split_k=4, split_layout="strided", split_tile=64)
