@@ -84,6 +84,7 @@ def _bind(path):
     L.dgo_gemm_at.argtypes = [P, vp, vp, vp, i64, i64, i64, vp, vp, i64, vp, i32]
     L.dgo_rowsum.argtypes = [P, vp, vp, i64, i64, i32]
     L.dgo_rmsnorm.argtypes = [P, vp, vp, f32, vp, vp, i64, i64, i32]
+    L.dgo_softmax.argtypes = [P, vp, vp, i64, i64, i32]
     L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
     L.dgo_group_update.restype = f32
     L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
@@ -227,6 +228,21 @@ def rmsnorm(desc, X, w=None, eps=0.0, nthreads=None, with_rinv=False):
     if st:
         raise OracleError("dgo_rmsnorm status %d" % st)
     return (Y, rinv) if with_rinv else Y
+
+
+def softmax(desc, X, nthreads=None):
+    """Softmax of each row of X (fp32) with the row sum in the descriptor's
+    order.  Returns fp32 values (out f32) or bf16 bits (out bf16)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    rows, cols = X.shape
+    d = dict(desc)
+    d["reduce"] = "sum"
+    p, keep = params(d)
+    Y = np.zeros((rows, cols), dtype=np.uint16 if p.out_bf16 else np.float32)
+    st = lib().dgo_softmax(ctypes.byref(p), X.ctypes.data, Y.ctypes.data, rows, cols, nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_softmax status %d" % st)
+    return Y
 
 
 def plan_cuts(desc, K):

@@ -713,6 +713,43 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
   return 0;
 }
 
+/* ------------------------------------------------------------- softmax */
+
+/* The normalisation on the other side of a row sum (the paper evaluates
+ * softmax kernels, Sec. 7): the shift by the row maximum is exact in order
+ * (a maximum has no rounding), the exponentials are dgo_exp, and the only
+ * order-sensitive step, the sum, is the descriptor's tree. */
+int dgo_softmax(const dgo_params* p, const float* X, void* Y, int64_t rows, int64_t cols,
+                int nthreads) {
+  if (p->leaf_w < 1 || rows < 0 || cols < 0 || p->sumsq) return 1;
+  const int64_t L = leaf_count(p, cols);
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    float* leaves = (float*)malloc(sizeof(float) * (size_t)(L > 0 ? L : 1));
+    float* e = (float*)malloc(sizeof(float) * (size_t)(cols > 0 ? cols : 1));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t r = 0; r < rows; ++r) {
+      const float* x = X + r * cols;
+      if (cols == 0) continue;
+      float m = x[0];
+      for (int64_t j = 1; j < cols; ++j)
+        if (m == m && (x[j] != x[j] || x[j] > m)) m = x[j];
+      for (int64_t j = 0; j < cols; ++j) e[j] = dgo_exp(x[j] - m);
+      float s = row_reduce(p, e, cols, leaves);
+      float rinv = 1.0f / s;
+      for (int64_t j = 0; j < cols; ++j) {
+        float y = e[j] * rinv;
+        if (p->out_bf16) ((uint16_t*)Y)[r * cols + j] = dgo_f32_to_bf16(y);
+        else ((float*)Y)[r * cols + j] = y;
+      }
+    }
+    free(leaves);
+    free(e);
+  }
+  return 0;
+}
+
 /* -------------------------------------------------- RMS normalisation */
 
 /* The step after the row's sum of squares (Sec. 3.1 tree; the normalisation

@@ -112,6 +112,14 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
 int dgo_rmsnorm(const dgo_params* p, const float* X, const uint16_t* w, float eps,
                 void* Y, float* rinv, int64_t rows, int64_t cols, int nthreads);
 
+/* Softmax of each row:  m = the row's largest element (a NaN anywhere makes
+ * it NaN; exact, so independent of order),  e_j = dgo_exp(RN32(x_j - m)),
+ * s = the sum of the e_j in the descriptor's leaf order (as dgo_rowsum with
+ * sumsq = 0),  rinv = RN32(1 / s),  out_j = RN_out(RN32(e_j * rinv)).
+ * Y receives rows*cols fp32 values (out_bf16 = 0) or bf16 bits. */
+int dgo_softmax(const dgo_params* p, const float* X, void* Y, int64_t rows, int64_t cols,
+                int nthreads);
+
 /* The count-down butterfly's tree over lanes 0..P-1 (P rounded up to a power
  * of two), lane j < n holding v[j], lanes from n on empty.  Exposed for tests. */
 float dgo_tree_bitrev(const float* v, int n, int P);

@@ -803,3 +803,61 @@ def test_rmsnorm_follows_the_rowsum_order_and_rounding_points():
     Pb = oracle.rmsnorm(dict(d, norm_round="pre_weight", out="bf16"), X, w, eps=1e-5)
     want = torch.from_numpy((bf(y) * wf).astype(np.float32)).to(torch.bfloat16).view(torch.int16).numpy()
     assert np.array_equal(Pb.view(np.int16), want)
+
+
+# ---------------------------------------------------------------- softmax
+
+
+def test_softmax_closed_forms():
+    """Constant rows: every shifted value is 0, exp(0) = 1, the sum is the
+    width exactly and each output is 1/width (a power of two here); the
+    shift by the maximum keeps rows of +-1000 finite."""
+    for cols in (1, 2, 64, 256, 4096):
+        for c in (-1000.0, -3.5, 0.0, 2.0, 1000.0):
+            X = np.full((3, cols), c, dtype=np.float32)
+            for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down")):
+                got = oracle.softmax(d, X)
+                assert np.all(got == np.float32(1.0 / cols)), (cols, c, d)
+                gb = oracle.softmax(dict(d, out="bf16"), X)
+                assert np.all(gb == inputs.f32_to_bf16_bits(np.float32(1.0 / cols))), (cols, c, d)
+
+
+def test_softmax_steps_and_rounding_points():
+    """Each row: the maximum, the oracle's exp of the exact-order shifted
+    values, the row sum in the descriptor's order (dg_rowsum's value), one
+    reciprocal, one product per element (not a division)."""
+    X = inputs.lognormal_f32(61, (6, 300), sigma=1.0)
+    for d in (dict(leaf_w=64), dict(leaf_w=32, leaf_layout="strided", lane_fold="down"),
+              dict(leaf_w=1, leaf_layout="strided")):
+        got = oracle.softmax(d, X)
+        for r in range(6):
+            m = X[r].max()
+            e = np.array([oracle.exp(np.float32(x - m)) for x in X[r]], dtype=np.float32)
+            s = oracle.rowsum(dict(d, reduce="sum"), e[None, :])[0]
+            rinv = np.float32(np.float32(1.0) / s)
+            assert np.array_equal(got[r], (e * rinv).astype(np.float32)), (d, r)
+    # a reciprocal multiply and a division part ways somewhere on these rows
+    e = np.array([oracle.exp(np.float32(x - X[0].max())) for x in X[0]], dtype=np.float32)
+    s = oracle.rowsum(dict(leaf_w=64), e[None, :])[0]
+    assert not np.array_equal((e * np.float32(np.float32(1.0) / s)).astype(np.float32), (e / s).astype(np.float32))
+
+
+def test_softmax_within_fp64_bound():
+    """Against float64: exp within 2 ulp, a sum of positive terms within
+    70 * 2^-24 relative, the reciprocal and the product one rounding each."""
+    X = inputs.lognormal_f32(62, (32, 8192), sigma=1.0)
+    X64 = X.astype(np.float64)
+    E = np.exp(X64 - X64.max(1, keepdims=True))
+    ref = E / E.sum(1, keepdims=True)
+    for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down")):
+        got = oracle.softmax(d, X).astype(np.float64)
+        assert np.all(np.abs(got - ref) <= 2.0 ** -17 * ref + 1e-45), d
+
+
+def test_softmax_special_values():
+    """IEEE cases: a NaN anywhere, or +inf (inf - inf), makes the row NaN;
+    -inf entries get exactly 0 beside finite ones."""
+    X = np.array([[1.0, np.nan, 2.0], [1.0, np.inf, 2.0], [0.0, -np.inf, 0.0]], dtype=np.float32)
+    got = oracle.softmax(dict(leaf_w=64), X)
+    assert np.all(np.isnan(got[0])) and np.all(np.isnan(got[1]))
+    assert got[2].tolist() == [0.5, 0.0, 0.5]

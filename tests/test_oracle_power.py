@@ -54,6 +54,11 @@ MUTANTS = {
         "if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (p->norm_pre_round) y = rnbf(y);"),
     "rmsnorm sums the row in index order": ("float s = row_reduce(p, x, cols, leaves);",
                                             "float s = 0.0f;\n      for (int64_t k = 0; k < cols; ++k) s = fmaf(x[k], x[k], s);"),
+    "softmax without the max shift": ("for (int64_t j = 0; j < cols; ++j) e[j] = dgo_exp(x[j] - m);",
+                                      "for (int64_t j = 0; j < cols; ++j) e[j] = dgo_exp(x[j]);"),
+    "softmax divides instead of multiplying": ("float y = e[j] * rinv;", "float y = e[j] / s;"),
+    "softmax sums in index order": ("float s = row_reduce(p, e, cols, leaves);",
+                                    "float s = 0.0f;\n      for (int64_t j = 0; j < cols; ++j) s = s + e[j];"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
     "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
@@ -84,6 +89,8 @@ CHECKS = [
     lambda: pins.test_rmsnorm_hand_example(),
     lambda: pins.test_rmsnorm_closed_forms(),
     lambda: pins.test_rmsnorm_follows_the_rowsum_order_and_rounding_points(),
+    lambda: pins.test_softmax_closed_forms(),
+    lambda: pins.test_softmax_steps_and_rounding_points(),
 ]
 
 
