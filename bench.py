@@ -171,6 +171,10 @@ def main():
     w_rms = inputs.normal_bf16(10, (X.shape[1],), 1.0)
     dw_rms = d_bf16(w_rms)
     Y_rms = torch.empty(X.shape, dtype=torch.bfloat16, device=dev)
+    # softmax of the same rows (as logits), sum over 256 strided lanes, bf16 out
+    desc_smx = dict(leaf_w=256, leaf_layout="strided", lane_fold="down", reduce="sum", out="bf16")
+    D_smx = dg.Desc(**desc_smx)
+    Y_smx = torch.empty(X.shape, dtype=torch.bfloat16, device=dev)
 
     C_sw = {M: torch.empty((M, 4096), dtype=torch.bfloat16, device=dev) for M in inputs.SWEEP_M}
     C_dec = {c: torch.empty((8, 4096), dtype=torch.bfloat16, device=dev) for c in ("seq", "tree")}
@@ -272,6 +276,21 @@ def main():
     b.record(stream)
     torch.cuda.synchronize()
     ms = a.elapsed_time(b) / args.steps
+    for _ in range(args.warmup):
+        dg.dg_softmax(D_smx, dX, Y_smx, stream=sptr)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(args.steps):
+        dg.dg_softmax(D_smx, dX, Y_smx, stream=sptr)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms_smx = a.elapsed_time(b) / args.steps
+    smx_bytes = X.nbytes + X.size * 2
+    rs["softmax_bf16"] = {"ms": round(ms_smx, 4), "GB/s": round(smx_bytes / ms_smx / 1e6, 1),
+                          "frac_hbm": round(smx_bytes / ms_smx / 1e6 / PEAK_HBM_GBS, 4),
+                          "what": "max shift, own exp, sum over 256 strided lanes (count-down fold), one "
+                                  "reciprocal, bf16 out; bytes = X + Y once"}
     rs["rmsnorm_bf16"] = {"ms": round(ms, 4), "GB/s": round(rms_bytes / ms / 1e6, 1),
                           "frac_hbm": round(rms_bytes / ms / 1e6 / PEAK_HBM_GBS, 4),
                           "what": "sum of squares over 256 strided lanes (count-down fold), then "
@@ -288,6 +307,7 @@ def main():
             torch.sum(dX, 1)
             torch.sum(dX * dX, 1)
             (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16) * dw_rms
+            torch.softmax(dX, 1).to(torch.bfloat16)
             for M in inputs.SWEEP_M:
                 torch.matmul(dA_sw_M[M], Bs_f)
         torch.cuda.synchronize()
@@ -309,6 +329,7 @@ def main():
         t_rs2 = timeit(lambda i: torch.sum(dX * dX, 1), args.steps)
         t_rms = timeit(lambda i: (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16)
                        * dw_rms, args.steps)
+        t_smx = timeit(lambda i: torch.softmax(dX, 1).to(torch.bfloat16), args.steps)
         t_sw_m = {M: timeit(lambda i, M=M: torch.matmul(dA_sw_M[M], dB_sw[i % len(dB_sw)]), args.steps)
                   for M in inputs.SWEEP_M}
         free = {"sweep_ms": round(t_sw, 4), "decode_ms_per_launch": round(t_dec, 4), "mlp_ms": round(t_mlp, 4),
@@ -321,11 +342,13 @@ def main():
                 "cost_rowsum_sumsq": round(rs["sumsq"]["ms"] / t_rs2, 3),
                 "rmsnorm_ms": round(t_rms, 4),
                 "cost_rmsnorm": round(rs["rmsnorm_bf16"]["ms"] / t_rms, 3),
+                "softmax_ms": round(t_smx, 4),
+                "cost_softmax": round(rs["softmax_bf16"]["ms"] / t_smx, 3),
                 "sweep_ms_by_M": {str(M): round(t, 4) for M, t in t_sw_m.items()},
                 "cost_sweep_by_M": {str(M): round(shapes["sweep_M%d" % M]["us_mean"] * 1e-3 / t, 3)
                                     for M, t in t_sw_m.items()},
                 "what": ("torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum / x * rsqrt(mean(x^2) + eps) "
-                         "-> bf16 * w on the same shapes; cost = t_dg / t_free")}
+                         "-> bf16 * w / torch.softmax -> bf16 on the same shapes; cost = t_dg / t_free")}
     except Exception as exc:  # the library under test never depends on this
         free = {"error": repr(exc)}
 
@@ -404,6 +427,10 @@ def main():
     got_rms = host(Y_rms)[rr]
     checked += want_rms.size
     matched += int(np.sum(got_rms == want_rms))
+    want_smx = oracle.softmax(desc_smx, X[rr])
+    got_smx = host(Y_smx)[rr]
+    checked += want_smx.size
+    matched += int(np.sum(got_smx == want_smx))
 
     # ------------------------------------------------------- CPU baseline
     ncpu = os.cpu_count() or 1

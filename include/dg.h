@@ -231,6 +231,27 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
 dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
                      int64_t rows, int64_t cols, void* stream);
 
+/* Softmax of each row, the row sum in the descriptor's order (exactly the
+ * value dg_rowsum returns for the descriptor with reduce_op DG_OP_SUM:
+ * leaf_w, leaf_layout and lane_fold apply; reduce_op must be DG_OP_SUM):
+ *   m = max_j x_j (a NaN anywhere gives NaN; a maximum has no rounding, so
+ *   its order is free),  e_j = exp(x_j - m) by the library's own binary32
+ *   exp (the one of the SiLU epilogue: Cody-Waite reduction, degree-7
+ *   Taylor polynomial, exact power-of-two scaling),  s = the sum of the e_j,
+ *   rinv = 1 / s,  out_j = RN_out(e_j * rinv)  (each step one binary32
+ *   operation).  The paper evaluates softmax kernels (Sec. 7); the sum is
+ *   the only order-sensitive step.
+ *   X: device, rows x cols fp32 row-major;  Y: device, rows x cols of
+ *   out_dtype (written, never read; may not overlap X).  rows = 0 or
+ *   cols = 0 is a no-op.  One launch when the descriptor has strided lanes
+ *   (64, 128 or 256) and a row fits in registers (cols <= 8192, aligned);
+ *   otherwise three launches through a library-owned workspace of
+ *   rows x (cols + 1) fp32 values per (device, stream) (DG_ERR_NOMEM if it
+ *   cannot grow).  Errors as dg_rowsum, plus DG_ERR_INVALID for a
+ *   descriptor whose reduce_op is not DG_OP_SUM. */
+dg_status dg_softmax(const dg_desc* d, const float* X, void* Y, int64_t rows, int64_t cols,
+                     void* stream);
+
 const char* dg_strerror(dg_status s);
 
 /* Library version (major * 10000 + minor * 100 + patch).  0.2.0 (200) added

@@ -473,6 +473,47 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows, 
   return DG_OK;
 }
 
+dg_status dg_softmax(const dg_desc* d, const float* X, void* Y, int64_t rows, int64_t cols, void* stream) {
+  if (!d || d->p.reduce_op != DG_OP_SUM) return DG_ERR_INVALID;
+  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
+  if (rows == 0 || cols == 0) return DG_OK;
+  if (!X || !Y) return DG_ERR_INVALID;
+  const bool out_bf16 = d->p.out_dtype == DG_BF16;
+  if (!aligned(X, 4) || !aligned(Y, out_bf16 ? 2 : 4)) return DG_ERR_ALIGN;
+  if (rows > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  hipStream_t st = (hipStream_t)stream;
+  dg::RowsumArgs a = rowsum_args(d, X, nullptr, rows, cols);
+  dg::NormArgs n;
+  std::memset(&n, 0, sizeof n);
+  n.X = X;
+  n.Y = Y;
+  n.rows = rows;
+  n.cols = cols;
+  n.out_bf16 = out_bf16;
+  if (dg::softmax_fused_ok(a, n)) {
+    if (dg::launch_softmax_fused(a, n, st) != hipSuccess) return DG_ERR_HIP;
+    return DG_OK;
+  }
+  // exponentials to the workspace, their reciprocal sums after them, then the products
+  void* ws = nullptr;
+  dg_status s = get_workspace(st, (size_t)rows * (size_t)(cols + 1) * sizeof(float), &ws);
+  if (s != DG_OK) return s;
+  float* E = (float*)ws;
+  float* rinv = E + rows * cols;
+  dg::NormArgs e = n;
+  e.Y = E;
+  e.out_bf16 = 0;
+  if (dg::launch_softmax_exp(e, st) != hipSuccess) return DG_ERR_HIP;
+  a.X = E;
+  a.out = rinv;
+  a.rms = 2;
+  if (dg::launch_rowsum(a, st) != hipSuccess) return DG_ERR_HIP;
+  n.X = E;
+  n.rinv = rinv;
+  if (dg::launch_rmsnorm_scale(n, st) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
 dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
                      int64_t rows, int64_t cols, void* stream) {
   if (!d || d->p.reduce_op != DG_OP_SUMSQ) return DG_ERR_INVALID;

@@ -47,7 +47,8 @@ struct RowsumArgs {
   int64_t rows, cols;
   int32_t leaf_w, sumsq, fma;
   int32_t strided, down;         // leaf layout and lane fold
-  int32_t rms;                   // 1: out[row] = the RMS-norm reciprocal root of the sum
+  int32_t rms;                   // 1: out[row] = the RMS-norm reciprocal root of the sum,
+                                 // 2: out[row] = 1 / sum
   float eps;
 };
 
@@ -79,5 +80,10 @@ hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm_scale(const NormArgs& a, hipStream_t s);
 bool rmsnorm_fused_ok(const RowsumArgs& r, const NormArgs& a);
 hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
+// softmax: one pass (strided lanes, row in registers), or the shifted
+// exponentials of each row into a.Y (fp32) for the three-pass path
+bool softmax_fused_ok(const RowsumArgs& r, const NormArgs& a);
+hipError_t launch_softmax_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
+hipError_t launch_softmax_exp(const NormArgs& a, hipStream_t s);
 
 }  // namespace dg

@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
   }
   if (live && lane == 0) {
     const float v = have ? r : 0.0f;
-    a.out[row] = a.rms ? rms_inv(v, cols, a.eps) : v;
+    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : v;
   }
 }
 
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256) void rowsum_strided(RowsumArgs a) {
   }
   if (live && q == 0) {
     const float v = cols ? r : 0.0f;
-    a.out[row] = a.rms ? rms_inv(v, cols, a.eps) : v;
+    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : v;
   }
 }
 
@@ -523,6 +523,170 @@ hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStrea
   else if (r.leaf_w == 128) r.down ? launch_fused_w<128, true>(r, a, st) : launch_fused_w<128, false>(r, a, st);
   else if (r.leaf_w == 256) r.down ? launch_fused_w<256, true>(r, a, st) : launch_fused_w<256, false>(r, a, st);
   else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------- softmax
+
+// Maximum with NaN propagation (a NaN operand wins).  Only the sign of a
+// zero maximum can depend on the order, and x - (+0) = x - (-0) for every
+// x except a zero, whose exp is 1 either way.
+__device__ __forceinline__ float max_nan(float a, float b) {
+  return (a != a) ? a : (b != b) ? b : (b > a ? b : a);
+}
+
+// One pass for strided lanes (W = 64, 128, 256), rows of at most 8192: the
+// row in registers as in rmsnorm_strided_fused; the maximum by a butterfly
+// (exact), the exponentials in place, their sum folded and met exactly as
+// rowsum_strided does (SUM), one reciprocal, one product per element.
+template <int W, bool DOWN>
+__global__ __launch_bounds__(256) void softmax_strided_fused(RowsumArgs ra, NormArgs a) {
+  constexpr int LPL = W / 64, NST = 128 / LPL;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * RS_WAVES + wave;
+  if (row >= a.rows) return;   // whole waves: every shuffle stays inside a live wave
+  const int64_t cols = a.cols, nfull = cols / W;
+  const float* x = a.X + row * cols + lane * LPL;
+  float v[NST + 1][LPL];
+#pragma unroll
+  for (int t = 0; t < NST; ++t) {
+    if (t < nfull) {
+      if constexpr (LPL == 4) {
+        const float4 f = *(const float4*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y; v[t][2] = f.z; v[t][3] = f.w;
+      } else if constexpr (LPL == 2) {
+        const float2 f = *(const float2*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y;
+      } else {
+        v[t][0] = x[(int64_t)t * W];
+      }
+    }
+  }
+  bool has[LPL];   // the short last step's elements present in this lane
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) {
+    has[u] = nfull * W + lane * LPL + u < cols;
+    v[NST][u] = has[u] ? x[nfull * W + u] : 0.0f;
+  }
+  float m = -__builtin_inff();
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) m = max_nan(m, v[t][u]);
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) m = max_nan(m, v[NST][u]);
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) m = max_nan(m, __shfl_xor(m, k, 64));
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) v[t][u] = exp_f32(v[t][u] - m);
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) v[NST][u] = exp_f32(v[NST][u] - m);
+  float s[LPL];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) s[u] = nfull ? v[0][u] : -0.0f;
+#pragma unroll
+  for (int t = 1; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + v[t][u];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) s[u] = nfull ? s[u] + v[NST][u] : v[NST][u];
+  float r;
+  if constexpr (!DOWN) {
+#pragma unroll
+    for (int h = 1; h < LPL; h <<= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
+    r = s[0];
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) r = r + __shfl_xor(r, k, 64);
+  } else {
+#pragma unroll
+    for (int k = 32; k >= 1; k >>= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], k, 64);
+#pragma unroll
+    for (int h = LPL / 2; h >= 1; h >>= 1)
+#pragma unroll
+      for (int u = 0; u < h; ++u) s[u] = s[u] + s[u + h];
+    r = s[0];
+  }
+  const float rinv = 1.0f / r;
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull) {
+      const int64_t j = (int64_t)t * W + lane * LPL;
+      float y[LPL];
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) y[u] = v[t][u] * rinv;
+      if (a.out_bf16) {
+        uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
+        if constexpr (LPL == 4)
+          *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
+                              (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+        else if constexpr (LPL == 2)
+          *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+        else
+          yp[0] = f32_bf16(y[0]);
+      } else {
+        float* yp = (float*)a.Y + row * cols + j;
+        if constexpr (LPL == 4) *(float4*)yp = float4{y[0], y[1], y[2], y[3]};
+        else if constexpr (LPL == 2) *(float2*)yp = float2{y[0], y[1]};
+        else yp[0] = y[0];
+      }
+    }
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) {
+      const int64_t j = nfull * W + lane * LPL + u;
+      const float y = v[NST][u] * rinv;
+      if (a.out_bf16) ((uint16_t*)a.Y)[row * cols + j] = f32_bf16(y);
+      else ((float*)a.Y)[row * cols + j] = y;
+    }
+}
+
+bool softmax_fused_ok(const RowsumArgs& r, const NormArgs& a) { return rmsnorm_fused_ok(r, a); }
+
+template <int W, bool DOWN>
+static void launch_smx_w(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)((a.rows + RS_WAVES - 1) / RS_WAVES)), block(64 * RS_WAVES);
+  hipLaunchKernelGGL((softmax_strided_fused<W, DOWN>), grid, block, 0, st, r, a);
+}
+
+hipError_t launch_softmax_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  if (r.leaf_w == 64) r.down ? launch_smx_w<64, true>(r, a, st) : launch_smx_w<64, false>(r, a, st);
+  else if (r.leaf_w == 128) r.down ? launch_smx_w<128, true>(r, a, st) : launch_smx_w<128, false>(r, a, st);
+  else if (r.leaf_w == 256) r.down ? launch_smx_w<256, true>(r, a, st) : launch_smx_w<256, false>(r, a, st);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// Three-pass path, first pass: one workgroup per row finds the maximum
+// (order free) and writes e_j = exp(x_j - m) as fp32 to a.Y.
+__global__ __launch_bounds__(256) void softmax_exp(NormArgs a) {
+  __shared__ float wm[4];
+  const int64_t row = blockIdx.x, cols = a.cols;
+  const float* x = a.X + row * cols;
+  float m = -__builtin_inff();
+  for (int64_t j = threadIdx.x; j < cols; j += 256) m = max_nan(m, x[j]);
+#pragma unroll
+  for (int k = 1; k < 64; k <<= 1) m = max_nan(m, __shfl_xor(m, k, 64));
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  m = max_nan(max_nan(wm[0], wm[1]), max_nan(wm[2], wm[3]));
+  float* e = (float*)a.Y + row * cols;
+  for (int64_t j = threadIdx.x; j < cols; j += 256) e[j] = exp_f32(x[j] - m);
+}
+
+hipError_t launch_softmax_exp(const NormArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(softmax_exp, dim3((unsigned)a.rows), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
