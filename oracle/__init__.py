@@ -85,6 +85,7 @@ def _bind(path):
     L.dgo_rowsum.argtypes = [P, vp, vp, i64, i64, i32]
     L.dgo_rmsnorm.argtypes = [P, vp, vp, f32, vp, vp, i64, i64, i32]
     L.dgo_softmax.argtypes = [P, vp, vp, i64, i64, i32]
+    L.dgo_layernorm.argtypes = [P, vp, vp, vp, f32, vp, i64, i64, i32]
     L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
     L.dgo_group_update.restype = f32
     L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
@@ -228,6 +229,22 @@ def rmsnorm(desc, X, w=None, eps=0.0, nthreads=None, with_rinv=False):
     if st:
         raise OracleError("dgo_rmsnorm status %d" % st)
     return (Y, rinv) if with_rinv else Y
+
+
+def layernorm(desc, X, w=None, b=None, eps=0.0, nthreads=None):
+    """Layer normalisation of each row of X (fp32), both row sums in the
+    descriptor's order, then the weight and bias (bf16 bits or None)."""
+    X = np.ascontiguousarray(X, dtype=np.float32)
+    rows, cols = X.shape
+    p, keep = params(desc)
+    w = None if w is None else _u16(w)
+    b = None if b is None else _u16(b)
+    Y = np.zeros((rows, cols), dtype=np.uint16 if p.out_bf16 else np.float32)
+    st = lib().dgo_layernorm(ctypes.byref(p), X.ctypes.data, _ptr(w), _ptr(b), float(np.float32(eps)),
+                             Y.ctypes.data, rows, cols, nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_layernorm status %d" % st)
+    return Y
 
 
 def softmax(desc, X, nthreads=None):

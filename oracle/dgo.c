@@ -713,6 +713,50 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
   return 0;
 }
 
+/* ------------------------------------------------- layer normalisation */
+
+/* The centred form: the mean first (the descriptor's SUM), then the
+ * descriptor's sum of squares of the centred values, so no large
+ * cancellation of E[x^2] - mean^2 enters the variance. */
+int dgo_layernorm(const dgo_params* p, const float* X, const uint16_t* w, const uint16_t* b,
+                  float eps, void* Y, int64_t rows, int64_t cols, int nthreads) {
+  if (p->leaf_w < 1 || rows < 0 || cols < 0) return 1;
+  const int64_t L = leaf_count(p, cols);
+  const float n = (float)cols;
+  dgo_params ps = *p, pq = *p;
+  ps.sumsq = 0;
+  pq.sumsq = 1;
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    float* leaves = (float*)malloc(sizeof(float) * (size_t)(L > 0 ? L : 1));
+    float* d = (float*)malloc(sizeof(float) * (size_t)(cols > 0 ? cols : 1));
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t r = 0; r < rows; ++r) {
+      const float* x = X + r * cols;
+      if (cols == 0) continue;
+      float mean = row_reduce(&ps, x, cols, leaves) / n;
+      for (int64_t j = 0; j < cols; ++j) d[j] = x[j] - mean;
+      float s2 = row_reduce(&pq, d, cols, leaves);
+      float var = s2 / n;
+      float v = var + eps;
+      float q = sqrtf(v);
+      float rinv = 1.0f / q;
+      for (int64_t j = 0; j < cols; ++j) {
+        float y = d[j] * rinv;
+        if (p->norm_pre_round) y = rnbf(y);
+        if (w) y = y * dgo_bf16_to_f32(w[j]);
+        if (b) y = y + dgo_bf16_to_f32(b[j]);
+        if (p->out_bf16) ((uint16_t*)Y)[r * cols + j] = dgo_f32_to_bf16(y);
+        else ((float*)Y)[r * cols + j] = y;
+      }
+    }
+    free(leaves);
+    free(d);
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------- softmax */
 
 /* The normalisation on the other side of a row sum (the paper evaluates

@@ -112,6 +112,17 @@ int dgo_rowsum(const dgo_params* p, const float* X, float* out, int64_t rows,
 int dgo_rmsnorm(const dgo_params* p, const float* X, const uint16_t* w, float eps,
                 void* Y, float* rinv, int64_t rows, int64_t cols, int nthreads);
 
+/* Layer normalisation of each row, both row sums in the descriptor's leaf
+ * order (leaf_w, leaf_strided, fold_down; the squares by the fma rule):
+ *   s1 = sum of x_j,  mean = RN32(s1 / n),  d_j = RN32(x_j - mean),
+ *   s2 = sum of squares of the d_j,  then as dgo_rmsnorm from s2:
+ *   v = RN32(RN32(s2 / n) + eps), q = RN32(sqrt(v)), rinv = RN32(1 / q),
+ *   y_j = RN32(d_j * rinv), y'_j = y_j or RN_bf16(y_j) (norm_pre_round),
+ *   out_j = RN_out(RN32(RN32(y'_j * w_j) + b_j)), each of w, b optional
+ *   (NULL: the step is left out).  w, b hold cols bf16 values. */
+int dgo_layernorm(const dgo_params* p, const float* X, const uint16_t* w, const uint16_t* b,
+                  float eps, void* Y, int64_t rows, int64_t cols, int nthreads);
+
 /* Softmax of each row:  m = the row's largest element (a NaN anywhere makes
  * it NaN; exact, so independent of order),  e_j = dgo_exp(RN32(x_j - m)),
  * s = the sum of the e_j in the descriptor's leaf order (as dgo_rowsum with

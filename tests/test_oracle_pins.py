@@ -861,3 +861,64 @@ def test_softmax_special_values():
     got = oracle.softmax(dict(leaf_w=64), X)
     assert np.all(np.isnan(got[0])) and np.all(np.isnan(got[1]))
     assert got[2].tolist() == [0.5, 0.0, 0.5]
+
+
+# ----------------------------------------------------- layer normalisation
+
+
+def test_layernorm_closed_forms():
+    """Rows c + a, c - a, c + a, ... over a power-of-two width, a a power of
+    two: the sum, mean c, centred values +-a, their squares and the variance
+    a^2 are all exact, so the normalised values are +-1 and the output is
+    +-w + b rounded once."""
+    rng = np.random.default_rng(71)
+    for cols in (2, 64, 256, 4096):
+        for c, a in ((0.0, 1.0), (3.0, 0.25), (-1000.0, 8.0), (2.0 ** 20, 2.0 ** -3)):
+            sign = np.tile(np.array([1.0, -1.0], dtype=np.float32), (3, cols // 2))
+            X = (np.float32(c) + sign * np.float32(a)).astype(np.float32)
+            w = inputs.normal_bf16(cols + 1, (cols,), 1.0)
+            b = inputs.normal_bf16(cols + 2, (cols,), 1.0)
+            wf, bf_ = inputs.bf16_bits_to_f32(w), inputs.bf16_bits_to_f32(b)
+            for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down"), dict(leaf_w=1)):
+                assert np.array_equal(oracle.layernorm(d, X), sign), (cols, c, a, d)
+                want = (sign * wf + bf_).astype(np.float32)
+                assert np.array_equal(oracle.layernorm(d, X, w, b), want), (cols, c, a, d)
+
+
+def test_layernorm_steps_and_rounding_points():
+    """Each row: the mean from the descriptor-ordered sum, the centred values,
+    their descriptor-ordered sum of squares, IEEE sqrt and reciprocal, then
+    the products and the bias; with pre_weight the normalised value is
+    rounded to bf16 (torch's conversion) before the weight."""
+    import torch
+    X = (inputs.lognormal_f32(72, (6, 300), sigma=1.0) + 5).astype(np.float32)
+    w = inputs.normal_bf16(73, (300,), 1.0)
+    b = inputs.normal_bf16(74, (300,), 1.0)
+    wf, bf_ = inputs.bf16_bits_to_f32(w), inputs.bf16_bits_to_f32(b)
+    for d in (dict(leaf_w=64), dict(leaf_w=32, leaf_layout="strided", lane_fold="down", fma=0)):
+        for nr in ("final", "pre_weight"):
+            got = oracle.layernorm(dict(d, norm_round=nr), X, w, b, eps=1e-5)
+            for r in range(6):
+                s1 = oracle.rowsum(dict(d, reduce="sum"), X[r:r + 1])[0]
+                mean = np.float32(s1 / np.float32(300))
+                dd = (X[r] - mean).astype(np.float32)
+                s2 = oracle.rowsum(dict(d, reduce="sumsq"), dd[None, :])[0]
+                v = rn32(f(rn32(f(s2) / 300)) + f(np.float32(1e-5)))
+                rinv = rn32(1 / f(rn32_sqrt(f(v))))
+                y = (dd * rinv).astype(np.float32)
+                if nr == "pre_weight":
+                    y = torch.from_numpy(y).to(torch.bfloat16).float().numpy()
+                want = ((y * wf).astype(np.float32) + bf_).astype(np.float32)
+                assert np.array_equal(got[r], want), (d, nr, r)
+
+
+def test_layernorm_within_fp64_bound():
+    """Against float64 on rows with a large common offset (the centred form
+    keeps the variance accurate)."""
+    X = (inputs.lognormal_f32(75, (32, 4096), sigma=1.0) + 100).astype(np.float32)
+    X64 = X.astype(np.float64)
+    mu = X64.mean(1, keepdims=True)
+    ref = (X64 - mu) / np.sqrt(((X64 - mu) ** 2).mean(1, keepdims=True) + np.float64(np.float32(1e-5)))
+    for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down")):
+        got = oracle.layernorm(d, X, eps=1e-5).astype(np.float64)
+        assert np.all(np.abs(got - ref) <= 2.0 ** -12 * (np.abs(ref) + 1)), d

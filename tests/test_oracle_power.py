@@ -59,6 +59,12 @@ MUTANTS = {
     "softmax divides instead of multiplying": ("float y = e[j] * rinv;", "float y = e[j] / s;"),
     "softmax sums in index order": ("float s = row_reduce(p, e, cols, leaves);",
                                     "float s = 0.0f;\n      for (int64_t j = 0; j < cols; ++j) s = s + e[j];"),
+    "layernorm squares the uncentred values": ("for (int64_t j = 0; j < cols; ++j) d[j] = x[j] - mean;",
+                                               "for (int64_t j = 0; j < cols; ++j) d[j] = x[j] - 0.0f * mean;"),
+    "layernorm bias before the weight": (
+        "if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (b) y = y + dgo_bf16_to_f32(b[j]);",
+        "if (b) y = y + dgo_bf16_to_f32(b[j]);\n        if (w) y = y * dgo_bf16_to_f32(w[j]);"),
+    "layernorm variance over cols - 1": ("float var = s2 / n;", "float var = s2 / (n - 1.0f);"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
     "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
@@ -91,6 +97,8 @@ CHECKS = [
     lambda: pins.test_rmsnorm_follows_the_rowsum_order_and_rounding_points(),
     lambda: pins.test_softmax_closed_forms(),
     lambda: pins.test_softmax_steps_and_rounding_points(),
+    lambda: pins.test_layernorm_closed_forms(),
+    lambda: pins.test_layernorm_steps_and_rounding_points(),
 ]
 
 
