@@ -46,12 +46,13 @@ MUTANTS = {
                                             "if (p->fold_down) return dgo_tree(leaves, (int)L, 0);"),
     "bit reversal one bit short": ("while ((1 << b) < P) ++b;", "while ((2 << b) < P) ++b;"),
     "empty lane adds zero": ("t[k] = (hl && hr) ? l + r : (hl ? l : r);", "t[k] = l + r;"),
-    "mean over cols - 1": ("const float n = (float)cols;", "const float n = (float)(cols - 1);"),
+    "mean over cols - 1": ("const float n = (float)cols;\n  if (nthreads < 1)",
+                           "const float n = (float)(cols - 1);\n  if (nthreads < 1)"),
     "eps added after the root": ("float v = ms + eps;\n      float q = sqrtf(v);",
                                  "float v = ms;\n      float q = sqrtf(v) + eps;"),
     "weight before the bf16 rounding": (
-        "if (p->norm_pre_round) y = rnbf(y);\n        if (w) y = y * dgo_bf16_to_f32(w[j]);",
-        "if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (p->norm_pre_round) y = rnbf(y);"),
+        "if (p->norm_pre_round) y = rnbf(y);\n        if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (p->out_bf16)",
+        "if (w) y = y * dgo_bf16_to_f32(w[j]);\n        if (p->norm_pre_round) y = rnbf(y);\n        if (p->out_bf16)"),
     "rmsnorm sums the row in index order": ("float s = row_reduce(p, x, cols, leaves);",
                                             "float s = 0.0f;\n      for (int64_t k = 0; k < cols; ++k) s = fmaf(x[k], x[k], s);"),
     "softmax without the max shift": ("for (int64_t j = 0; j < cols; ++j) e[j] = dgo_exp(x[j] - m);",
