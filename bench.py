@@ -175,6 +175,12 @@ def main():
     desc_smx = dict(leaf_w=256, leaf_layout="strided", lane_fold="down", reduce="sum", out="bf16")
     D_smx = dg.Desc(**desc_smx)
     Y_smx = torch.empty(X.shape, dtype=torch.bfloat16, device=dev)
+    # layer normalisation, same lanes, bf16 weight and bias, bf16 out
+    desc_ln = dict(leaf_w=256, leaf_layout="strided", lane_fold="down", out="bf16")
+    D_ln = dg.Desc(**desc_ln)
+    b_ln = inputs.normal_bf16(11, (X.shape[1],), 1.0)
+    db_ln = d_bf16(b_ln)
+    Y_ln = torch.empty(X.shape, dtype=torch.bfloat16, device=dev)
 
     C_sw = {M: torch.empty((M, 4096), dtype=torch.bfloat16, device=dev) for M in inputs.SWEEP_M}
     C_dec = {c: torch.empty((8, 4096), dtype=torch.bfloat16, device=dev) for c in ("seq", "tree")}
@@ -291,6 +297,21 @@ def main():
                           "frac_hbm": round(smx_bytes / ms_smx / 1e6 / PEAK_HBM_GBS, 4),
                           "what": "max shift, own exp, sum over 256 strided lanes (count-down fold), one "
                                   "reciprocal, bf16 out; bytes = X + Y once"}
+    for _ in range(args.warmup):
+        dg.dg_layernorm(D_ln, dX, dw_rms, db_ln, 1e-5, Y_ln, stream=sptr)
+    a, b = ev(), ev()
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(args.steps):
+        dg.dg_layernorm(D_ln, dX, dw_rms, db_ln, 1e-5, Y_ln, stream=sptr)
+    b.record(stream)
+    torch.cuda.synchronize()
+    ms_ln = a.elapsed_time(b) / args.steps
+    ln_bytes = X.nbytes + X.size * 2 + X.shape[1] * 4
+    rs["layernorm_bf16"] = {"ms": round(ms_ln, 4), "GB/s": round(ln_bytes / ms_ln / 1e6, 1),
+                            "frac_hbm": round(ln_bytes / ms_ln / 1e6 / PEAK_HBM_GBS, 4),
+                            "what": "mean and centred sum of squares over 256 strided lanes (count-down "
+                                    "fold), bf16 weight and bias, bf16 out; bytes = X + Y once"}
     rs["rmsnorm_bf16"] = {"ms": round(ms, 4), "GB/s": round(rms_bytes / ms / 1e6, 1),
                           "frac_hbm": round(rms_bytes / ms / 1e6 / PEAK_HBM_GBS, 4),
                           "what": "sum of squares over 256 strided lanes (count-down fold), then "
@@ -308,6 +329,7 @@ def main():
             torch.sum(dX * dX, 1)
             (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16) * dw_rms
             torch.softmax(dX, 1).to(torch.bfloat16)
+            torch.nn.functional.layer_norm(dX, (X.shape[1],), dw_rms.float(), db_ln.float(), 1e-5).to(torch.bfloat16)
             for M in inputs.SWEEP_M:
                 torch.matmul(dA_sw_M[M], Bs_f)
         torch.cuda.synchronize()
@@ -330,6 +352,9 @@ def main():
         t_rms = timeit(lambda i: (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16)
                        * dw_rms, args.steps)
         t_smx = timeit(lambda i: torch.softmax(dX, 1).to(torch.bfloat16), args.steps)
+        wf_ln, bf_ln = dw_rms.float(), db_ln.float()
+        t_ln = timeit(lambda i: torch.nn.functional.layer_norm(dX, (X.shape[1],), wf_ln, bf_ln, 1e-5)
+                      .to(torch.bfloat16), args.steps)
         t_sw_m = {M: timeit(lambda i, M=M: torch.matmul(dA_sw_M[M], dB_sw[i % len(dB_sw)]), args.steps)
                   for M in inputs.SWEEP_M}
         free = {"sweep_ms": round(t_sw, 4), "decode_ms_per_launch": round(t_dec, 4), "mlp_ms": round(t_mlp, 4),
@@ -344,11 +369,14 @@ def main():
                 "cost_rmsnorm": round(rs["rmsnorm_bf16"]["ms"] / t_rms, 3),
                 "softmax_ms": round(t_smx, 4),
                 "cost_softmax": round(rs["softmax_bf16"]["ms"] / t_smx, 3),
+                "layernorm_ms": round(t_ln, 4),
+                "cost_layernorm": round(rs["layernorm_bf16"]["ms"] / t_ln, 3),
                 "sweep_ms_by_M": {str(M): round(t, 4) for M, t in t_sw_m.items()},
                 "cost_sweep_by_M": {str(M): round(shapes["sweep_M%d" % M]["us_mean"] * 1e-3 / t, 3)
                                     for M, t in t_sw_m.items()},
                 "what": ("torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum / x * rsqrt(mean(x^2) + eps) "
-                         "-> bf16 * w / torch.softmax -> bf16 on the same shapes; cost = t_dg / t_free")}
+                         "-> bf16 * w / torch.softmax -> bf16 / layer_norm -> bf16 on the same shapes; "
+                         "cost = t_dg / t_free")}
     except Exception as exc:  # the library under test never depends on this
         free = {"error": repr(exc)}
 
@@ -431,6 +459,10 @@ def main():
     got_smx = host(Y_smx)[rr]
     checked += want_smx.size
     matched += int(np.sum(got_smx == want_smx))
+    want_ln = oracle.layernorm(desc_ln, X[rr], w_rms, b_ln, eps=1e-5)
+    got_ln = host(Y_ln)[rr]
+    checked += want_ln.size
+    matched += int(np.sum(got_ln == want_ln))
 
     # ------------------------------------------------------- CPU baseline
     ncpu = os.cpu_count() or 1

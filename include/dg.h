@@ -231,6 +231,26 @@ dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
 dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
                      int64_t rows, int64_t cols, void* stream);
 
+/* Layer normalisation of each row in the centred form, both row sums in the
+ * descriptor's leaf order (leaf_w, leaf_layout, lane_fold; the squares by
+ * its fma rule; reduce_op is not used):
+ *   s1 = the sum of x_j,  mean = s1 / n (n = cols as binary32),
+ *   d_j = x_j - mean,  s2 = the sum of squares of the d_j,
+ *   v = s2 / n + eps,  rinv = 1 / sqrt(v),  y_j = d_j * rinv,
+ *   y'_j = y_j (DG_NORM_FINAL) or RN_bf16(y_j) (DG_NORM_PRE_WEIGHT),
+ *   out_j = RN_out((y'_j * w_j) + b_j),
+ * each step one IEEE binary32 operation; w and b (device, cols bf16 each)
+ * are optional (NULL leaves the step out).  The paper evaluates layernorm
+ * kernels (Sec. 7); the two sums are the order-sensitive steps.
+ *   X: device, rows x cols fp32;  Y: device, rows x cols of out_dtype (may
+ *   not overlap X).  rows = 0 or cols = 0 is a no-op.  One launch for
+ *   strided lanes (64, 128 or 256) with rows of at most 8192 aligned
+ *   elements; otherwise four launches through a library-owned workspace of
+ *   rows x (cols + 2) fp32 values per (device, stream).  Errors as
+ *   dg_rowsum. */
+dg_status dg_layernorm(const dg_desc* d, const float* X, const void* w, const void* b, float eps,
+                       void* Y, int64_t rows, int64_t cols, void* stream);
+
 /* Softmax of each row, the row sum in the descriptor's order (exactly the
  * value dg_rowsum returns for the descriptor with reduce_op DG_OP_SUM:
  * leaf_w, leaf_layout and lane_fold apply; reduce_op must be DG_OP_SUM):

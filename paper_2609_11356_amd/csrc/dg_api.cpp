@@ -514,6 +514,59 @@ dg_status dg_softmax(const dg_desc* d, const float* X, void* Y, int64_t rows, in
   return DG_OK;
 }
 
+dg_status dg_layernorm(const dg_desc* d, const float* X, const void* w, const void* b, float eps, void* Y,
+                       int64_t rows, int64_t cols, void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (rows < 0 || cols < 0) return DG_ERR_SHAPE;
+  if (rows == 0 || cols == 0) return DG_OK;
+  if (!X || !Y) return DG_ERR_INVALID;
+  const bool out_bf16 = d->p.out_dtype == DG_BF16;
+  if (!aligned(X, 4) || !aligned(Y, out_bf16 ? 2 : 4) || (w && !aligned(w, 2)) || (b && !aligned(b, 2)))
+    return DG_ERR_ALIGN;
+  if (rows > (int64_t)0x7fffffff) return DG_ERR_SHAPE;
+  hipStream_t st = (hipStream_t)stream;
+  dg::RowsumArgs a = rowsum_args(d, X, nullptr, rows, cols);
+  a.eps = eps;
+  dg::NormArgs n;
+  std::memset(&n, 0, sizeof n);
+  n.X = X;
+  n.w = (const uint16_t*)w;
+  n.b = (const uint16_t*)b;
+  n.Y = Y;
+  n.rows = rows;
+  n.cols = cols;
+  n.out_bf16 = out_bf16;
+  n.pre_round = d->p.norm_round == DG_NORM_PRE_WEIGHT;
+  if (dg::rmsnorm_fused_ok(a, n)) {
+    if (dg::launch_layernorm_fused(a, n, st) != hipSuccess) return DG_ERR_HIP;
+    return DG_OK;
+  }
+  // means, centred values, reciprocal roots, then the scaling
+  void* ws = nullptr;
+  dg_status s = get_workspace(st, (size_t)rows * (size_t)(cols + 2) * sizeof(float), &ws);
+  if (s != DG_OK) return s;
+  float* D = (float*)ws;
+  float* mean = D + rows * cols;
+  float* rinv = mean + rows;
+  a.sumsq = 0;
+  a.out = mean;
+  a.rms = 3;
+  if (dg::launch_rowsum(a, st) != hipSuccess) return DG_ERR_HIP;
+  dg::NormArgs c = n;
+  c.rinv = mean;
+  c.Y = D;
+  if (dg::launch_layernorm_center(c, st) != hipSuccess) return DG_ERR_HIP;
+  a.X = D;
+  a.sumsq = 1;
+  a.out = rinv;
+  a.rms = 1;
+  if (dg::launch_rowsum(a, st) != hipSuccess) return DG_ERR_HIP;
+  n.X = D;
+  n.rinv = rinv;
+  if (dg::launch_rmsnorm_scale(n, st) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
 dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps, void* Y,
                      int64_t rows, int64_t cols, void* stream) {
   if (!d || d->p.reduce_op != DG_OP_SUMSQ) return DG_ERR_INVALID;
@@ -528,6 +581,7 @@ dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps,
   a.rms = 1;
   a.eps = eps;
   dg::NormArgs n;
+  std::memset(&n, 0, sizeof n);
   n.X = X;
   n.rinv = nullptr;
   n.w = (const uint16_t*)w;

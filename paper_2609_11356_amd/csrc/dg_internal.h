@@ -48,7 +48,7 @@ struct RowsumArgs {
   int32_t leaf_w, sumsq, fma;
   int32_t strided, down;         // leaf layout and lane fold
   int32_t rms;                   // 1: out[row] = the RMS-norm reciprocal root of the sum,
-                                 // 2: out[row] = 1 / sum
+                                 // 2: out[row] = 1 / sum, 3: out[row] = sum / cols
   float eps;
 };
 
@@ -56,6 +56,7 @@ struct NormArgs {
   const float* X;
   const float* rinv;             // per row
   const uint16_t* w;             // bf16 weight or null
+  const uint16_t* b;             // bf16 bias or null
   void* Y;
   int64_t rows, cols;
   int32_t out_bf16, pre_round;
@@ -85,5 +86,9 @@ hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStrea
 bool softmax_fused_ok(const RowsumArgs& r, const NormArgs& a);
 hipError_t launch_softmax_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
 hipError_t launch_softmax_exp(const NormArgs& a, hipStream_t s);
+// layer normalisation: one pass (strided lanes, row in registers), or the
+// centred values into a.Y given the means in a.rinv (three-pass path)
+hipError_t launch_layernorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
+hipError_t launch_layernorm_center(const NormArgs& a, hipStream_t s);
 
 }  // namespace dg

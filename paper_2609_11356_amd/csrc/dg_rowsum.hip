@@ -145,7 +145,7 @@ __global__ __launch_bounds__(256) void rowsum_kernel(RowsumArgs a) {
   }
   if (live && lane == 0) {
     const float v = have ? r : 0.0f;
-    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : v;
+    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : a.rms == 3 ? v / (float)cols : v;
   }
 }
 
@@ -247,7 +247,7 @@ __global__ __launch_bounds__(256) void rowsum_strided(RowsumArgs a) {
   }
   if (live && q == 0) {
     const float v = cols ? r : 0.0f;
-    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : v;
+    a.out[row] = a.rms == 1 ? rms_inv(v, cols, a.eps) : a.rms == 2 ? 1.0f / v : a.rms == 3 ? v / (float)cols : v;
   }
 }
 
@@ -305,6 +305,7 @@ __global__ __launch_bounds__(256) void rmsnorm_scale(NormArgs a) {
     float y = xv * r;
     if (a.pre_round) y = round_bf16(y);
     if (a.w) y = y * bf16_f32(a.w[j]);
+    if (a.b) y = y + bf16_f32(a.b[j]);
     return y;
   };
   if (VEC) {
@@ -322,7 +323,7 @@ __global__ __launch_bounds__(256) void rmsnorm_scale(NormArgs a) {
         const int64_t j = j0 + 1024 * i;
         if (j >= cols) break;
         float y0, y1, y2, y3;
-        if (a.w && ((uintptr_t)a.w) % 8 == 0) {
+        if (a.w && !a.b && ((uintptr_t)a.w) % 8 == 0) {
           // the four weights in one 8-byte load
           const uint2 q = *(const uint2*)&a.w[j];
           const float xs[4] = {xv[i].x, xv[i].y, xv[i].z, xv[i].w};
@@ -523,6 +524,210 @@ hipError_t launch_rmsnorm_fused(const RowsumArgs& r, const NormArgs& a, hipStrea
   else if (r.leaf_w == 128) r.down ? launch_fused_w<128, true>(r, a, st) : launch_fused_w<128, false>(r, a, st);
   else if (r.leaf_w == 256) r.down ? launch_fused_w<256, true>(r, a, st) : launch_fused_w<256, false>(r, a, st);
   else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// ------------------------------------------------- layer normalisation
+
+// The lanes' partial results meet in the descriptor's tree (W lanes, leaf
+// q LPL + u in lane q, slot u): leaf order = in-lane levels then the xor
+// butterfly counting up; bit-reversed order = the butterfly counting down
+// then the in-lane levels from the highest leaf bit.  Every lane ends with
+// the result.
+template <int LPL, bool DOWN>
+__device__ __forceinline__ float lanes_meet(float (&s)[LPL]) {
+  if constexpr (!DOWN) {
+#pragma unroll
+    for (int h = 1; h < LPL; h <<= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
+    float r = s[0];
+#pragma unroll
+    for (int k = 1; k < 64; k <<= 1) r = r + __shfl_xor(r, k, 64);
+    return r;
+  } else {
+#pragma unroll
+    for (int k = 32; k >= 1; k >>= 1)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], k, 64);
+#pragma unroll
+    for (int h = LPL / 2; h >= 1; h >>= 1)
+#pragma unroll
+      for (int u = 0; u < h; ++u) s[u] = s[u] + s[u + h];
+    return s[0];
+  }
+}
+
+// One pass for strided lanes (W = 64, 128, 256), rows of at most 8192, the
+// row in registers as in rmsnorm_strided_fused: the sum (the descriptor's
+// leaf folds and tree) gives the mean, the values are centred in place,
+// their sum of squares (same order, the fma rule OP) gives the reciprocal
+// root, then y = d * rinv, the optional bf16 rounding, weight and bias
+// (staged in LDS once per workgroup).
+template <int W, int OP, bool DOWN>
+__global__ __launch_bounds__(256) void layernorm_strided_fused(RowsumArgs ra, NormArgs a) {
+  constexpr int LPL = W / 64, NST = 128 / LPL;
+  constexpr int fma = OP == 1;
+  __shared__ __attribute__((aligned(16))) uint16_t wl[8192];
+  __shared__ __attribute__((aligned(16))) uint16_t bl[8192];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t row = (int64_t)blockIdx.x * RS_WAVES + wave;
+  const bool live = row < a.rows;
+  const int64_t cols = a.cols, nfull = live ? cols / W : 0;
+  const float* x = a.X + (live ? row : 0) * cols + lane * LPL;
+  auto stage = [&](const uint16_t* g, uint16_t* l) {
+    if (((uintptr_t)g) % 16 == 0 && cols % 8 == 0) {
+      for (int64_t j = 8 * (int64_t)threadIdx.x; j < cols; j += 8 * 256) *(uint4*)&l[j] = *(const uint4*)&g[j];
+    } else {
+      for (int64_t j = threadIdx.x; j < cols; j += 256) l[j] = g[j];
+    }
+  };
+  if (a.w) stage(a.w, wl);
+  if (a.b) stage(a.b, bl);
+  __syncthreads();
+  float v[NST + 1][LPL];
+#pragma unroll
+  for (int t = 0; t < NST; ++t) {
+    if (t < nfull) {
+      if constexpr (LPL == 4) {
+        const float4 f = *(const float4*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y; v[t][2] = f.z; v[t][3] = f.w;
+      } else if constexpr (LPL == 2) {
+        const float2 f = *(const float2*)(x + (int64_t)t * W);
+        v[t][0] = f.x; v[t][1] = f.y;
+      } else {
+        v[t][0] = x[(int64_t)t * W];
+      }
+    }
+  }
+  bool has[LPL];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) {
+    has[u] = live && nfull * W + lane * LPL + u < cols;
+    v[NST][u] = has[u] ? x[nfull * W + u] : 0.0f;
+  }
+  // the mean
+  float s[LPL];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) s[u] = nfull ? v[0][u] : -0.0f;
+#pragma unroll
+  for (int t = 1; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = s[u] + v[t][u];
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) s[u] = nfull ? s[u] + v[NST][u] : v[NST][u];
+  const float mean = lanes_meet<LPL, DOWN>(s) / (float)cols;
+  // centre in place; the sum of squares of the centred values
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) v[t][u] = v[t][u] - mean;
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) v[NST][u] = v[NST][u] - mean;
+#pragma unroll
+  for (int u = 0; u < LPL; ++u) s[u] = nfull ? v[0][u] * v[0][u] : -0.0f;
+#pragma unroll
+  for (int t = 1; t < NST; ++t)
+    if (t < nfull)
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) s[u] = leaf_step(s[u], v[t][u], 1, fma);
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) s[u] = nfull ? leaf_step(s[u], v[NST][u], 1, fma) : v[NST][u] * v[NST][u];
+  const float rinv = rms_inv(lanes_meet<LPL, DOWN>(s), cols, ra.eps);
+  if (!live) return;
+  auto one = [&](float d, int64_t j) {
+    float y = d * rinv;
+    if (a.pre_round) y = round_bf16(y);
+    if (a.w) y = y * bf16_f32(wl[j]);
+    if (a.b) y = y + bf16_f32(bl[j]);
+    return y;
+  };
+  // the LPL bf16 values of a step in one LDS read
+  auto chunk = [&](const uint16_t* l, int64_t j, float* out) {
+    if constexpr (LPL == 4) {
+      const uint2 q = *(const uint2*)&l[j];
+      out[0] = bits_f32(q.x << 16); out[1] = bits_f32(q.x & 0xffff0000u);
+      out[2] = bits_f32(q.y << 16); out[3] = bits_f32(q.y & 0xffff0000u);
+    } else if constexpr (LPL == 2) {
+      const uint32_t q = *(const uint32_t*)&l[j];
+      out[0] = bits_f32(q << 16); out[1] = bits_f32(q & 0xffff0000u);
+    } else {
+      out[0] = bf16_f32(l[j]);
+    }
+  };
+#pragma unroll
+  for (int t = 0; t < NST; ++t)
+    if (t < nfull) {
+      const int64_t j = (int64_t)t * W + lane * LPL;
+      float y[LPL], wv[LPL], bv[LPL];
+      if (a.w) chunk(wl, j, wv);
+      if (a.b) chunk(bl, j, bv);
+#pragma unroll
+      for (int u = 0; u < LPL; ++u) {
+        float yy = v[t][u] * rinv;
+        if (a.pre_round) yy = round_bf16(yy);
+        if (a.w) yy = yy * wv[u];
+        if (a.b) yy = yy + bv[u];
+        y[u] = yy;
+      }
+      if (a.out_bf16) {
+        uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
+        if constexpr (LPL == 4)
+          *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
+                              (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+        else if constexpr (LPL == 2)
+          *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+        else
+          yp[0] = f32_bf16(y[0]);
+      } else {
+        float* yp = (float*)a.Y + row * cols + j;
+        if constexpr (LPL == 4) *(float4*)yp = float4{y[0], y[1], y[2], y[3]};
+        else if constexpr (LPL == 2) *(float2*)yp = float2{y[0], y[1]};
+        else yp[0] = y[0];
+      }
+    }
+#pragma unroll
+  for (int u = 0; u < LPL; ++u)
+    if (has[u]) {
+      const int64_t j = nfull * W + lane * LPL + u;
+      const float y = one(v[NST][u], j);
+      if (a.out_bf16) ((uint16_t*)a.Y)[row * cols + j] = f32_bf16(y);
+      else ((float*)a.Y)[row * cols + j] = y;
+    }
+}
+
+template <int W, bool DOWN>
+static void launch_ln_w(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  const dim3 grid((unsigned)((a.rows + RS_WAVES - 1) / RS_WAVES)), block(64 * RS_WAVES);
+  if (r.fma) hipLaunchKernelGGL((layernorm_strided_fused<W, 1, DOWN>), grid, block, 0, st, r, a);
+  else hipLaunchKernelGGL((layernorm_strided_fused<W, 2, DOWN>), grid, block, 0, st, r, a);
+}
+
+hipError_t launch_layernorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t st) {
+  if (r.leaf_w == 64) r.down ? launch_ln_w<64, true>(r, a, st) : launch_ln_w<64, false>(r, a, st);
+  else if (r.leaf_w == 128) r.down ? launch_ln_w<128, true>(r, a, st) : launch_ln_w<128, false>(r, a, st);
+  else if (r.leaf_w == 256) r.down ? launch_ln_w<256, true>(r, a, st) : launch_ln_w<256, false>(r, a, st);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+// Three-pass path, second pass: the centred values d_j = x_j - mean[row]
+// as fp32 into a.Y (a.rinv holds the means).
+__global__ __launch_bounds__(256) void layernorm_center(NormArgs a) {
+  const int64_t row = blockIdx.x, cols = a.cols;
+  const float m = a.rinv[row];
+  const float* x = a.X + row * cols;
+  float* d = (float*)a.Y + row * cols;
+  for (int64_t j = threadIdx.x; j < cols; j += 256) d[j] = x[j] - m;
+}
+
+hipError_t launch_layernorm_center(const NormArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(layernorm_center, dim3((unsigned)a.rows), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

@@ -67,11 +67,12 @@ def lib():
         L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
         L.dg_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_softmax.argtypes = [vp, vp, vp, i64, i64, vp]
+        L.dg_layernorm.argtypes = [vp, vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_strerror.argtypes = [ctypes.c_int]
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
         for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm",
-                  "dg_softmax"):
+                  "dg_softmax", "dg_layernorm"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -241,6 +242,23 @@ def dg_rmsnorm(desc: Desc, X, w, eps, Y, rows=None, cols=None, stream=None):
     return Y
 
 
+def dg_layernorm(desc: Desc, X, w, b, eps, Y, rows=None, cols=None, stream=None):
+    """Y = layer normalisation of the rows of X (fp32), both row sums in the
+    descriptor's order, then the bf16 weight and bias (each may be None)."""
+    import torch
+    if isinstance(X, torch.Tensor):
+        assert X.dtype == torch.float32 and X.is_contiguous() and X.is_cuda
+        assert Y.is_contiguous() and Y.is_cuda and Y.shape == X.shape
+        for t in (w, b):
+            assert t is None or (t.dtype == torch.bfloat16 and t.is_contiguous() and t.numel() == X.shape[1])
+        rows, cols = X.shape
+    st = lib().dg_layernorm(desc.handle, _ptr(X), _ptr(w), _ptr(b), ctypes.c_float(eps), _ptr(Y), rows, cols,
+                            _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_layernorm")
+    return Y
+
+
 def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
     """Y = softmax of the rows of X (fp32), the row sum in the descriptor's
     order (its reduce must be "sum")."""
@@ -258,4 +276,4 @@ def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
 def exported_symbols():
     """Names of the entry points include/dg.h declares."""
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs",
-            "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_strerror", "dg_version"]
+            "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_strerror", "dg_version"]

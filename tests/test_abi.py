@@ -173,6 +173,13 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_softmax(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
     assert lib.dg_softmax(d.handle, None, 16, 4, 5, None) == dg.DG_ERR_INVALID
     assert lib.dg_softmax(d.handle, 18, 16, 4, 5, None) == dg.DG_ERR_ALIGN
+    # layer normalisation
+    assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, 16, 0, 5, None) == dg.DG_OK
+    assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, 16, 4, 0, None) == dg.DG_OK
+    assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, 16, -1, 5, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, None, 4, 5, None) == dg.DG_ERR_INVALID
+    assert lib.dg_layernorm(d.handle, 16, None, 19, 0.0, 16, 4, 5, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_layernorm(None, 16, None, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_INVALID
     # row reduction
     assert lib.dg_rowsum(d.handle, 16, 16, 0, 5, None) == dg.DG_OK
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
