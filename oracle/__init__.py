@@ -86,6 +86,7 @@ def _bind(path):
     L.dgo_rmsnorm.argtypes = [P, vp, vp, f32, vp, vp, i64, i64, i32]
     L.dgo_softmax.argtypes = [P, vp, vp, i64, i64, i32]
     L.dgo_layernorm.argtypes = [P, vp, vp, vp, f32, vp, i64, i64, i32]
+    L.dgo_colsum.argtypes = [vp, i32, i64, i64, vp, i32]
     L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
     L.dgo_group_update.restype = f32
     L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
@@ -229,6 +230,19 @@ def rmsnorm(desc, X, w=None, eps=0.0, nthreads=None, with_rinv=False):
     if st:
         raise OracleError("dgo_rmsnorm status %d" % st)
     return (Y, rinv) if with_rinv else Y
+
+
+def colsum(C, nthreads=None):
+    """Column sums of a GEMM output C (fp32 values, or bf16 bits as uint16):
+    the balanced tree over each column's rows in order."""
+    C = np.ascontiguousarray(C)
+    assert C.dtype in (np.float32, np.uint16)
+    M, N = C.shape
+    out = np.zeros(N, dtype=np.float32)
+    st = lib().dgo_colsum(C.ctypes.data, int(C.dtype == np.uint16), M, N, out.ctypes.data, nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_colsum status %d" % st)
+    return out
 
 
 def layernorm(desc, X, w=None, b=None, eps=0.0, nthreads=None):

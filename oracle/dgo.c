@@ -757,6 +757,25 @@ int dgo_layernorm(const dgo_params* p, const float* X, const uint16_t* w, const 
   return 0;
 }
 
+/* ------------------------------------------------------ column sums */
+
+int dgo_colsum(const void* C, int out_bf16, int64_t M, int64_t N, float* colsum, int nthreads) {
+  if (M < 0 || N < 0) return 1;
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    float* col = (float*)malloc(sizeof(float) * (size_t)(M > 0 ? M : 1));
+#pragma omp for schedule(static)
+    for (int64_t j = 0; j < N; ++j) {
+      for (int64_t i = 0; i < M; ++i)
+        col[i] = out_bf16 ? dgo_bf16_to_f32(((const uint16_t*)C)[i * N + j]) : ((const float*)C)[i * N + j];
+      colsum[j] = dgo_tree(col, (int)M, 0);
+    }
+    free(col);
+  }
+  return 0;
+}
+
 /* ------------------------------------------------------------- softmax */
 
 /* The normalisation on the other side of a row sum (the paper evaluates

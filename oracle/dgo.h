@@ -89,6 +89,12 @@ int dgo_gemm(const dgo_params* p, const uint16_t* A, const uint16_t* B,
              const uint16_t* bias, void* C, int64_t M, int64_t N, int64_t K,
              int nthreads);
 
+/* Column sums of a GEMM's output (the epilogue reduction the paper times,
+ * Sec. 7): colsum[j] = the balanced tree (count-up, rows in order) over the
+ * M output values of column j, each taken as stored (a bf16 output widened
+ * exactly to fp32).  C holds M*N fp32 values or bf16 bits (out_bf16). */
+int dgo_colsum(const void* C, int out_bf16, int64_t M, int64_t N, float* colsum, int nthreads);
+
 /* Selected outputs (i[t], j[t]) of the same GEMM; out[t] is the output value
  * widened to fp32 (a bf16 output is exactly representable in fp32).  Row i of
  * A is read through A + i*K, so only the sampled rows need to exist. */

@@ -922,3 +922,26 @@ def test_layernorm_within_fp64_bound():
     for d in (dict(leaf_w=64), dict(leaf_w=256, leaf_layout="strided", lane_fold="down")):
         got = oracle.layernorm(d, X, eps=1e-5).astype(np.float64)
         assert np.all(np.abs(got - ref) <= 2.0 ** -12 * (np.abs(ref) + 1)), d
+
+
+# ------------------------------------------------- GEMM column-sum epilogue
+
+
+def test_colsum_is_the_tree_down_each_column():
+    """The hand walk down a column ([2^24, 1, -2^24, 1]: count-up tree 1,
+    where a chain gives 0 and the exact sum 2), bf16 outputs widened
+    exactly, small integers exact, and recursive halving over -0 padding
+    for any row count."""
+    C = np.array([[2.0 ** 24], [1.0], [-2.0 ** 24], [1.0]], dtype=np.float32)
+    assert oracle.colsum(C)[0] == 1.0
+    rng = np.random.default_rng(81)
+    Z = rng.integers(-1000, 1000, (777, 33)).astype(np.float32)
+    assert oracle.colsum(Z).tolist() == Z.sum(0, dtype=np.float64).tolist()
+    W = rng.integers(-250, 250, (777, 33)).astype(np.float32)      # bf16 holds these exactly
+    assert oracle.colsum(inputs.f32_to_bf16_bits(W)).tolist() == W.sum(0, dtype=np.float64).tolist()
+    X = inputs.lognormal_f32(82, (100, 5))
+    got = oracle.colsum(X)
+    for j in range(5):
+        p = 128
+        padded = np.concatenate([X[:, j], np.full(p - 100, -0.0, dtype=np.float32)])
+        assert got[j].view(np.uint32) == _halving(padded).view(np.uint32)
