@@ -254,6 +254,30 @@ def main():
     ms_per_step = total_ms / args.steps
     value = step_flops / (ms_per_step * 1e-3) / 1e12
 
+    # ------------------------------- GEMM with a column-sum epilogue (fp32 out)
+    desc_cs = dict(mma="16x16x32", tile_k=64)
+    D_cs = dg.Desc(**desc_cs)
+    C_cs = torch.empty((2048, 14336), dtype=torch.float32, device=dev)
+    cs_out = torch.empty(14336, dtype=torch.float32, device=dev)
+    colsum = {}
+    for name, fn in (("gemm_f32", lambda i: dg.dg_gemm(D_cs, dA_mlp, dB_mlp[i % len(dB_mlp)], None, C_cs,
+                                                         stream=sptr)),
+                     ("gemm_f32_colsum", lambda i: dg.dg_gemm_colsum(D_cs, dA_mlp, dB_mlp[i % len(dB_mlp)], None,
+                                                                       C_cs, cs_out, stream=sptr))):
+        for i in range(args.warmup):
+            fn(i)
+        a, b = ev(), ev()
+        torch.cuda.synchronize()
+        a.record(stream)
+        for i in range(args.steps):
+            fn(i)
+        b.record(stream)
+        torch.cuda.synchronize()
+        colsum[name + "_ms"] = round(a.elapsed_time(b) / args.steps, 4)
+    colsum["colsum_overhead_ms"] = round(colsum["gemm_f32_colsum_ms"] - colsum["gemm_f32_ms"], 4)
+    colsum["what"] = ("2048x14336x4096 GEMM, fp32 out, then the balanced tree down each of the 14336 columns "
+                      "(runs of 256 rows folded in parallel, then their roots)")
+
     # ------------------------------------------------------ row reduction
     rs_bytes = X.nbytes + X.shape[0] * 4
     rs = {}
@@ -329,6 +353,7 @@ def main():
             torch.sum(dX * dX, 1)
             (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16) * dw_rms
             torch.softmax(dX, 1).to(torch.bfloat16)
+            torch.matmul(dA_mlp, Bm_f).float().sum(0)
             torch.nn.functional.layer_norm(dX, (X.shape[1],), dw_rms.float(), db_ln.float(), 1e-5).to(torch.bfloat16)
             for M in inputs.SWEEP_M:
                 torch.matmul(dA_sw_M[M], Bs_f)
@@ -352,6 +377,7 @@ def main():
         t_rms = timeit(lambda i: (dX * torch.rsqrt(dX.pow(2).mean(1, keepdim=True) + 1e-5)).to(torch.bfloat16)
                        * dw_rms, args.steps)
         t_smx = timeit(lambda i: torch.softmax(dX, 1).to(torch.bfloat16), args.steps)
+        t_cs = timeit(lambda i: torch.matmul(dA_mlp, dB_mlp[i % len(dB_mlp)]).float().sum(0), args.steps)
         wf_ln, bf_ln = dw_rms.float(), db_ln.float()
         t_ln = timeit(lambda i: torch.nn.functional.layer_norm(dX, (X.shape[1],), wf_ln, bf_ln, 1e-5)
                       .to(torch.bfloat16), args.steps)
@@ -369,13 +395,16 @@ def main():
                 "cost_rmsnorm": round(rs["rmsnorm_bf16"]["ms"] / t_rms, 3),
                 "softmax_ms": round(t_smx, 4),
                 "cost_softmax": round(rs["softmax_bf16"]["ms"] / t_smx, 3),
+                "gemm_colsum_ms": round(t_cs, 4),
+                "cost_gemm_colsum": round(colsum["gemm_f32_colsum_ms"] / t_cs, 3),
                 "layernorm_ms": round(t_ln, 4),
                 "cost_layernorm": round(rs["layernorm_bf16"]["ms"] / t_ln, 3),
                 "sweep_ms_by_M": {str(M): round(t, 4) for M, t in t_sw_m.items()},
                 "cost_sweep_by_M": {str(M): round(shapes["sweep_M%d" % M]["us_mean"] * 1e-3 / t, 3)
                                     for M, t in t_sw_m.items()},
                 "what": ("torch.matmul (hipBLASLt) / matmul+bias+silu / torch.sum / x * rsqrt(mean(x^2) + eps) "
-                         "-> bf16 * w / torch.softmax -> bf16 / layer_norm -> bf16 on the same shapes; "
+                         "-> bf16 * w / torch.softmax -> bf16 / layer_norm -> bf16 / matmul -> float().sum(0) "
+                         "on the same shapes; "
                          "cost = t_dg / t_free")}
     except Exception as exc:  # the library under test never depends on this
         free = {"error": repr(exc)}
@@ -459,6 +488,10 @@ def main():
     got_smx = host(Y_smx)[rr]
     checked += want_smx.size
     matched += int(np.sum(got_smx == want_smx))
+    Ccs = C_cs.cpu().numpy()
+    want_cs = oracle.colsum(Ccs)
+    checked += want_cs.size
+    matched += int(np.sum(cs_out.cpu().numpy().view(np.uint32) == want_cs.view(np.uint32)))
     want_ln = oracle.layernorm(desc_ln, X[rr], w_rms, b_ln, eps=1e-5)
     got_ln = host(Y_ln)[rr]
     checked += want_ln.size
@@ -514,6 +547,7 @@ def main():
                      "achieved": round(mlp_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(mlp_tflops / PEAK_BF16_TFLOPS, 4), "traffic": mlp_traffic()},
         "rowsum": rs,
+        "gemm_colsum": colsum,
         "free_order": free,
         "hipblaslt_order": vendor,
         "bit_match": {"checked": checked, "matched": matched,

@@ -163,6 +163,21 @@ dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n);
 dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias,
                   void* C, int64_t M, int64_t N, int64_t K, void* stream);
 
+/* dg_gemm followed by the column sums of its output, an epilogue reduction
+ * (the paper times a GEMM whose epilogue emits a column sum, Sec. 7):
+ * colsum[j] = the balanced tree over the rows of column j in order (count
+ * up; equal to the perfect tree over the rows padded to a power of two, the
+ * padding taking no part), each output taken as stored (a bf16 output
+ * widened exactly).  C is written exactly as dg_gemm writes it.
+ *   colsum: device, N fp32 (written).  M = 0 gives +0 sums; N = 0 is a
+ *   no-op.  Aligned runs of 256 rows are folded in parallel and their roots
+ *   combined, through a library-owned workspace of ceil(M / 256) x N fp32
+ *   values per (device, stream) when M > 256.  Errors as dg_gemm, plus
+ *   DG_ERR_INVALID for a NULL colsum, DG_ERR_ALIGN for a misaligned one,
+ *   DG_ERR_SHAPE for M > 65535 * 256. */
+dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const void* bias,
+                         void* C, float* colsum, int64_t M, int64_t N, int64_t K, void* stream);
+
 /* Speed knobs for dg_gemm_knobs.  Any value gives the same bits as
  * dg_gemm; they exist so that this can be checked.  0 = the library's
  * choice. */

@@ -445,6 +445,34 @@ dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bi
   return dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
 }
 
+dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                         float* colsum, int64_t M, int64_t N, int64_t K, void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (M < 0 || N < 0 || K < 0) return DG_ERR_SHAPE;
+  if (N > 0 && !colsum) return DG_ERR_INVALID;
+  if (colsum && !aligned(colsum, 4)) return DG_ERR_ALIGN;
+  const int64_t nrun = (M + 255) / 256;
+  if (nrun > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
+  dg_status s = dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
+  if (s != DG_OK || N == 0) return s;
+  hipStream_t st = (hipStream_t)stream;
+  dg::ColsumArgs c;
+  c.C = C;
+  c.part = nullptr;
+  c.colsum = colsum;
+  c.M = M;
+  c.N = N;
+  c.out_bf16 = d->p.out_dtype == DG_BF16;
+  if (nrun > 1) {
+    void* ws = nullptr;
+    s = get_workspace(st, (size_t)nrun * (size_t)N * sizeof(float), &ws);
+    if (s != DG_OK) return s;
+    c.part = (float*)ws;
+  }
+  if (dg::launch_colsum(c, st) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
 static dg::RowsumArgs rowsum_args(const dg_desc* d, const float* X, float* out, int64_t rows, int64_t cols) {
   dg::RowsumArgs a;
   std::memset(&a, 0, sizeof a);

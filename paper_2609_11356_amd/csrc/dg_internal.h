@@ -62,6 +62,14 @@ struct NormArgs {
   int32_t out_bf16, pre_round;
 };
 
+struct ColsumArgs {
+  const void* C;                 // M x N output, fp32 or bf16
+  float* part;                   // [nchunk][N] subtree roots (nchunk > 1)
+  float* colsum;                 // N
+  int64_t M, N;
+  int32_t out_bf16;
+};
+
 // launchers (return hipSuccess or the launch error)
 hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
@@ -90,5 +98,7 @@ hipError_t launch_softmax_exp(const NormArgs& a, hipStream_t s);
 // centred values into a.Y given the means in a.rinv (three-pass path)
 hipError_t launch_layernorm_fused(const RowsumArgs& r, const NormArgs& a, hipStream_t s);
 hipError_t launch_layernorm_center(const NormArgs& a, hipStream_t s);
+// column sums of a GEMM output: subtrees of 256 rows, then their tree
+hipError_t launch_colsum(const ColsumArgs& a, hipStream_t s);
 
 }  // namespace dg

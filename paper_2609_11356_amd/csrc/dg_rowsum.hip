@@ -731,6 +731,95 @@ hipError_t launch_layernorm_center(const NormArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ------------------------------------------------ GEMM column sums
+
+// The balanced tree down each column of a GEMM output equals the perfect
+// tree over the rows padded with -0 (the exact identity) to a power of two,
+// so aligned runs of 256 rows are exact subtrees: one thread per (column,
+// run) folds its run as a perfect tree (compile-time shape, loads of 16 rows
+// in flight), and the run roots meet in the balanced tree (a binary-counter
+// stack flushed low to high).  Threads of a wave take consecutive columns,
+// so every row load is contiguous across the wave.
+constexpr int CS_RUN = 256;
+
+template <bool BF16>
+__device__ __forceinline__ float cs_load(const ColsumArgs& a, int64_t i, int64_t j) {
+  if constexpr (BF16) return bf16_f32(((const uint16_t*)a.C)[i * a.N + j]);
+  else return ((const float*)a.C)[i * a.N + j];
+}
+
+template <bool BF16>
+__global__ __launch_bounds__(256) void colsum_runs(ColsumArgs a) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x, c = blockIdx.y;
+  if (j >= a.N) return;
+  const int64_t i0 = c * CS_RUN;
+  float st[9];            // st[l]: the pending root of 2^l rows
+  constexpr int B = 16;   // rows whose loads are in flight together
+#pragma unroll
+  for (int b = 0; b < CS_RUN / B; ++b) {
+    float v[B];
+#pragma unroll
+    for (int k = 0; k < B; ++k) {
+      const int64_t i = i0 + b * B + k;
+      v[k] = i < a.M ? cs_load<BF16>(a, i, j) : -0.0f;
+    }
+    // the perfect tree of the 16 rows, then merged into the run's counter
+#pragma unroll
+    for (int w = 1; w < B; w <<= 1)
+#pragma unroll
+      for (int k = 0; k < B; k += 2 * w) v[k] = v[k] + v[k + w];
+    float x = v[0];
+    int l = 4;                       // 16 = 2^4 rows
+#pragma unroll
+    for (int bb = b; bb & 1; bb >>= 1) x = st[l++] + x;
+    st[l] = x;
+  }
+  const float root = st[8];
+  if (gridDim.y == 1) a.colsum[j] = root;
+  else a.part[c * a.N + j] = root;
+}
+
+__global__ __launch_bounds__(256) void colsum_merge(ColsumArgs a, int64_t nrun) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= a.N) return;
+  float st[40];
+  uint64_t count = 0;
+  for (int64_t c = 0; c < nrun; ++c) {
+    float v = a.part[c * a.N + j];
+    int l = 0;
+    for (uint64_t k = count; k & 1; k >>= 1) v = st[l++] + v;
+    st[l] = v;
+    ++count;
+  }
+  float r = 0.0f;
+  bool have = false;
+  for (int l = 0; l < 40; ++l)
+    if ((count >> l) & 1) {
+      r = have ? st[l] + r : st[l];
+      have = true;
+    }
+  a.colsum[j] = r;
+}
+
+// no rows: every column sums to +0
+__global__ __launch_bounds__(256) void colsum_zero(ColsumArgs a) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j < a.N) a.colsum[j] = 0.0f;
+}
+
+hipError_t launch_colsum(const ColsumArgs& a, hipStream_t st) {
+  if (a.M == 0) {
+    hipLaunchKernelGGL(colsum_zero, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
+  const int64_t nrun = (a.M + CS_RUN - 1) / CS_RUN;
+  const dim3 grid((unsigned)((a.N + 255) / 256), (unsigned)nrun);
+  if (a.out_bf16) hipLaunchKernelGGL(colsum_runs<true>, grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL(colsum_runs<false>, grid, dim3(256), 0, st, a);
+  if (nrun > 1) hipLaunchKernelGGL(colsum_merge, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, st, a, nrun);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------- softmax
 
 // Maximum with NaN propagation (a NaN operand wins).  Only the sign of a

@@ -68,11 +68,12 @@ def lib():
         L.dg_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_softmax.argtypes = [vp, vp, vp, i64, i64, vp]
         L.dg_layernorm.argtypes = [vp, vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
+        L.dg_gemm_colsum.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_strerror.argtypes = [ctypes.c_int]
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
         for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm",
-                  "dg_softmax", "dg_layernorm"):
+                  "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -242,6 +243,21 @@ def dg_rmsnorm(desc: Desc, X, w, eps, Y, rows=None, cols=None, stream=None):
     return Y
 
 
+def dg_gemm_colsum(desc: Desc, A, B, bias, C, colsum, M=None, N=None, K=None, stream=None):
+    """dg_gemm, then colsum[j] = the balanced tree down column j of C (fp32)."""
+    import torch
+    if isinstance(A, torch.Tensor):
+        M, K = A.shape
+        N = B.shape[1]
+        assert colsum.dtype == torch.float32 and colsum.is_cuda and colsum.numel() == N
+        assert tuple(C.shape) == (M, N) and C.is_contiguous() and C.is_cuda
+    st = lib().dg_gemm_colsum(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), _ptr(colsum), M, N, K,
+                              _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_gemm_colsum")
+    return C
+
+
 def dg_layernorm(desc: Desc, X, w, b, eps, Y, rows=None, cols=None, stream=None):
     """Y = layer normalisation of the rows of X (fp32), both row sums in the
     descriptor's order, then the bf16 weight and bias (each may be None)."""
@@ -276,4 +292,5 @@ def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
 def exported_symbols():
     """Names of the entry points include/dg.h declares."""
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs",
-            "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_strerror", "dg_version"]
+            "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
+            "dg_version"]

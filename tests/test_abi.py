@@ -173,6 +173,11 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_softmax(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
     assert lib.dg_softmax(d.handle, None, 16, 4, 5, None) == dg.DG_ERR_INVALID
     assert lib.dg_softmax(d.handle, 18, 16, 4, 5, None) == dg.DG_ERR_ALIGN
+    # GEMM with column sums: a NULL or misaligned colsum is rejected before any launch
+    assert lib.dg_gemm_colsum(d.handle, 16, 16, None, 16, None, 8, 8, 8, None) == dg.DG_ERR_INVALID
+    assert lib.dg_gemm_colsum(d.handle, 16, 16, None, 16, 18, 8, 8, 8, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_gemm_colsum(d.handle, 16, 16, None, 16, 16, 65536 * 256, 8, 8, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_gemm_colsum(d.handle, 16, 16, None, 16, None, 8, 0, 8, None) == dg.DG_OK
     # layer normalisation
     assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, 16, 0, 5, None) == dg.DG_OK
     assert lib.dg_layernorm(d.handle, 16, None, None, 0.0, 16, 4, 0, None) == dg.DG_OK
