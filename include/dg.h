@@ -191,7 +191,9 @@ typedef struct {
                       256 x 256 blocks on the first split_n columns and
                       256 x 192 blocks on the rest, in one launch, 7 as 6 (or
                       256 x 256 blocks alone when split_n is 0 and no split
-                      helps) with direct-to-LDS loads */
+                      helps) with direct-to-LDS loads, 8 the few-row kernel with
+                      a ring of depth (0 = 8) LDS slots filled by direct-to-LDS
+                      loads (tile_m 0 = 16, tile_n 0 = 16, slab_k 0 = 256) */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
   int32_t order;   /* kernels 3 and 5: block order: 0 library's choice, 1 row-major
@@ -199,7 +201,8 @@ typedef struct {
                       eight block rows walked column by column, 3 as 2 with
                       each of the eight XCDs given a contiguous range */
   int32_t occupancy; /* kernel 3: 0 library's choice, 1 or 2 workgroups per CU */
-  int32_t depth;   /* kernel 4: slabs of loads kept in flight (0 = 4; 2, 4 or 8) */
+  int32_t depth;   /* kernel 4: slabs of loads kept in flight (0 = 4; 2, 4 or 8);
+                      kernel 8: LDS ring slots */
   int32_t slab_k;  /* kernel 4: k per slab (0 = 64; 64, 128 or 256).  Kernel 4
                       builds a fixed list of (tile_m, tile_n, depth, slab_k);
                       others return DG_ERR_UNSUPPORTED */

@@ -269,21 +269,23 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 7) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 8) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
   if (kern != 6 && kern != 7 && split_n) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && kern != 8 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
   if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth, slab_k)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && kern != 5 && (tm || tn) &&
+  if (kern == 8 && !dg::skinny_dma_supported(tm ? tm : 16, tn ? tn : 16, depth ? depth : 8, slab_k ? slab_k : 256))
+    return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && kern != 5 && kern != 8 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
   // A strided split runs on the generic kernel or on the few-row kernel with
   // one dealt tile per slab.
   if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 &&
-      !(kern == 4 && slab_k == p.split_tile))
+      !((kern == 4 || kern == 8) && slab_k == p.split_tile))
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
   if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
@@ -377,7 +379,16 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     slab_k = c.slab_k;
   }
   hipError_t e;
-  if (kern == 4) {
+  if (kern == 8) {
+    if (!tm) tm = 16;
+    if (!tn) tn = 16;
+    if (!depth) depth = 8;
+    if (!slab_k) slab_k = 256;
+    // buffer offsets: a B row run and the slab offset past the part end stay in 31 bits
+    const int64_t lim = 0x7fffffff;
+    if ((K + (int64_t)(depth + 1) * slab_k * a.S) * N * 2 > lim || (int64_t)tm * K * 2 > lim) return DG_ERR_UNSUPPORTED;
+    e = dg::launch_gemm_skinny_dma(a, tm, tn, depth, slab_k, st);
+  } else if (kern == 4) {
     e = dg::launch_gemm_skinny(a, tm ? tm : 16, tn ? tn : 64, depth, slab_k, st);
   } else if (kern == 3) {
     if (!tm) { tm = 128; tn = 128; }

@@ -1254,6 +1254,168 @@ hipError_t launch_gemm_wide(const GemmArgs& a, int tm, int tn, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+// ------------------------------------------ few rows, direct-to-LDS ring
+//
+// The few-row kernel's order and LDS layouts, with the slabs loaded from
+// memory straight into a ring of NS LDS slots (separate arrays, so that the
+// compiler waits only for the slot it reads) instead of through registers:
+// NS - 1 slabs stay in flight per workgroup, limited by LDS rather than by
+// registers, which is what a B stream from HBM needs.  One barrier per slab:
+// a thread waits until its loads of slab s have landed, the barrier makes
+// every thread's visible, the slab is computed, and the loads of slab
+// s + NS - 1 go into the slot slab s - 1 left (free once every thread has
+// passed this barrier).  Each load instruction fills 1 KB of a slot with the
+// lanes in layout order; each lane fetches the chunk the swizzle puts there.
+template <int TMS, int BN, int NS, int BK>
+__global__ __launch_bounds__(256) void gemm_skinny_dma(GemmArgs a) {
+  constexpr int CPR = BK / 8, BM = 16 * TMS, NWC = BN / 16, BROW = BN / 8;
+  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN, SLOT = A_ELEMS + B_ELEMS;
+  constexpr int NA = BM * BK / 2048, NB = BK * BN / 2048;      // 1 KB loads per wave per slab
+  constexpr int ND = NA + NB;
+  static_assert(NA >= 1 && NB >= 1 && BM * BK % 2048 == 0 && BK * BN % 2048 == 0, "whole 1 KB loads per wave");
+  static_assert(CPR >= 8 && (BN == 16 || BN == 32 || BN == 64), "layouts of the few-row kernel");
+  static_assert(NS >= 3 && NS <= 8, "ring depth");
+  __shared__ __attribute__((aligned(1024))) uint16_t q0[SLOT], q1[SLOT], q2[SLOT], q3[SLOT];
+  __shared__ __attribute__((aligned(1024))) uint16_t q4[NS > 4 ? SLOT : 8], q5[NS > 5 ? SLOT : 8];
+  __shared__ __attribute__((aligned(1024))) uint16_t q6[NS > 6 ? SLOT : 8], q7[NS > 7 ? SLOT : 8];
+  auto slot = [&](auto S) -> uint16_t* {
+    constexpr int i = decltype(S)::value;
+    if constexpr (i == 0) return q0;
+    else if constexpr (i == 1) return q1;
+    else if constexpr (i == 2) return q2;
+    else if constexpr (i == 3) return q3;
+    else if constexpr (i == 4) return q4;
+    else if constexpr (i == 5) return q5;
+    else if constexpr (i == 6) return q6;
+    else return q7;
+  };
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nt = gridDim.x, x = blockIdx.x;
+  const int tile = (nt % 8 == 0) ? (x % 8) * (nt / 8) + x / 8 : x;
+  const int64_t i0 = (int64_t)blockIdx.y * BM, j0 = (int64_t)tile * BN;
+  const int s = blockIdx.z;
+  const bool strided = a.split_w != 0;
+  const int64_t k0 = strided ? (int64_t)s * BK : a.cuts[s];
+  const int64_t k1 = strided ? a.K : a.cuts[s + 1];
+  const int64_t kstep = strided ? (int64_t)a.S * BK : BK;
+  const int nslab = (k1 > k0) ? (int)((k1 - k0 + kstep - 1) / kstep) : 0;
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row >> 1) & 7)); };
+  auto ldsB = [](int k, int c) { return k * BROW + ((c ^ ((k & 3) << 1)) & (BROW - 1)); };
+
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = a.K * a.N * 2;
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)a.B, (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
+  // load t of the wave: A runs first (64 / CPR rows per KB), then B runs
+  // (64 / BROW k-rows per KB); lane l holds the run's l-th 16-byte slot
+  uint32_t off[ND];
+  int kc[ND], dst[ND];
+#pragma unroll
+  for (int t = 0; t < ND; ++t) {
+    const int run = wave * ND + t;   // runs 0 .. 4 ND - 1 of the slab: 4 NA of A, then 4 NB of B
+    if (run < 4 * NA) {
+      const int row = run * (64 / CPR) + lane / CPR, pc = lane % CPR;
+      const int c = pc ^ ((row >> 1) & 7);
+      off[t] = (i0 + row < a.M) ? (uint32_t)((row * a.K + 8 * c) * 2) : OOB;
+      kc[t] = 8 * c;
+      dst[t] = 8 * ldsA(row, c) - 8 * lane;   // the run's first element (lanes in layout order)
+    } else {
+      const int rb = run - 4 * NA;
+      const int kr = rb * (64 / BROW) + lane / BROW, pc = lane % BROW;
+      const int c = (pc ^ ((kr & 3) << 1)) & (BROW - 1);
+      off[t] = (j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
+      kc[t] = kr;
+      dst[t] = A_ELEMS + 8 * ldsB(kr, c) - 8 * lane;
+    }
+  }
+  auto dma = [&](auto S, int sl) {
+    uint16_t* base = slot(S);
+    const int64_t ks = k0 + (int64_t)sl * kstep, lim = k1 - ks;
+#pragma unroll
+    for (int t = 0; t < ND; ++t) {
+      const uint32_t o = kc[t] < lim ? off[t] : OOB;
+      const int d = __builtin_amdgcn_readfirstlane(dst[t]);
+      if (wave * ND + t < 4 * NA)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(base + d), 16, o, (int)(ks * 2), 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(base + d), 16, o, (int)(ks * a.N * 2), 0, 0);
+    }
+  };
+  floatx4 acc[TMS];
+#pragma unroll
+  for (int mi = 0; mi < TMS; ++mi) acc[mi] = floatx4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](auto S) {
+    if (wave >= NWC) return;
+    const uint16_t* As = slot(S);
+    const uint16_t* Bs = As + A_ELEMS;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      const int i = lane & 15, g = lane >> 4;
+      const int n = 16 * wave + 4 * (i & 3);
+      const int kr0 = kk + 8 * g + (i >> 2), kr1 = kr0 + 4;
+      const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+      const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+      const shortx8 bfr = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+#pragma unroll
+      for (int mi = 0; mi < TMS; ++mi) {
+        const shortx8 af = *(const shortx8*)&As[8 * ldsA(16 * mi + (lane & 15), kk / 8 + (lane >> 4))];
+        acc[mi] = mfma16(af, bfr, acc[mi]);
+      }
+    }
+  };
+  // prologue: slabs 0 .. NS-2 in flight
+  static_for<0, NS - 1>([&](auto u) { dma(u, u); });
+  for (int base = 0; base < nslab; base += NS) {
+    static_for<0, NS>([&](auto u) {
+      const int sl = base + u;
+      __builtin_amdgcn_s_waitcnt(vmcnt_only((NS - 2) * ND));   // slab sl landed
+      barrier_nofence();
+      if (sl < nslab) compute(u);
+      dma(std::integral_constant<int, (u + NS - 1) % NS>{}, sl + NS - 1);
+    });
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+  if (wave < NWC) {
+#pragma unroll
+    for (int mi = 0; mi < TMS; ++mi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t i = i0 + 16 * mi + 4 * (lane >> 4) + r, j = j0 + 16 * wave + (lane & 15);
+        if (i < a.M && j < a.N) finish(a, s, i, j, acc[mi][r]);
+      }
+  }
+}
+
+template <int TMS, int BN, int NS, int BK>
+static hipError_t launch_skinny_dma_t(const GemmArgs& a, hipStream_t st) {
+  dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
+  hipLaunchKernelGGL((gemm_skinny_dma<TMS, BN, NS, BK>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+// (tile_m, tile_n, ring slots, slab_k) combinations built
+#define DG_SKINNY_DMA_LIST(X) \
+  X(16, 16, 4, 256) X(16, 16, 8, 256) X(16, 32, 4, 256) X(16, 32, 6, 256) X(32, 32, 4, 128) X(32, 32, 6, 128) \
+  X(64, 32, 4, 128) X(64, 32, 3, 128) X(16, 64, 4, 128) X(16, 64, 6, 128)
+
+bool skinny_dma_supported(int tm, int tn, int slots, int slab_k) {
+#define DG_SKDMA_HAS(TM_, TN_, NS_, BK_) \
+  if (tm == TM_ && tn == TN_ && slots == NS_ && slab_k == BK_) return true;
+  DG_SKINNY_DMA_LIST(DG_SKDMA_HAS)
+#undef DG_SKDMA_HAS
+  return false;
+}
+
+hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tm, int tn, int slots, int slab_k, hipStream_t st) {
+#define DG_SKDMA_RUN(TM_, TN_, NS_, BK_) \
+  if (tm == TM_ && tn == TN_ && slots == NS_ && slab_k == BK_) return launch_skinny_dma_t<TM_ / 16, TN_, NS_, BK_>(a, st);
+  DG_SKINNY_DMA_LIST(DG_SKDMA_RUN)
+#undef DG_SKDMA_RUN
+  return hipErrorInvalidValue;
+}
+
 template <int TMS, int BN, int D, int BK>
 static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);

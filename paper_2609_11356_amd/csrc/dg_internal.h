@@ -84,6 +84,8 @@ hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t s);   // n_split 
 hipError_t launch_gemm_ppd(const GemmArgs& a, bool mixed, hipStream_t s);
 hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, int slab_k, hipStream_t s);
 bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
+hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tile_m, int tile_n, int slots, int slab_k, hipStream_t s);
+bool skinny_dma_supported(int tile_m, int tile_n, int slots, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);
 hipError_t launch_rmsnorm_scale(const NormArgs& a, hipStream_t s);
