@@ -22,7 +22,7 @@ _HDR = os.path.join(_HERE, "dgo.h")
 _LIB = os.path.join(_HERE, "libdgo.so")
 
 # Group width of each gfx950 bf16 MFMA instruction (its K).
-INSTRUCTION_K = {"16x16x32": 32, "32x32x16": 16, "16x16x16": 16, "exact8": 8}
+INSTRUCTION_K = {"16x16x32": 32, "32x32x16": 16, "16x16x16": 16, "exact8": 8, "scalar": 1}
 MODEL_EXACT, MODEL_GFX950 = 0, 1
 CARRY, SEQ, TREE = 0, 1, 2
 EPI = {"none": 0, "bias": 1, "bias_silu": 2}
@@ -126,7 +126,9 @@ def params(desc: dict):
     if d["k_cuts"] is not None:
         cuts = np.ascontiguousarray(np.asarray(d["k_cuts"], dtype=np.int64))
     p = _Params()
-    p.model = MODEL_GFX950 if d["model"] == "gfx950" else MODEL_EXACT
+    # the scalar path (one fused multiply-add per product) is the exact model
+    # with groups of one: a bf16 product is exact in binary32
+    p.model = MODEL_GFX950 if d["model"] == "gfx950" and d["mma"] != "scalar" else MODEL_EXACT
     p.g = int(d["g"]) if "g" in d else INSTRUCTION_K[d["mma"]]
     p.tile_k = int(d["tile_k"])
     p.split_k = int(d["split_k"])

@@ -945,3 +945,59 @@ def test_colsum_is_the_tree_down_each_column():
         p = 128
         padded = np.concatenate([X[:, j], np.full(p - 100, -0.0, dtype=np.float32)])
         assert got[j].view(np.uint32) == _halving(padded).view(np.uint32)
+
+
+# ------------------------------------- the scalar path: chained chunks
+
+
+def _chained_chunks_rational(a, b, S, T, tile_combine, split_combine):
+    """Sec. 3.2.2 chained chunks written out in exact rationals: K cut into S
+    contiguous chunks by the span rule (span rounded up to whole sub-blocks),
+    each chunk into sub-blocks of T from its start, each sub-block an FMA
+    chain from +0 (one rounding per product), the sub-blocks chained or
+    met in the balanced tree, the chunks chained or met in the tree."""
+    K = len(a)
+    span = -(-K // S)
+    span = -(-span // T) * T
+    def tree(v):
+        while len(v) > 1:
+            w = [rn32(f(v[2 * i]) + f(v[2 * i + 1])) for i in range(len(v) // 2)]
+            if len(v) % 2:
+                w.append(v[-1])
+            v = w
+        return v[0]
+    def chain(v):
+        s = v[0]
+        for x in v[1:]:
+            s = rn32(f(s) + f(x))
+        return s
+    parts = []
+    for s in range(S):
+        lo, hi = s * span, min((s + 1) * span, K)
+        tiles = []
+        acc = np.float32(0.0)
+        for t0 in range(lo, hi, T):
+            if tile_combine != "carry":
+                acc = np.float32(0.0)
+            for k in range(t0, min(t0 + T, hi)):
+                acc = rn32(f(acc) + bf(a[k]) * bf(b[k]))
+            tiles.append(acc)
+        part = tiles[-1] if tile_combine == "carry" else (chain(tiles) if tile_combine == "seq" else tree(tiles))
+        parts.append(part)
+    return chain(parts) if split_combine == "seq" else tree(parts)
+
+
+@pytest.mark.parametrize("S,T,tc,sc", [(1, 1024, "carry", "seq"), (4, 16, "seq", "tree"), (8, 8, "tree", "seq"),
+                                       (3, 32, "tree", "tree"), (16, 1, "seq", "seq")])
+def test_scalar_chained_chunks_match_rationals(S, T, tc, sc):
+    """The descriptor with the scalar instruction (groups of one) against the
+    chained-chunk walk in exact rationals, on exponent-spread operands."""
+    K = 290
+    A = inputs.spread_bf16(91, (2, K))
+    B = inputs.spread_bf16(92, (K, 3))
+    d = dict(mma="scalar", tile_k=T, split_k=S, tile_combine=tc, split_combine=sc)
+    C = oracle.gemm(d, A, B)
+    for i in range(2):
+        for j in range(3):
+            want = _chained_chunks_rational(A[i], B[:, j], S, T, tc, sc)
+            assert C[i, j].view(np.uint32) == np.float32(want).view(np.uint32), (i, j)
