@@ -254,6 +254,35 @@ def main():
     ms_per_step = total_ms / args.steps
     value = step_flops / (ms_per_step * 1e-3) / 1e12
 
+    # -------------------- the scalar path: chained chunks on the few-row shapes
+    scal = {}
+    scal_cases = [("sweep_M1", dA_sw_M[1], dB_sw, dict(mma="scalar", tile_k=16, split_k=32, tile_combine="seq",
+                                                          split_combine="tree", out="bf16")),
+                  ("decode", dA_dec, dB_dec, dict(mma="scalar", tile_k=16, split_k=64, split_combine="tree",
+                                                  out="bf16"))]
+    scal_out = {}
+    for name, A_, Bl, dd in scal_cases:
+        Dv = dg.Desc(**dd)
+        C_ = torch.empty((A_.shape[0], Bl[0].shape[1]), dtype=torch.bfloat16, device=dev)
+        for i in range(args.warmup):
+            dg.dg_gemm(Dv, A_, Bl[i % len(Bl)], None, C_, stream=sptr)
+        ts = []
+        for i in range(args.steps):
+            a, b = ev(), ev()
+            a.record(stream)
+            dg.dg_gemm(Dv, A_, Bl[i % len(Bl)], None, C_, stream=sptr)
+            b.record(stream)
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        med = float(np.median(ts))
+        by = Bl[0].numel() * 2 + A_.numel() * 2 + C_.numel() * 2
+        dg.dg_gemm(Dv, A_, Bl[0], None, C_, stream=sptr)
+        torch.cuda.synchronize()
+        scal_out[name] = (dd, C_)
+        scal[name] = {"desc": "scalar FMA chains, %d chunks, %s sub-blocks of 16, tree merge"
+                              % (dd["split_k"], dd.get("tile_combine", "carry")),
+                      "us_median": round(med * 1e3, 2), "GB/s": round(by / (med * 1e-3) / 1e9, 1)}
+
     # ------------------------------- GEMM with a column-sum epilogue (fp32 out)
     desc_cs = dict(mma="16x16x32", tile_k=64)
     D_cs = dg.Desc(**desc_cs)
@@ -488,6 +517,11 @@ def main():
     got_smx = host(Y_smx)[rr]
     checked += want_smx.size
     matched += int(np.sum(got_smx == want_smx))
+    for name, (dd, C_) in scal_out.items():
+        A_h, B_h = (A_sw[:1], B_sw) if name == "sweep_M1" else (A_dec, B_dec)
+        ii = rng.integers(0, A_h.shape[0], 300)
+        jj = rng.integers(0, B_h.shape[1], 300)
+        tally(host(C_)[ii, jj], oracle.gemm_at(dd, A_h, B_h, None, ii, jj))
     Ccs = C_cs.cpu().numpy()
     want_cs = oracle.colsum(Ccs)
     checked += want_cs.size
@@ -548,6 +582,7 @@ def main():
                      "frac": round(mlp_tflops / PEAK_BF16_TFLOPS, 4), "traffic": mlp_traffic()},
         "rowsum": rs,
         "gemm_colsum": colsum,
+        "scalar_path": scal,
         "free_order": free,
         "hipblaslt_order": vendor,
         "bit_match": {"checked": checked, "matched": matched,

@@ -39,13 +39,16 @@ dg_status plan_cuts(const dg_desc* d, int64_t K, int64_t* cuts) {
 void make_signature(dg_desc* d) {
   const dg_desc_params& p = d->p;
   // fma = 1 folds the same 8-k chunks whatever the instruction's K
+  // on the scalar path a bf16 product is exact, so fma cannot change bits
   char grp[32];
-  if (p.fma) std::snprintf(grp, sizeof grp, "chunk8");
+  const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
+  if (scalar) std::snprintf(grp, sizeof grp, "scalar-fma");
+  else if (p.fma) std::snprintf(grp, sizeof grp, "chunk8");
   else std::snprintf(grp, sizeof grp, "group%d", d->group);
   int n = std::snprintf(d->sig, sizeof d->sig,
-                        "gfx950-bf16-mfma/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
+                        "gfx950-bf16-%s/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
                         "out-%s/epi%d/%s/leaf%d/%s",
-                        grp, p.fma, p.tile_k,
+                        scalar ? "fma" : "mfma", grp, scalar ? 1 : p.fma, p.tile_k,
                         p.tile_combine == DG_CARRY ? "carry" : p.tile_combine == DG_SEQ ? "seq" : "tree",
                         p.split_k, p.tail == DG_TAIL_FIRST ? "tail-first" : "tail-last",
                         p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
@@ -201,6 +204,7 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   int group;
   if (p->mma == DG_MMA_16X16X32_BF16) group = 32;
   else if (p->mma == DG_MMA_32X32X16_BF16) group = 16;
+  else if (p->mma == DG_MMA_SCALAR_FMA) group = 1;
   else return DG_ERR_INVALID;
   if (p->tile_k < group || p->tile_k % group != 0 || p->tile_k > (1 << 30)) return DG_ERR_INVALID;
   if (!in(p->split_k, 1, DG_MAX_SPLIT)) return DG_ERR_INVALID;
@@ -269,7 +273,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 8) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 9) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  // the scalar instruction runs on kernel 9 only, and kernel 9 runs nothing else
+  const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
+  if (scalar ? (kern != 0 && kern != 9) : kern == 9) return DG_ERR_UNSUPPORTED;
+  if (kern == 9 && (tm || tn || order || occ || depth || slab_k || split_n)) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
   if (kern != 6 && kern != 7 && split_n) return DG_ERR_UNSUPPORTED;
@@ -284,7 +292,7 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     return DG_ERR_UNSUPPORTED;
   // A strided split runs on the generic kernel or on the few-row kernel with
   // one dealt tile per slab.
-  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 &&
+  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 && kern != 9 &&
       !((kern == 4 || kern == 8) && slab_k == p.split_tile))
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
@@ -344,7 +352,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     int64_t len = a.cuts[s + 1] - a.cuts[s];
     if (a.tail_first && (len % p.tile_k) % 8) tiled_ok = false;
   }
-  if (kern >= 2 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (scalar) {
+    tiled_ok = false;
+    kern = 9;
+  }
+  if (kern >= 2 && kern != 9 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (strided && kern == 0) {
     const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
     const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
@@ -379,7 +391,10 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     slab_k = c.slab_k;
   }
   hipError_t e;
-  if (kern == 8) {
+  if (kern == 9) {
+    if ((M + 3) / 4 > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
+    e = dg::launch_gemm_scalar(a, st);
+  } else if (kern == 8) {
     if (!tm) tm = 16;
     if (!tn) tn = 16;
     if (!depth) depth = 8;

@@ -117,6 +117,149 @@ __device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int
   }
 }
 
+// --------------------------------------------- scalar path (chained chunks)
+//
+// The descriptor with the scalar instruction (groups of one product, each
+// joining the accumulator by one fused multiply-add: the scalar path of
+// Sec. 3.2.2, where a chunk of the axis is an explicit FMA chain).  One
+// thread per output column and part, MR rows at once; the part's positions
+// are walked in order (contiguous part, or the dealt tiles of a strided
+// split), in windows whose A values the workgroup stages in LDS (every
+// thread reads the same value: a broadcast); accumulator tiles close every
+// tile_k positions from the part start (a short first tile when tail-first)
+// and are carried, chained or met in the balanced tree.  No MFMA row waste:
+// the shape of choice for one or a few rows split over many chunks.
+template <int MR, int CPT>
+__global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
+  constexpr int W = 256;                  // positions per staged window
+  constexpr int U = 16;                   // positions whose loads are in flight together
+  __shared__ __attribute__((aligned(16))) float As[MR][W];
+  const int64_t j = ((int64_t)blockIdx.x * 256 + threadIdx.x) * CPT;   // first of CPT columns
+  const bool col = j < a.N;
+  const int64_t i0 = (int64_t)blockIdx.y * MR;
+  const int s = blockIdx.z;
+  const int64_t tk = a.tile_k, w = a.split_w, K = a.K;
+  const bool strided = w != 0;
+  // positions of the part
+  int64_t len;
+  if (strided) {
+    len = 0;
+    for (int64_t u = s; u * w < K; u += a.S) len += (K - u * w < w) ? K - u * w : w;
+  } else {
+    len = a.cuts[s + 1] - a.cuts[s];
+  }
+  auto kpos = [&](int64_t q) -> int64_t {
+    return strided ? (s + a.S * (q / w)) * w + q % w : a.cuts[s] + q;
+  };
+  const int64_t off = (!strided && a.tail_first) ? len % tk : 0;   // short first tile
+  auto next_start = [&](int64_t q) -> int64_t {                     // first tile start after q
+    if (off > 0 && q < off) return off;
+    return off + ((q - off) / tk + 1) * tk;
+  };
+  // CPT consecutive columns of row k of B (zero past N)
+  auto bload = [&](int64_t k, float* v) {
+    const uint16_t* bp = a.B + k * a.N + j;
+    if constexpr (CPT == 4) {
+      const uint2 q = col ? *(const uint2*)bp : uint2{0u, 0u};
+      v[0] = bits_f32(q.x << 16); v[1] = bits_f32(q.x & 0xffff0000u);
+      v[2] = bits_f32(q.y << 16); v[3] = bits_f32(q.y & 0xffff0000u);
+    } else {
+      v[0] = col ? bf16_f32(bp[0]) : 0.0f;
+    }
+  };
+  float acc[MR][CPT], part[MR][CPT], st[MR][CPT][32];
+#pragma unroll
+  for (int r = 0; r < MR; ++r)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) acc[r][c] = part[r][c] = 0.0f;
+  bool have = false;
+  uint32_t count = 0;
+  auto push = [&](float v, int r, int c) {
+    int l = 0;
+    for (uint32_t cc = count; cc & 1u; cc >>= 1) v = st[r][c][l++] + v;
+    st[r][c][l] = v;
+  };
+  auto close = [&]() {
+    if (a.tile_combine == DG_CARRY) return;
+#pragma unroll
+    for (int r = 0; r < MR; ++r)
+#pragma unroll
+      for (int c = 0; c < CPT; ++c) {
+        if (a.tile_combine == DG_SEQ) part[r][c] = have ? part[r][c] + acc[r][c] : acc[r][c];
+        else push(acc[r][c], r, c);
+        acc[r][c] = 0.0f;
+      }
+    have = true;
+    ++count;
+  };
+  for (int64_t w0 = 0; w0 < len; w0 += W) {
+    const int n = (int)((len - w0 < W) ? len - w0 : W);
+    __syncthreads();   // the previous window has been read
+    for (int e = threadIdx.x; e < MR * W; e += 256) {
+      const int r = e / W, qq = e % W;
+      As[r][qq] = (qq < n && i0 + r < a.M) ? bf16_f32(a.A[(i0 + r) * K + kpos(w0 + qq)]) : 0.0f;
+    }
+    __syncthreads();
+    int qq = 0;
+    while (qq < n) {
+      const int64_t q = w0 + qq;
+      if (q != 0 && (q == off || (q > off && (q - off) % tk == 0))) close();
+      const int64_t nx = next_start(q);
+      const int end = (int)((nx - w0 < n) ? nx - w0 : n);
+      // positions [qq, end) lie in one tile and one dealt tile: consecutive k
+      const int64_t kq = kpos(q);
+      const int cnt = end - qq;
+      int t = 0;
+      for (; t + U <= cnt; t += U) {
+        float bv[U][CPT];
+#pragma unroll
+        for (int e = 0; e < U; ++e) bload(kq + t + e, bv[e]);
+#pragma unroll
+        for (int e = 0; e < U; ++e)
+#pragma unroll
+          for (int r = 0; r < MR; ++r) {
+            const float av = As[r][qq + t + e];
+#pragma unroll
+            for (int c = 0; c < CPT; ++c) acc[r][c] = __builtin_fmaf(av, bv[e][c], acc[r][c]);
+          }
+      }
+      for (; t < cnt; ++t) {
+        float bv[CPT];
+        bload(kq + t, bv);
+#pragma unroll
+        for (int r = 0; r < MR; ++r)
+#pragma unroll
+          for (int c = 0; c < CPT; ++c) acc[r][c] = __builtin_fmaf(As[r][qq + t], bv[c], acc[r][c]);
+      }
+      qq = end;
+    }
+  }
+  // the part's value: the last tile joins as every other did
+#pragma unroll
+  for (int r = 0; r < MR; ++r)
+#pragma unroll
+    for (int c = 0; c < CPT; ++c) {
+      float pv;
+      if (a.tile_combine == DG_CARRY || len == 0) {
+        pv = acc[r][c];
+      } else if (a.tile_combine == DG_SEQ) {
+        pv = have ? part[r][c] + acc[r][c] : acc[r][c];
+      } else {
+        push(acc[r][c], r, c);
+        const uint32_t cnt2 = count + 1;
+        float res = 0.0f;
+        bool h = false;
+        for (int lv = 0; lv < 32; ++lv)
+          if ((cnt2 >> lv) & 1u) {
+            res = h ? st[r][c][lv] + res : st[r][c][lv];
+            h = true;
+          }
+        pv = res;
+      }
+      if (col && i0 + r < a.M && j + c < a.N) finish(a, s, i0 + r, j + c, pv);
+    }
+}
+
 // ------------------------------------------------------------- generic
 
 __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
@@ -1185,6 +1328,28 @@ __global__ __launch_bounds__(256) void splitk_combine(CombineArgs a) {
 }
 
 // ----------------------------------------------------------- launchers
+
+template <int MR, int CPT>
+static void launch_scalar_t(const GemmArgs& a, hipStream_t st) {
+  dim3 grid((unsigned)((a.N + 256 * CPT - 1) / (256 * CPT)), (unsigned)((a.M + MR - 1) / MR), (unsigned)a.S);
+  hipLaunchKernelGGL((gemm_scalar<MR, CPT>), grid, dim3(256), 0, st, a);
+}
+
+hipError_t launch_gemm_scalar(const GemmArgs& a, hipStream_t st) {
+  const int mr = a.M >= 4 ? 4 : a.M >= 2 ? 2 : 1;
+  // four columns per thread (one 8-byte load per row of B) when rows allow it
+  const bool vec = a.N % 4 == 0 && ((uintptr_t)a.B) % 8 == 0;
+  if (vec) {
+    if (mr == 4) launch_scalar_t<4, 4>(a, st);
+    else if (mr == 2) launch_scalar_t<2, 4>(a, st);
+    else launch_scalar_t<1, 4>(a, st);
+  } else {
+    if (mr == 4) launch_scalar_t<4, 1>(a, st);
+    else if (mr == 2) launch_scalar_t<2, 1>(a, st);
+    else launch_scalar_t<1, 1>(a, st);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + 15) / 16), (unsigned)((a.M + 15) / 16), (unsigned)a.S);

@@ -72,6 +72,7 @@ struct ColsumArgs {
 
 // launchers (return hipSuccess or the launch error)
 hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_scalar(const GemmArgs& a, hipStream_t s);   // groups of one (scalar FMA)
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool tiled_supported(int tile_m, int tile_n);
 hipError_t launch_gemm_v3(const GemmArgs& a, int tile_m, int tile_n, int occupancy, hipStream_t s);

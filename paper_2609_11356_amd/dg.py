@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdg.so")
 
 DG_OK, DG_ERR_INVALID, DG_ERR_UNSUPPORTED, DG_ERR_SHAPE, DG_ERR_ALIGN, DG_ERR_NOMEM, DG_ERR_HIP = range(7)
-MMA = {"16x16x32": 1, "32x32x16": 2}
+MMA = {"16x16x32": 1, "32x32x16": 2, "scalar": 3}
 COMBINE = {"carry": 0, "seq": 1, "tree": 2}
 TAIL = {"last": 0, "first": 1}
 DTYPE = {"f32": 0, "bf16": 1}

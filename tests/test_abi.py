@@ -99,6 +99,9 @@ def test_signature_canonical(dg):
     assert dg.Desc(split_k=3, k_cuts=[100, 200]).signature().endswith("cuts:100:200")
     st = dg.Desc(split_k=4, split_layout="strided", split_tile=64).signature()
     assert st.endswith("strided:64") and st != dg.Desc(split_k=4).signature()
+    # the scalar path: fma cannot change bits, so it is normalised away
+    assert dg.Desc(mma="scalar", tile_k=7, fma=0).signature() == dg.Desc(mma="scalar", tile_k=7).signature()
+    assert dg.Desc(mma="scalar", tile_k=64).signature() != dg.Desc(tile_k=64).signature()
     # one strided part is the whole axis: the same order as one contiguous part
     assert dg.Desc(split_layout="strided", split_tile=64).signature() == dg.Desc().signature()
     # leaf layout and fold appear when they are not the defaults; one lane has no fold
@@ -153,6 +156,11 @@ def test_argument_errors_need_no_gpu(dg):
                    dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 512), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, -256)):
             assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
                 dg.DG_ERR_UNSUPPORTED
+    sc = dg.Desc(mma="scalar", tile_k=16)
+    for kn in (dg.dg_knobs(5, 0, 0, 0, 0, 0, 0, 0), dg.dg_knobs(1, 0, 0, 0, 0, 0, 0, 0),
+               dg.dg_knobs(9, 16, 0, 0, 0, 0, 0, 0)):
+        assert lib.dg_gemm_knobs(sc.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED
     for kn in (dg.dg_knobs(5, 256, 256, 0, 0, 0, 0, 256), dg.dg_knobs(9, 0, 0, 0, 0, 0, 0, 0),
                dg.dg_knobs(8, 16, 16, 0, 0, 5, 256, 0), dg.dg_knobs(8, 48, 16, 0, 0, 0, 0, 0)):
         assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \

@@ -78,6 +78,12 @@ DESCS = [
     dict(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu"),
     dict(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", epi_round="pre_act"),
     dict(mma="16x16x32", tile_k=64, split_k=4, out="bf16", epilogue="bias_silu"),
+    # the scalar path: chained chunks (groups of one, FMA chains)
+    dict(mma="scalar", tile_k=64),
+    dict(mma="scalar", tile_k=16, split_k=4, tile_combine="seq", split_combine="tree"),
+    dict(mma="scalar", tile_k=5, split_k=3, tile_combine="tree", tail="first"),
+    dict(mma="scalar", tile_k=8, split_k=2, tile_combine="tree", out="bf16", epilogue="bias_silu"),
+    dict(mma="scalar", tile_k=1, out="bf16", epilogue="bias"),
 ]
 
 
@@ -150,6 +156,20 @@ KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, ti
          dict(kernel=8), dict(kernel=8, tile_m=16, tile_n=32, depth=6, slab_k=256),
          dict(kernel=8, tile_m=32, tile_n=32, depth=4, slab_k=128), dict(kernel=8, tile_m=64, tile_n=32, depth=3, slab_k=128),
          dict(kernel=8, tile_m=16, tile_n=64, depth=6, slab_k=128), None]
+
+
+def test_scalar_path_strided_and_many_chunks(dg):
+    """Chained chunks with many parts (the GEMV shape), strided dealing, and
+    more rows than one thread carries."""
+    for desc, shape in ((dict(mma="scalar", tile_k=16, split_k=64, tile_combine="seq", split_combine="tree"),
+                         (1, 300, 4096)),
+                        (dict(mma="scalar", tile_k=16, split_k=4, split_layout="strided", split_tile=32,
+                              split_combine="tree"), (9, 72, 1000)),
+                        (dict(mma="scalar", tile_k=32, split_k=8, out="bf16"), (8, 4096, 2048))):
+        M, N, K = shape
+        A = inputs.spread_bf16(M + 7, (M, K))
+        B = inputs.spread_bf16(N + 8, (K, N))
+        check_full(dg, desc, A, B, what="%s %s" % (desc, shape))
 
 
 @pytest.mark.parametrize("desc", [dict(tile_k=64, out="bf16"), dict(tile_k=64, split_k=4, split_combine="tree"),
