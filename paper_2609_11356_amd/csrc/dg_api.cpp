@@ -273,14 +273,15 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 9) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 10) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   // the scalar instruction runs on kernel 9 only, and kernel 9 runs nothing else
   const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
   if (scalar ? (kern != 0 && kern != 9) : kern == 9) return DG_ERR_UNSUPPORTED;
   if (kern == 9 && (tm || tn || order || occ || depth || slab_k || split_n)) return DG_ERR_UNSUPPORTED;
-  if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && order) return DG_ERR_UNSUPPORTED;
-  if ((kern == 6 || kern == 7) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N)) return DG_ERR_UNSUPPORTED;
-  if (kern != 6 && kern != 7 && split_n) return DG_ERR_UNSUPPORTED;
+  if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
+  if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
+    return DG_ERR_UNSUPPORTED;
+  if (kern != 6 && kern != 7 && kern != 10 && split_n) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && kern != 8 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
@@ -416,6 +417,17 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     a.order = order ? order : 3;
     if (dg::wide_is_pp(tm, tn) && !pp_fits(a)) return DG_ERR_UNSUPPORTED;
     e = dg::launch_gemm_wide(a, tm, tn, st);
+  } else if (kern == 10) {
+    if (!pp_fits(a)) return DG_ERR_UNSUPPORTED;
+    // split_n 0: the library's split, or 256-wide blocks alone when no split helps
+    if (split_n == 0) {
+      const int64_t sp = mixed_split(M, N, a.S, cu_count());
+      split_n = sp < 0 ? (N + 255) / 256 * 256 : sp;
+    }
+    if (((M + 255) / 256) * ((split_n + 255) / 256 + (N - split_n + 191) / 192) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = order ? order : 1;
+    a.n_split = split_n;
+    e = dg::launch_gemm_w4(a, st);
   } else if (kern == 7) {
     if (!pp_fits(a)) return DG_ERR_UNSUPPORTED;
     // split_n 0: the library's split, or 256-wide blocks alone when no split helps

@@ -63,6 +63,24 @@ __device__ __forceinline__ floatx4 mfma16(shortx8 a, shortx8 b, floatx4 c) {
                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// The same instruction with the accumulator tied to one accumulation
+// register quad (input and output the same registers), for kernels whose
+// accumulators fill that register file: the compiler otherwise renames
+// accumulators between loop iterations and copies them back.  The compiler
+// does not see an MFMA here, so a reader of the accumulator through another
+// instruction must first wait for the last one to finish (mfma_drain).
+__device__ __forceinline__ void mfma16_tied(floatx4& acc, const shortx8& a, const shortx8& b) {
+  asm("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(a), "v"(b));
+}
+
+// Wait states after an MFMA before its result is read by a non-MFMA
+// instruction (more than the 16x16x32 instruction's latency).
+__device__ __forceinline__ void mfma_drain() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7\n\ts_nop 7" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // Finish one output: partial rounding, then either the split-K partial store
 // or the epilogue (z = y (+) bias_j; optional pre-activation bf16 rounding;
 // SiLU; rounding to the output type).
@@ -83,8 +101,9 @@ __device__ __forceinline__ void finish(const GemmArgs& a, int s, int64_t i, int6
 }
 
 // finish() for four consecutive columns j..j+3 (all < N: the tiled path
-// requires N % 8 == 0 and 16-byte aligned C), with one vector store.
-__device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4) {
+// requires N % 8 == 0 and 16-byte aligned C), with one vector store; b4 holds
+// the bias of those columns as binary32 (used only by the epilogue).
+__device__ __forceinline__ void finish4v(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4, float4 b4) {
   float y[4] = {y4.x, y4.y, y4.z, y4.w};
 #pragma unroll
   for (int e = 0; e < 4; ++e)
@@ -94,9 +113,7 @@ __device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int
     return;
   }
   if (a.epilogue != DG_EPI_NONE) {
-    const uint2 bb = *(const uint2*)&a.bias[j];
-    const float b[4] = {bits_f32(bb.x << 16), bits_f32(bb.x & 0xffff0000u), bits_f32(bb.y << 16),
-                        bits_f32(bb.y & 0xffff0000u)};
+    const float b[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) y[e] = y[e] + b[e];
   }
@@ -109,11 +126,68 @@ __device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int
     }
   }
   if (a.out_bf16) {
-    const uint32_t lo = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
-    const uint32_t hi = (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16);
+    const uint32_t lo = f32x2_bf16x2(y[0], y[1]);
+    const uint32_t hi = f32x2_bf16x2(y[2], y[3]);
     *(uint2*)&((uint16_t*)a.C)[i * a.N + j] = uint2{lo, hi};
   } else {
     *(float4*)&((float*)a.C)[i * a.N + j] = float4{y[0], y[1], y[2], y[3]};
+  }
+}
+
+// finish4v with the bias read from memory.
+__device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4) {
+  float4 b4 = float4{0.f, 0.f, 0.f, 0.f};
+  if (a.S == 1 && a.epilogue != DG_EPI_NONE) {
+    const uint2 bb = *(const uint2*)&a.bias[j];
+    b4 = float4{bits_f32(bb.x << 16), bits_f32(bb.x & 0xffff0000u), bits_f32(bb.y << 16), bits_f32(bb.y & 0xffff0000u)};
+  }
+  finish4v(a, s, i, j, y4, b4);
+}
+
+// Whether the epilogue reads the bias (a single part, bias epilogue).
+__device__ __forceinline__ bool needs_bias(const GemmArgs& a) { return a.S == 1 && a.epilogue != DG_EPI_NONE; }
+
+// The bias of columns [j0, j0 + n) as binary32 into LDS (zero past N), by
+// all threads of the workgroup; the caller synchronises afterwards.
+__device__ __forceinline__ void stage_bias(const GemmArgs& a, int64_t j0, int n, float* bsh) {
+  if (!needs_bias(a)) return;
+  for (int c = threadIdx.x; c < n; c += blockDim.x) bsh[c] = j0 + c < a.N ? bf16_f32(a.bias[j0 + c]) : 0.f;
+}
+
+// Wait for the wave's own LDS operations (and keep the compiler from moving
+// memory operations across).  LDS operations of one wave run in issue order,
+// so after this a read sees what the wave wrote before.
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+// Epilogue of one wave's (16 TM) x (16 TN) tile of 16x16 MFMA accumulators
+// (lane l holds rows 4 (l / 16) .. +3, column l % 16 of each), rows from ib
+// and columns from jb.  Each 16-row band passes through the wave's own LDS
+// area cs (16 rows of pitch 16 TN + 4 floats: rows 4 apart start 16 banks
+// apart) and leaves as four-column vectors; the bias of the wave's columns
+// comes from bsh (staged by stage_bias), so no global load waits inside the
+// loop.  Only the wave itself touches cs, so no workgroup barrier is needed.
+template <int TM, int TN, typename Acc>
+__device__ __forceinline__ void wave_epilogue(const GemmArgs& a, int s, int64_t ib, int64_t jb, float* cs,
+                                              const float* bsh, const Acc& acc) {
+  constexpr int WTN = 16 * TN, CSP = WTN + 4;
+  const int lane = threadIdx.x & 63;
+  const bool bias = needs_bias(a);
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+    lds_wait();
+#pragma unroll 1
+    for (int q = lane; q < 16 * WTN / 4; q += 64) {
+      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+      const int64_t i = ib + 16 * mi + rr, j = jb + cc;
+      const float4 y4 = *(const float4*)&cs[rr * CSP + cc];
+      const float4 b4 = bias ? *(const float4*)&bsh[cc] : float4{0.f, 0.f, 0.f, 0.f};
+      if (i < a.M && j < a.N) finish4v(a, s, i, j, y4, b4);
+    }
+    lds_wait();
   }
 }
 
@@ -884,24 +958,14 @@ __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j
   }
   if (grp == 0) __syncthreads();
 
-  constexpr int CSP = WTN + 4;   // staging pitch: rows 4 apart start 16 banks apart
+  constexpr int CSP = WTN + 4;
   float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
-  static_assert(8 * 16 * CSP * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
-#pragma unroll
-  for (int mi = 0; mi < TM; ++mi) {
-    __syncthreads();
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
-    __syncthreads();
-#pragma unroll 1
-    for (int q = lane; q < 16 * WTN / 4; q += 64) {
-      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
-      const int64_t i = i0 + grp * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
-      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
-    }
-  }
+  float* bsh = reinterpret_cast<float*>(smem) + 8 * 16 * CSP;
+  static_assert((8 * 16 * CSP + BNC) * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
+  __syncthreads();
+  stage_bias(a, j0, BNC, bsh);
+  __syncthreads();
+  wave_epilogue<TM, TN>(a, s, i0 + grp * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
 }
 
 // ------------------------------------- ping-pong with direct-to-LDS loads
@@ -1078,26 +1142,16 @@ __device__ __forceinline__ void ppd_body(const GemmArgs& a, int64_t i0, int64_t 
   __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
   __syncthreads();
 
-  // epilogue: wave w stages through slot w % 4, at (w / 4) * 16 rows of pitch CSP
+  // epilogue: wave w stages through slot w % 4, at (w / 4) * 16 rows of pitch
+  // CSP; the bias sits in slot 0 after its two staging areas
   constexpr int CSP = WTN + 4;
-  static_assert(2 * 16 * CSP * 4 <= PPD_SLOT * 2, "epilogue staging fits");
+  static_assert((2 * 16 * CSP + BNC) * 4 <= PPD_SLOT * 2, "epilogue staging fits");
   uint16_t* sb = (wave & 3) == 0 ? ppd_s0 : (wave & 3) == 1 ? ppd_s1 : (wave & 3) == 2 ? ppd_s2 : ppd_s3;
   float* cs = reinterpret_cast<float*>(sb) + (wave >> 2) * 16 * CSP;
-#pragma unroll
-  for (int mi = 0; mi < TM; ++mi) {
-    __syncthreads();
-#pragma unroll
-    for (int ni = 0; ni < TN; ++ni)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
-    __syncthreads();
-#pragma unroll 1
-    for (int q = lane; q < 16 * WTN / 4; q += 64) {
-      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
-      const int64_t i = i0 + grp * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
-      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
-    }
-  }
+  float* bsh = reinterpret_cast<float*>(ppd_s0) + 2 * 16 * CSP;
+  stage_bias(a, j0, BNC, bsh);
+  __syncthreads();
+  wave_epilogue<TM, TN>(a, s, i0 + grp * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
 }
 
 __global__ __launch_bounds__(512) void gemm_ppd(GemmArgs a) {
@@ -1149,6 +1203,158 @@ __global__ __launch_bounds__(512) void gemm_pp_mixed(GemmArgs a) {
     const int tn2 = (int)((a.N - a.n_split + 191) / 192);
     grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
     pp_body<256, 256, BK, 192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
+  }
+}
+
+// ------------------------------------ four waves, 128-row wave sub-tiles
+//
+// One wave per SIMD, each owning a 128 x (BNC/2) sub-tile of the 256 x BNC
+// block with its accumulators (up to 256 registers) in the accumulation
+// register file.  Against the eight-wave ping-pong this reads a third fewer
+// fragment bytes from LDS per MFMA (each A fragment is read by two waves,
+// not four).  The wave overlaps its own MFMAs with its LDS and global work;
+// in iteration s, between the MFMAs of slab s (fragments in register set
+// s % 2):
+//   * the fragments of slab s+1 are read from LDS buffer (s+1) % 2 into the
+//     other set;
+//   * slab s+2 is written from global-load register set s % 2 into LDS
+//     buffer s % 2 (which held slab s, read during iteration s-1);
+//   * the loads of slab s+4 are issued into that register set;
+// and one barrier closes the iteration.  Same chunk order as every tiled
+// kernel (16x16x32 MFMA chain, 8-k chunks from the part start).
+template <int BNC>
+__device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j0, uint16_t* smem) {
+  constexpr int BM = 256, BN = 256, BK = 32, CPR = BK / 8, BROW = BN / 8;
+  constexpr int WTM = 128, WTN = BNC / 2, TM = WTM / 16, TN = WTN / 16;
+  constexpr int NA = BM * CPR / 256, NB = BK * BROW / 256, NL = NA + NB;
+  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
+  static_assert(BNC <= BN && BNC % 32 == 0 && NL == TM && TN <= TM, "one load slot per MFMA group");
+  uint16_t* As0 = smem;
+  uint16_t* Bs0 = smem + 2 * A_ELEMS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / 4) % CPR)); };
+  auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
+
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = (a.K - k0) * a.N * 2;
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(a.B + k0 * a.N), (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
+  // load t < NA: A row tid / 4 + 64 t, chunk tid % 4; load NA + t: B k-row
+  // tid / 32 + 8 t, chunk tid % 32.  Rows 64 apart (A) keep the chunk
+  // swizzle, k-rows 8 apart flip bit 3 of it (B).
+  const int rowA = tid / CPR, cA = tid % CPR, krB = tid / BROW, cB = tid % BROW;
+  const uint32_t offA = (uint32_t)((rowA * a.K + 8 * cA) * 2), strideA = (uint32_t)(64 * a.K * 2);
+  const bool colok = 8 * cB < BNC && j0 + 8 * cB < a.N;
+  const uint32_t offB = colok ? (uint32_t)((krB * a.N + j0 + 8 * cB) * 2) : OOB, strideB = (uint32_t)(8 * a.N * 2);
+  const int ldA0 = ldsA(rowA, cA), ldB0 = ldsB(krB, cB), ldB1 = ldsB(krB + 8, cB);
+  u32x4 g[2][NL];
+  auto gload1 = [&](int sl, auto T, u32x4& dst) {
+    constexpr int t = decltype(T)::value;
+    const int64_t ks = k0 + (int64_t)sl * BK, lim = k1 - ks;
+    if constexpr (t < NA) {
+      const uint32_t o = (8 * cA < lim && i0 + rowA + 64 * t < a.M) ? offA + t * strideA : OOB;
+      dst = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, o, (int)(ks * 2), 0));
+    } else {
+      constexpr int u = t - NA;
+      const uint32_t o = (krB + 8 * u < lim && colok) ? offB + u * strideB : OOB;
+      dst = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, o, (int)((ks - k0) * a.N * 2), 0));
+    }
+  };
+  // chunk t of a slab into LDS buffer buf
+  auto lstore1 = [&](int buf, auto T, const u32x4& v) {
+    constexpr int t = decltype(T)::value;
+    if constexpr (t < NA) {
+      *(u32x4*)&As0[buf * A_ELEMS + 8 * ldA0 + 64 * BK * t] = v;
+    } else {
+      constexpr int u = t - NA;
+      if (BNC == BN || colok) *(u32x4*)&Bs0[buf * B_ELEMS + 8 * (u & 1 ? ldB1 : ldB0) + 8 * BN * (u & ~1)] = v;
+    }
+  };
+
+  floatx4 acc[TM][TN];
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
+  shortx8 fa[2][TM], fb[2][TN];
+  auto rdA = [&](int buf, int mi, shortx8& f) {
+    const int row = wm * WTM + 16 * mi + (lane & 15);
+    f = *(const shortx8*)&As0[buf * A_ELEMS + 8 * ldsA(row, lane >> 4)];
+  };
+  auto rdB = [&](int buf, int ni, shortx8& f) {
+    const uint16_t* Bs = Bs0 + buf * B_ELEMS;
+    const int i = lane & 15, gq = lane >> 4;
+    const int n = wn * WTN + 16 * ni + 4 * (i & 3);
+    const int kr0 = 8 * gq + (i >> 2), kr1 = kr0 + 4;
+    const shortx4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr0, n / 8) + (n & 7)]));
+    const shortx4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
+    f = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+
+  // prologue: slab 0 in buffer 0 and read into fragment set 0, slab 1 in
+  // buffer 1, slabs 2 and 3 in the global-load sets
+  static_for<0, NL>([&](auto t) { gload1(0, t, g[0][t]); });
+  static_for<0, NL>([&](auto t) { gload1(1, t, g[1][t]); });
+  static_for<0, NL>([&](auto t) { lstore1(0, t, g[0][t]); });
+  static_for<0, NL>([&](auto t) { gload1(2, t, g[0][t]); });
+  static_for<0, NL>([&](auto t) { lstore1(1, t, g[1][t]); });
+  static_for<0, NL>([&](auto t) { gload1(3, t, g[1][t]); });
+  __syncthreads();
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) rdA(0, mi, fa[0][mi]);
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) rdB(0, ni, fb[0][ni]);
+  __syncthreads();
+
+  auto step = [&](int sl, auto CUR) {
+    constexpr int cur = decltype(CUR)::value, nxt = cur ^ 1;
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, TM>([&](auto mi) {
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) mfma16_tied(acc[mi][ni], fa[cur][mi], fb[cur][ni]);
+      __builtin_amdgcn_sched_barrier(0);
+      rdA(nxt, mi, fa[nxt][mi]);
+      if constexpr (mi < TN) rdB(nxt, mi, fb[nxt][mi]);
+      lstore1(cur, mi, g[cur][mi]);
+      gload1(sl + 4, mi, g[cur][mi]);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    __syncthreads();
+  };
+  for (int sl = 0; sl < nslab; sl += 2) {
+    step(sl, std::integral_constant<int, 0>{});
+    step(sl + 1, std::integral_constant<int, 1>{});
+  }
+  mfma_drain();
+
+  constexpr int CSP = WTN + 4;
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
+  float* bsh = reinterpret_cast<float*>(smem) + 4 * 16 * CSP;
+  static_assert((4 * 16 * CSP + BNC) * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
+  stage_bias(a, j0, BNC, bsh);
+  __syncthreads();
+  wave_epilogue<TM, TN>(a, s, i0 + wm * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
+}
+
+// Columns [0, n_split) in 256 x 256 blocks, the rest in 256 x 192 blocks.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_w4_mixed(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (256 * 32 + 32 * 256)];
+  const int tiles_m = (int)((a.M + 255) / 256);
+  const int tn1 = (int)((a.n_split + 255) / 256), nb1 = tiles_m * tn1;
+  int ty, tx;
+  if ((int)blockIdx.x < nb1) {
+    grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
+    w4_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
+  } else {
+    const int tn2 = (int)((a.N - a.n_split + 191) / 192);
+    grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
+    w4_body<192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
   }
 }
 
@@ -1390,6 +1596,12 @@ static hipError_t launch_pp_t(const GemmArgs& a, hipStream_t st) {
 hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + 255) / 256, tn = a.n_split / 256 + (a.N - a.n_split + 191) / 192;
   hipLaunchKernelGGL((gemm_pp_mixed<32>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_w4(const GemmArgs& a, hipStream_t st) {
+  const int64_t tm = (a.M + 255) / 256, tn = (a.n_split + 255) / 256 + (a.N - a.n_split + 191) / 192;
+  hipLaunchKernelGGL(gemm_w4_mixed, dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

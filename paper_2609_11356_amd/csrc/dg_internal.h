@@ -83,6 +83,7 @@ bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resou
 hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t s);   // n_split set
 // direct-to-LDS ping-pong: 256 x 256 blocks, or (mixed) the kernel-6 split
 hipError_t launch_gemm_ppd(const GemmArgs& a, bool mixed, hipStream_t s);
+hipError_t launch_gemm_w4(const GemmArgs& a, hipStream_t st);
 hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, int slab_k, hipStream_t s);
 bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
 hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tile_m, int tile_n, int slots, int slab_k, hipStream_t s);

@@ -340,8 +340,8 @@ __global__ __launch_bounds__(256) void rmsnorm_scale(NormArgs a) {
           y0 = one(xv[i].x, j); y1 = one(xv[i].y, j + 1); y2 = one(xv[i].z, j + 2); y3 = one(xv[i].w, j + 3);
         }
         if (a.out_bf16) {
-          const uint32_t lo = (uint32_t)f32_bf16(y0) | ((uint32_t)f32_bf16(y1) << 16);
-          const uint32_t hi = (uint32_t)f32_bf16(y2) | ((uint32_t)f32_bf16(y3) << 16);
+          const uint32_t lo = f32x2_bf16x2(y0, y1);
+          const uint32_t hi = f32x2_bf16x2(y2, y3);
           *(uint2*)&((uint16_t*)a.Y)[row * cols + j] = uint2{lo, hi};
         } else {
           *(float4*)&((float*)a.Y)[row * cols + j] = float4{y0, y1, y2, y3};
@@ -450,10 +450,10 @@ __global__ __launch_bounds__(256) void rmsnorm_strided_fused(RowsumArgs ra, Norm
     if (a.out_bf16) {
       uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
       if (n == 4) {
-        *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
-                            (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+        *(uint2*)yp = uint2{f32x2_bf16x2(y[0], y[1]),
+                            f32x2_bf16x2(y[2], y[3])};
       } else if (n == 2) {
-        *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+        *(uint32_t*)yp = f32x2_bf16x2(y[0], y[1]);
       } else {
         for (int u = 0; u < n; ++u) yp[u] = f32_bf16(y[u]);
       }
@@ -678,10 +678,10 @@ __global__ __launch_bounds__(256) void layernorm_strided_fused(RowsumArgs ra, No
       if (a.out_bf16) {
         uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
         if constexpr (LPL == 4)
-          *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
-                              (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+          *(uint2*)yp = uint2{f32x2_bf16x2(y[0], y[1]),
+                              f32x2_bf16x2(y[2], y[3])};
         else if constexpr (LPL == 2)
-          *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+          *(uint32_t*)yp = f32x2_bf16x2(y[0], y[1]);
         else
           yp[0] = f32_bf16(y[0]);
       } else {
@@ -923,10 +923,10 @@ __global__ __launch_bounds__(256) void softmax_strided_fused(RowsumArgs ra, Norm
       if (a.out_bf16) {
         uint16_t* yp = (uint16_t*)a.Y + row * cols + j;
         if constexpr (LPL == 4)
-          *(uint2*)yp = uint2{(uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16),
-                              (uint32_t)f32_bf16(y[2]) | ((uint32_t)f32_bf16(y[3]) << 16)};
+          *(uint2*)yp = uint2{f32x2_bf16x2(y[0], y[1]),
+                              f32x2_bf16x2(y[2], y[3])};
         else if constexpr (LPL == 2)
-          *(uint32_t*)yp = (uint32_t)f32_bf16(y[0]) | ((uint32_t)f32_bf16(y[1]) << 16);
+          *(uint32_t*)yp = f32x2_bf16x2(y[0], y[1]);
         else
           yp[0] = f32_bf16(y[0]);
       } else {

@@ -150,8 +150,8 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(3, 0, 0, 0, 0, 0, 128)        # slab_k is a kernel-4 knob
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
-    # kernels 6 and 7 take no tile shape; split_n is a multiple of 256 within N, and only for them
-    for k in (6, 7):
+    # kernels 6, 7 and 10 take no tile shape; split_n is a multiple of 256 within N, and only for them
+    for k in (6, 7, 10):
         for kn in (dg.dg_knobs(k, 256, 256, 0, 0, 0, 0, 0), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 100),
                    dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 512), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, -256)):
             assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
