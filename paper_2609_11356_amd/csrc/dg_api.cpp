@@ -424,7 +424,8 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
       const int64_t sp = mixed_split(M, N, a.S, cu_count());
       split_n = sp < 0 ? (N + 255) / 256 * 256 : sp;
     }
-    if (((M + 255) / 256) * ((split_n + 255) / 256 + (N - split_n + 191) / 192) > INT32_MAX) return DG_ERR_SHAPE;
+    if (((M + 255) / 256) * ((split_n + 255) / 256 + (N > split_n ? (N - split_n + 191) / 192 : 0)) > INT32_MAX)
+      return DG_ERR_SHAPE;
     a.order = order ? order : 1;
     a.n_split = split_n;
     e = dg::launch_gemm_w4(a, st);

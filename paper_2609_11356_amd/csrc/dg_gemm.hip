@@ -1352,7 +1352,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
     w4_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
   } else {
-    const int tn2 = (int)((a.N - a.n_split + 191) / 192);
+    const int tn2 = a.N > a.n_split ? (int)((a.N - a.n_split + 191) / 192) : 0;
     grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
     w4_body<192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
   }
@@ -1600,7 +1600,7 @@ hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_gemm_w4(const GemmArgs& a, hipStream_t st) {
-  const int64_t tm = (a.M + 255) / 256, tn = (a.n_split + 255) / 256 + (a.N - a.n_split + 191) / 192;
+  const int64_t tm = (a.M + 255) / 256, tn = (a.n_split + 255) / 256 + (a.N > a.n_split ? (a.N - a.n_split + 191) / 192 : 0);
   hipLaunchKernelGGL(gemm_w4_mixed, dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(256), 0, st, a);
   return hipGetLastError();
 }
