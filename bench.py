@@ -304,8 +304,8 @@ def main():
         torch.cuda.synchronize()
         colsum[name + "_ms"] = round(a.elapsed_time(b) / args.steps, 4)
     colsum["colsum_overhead_ms"] = round(colsum["gemm_f32_colsum_ms"] - colsum["gemm_f32_ms"], 4)
-    colsum["what"] = ("2048x14336x4096 GEMM, fp32 out, then the balanced tree down each of the 14336 columns "
-                      "(runs of 256 rows folded in parallel, then their roots)")
+    colsum["what"] = ("2048x14336x4096 GEMM, fp32 out, and the balanced tree down each of the 14336 columns "
+                      "(each 256-row run folded in the GEMM's epilogue, then the run roots met)")
 
     # ------------------------------------------------------ row reduction
     rs_bytes = X.nbytes + X.shape[0] * 4

@@ -262,8 +262,13 @@ dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n) {
   return DG_OK;
 }
 
-dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
-                        int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream) {
+// The GEMM; with colsum_part set, a launch on 256-row blocks of one part
+// also writes the column sums of each 256-row run of C there, and *fused says
+// whether it did.
+static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                           int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream,
+                           float* colsum_part, bool* fused) {
+  if (fused) *fused = false;
   if (!d) return DG_ERR_INVALID;
   if (M < 0 || N < 0 || K < 0) return DG_ERR_SHAPE;
   const dg_desc_params& p = d->p;
@@ -391,6 +396,10 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
     depth = c.depth;
     slab_k = c.slab_k;
   }
+  if (colsum_part && a.S == 1 && (kern == 6 || (kern == 5 && tm == 256))) {
+    a.colsum_part = colsum_part;
+    *fused = true;
+  }
   hipError_t e;
   if (kern == 9) {
     if ((M + 3) / 4 > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
@@ -479,6 +488,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
   return DG_OK;
 }
 
+dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                        int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream) {
+  return gemm_impl(d, A, B, bias, C, M, N, K, knobs, stream, nullptr, nullptr);
+}
+
 dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
                   int64_t M, int64_t N, int64_t K, void* stream) {
   return dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
@@ -492,8 +506,6 @@ dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const v
   if (colsum && !aligned(colsum, 4)) return DG_ERR_ALIGN;
   const int64_t nrun = (M + 255) / 256;
   if (nrun > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
-  dg_status s = dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
-  if (s != DG_OK || N == 0) return s;
   hipStream_t st = (hipStream_t)stream;
   dg::ColsumArgs c;
   c.C = C;
@@ -502,7 +514,27 @@ dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const v
   c.M = M;
   c.N = N;
   c.out_bf16 = d->p.out_dtype == DG_BF16;
-  if (nrun > 1) {
+  // One part: the GEMM's epilogue may fold the 256-row runs itself (run roots
+  // straight into colsum when there is one run); the workspace is free then.
+  bool fused = false;
+  dg_status s;
+  if (d->p.split_k == 1 && M > 0 && N > 0) {
+    if (nrun > 1) {
+      void* ws = nullptr;
+      s = get_workspace(st, (size_t)nrun * (size_t)N * sizeof(float), &ws);
+      if (s != DG_OK) return s;
+      c.part = (float*)ws;
+    }
+    s = gemm_impl(d, A, B, bias, C, M, N, K, nullptr, stream, nrun > 1 ? c.part : colsum, &fused);
+  } else {
+    s = dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
+  }
+  if (s != DG_OK || N == 0) return s;
+  if (fused) {
+    if (nrun > 1 && dg::launch_colsum_merge(c, st) != hipSuccess) return DG_ERR_HIP;
+    return DG_OK;
+  }
+  if (nrun > 1 && !c.part) {
     void* ws = nullptr;
     s = get_workspace(st, (size_t)nrun * (size_t)N * sizeof(float), &ws);
     if (s != DG_OK) return s;

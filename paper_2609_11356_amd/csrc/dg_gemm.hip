@@ -102,15 +102,16 @@ __device__ __forceinline__ void finish(const GemmArgs& a, int s, int64_t i, int6
 
 // finish() for four consecutive columns j..j+3 (all < N: the tiled path
 // requires N % 8 == 0 and 16-byte aligned C), with one vector store; b4 holds
-// the bias of those columns as binary32 (used only by the epilogue).
-__device__ __forceinline__ void finish4v(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4, float4 b4) {
+// the bias of those columns as binary32 (used only by the epilogue).  Returns
+// the four values as stored in C, as binary32 (the partials when S > 1).
+__device__ __forceinline__ float4 finish4v(const GemmArgs& a, int s, int64_t i, int64_t j, float4 y4, float4 b4) {
   float y[4] = {y4.x, y4.y, y4.z, y4.w};
 #pragma unroll
   for (int e = 0; e < 4; ++e)
     if (a.partial_bf16) y[e] = round_bf16(y[e]);
   if (a.S > 1) {
     *(float4*)&a.ws[((int64_t)s * a.M + i) * a.N + j] = float4{y[0], y[1], y[2], y[3]};
-    return;
+    return float4{y[0], y[1], y[2], y[3]};
   }
   if (a.epilogue != DG_EPI_NONE) {
     const float b[4] = {b4.x, b4.y, b4.z, b4.w};
@@ -129,9 +130,10 @@ __device__ __forceinline__ void finish4v(const GemmArgs& a, int s, int64_t i, in
     const uint32_t lo = f32x2_bf16x2(y[0], y[1]);
     const uint32_t hi = f32x2_bf16x2(y[2], y[3]);
     *(uint2*)&((uint16_t*)a.C)[i * a.N + j] = uint2{lo, hi};
-  } else {
-    *(float4*)&((float*)a.C)[i * a.N + j] = float4{y[0], y[1], y[2], y[3]};
+    return float4{bits_f32(lo << 16), bits_f32(lo & 0xffff0000u), bits_f32(hi << 16), bits_f32(hi & 0xffff0000u)};
   }
+  *(float4*)&((float*)a.C)[i * a.N + j] = float4{y[0], y[1], y[2], y[3]};
+  return float4{y[0], y[1], y[2], y[3]};
 }
 
 // finish4v with the bias read from memory.
@@ -141,7 +143,7 @@ __device__ __forceinline__ void finish4(const GemmArgs& a, int s, int64_t i, int
     const uint2 bb = *(const uint2*)&a.bias[j];
     b4 = float4{bits_f32(bb.x << 16), bits_f32(bb.x & 0xffff0000u), bits_f32(bb.y << 16), bits_f32(bb.y & 0xffff0000u)};
   }
-  finish4v(a, s, i, j, y4, b4);
+  (void)finish4v(a, s, i, j, y4, b4);
 }
 
 // Whether the epilogue reads the bias (a single part, bias epilogue).
@@ -166,12 +168,19 @@ __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)"
 // apart) and leaves as four-column vectors; the bias of the wave's columns
 // comes from bsh (staged by stage_bias), so no global load waits inside the
 // loop.  Only the wave itself touches cs, so no workgroup barrier is needed.
+// With croot set, the wave also folds each of its columns down its 16 TM
+// rows as the perfect tree of the values stored in C (rows past M count as
+// -0, the exact identity): the band's values go back into cs, lane c takes
+// column c of the band (rows paired from the top, 16-row band roots paired
+// the same way), and the root lands in croot[c].
 template <int TM, int TN, typename Acc>
 __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, int s, int64_t ib, int64_t jb, float* cs,
-                                              const float* bsh, const Acc& acc) {
+                                              const float* bsh, const Acc& acc, float* croot = nullptr) {
   constexpr int WTN = 16 * TN, CSP = WTN + 4;
+  static_assert((TM & (TM - 1)) == 0, "a power-of-two band count");
   const int lane = threadIdx.x & 63;
-  const bool bias = needs_bias(a);
+  const bool bias = needs_bias(a), tree = WTN <= 64 && croot != nullptr;   // one column per lane
+  float band[TM];
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
@@ -183,11 +192,32 @@ __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, int s, int64_t 
     for (int q = lane; q < 16 * WTN / 4; q += 64) {
       const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
       const int64_t i = ib + 16 * mi + rr, j = jb + cc;
-      const float4 y4 = *(const float4*)&cs[rr * CSP + cc];
+      float4* p = (float4*)&cs[rr * CSP + cc];
+      const float4 y4 = *p;
       const float4 b4 = bias ? *(const float4*)&bsh[cc] : float4{0.f, 0.f, 0.f, 0.f};
-      if (i < a.M && j < a.N) finish4v(a, s, i, j, y4, b4);
+      float4 v = float4{-0.f, -0.f, -0.f, -0.f};
+      if (i < a.M && j < a.N) v = finish4v(a, s, i, j, y4, b4);
+      if (tree) *p = v;
     }
     lds_wait();
+    if (WTN <= 64 && tree) {
+      float v[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = lane < WTN ? cs[r * CSP + lane] : 0.f;
+#pragma unroll
+      for (int w = 1; w < 16; w <<= 1)
+#pragma unroll
+        for (int r = 0; r < 16; r += 2 * w) v[r] = v[r] + v[r + w];
+      band[mi] = v[0];
+      lds_wait();
+    }
+  }
+  if (WTN <= 64 && tree) {
+#pragma unroll
+    for (int w = 1; w < TM; w <<= 1)
+#pragma unroll
+      for (int mi = 0; mi < TM; mi += 2 * w) band[mi] = band[mi] + band[mi + w];
+    if (lane < WTN) croot[lane] = band[0];
   }
 }
 
@@ -961,11 +991,21 @@ __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j
   constexpr int CSP = WTN + 4;
   float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
   float* bsh = reinterpret_cast<float*>(smem) + 8 * 16 * CSP;
-  static_assert((8 * 16 * CSP + BNC) * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
+  float* croot = bsh + BNC;   // [group][column]: each group's column roots
+  static_assert((8 * 16 * CSP + 3 * BNC) * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
   __syncthreads();
   stage_bias(a, j0, BNC, bsh);
   __syncthreads();
-  wave_epilogue<TM, TN>(a, s, i0 + grp * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
+  // a 256-row block is one run of the column sums: each group folds its 128
+  // rows, and the two roots meet (group 0's rows first)
+  const bool tree = BM == 256 && a.colsum_part != nullptr;
+  wave_epilogue<TM, TN>(a, s, i0 + grp * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc,
+                        tree ? croot + grp * BNC + wn * WTN : nullptr);
+  if (tree) {
+    __syncthreads();
+    for (int c = tid; c < BNC; c += 512)
+      if (j0 + c < a.N) a.colsum_part[(i0 / 256) * a.N + j0 + c] = croot[c] + croot[BNC + c];
+  }
 }
 
 // ------------------------------------- ping-pong with direct-to-LDS loads

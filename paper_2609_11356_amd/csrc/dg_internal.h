@@ -30,6 +30,8 @@ struct GemmArgs {
   int32_t order;                 // block order of the v3 kernels (speed only)
   int64_t split_w;               // strided split: dealt tile width (0: contiguous parts)
   int64_t n_split;               // mixed-width ping-pong: first column of the 192-wide blocks
+  float* colsum_part;            // set (single part, 256-row blocks): column sums of each 256-row
+                                 // run of C, [ceil(M / 256)][N], folded in the epilogue
 };
 
 struct CombineArgs {
@@ -104,5 +106,6 @@ hipError_t launch_layernorm_fused(const RowsumArgs& r, const NormArgs& a, hipStr
 hipError_t launch_layernorm_center(const NormArgs& a, hipStream_t s);
 // column sums of a GEMM output: subtrees of 256 rows, then their tree
 hipError_t launch_colsum(const ColsumArgs& a, hipStream_t s);
+hipError_t launch_colsum_merge(const ColsumArgs& a, hipStream_t s);   // run roots in a.part only
 
 }  // namespace dg

@@ -807,6 +807,12 @@ __global__ __launch_bounds__(256) void colsum_zero(ColsumArgs a) {
   if (j < a.N) a.colsum[j] = 0.0f;
 }
 
+hipError_t launch_colsum_merge(const ColsumArgs& a, hipStream_t st) {
+  const int64_t nrun = (a.M + CS_RUN - 1) / CS_RUN;
+  hipLaunchKernelGGL(colsum_merge, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, st, a, nrun);
+  return hipGetLastError();
+}
+
 hipError_t launch_colsum(const ColsumArgs& a, hipStream_t st) {
   if (a.M == 0) {
     hipLaunchKernelGGL(colsum_zero, dim3((unsigned)((a.N + 255) / 256)), dim3(256), 0, st, a);

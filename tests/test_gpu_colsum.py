@@ -73,3 +73,23 @@ def test_colsum_no_rows(dg):
     dg.dg_gemm_colsum(d, A, B, None, C, cs)
     torch.cuda.synchronize()
     assert np.all(cs.cpu().numpy() == 0.0) and not np.any(np.signbit(cs.cpu().numpy()))
+
+
+@pytest.mark.parametrize("M,desc", [(1000, dict(tile_k=64, out="bf16", epilogue="bias_silu")),
+                                    (769, dict(tile_k=64)), (256, dict(tile_k=64, out="bf16"))])
+def test_colsum_folded_in_epilogue(dg, M, desc):
+    """Shapes large enough for the 256-row-block kernels, whose epilogue folds
+    each 256-row run of the stored values (rows past M as -0) before the
+    runs meet: a partial last run, bf16 output with bias and SiLU, a single
+    run.  The sums against the oracle's tree over the GPU's C, and sampled C
+    against the oracle."""
+    N, K = 12288, 128
+    A = inputs.spread_bf16(M + 5, (M, K))
+    B = inputs.spread_bf16(N + 6, (K, N))
+    bias = inputs.normal_bf16(7, (N,), 0.5)
+    use_bias = desc.get("epilogue", "none") != "none"
+    C, cs = run(dg, desc, A, B, bias if use_bias else None)
+    assert_bits_equal(cs, oracle.colsum(C), "colsum %s M %d" % (desc, M))
+    rng = np.random.default_rng(M)
+    ii, jj = rng.integers(0, M, 200), rng.integers(0, N, 200)
+    assert_bits_equal(C[ii, jj], oracle.gemm_at(desc, A, B, bias if use_bias else None, ii, jj), "sampled C")
