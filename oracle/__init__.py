@@ -48,7 +48,7 @@ class _Params(ctypes.Structure):
         (n, ctypes.c_int32) for n in (
             "tile_combine", "split_combine", "tail_first", "fma", "partial_bf16",
             "merge_bf16", "out_bf16", "epilogue", "pre_act_round", "leaf_w", "sumsq",
-            "split_strided", "split_tile", "leaf_strided", "fold_down", "norm_pre_round")]
+            "split_strided", "split_tile", "leaf_strided", "fold_down", "norm_pre_round", "in_f16")]
 
 
 _lib = None
@@ -89,12 +89,18 @@ def _bind(path):
     L.dgo_colsum.argtypes = [vp, i32, i64, i64, vp, i32]
     L.dgo_group_update.argtypes = [i32, f32, vp, vp, i32, i32, i32]
     L.dgo_group_update.restype = f32
-    L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32]
+    L.dgo_group_update_batch.argtypes = [i32, i64, vp, vp, vp, i32, i32, i32, vp, i32, i32]
     L.dgo_group_update_batch.restype = None
     L.dgo_chunk8.argtypes = [f32, vp, vp, i32]
     L.dgo_chunk8.restype = f32
     L.dgo_exact_dot_rn32.argtypes = [f32, vp, vp, i32]
     L.dgo_exact_dot_rn32.restype = f32
+    L.dgo_chunk8_fmt.argtypes = [i32, f32, vp, vp, i32]
+    L.dgo_chunk8_fmt.restype = f32
+    L.dgo_exact_dot_rn32_fmt.argtypes = [i32, f32, vp, vp, i32]
+    L.dgo_exact_dot_rn32_fmt.restype = f32
+    L.dgo_f16_to_f32.argtypes = [ctypes.c_uint16]
+    L.dgo_f16_to_f32.restype = f32
     L.dgo_tree.argtypes = [vp, i32, i32]
     L.dgo_tree.restype = f32
     L.dgo_tree_bitrev.argtypes = [vp, i32, i32]
@@ -115,7 +121,7 @@ DEFAULTS = dict(model="gfx950", mma="16x16x32", tile_k=64, split_k=1, k_cuts=Non
                 tile_combine="carry", split_combine="seq", tail="last", fma=1,
                 partial="f32", merge="f32", out="f32", epilogue="none",
                 epi_round="final", leaf_w=64, reduce="sum", split_layout="contiguous", split_tile=0,
-                leaf_layout="contiguous", lane_fold="up", norm_round="final")
+                leaf_layout="contiguous", lane_fold="up", norm_round="final", in_dtype="bf16")
 
 
 def params(desc: dict):
@@ -149,6 +155,7 @@ def params(desc: dict):
     p.leaf_strided = {"contiguous": 0, "strided": 1}[d["leaf_layout"]]
     p.fold_down = {"up": 0, "down": 1}[d["lane_fold"]]
     p.norm_pre_round = {"final": 0, "pre_weight": 1}[d["norm_round"]]
+    p.in_f16 = {"bf16": 0, "f16": 1}[d["in_dtype"]]
     return p, cuts
 
 
@@ -294,26 +301,34 @@ def group_update(acc, a, b, g, fma, model="gfx950"):
                                              len(a), g, fma))
 
 
-def group_update_batch(acc, a, b, g, fma, model="gfx950", nthreads=None):
-    """acc (count,), a and b (count, n) bf16 bits -> (count,) float32."""
+def group_update_batch(acc, a, b, g, fma, model="gfx950", nthreads=None, in_dtype="bf16"):
+    """acc (count,), a and b (count, n) operand bits (bf16, or binary16 with
+    in_dtype="f16") -> (count,) float32."""
     acc = np.ascontiguousarray(acc, dtype=np.float32)
     a, b = _u16(a), _u16(b)
     count, n = a.shape
     out = np.zeros(count, dtype=np.float32)
     m = MODEL_GFX950 if model == "gfx950" else MODEL_EXACT
     lib().dgo_group_update_batch(m, count, acc.ctypes.data, a.ctypes.data, b.ctypes.data,
-                                 n, g, fma, out.ctypes.data, nthreads or os.cpu_count())
+                                 n, g, fma, out.ctypes.data, nthreads or os.cpu_count(),
+                                 {"bf16": 0, "f16": 1}[in_dtype])
     return out
 
 
-def chunk8(acc, a, b):
+def chunk8(acc, a, b, in_dtype="bf16"):
     a, b = _u16(a), _u16(b)
-    return np.float32(lib().dgo_chunk8(float(acc), a.ctypes.data, b.ctypes.data, len(a)))
+    return np.float32(lib().dgo_chunk8_fmt({"bf16": 0, "f16": 1}[in_dtype], float(acc),
+                                           a.ctypes.data, b.ctypes.data, len(a)))
 
 
-def exact_dot_rn32(c, a, b):
+def exact_dot_rn32(c, a, b, in_dtype="bf16"):
     a, b = _u16(a), _u16(b)
-    return np.float32(lib().dgo_exact_dot_rn32(float(c), a.ctypes.data, b.ctypes.data, len(a)))
+    return np.float32(lib().dgo_exact_dot_rn32_fmt({"bf16": 0, "f16": 1}[in_dtype], float(c),
+                                                   a.ctypes.data, b.ctypes.data, len(a)))
+
+
+def f16_to_f32(h):
+    return np.float32(lib().dgo_f16_to_f32(int(h)))
 
 
 def tree(v, bf16_round=False):

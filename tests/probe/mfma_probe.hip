@@ -1,4 +1,4 @@
-// mfma_probe.hip -- test infrastructure: issues raw gfx950 bf16 MFMAs on
+// mfma_probe.hip -- test infrastructure: issues raw gfx950 bf16 / fp16 MFMAs on
 // operand slots the host supplies, so that the CPU oracle's model of one
 // instruction can be checked against the hardware (paper Sec. 4: numerical
 // experiments on crafted inputs read the arithmetic off the instruction).
@@ -8,6 +8,7 @@
 #include <stdint.h>
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef short shortx8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
@@ -30,7 +31,26 @@ __global__ __launch_bounds__(64) void probe32(const shortx8* A, const shortx8* B
                                                  __builtin_bit_cast(bf16x8, B[i]), C[i], 0, 0, 0);
 }
 
-// instr 0: 16x16x32 (4 accumulator floats per lane), 1: 32x32x16 (16).
+__global__ __launch_bounds__(64) void probe16h(const shortx8* A, const shortx8* B, const floatx4* C,
+                                               floatx4* D, int ncases) {
+  const int c = blockIdx.x, l = threadIdx.x;
+  if (c >= ncases) return;
+  const size_t i = (size_t)c * 64 + l;
+  D[i] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, A[i]),
+                                                __builtin_bit_cast(f16x8, B[i]), C[i], 0, 0, 0);
+}
+
+__global__ __launch_bounds__(64) void probe32h(const shortx8* A, const shortx8* B, const floatx16* C,
+                                               floatx16* D, int ncases) {
+  const int c = blockIdx.x, l = threadIdx.x;
+  if (c >= ncases) return;
+  const size_t i = (size_t)c * 64 + l;
+  D[i] = __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, A[i]),
+                                                __builtin_bit_cast(f16x8, B[i]), C[i], 0, 0, 0);
+}
+
+// instr 0: 16x16x32 bf16 (4 accumulator floats per lane), 1: 32x32x16 bf16
+// (16); 2 and 3: the same shapes with fp16 operands.
 // All pointers are device pointers sized for ncases.
 extern "C" int mfma_probe(int instr, int ncases, const void* A, const void* B, const void* C,
                           void* D, void* stream) {
@@ -41,6 +61,12 @@ extern "C" int mfma_probe(int instr, int ncases, const void* A, const void* B, c
                        (const floatx4*)C, (floatx4*)D, ncases);
   else if (instr == 1)
     hipLaunchKernelGGL(probe32, dim3(ncases), dim3(64), 0, s, (const shortx8*)A, (const shortx8*)B,
+                       (const floatx16*)C, (floatx16*)D, ncases);
+  else if (instr == 2)
+    hipLaunchKernelGGL(probe16h, dim3(ncases), dim3(64), 0, s, (const shortx8*)A, (const shortx8*)B,
+                       (const floatx4*)C, (floatx4*)D, ncases);
+  else if (instr == 3)
+    hipLaunchKernelGGL(probe32h, dim3(ncases), dim3(64), 0, s, (const shortx8*)A, (const shortx8*)B,
                        (const floatx16*)C, (floatx16*)D, ncases);
   else
     return -1;

@@ -1,4 +1,4 @@
-"""The oracle's model of one gfx950 bf16 MFMA, checked against the hardware
+"""The oracle's model of one gfx950 bf16 or fp16 MFMA, checked against the hardware
 on crafted and random single-instruction cases (compared at run time; no
 hardware output is stored).  Operand slot layouts: 16x16x32 -- lane l holds
 A[l%16][8(l/16)+e], B[8(l/16)+e][l%16], and rows 4(l/16)+r of column l%16 of
@@ -15,7 +15,7 @@ import oracle
 from paper_2609_11356_amd import inputs
 
 pytestmark = pytest.mark.gpu
-GEO = {0: (16, 32, 16), 1: (32, 16, 32)}
+GEO = {0: (16, 32, 16), 1: (32, 16, 32), 2: (16, 32, 16), 3: (32, 16, 32)}   # 2, 3: fp16 operands
 
 
 @pytest.fixture(scope="module")
@@ -33,6 +33,7 @@ def probe():
 
 
 def to_slots(instr, A, B, C):
+    instr %= 2
     n = A.shape[0]
     l = np.arange(64)
     As = np.zeros((n, 64, 8), np.uint16)
@@ -51,6 +52,7 @@ def to_slots(instr, A, B, C):
 
 
 def from_slots(instr, Ds):
+    instr %= 2
     R, _, Cc = GEO[instr]
     n = Ds.shape[0]
     D = np.zeros((n, R, Cc), np.float32)
@@ -83,7 +85,7 @@ def model(instr, A, B, C):
     n = A.shape[0]
     a = np.broadcast_to(A[:, :, None, :], (n, R, Cc, Kc)).reshape(-1, Kc)
     b = np.broadcast_to(np.transpose(B, (0, 2, 1))[:, None, :, :], (n, R, Cc, Kc)).reshape(-1, Kc)
-    out = oracle.group_update_batch(C.reshape(-1), a, b, g=Kc, fma=1)
+    out = oracle.group_update_batch(C.reshape(-1), a, b, g=Kc, fma=1, in_dtype="f16" if instr >= 2 else "bf16")
     return out.reshape(n, R, Cc)
 
 
@@ -168,3 +170,65 @@ def test_edge_values(probe):
         C[c, i, i] = acc
     Ab, Bb = bits(A), bits(B)
     compare(run_probe(probe, 0, Ab, Bb, C), model(0, Ab, Bb, C), "edge values")
+
+
+def h16(x):
+    return np.asarray(x, dtype=np.float16).view(np.uint16)
+
+
+@pytest.mark.parametrize("instr", [2, 3])
+@pytest.mark.parametrize("mode", ["normal", "spread", "wide", "subnormal", "accdom", "cancel"])
+def test_random_single_instructions_f16(probe, instr, mode):
+    """fp16 operands: the same chunk model with binary16 exponents."""
+    R, Kc, Cc = GEO[instr]
+    n = 2000 if instr == 2 else 500
+    rng = np.random.default_rng(77 * instr + hash(mode) % 991)
+    sp = lambda shape, lo, hi: h16(rng.choice([-1, 1], shape) * (1 + rng.random(shape)) *
+                                   np.exp2(rng.integers(lo, hi, shape)))
+    C = (rng.standard_normal((n, R, Cc)) * np.exp2(rng.integers(-20, 20, (n, R, Cc)))).astype(np.float32)
+    if mode == "normal":
+        A, B = h16(rng.standard_normal((n, R, Kc))), h16(rng.standard_normal((n, Kc, Cc)))
+        C = rng.standard_normal((n, R, Cc)).astype(np.float32)
+    elif mode == "spread":
+        A, B = sp((n, R, Kc), -12, 12), sp((n, Kc, Cc), -12, 12)
+    elif mode == "wide":
+        A, B = sp((n, R, Kc), -24, 15), sp((n, Kc, Cc), -24, 15)
+    elif mode == "subnormal":
+        A, B = sp((n, R, Kc), -24, -13), sp((n, Kc, Cc), -24, 4)
+        C = (rng.standard_normal((n, R, Cc)) * np.exp2(rng.integers(-50, -20, (n, R, Cc)))).astype(np.float32)
+    elif mode == "accdom":
+        A, B = sp((n, R, Kc), -8, 8), sp((n, Kc, Cc), -8, 8)
+        C = (rng.choice([-1, 1], (n, R, Cc)) * np.exp2(rng.integers(10, 40, (n, R, Cc))) *
+             (1 + rng.random((n, R, Cc)))).astype(np.float32)
+    else:
+        A, B = sp((n, R, Kc), -6, 6), sp((n, Kc, Cc), -6, 6)
+        A[:, :, 1] = A[:, :, 0] ^ 0x8000
+        B[:, 1, :] = B[:, 0, :]
+    compare(run_probe(probe, instr, A, B, C), model(instr, A, B, C), "f16 %d %s" % (instr, mode))
+
+
+def test_edge_values_f16(probe):
+    """Binary16 window width, ties, subnormal factors, the largest values,
+    infinities and zeros in one 16x16x32 fp16 instruction each."""
+    cases = []
+    for e in range(0, 31):
+        ea, eb = min(e, 15), e - min(e, 15)
+        cases.append(([(2.0 ** ea, 2.0 ** eb), (-(2.0 ** ea), 2.0 ** eb), (1, 1)], 0.0))
+    for d in range(12, 25):
+        cases.append(([(2.0 ** -12, 2.0 ** -12), (2.0 ** -d, 1)], 1.0))
+        cases.append(([(-(2.0 ** -12), 2.0 ** -12), (-(2.0 ** -d), 1)], -1.0))
+    cases += [([(1, 1), (2.0 ** -12, 2.0 ** -12), (2.0 ** -15, 2.0 ** -15)], 0.0),
+              ([(65504, 65504), (-65504, 65504), (2.0 ** -24, 1)], 0.0),
+              ([(np.inf, 1)], 0.0), ([(np.inf, 0)], 0.0), ([(-0.0, 1), (0.0, -1)], -0.0),
+              ([(1, 1)], np.inf), ([(2.0 ** -24, 2.0 ** -24)], 0.0), ([(2.0 ** -24, 2.0 ** -24)], 2.0 ** -60)]
+    n = (len(cases) + 15) // 16
+    A = np.zeros((n, 16, 32), np.float32)
+    B = np.zeros((n, 32, 16), np.float32)
+    C = np.zeros((n, 16, 16), np.float32)
+    for t, (prods, acc) in enumerate(cases):
+        c, i = divmod(t, 16)
+        for q, (x, y) in enumerate(prods):
+            A[c, i, q], B[c, q, i] = x, y
+        C[c, i, i] = acc
+    Ah, Bh = h16(A), h16(B)
+    compare(run_probe(probe, 2, Ah, Bh, C), model(2, Ah, Bh, C), "f16 edge values")

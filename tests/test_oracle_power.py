@@ -68,8 +68,12 @@ MUTANTS = {
     "layernorm variance over cols - 1": ("float var = s2 / n;", "float var = s2 / (n - 1.0f);"),
     "SUMSQ fma never fused": ("else if (p->fma) s = fmaf(x[k], x[k], s);", "else if (0) s = fmaf(x[k], x[k], s);"),
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
-    "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (bf16_isnan(a[t])",
-                               "int sign = 0;\n    if (bf16_isnan(a[t])"),
+    "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (op_isnan(a[t], f16)",
+                               "int sign = 0;\n    if (op_isnan(a[t], f16)"),
+    "binary16 exponent bias off by one": ("eb = f16 ? 5 : 8, bias = f16 ? 15 : 127;",
+                                          "eb = f16 ? 5 : 8, bias = f16 ? 14 : 127;"),
+    "binary16 product scale off by one": ("const int fb2 = 2 * op_frac(f16);",
+                                          "const int fb2 = 2 * op_frac(f16) - f16;"),
 }
 
 CHECKS = [
@@ -100,6 +104,10 @@ CHECKS = [
     lambda: pins.test_softmax_steps_and_rounding_points(),
     lambda: pins.test_layernorm_closed_forms(),
     lambda: pins.test_layernorm_steps_and_rounding_points(),
+    lambda: pins.test_f16_decoding_matches_numpy_on_every_pattern(),
+    lambda: pins.test_f16_exact_dot_is_the_rational_sum_rounded_once(),
+    lambda: pins.test_f16_chunk_model_hand_examples(),
+    lambda: pins.test_f16_chunk_model_equals_exact_when_window_holds_everything(),
 ]
 
 
