@@ -70,6 +70,7 @@ enum { DG_SPLIT_CONTIGUOUS = 0, DG_SPLIT_STRIDED = 1 };  /* layout of the split 
 enum { DG_LEAF_CONTIGUOUS = 0, DG_LEAF_STRIDED = 1 };    /* row-reduction leaf layout */
 enum { DG_FOLD_UP = 0, DG_FOLD_DOWN = 1 };               /* how the leaves meet */
 enum { DG_NORM_FINAL = 0, DG_NORM_PRE_WEIGHT = 1 };      /* RMS-norm rounding point */
+enum { DG_IN_BF16 = 0, DG_IN_F16 = 1 };                  /* GEMM operand format */
 
 #define DG_MAX_SPLIT 64
 
@@ -132,6 +133,12 @@ typedef struct {
                              it is rounded to bf16 first (an unfused "normalise
                              in fp32, cast to bf16, scale by the bf16 weight"
                              pair) */
+  int32_t in_dtype;       /* GEMM operands A and B.  DG_IN_BF16 (default) or
+                             DG_IN_F16: IEEE binary16, folded by the fp16
+                             instruction of the same shape, whose chunks follow
+                             the same rules with binary16 exponents (a product
+                             of two binary16 values is exact in binary32, so the
+                             scalar path is unchanged).  The bias stays bf16. */
 } dg_desc_params;
 
 typedef struct dg_desc dg_desc; /* opaque, immutable */
@@ -154,7 +161,8 @@ void dg_desc_destroy(dg_desc* d);
 dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n);
 
 /* C = epilogue(A . B) in the descriptor's order.
- *   A: device, M x K bf16 row-major;  B: device, K x N bf16 row-major;
+ *   A: device, M x K row-major;  B: device, K x N row-major; both bf16, or
+ *   binary16 when in_dtype = DG_IN_F16;
  *   bias: device, N bf16, required iff the epilogue uses it (else ignored);
  *   C: device, M x N of out_dtype, row-major (written, never read).
  * M = 0 or N = 0 is a no-op returning DG_OK.  K = 0 is allowed when

@@ -61,6 +61,8 @@ void make_signature(dg_desc* d) {
                        p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
   if (p.norm_round == DG_NORM_PRE_WEIGHT && n > 0 && n < (int)sizeof d->sig)
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/norm-pre-weight");
+  if (p.in_dtype == DG_IN_F16 && n > 0 && n < (int)sizeof d->sig)
+    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/in-f16");
   // one strided part is the whole axis, as one contiguous part is
   if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && n > 0 && n < (int)sizeof d->sig)
     n += std::snprintf(d->sig + n, sizeof d->sig - n, "/strided:%d", p.split_tile);
@@ -225,6 +227,7 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   if (!in(p->leaf_layout, DG_LEAF_CONTIGUOUS, DG_LEAF_STRIDED) || !in(p->lane_fold, DG_FOLD_UP, DG_FOLD_DOWN))
     return DG_ERR_INVALID;
   if (!in(p->norm_round, DG_NORM_FINAL, DG_NORM_PRE_WEIGHT)) return DG_ERR_INVALID;
+  if (!in(p->in_dtype, DG_IN_BF16, DG_IN_F16)) return DG_ERR_INVALID;
   if (p->split_layout == DG_SPLIT_STRIDED) {
     if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
       return DG_ERR_INVALID;
@@ -283,6 +286,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
   if (scalar ? (kern != 0 && kern != 9) : kern == 9) return DG_ERR_UNSUPPORTED;
   if (kern == 9 && (tm || tn || order || occ || depth || slab_k || split_n)) return DG_ERR_UNSUPPORTED;
+  // binary16 operands: the generic, v3, few-row, ping-pong and scalar kernels
+  const bool f16 = p.in_dtype == DG_IN_F16;
+  if (f16 && (kern == 2 || kern == 7 || kern == 8 || kern == 10)) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
     return DG_ERR_UNSUPPORTED;
@@ -339,6 +345,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   a.out_bf16 = p.out_dtype == DG_BF16;
   a.epilogue = p.epilogue;
   a.pre_act = p.epi_round == DG_ROUND_PRE_ACT;
+  a.in_f16 = f16;
   if ((M + 15) / 16 > 65535 || (N + 15) / 16 > (int64_t)1 << 31) return DG_ERR_SHAPE;
 
   hipStream_t st = (hipStream_t)stream;

@@ -63,6 +63,27 @@ __device__ __forceinline__ floatx4 mfma16(shortx8 a, shortx8 b, floatx4 c) {
                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// The fp16 instruction of the same shape (binary16 operands; its chunks
+// fold by the same rules, with exponents read from the binary16 fields).
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ floatx4 mfma16h(shortx8 a, shortx8 b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                               __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+template <bool F16>
+__device__ __forceinline__ floatx4 mfma16t(shortx8 a, shortx8 b, floatx4 c) {
+  if constexpr (F16) return mfma16h(a, b, c);
+  else return mfma16(a, b, c);
+}
+
+// An operand as binary32 (exact for both formats).
+template <bool F16>
+__device__ __forceinline__ float op_f32(uint16_t h) {
+  if constexpr (F16) return (float)__builtin_bit_cast(_Float16, h);
+  else return bf16_f32(h);
+}
+
 // The same instruction with the accumulator tied to one accumulation
 // register quad (input and output the same registers), for kernels whose
 // accumulators fill that register file: the compiler otherwise renames
@@ -233,7 +254,7 @@ __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, int s, int64_t 
 // tile_k positions from the part start (a short first tile when tail-first)
 // and are carried, chained or met in the balanced tree.  No MFMA row waste:
 // the shape of choice for one or a few rows split over many chunks.
-template <int MR, int CPT>
+template <int MR, int CPT, bool F16>
 __global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
   constexpr int W = 256;                  // positions per staged window
   constexpr int U = 16;                   // positions whose loads are in flight together
@@ -265,10 +286,10 @@ __global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
     const uint16_t* bp = a.B + k * a.N + j;
     if constexpr (CPT == 4) {
       const uint2 q = col ? *(const uint2*)bp : uint2{0u, 0u};
-      v[0] = bits_f32(q.x << 16); v[1] = bits_f32(q.x & 0xffff0000u);
-      v[2] = bits_f32(q.y << 16); v[3] = bits_f32(q.y & 0xffff0000u);
+      v[0] = op_f32<F16>((uint16_t)q.x); v[1] = op_f32<F16>((uint16_t)(q.x >> 16));
+      v[2] = op_f32<F16>((uint16_t)q.y); v[3] = op_f32<F16>((uint16_t)(q.y >> 16));
     } else {
-      v[0] = col ? bf16_f32(bp[0]) : 0.0f;
+      v[0] = col ? op_f32<F16>(bp[0]) : 0.0f;
     }
   };
   float acc[MR][CPT], part[MR][CPT], st[MR][CPT][32];
@@ -301,7 +322,7 @@ __global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
     __syncthreads();   // the previous window has been read
     for (int e = threadIdx.x; e < MR * W; e += 256) {
       const int r = e / W, qq = e % W;
-      As[r][qq] = (qq < n && i0 + r < a.M) ? bf16_f32(a.A[(i0 + r) * K + kpos(w0 + qq)]) : 0.0f;
+      As[r][qq] = (qq < n && i0 + r < a.M) ? op_f32<F16>(a.A[(i0 + r) * K + kpos(w0 + qq)]) : 0.0f;
     }
     __syncthreads();
     int qq = 0;
@@ -393,9 +414,9 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
         bv[e] = (ok && bcol < a.N) ? (short)a.B[k * a.N + bcol] : (short)0;
       }
       if (a.fma) {
-        v = mfma16(av, bv, v);
+        v = a.in_f16 ? mfma16h(av, bv, v) : mfma16(av, bv, v);
       } else {
-        floatx4 w = mfma16(av, bv, zero);
+        floatx4 w = a.in_f16 ? mfma16h(av, bv, zero) : mfma16(av, bv, zero);
         v = v + w;
       }
     }
@@ -641,7 +662,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4* lds_s4;
 
-template <int BM, int BN, int WM, int WN, int V3_BK>
+template <int BM, int BN, int WM, int WN, int V3_BK, bool F16>
 __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j0) {
   static_assert(WM * WN == 4, "four waves");
   constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -735,7 +756,7 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
 #pragma unroll
       for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[mi], bfr[ni], acc[mi][ni]);
+        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16t<F16>(af[mi], bfr[ni], acc[mi][ni]);
     }
   };
 
@@ -798,20 +819,20 @@ __device__ __forceinline__ void grouped_tile(int w, int tiles_m, int tiles_n, in
   *tx = in_group / rows;
 }
 
-template <int BM, int BN, int WM, int WN, int BK>
+template <int BM, int BN, int WM, int WN, int BK, bool F16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_v3(GemmArgs a) {
   const int tiles_m = (int)((a.M + BM - 1) / BM);
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  v3_body<BM, BN, WM, WN, BK>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+  v3_body<BM, BN, WM, WN, BK, F16>(a, (int64_t)ty * BM, (int64_t)tx * BN);
 }
 
-template <int BM, int BN, int WM, int WN, int BK>
+template <int BM, int BN, int WM, int WN, int BK, bool F16>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_v3x2(GemmArgs a) {
   const int tiles_m = (int)((a.M + BM - 1) / BM);
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  v3_body<BM, BN, WM, WN, BK>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+  v3_body<BM, BN, WM, WN, BK, F16>(a, (int64_t)ty * BM, (int64_t)tx * BN);
 }
 
 // ------------------------------------------------- ping-pong (eight waves)
@@ -842,7 +863,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 // BNC <= BN is the number of columns the block computes; the B slab keeps
 // the BN-wide LDS layout and load mapping, and its chunks past BNC are
 // neither loaded nor stored.
-template <int BM, int BN, int BK, int BNC>
+template <int BM, int BN, int BK, int BNC, bool F16>
 __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j0, uint16_t* smem) {
   constexpr int CPR = BK / 8, KK = BK / 32, WTM = BM / 2, WTN = BNC / 4, TM = WTM / 16, TN = WTN / 16;
   constexpr int BROW = BN / 8;
@@ -949,7 +970,7 @@ __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j
   auto mm_pair = [&](int p) {
     const int h = p / TM, mi = p % TM;
 #pragma unroll
-    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16(af[h][mi], bf[h][ni], acc[mi][ni]);
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16t<F16>(af[h][mi], bf[h][ni], acc[mi][ni]);
   };
 
   // prologue: slab 0 in buffer 0, slabs 1 and 2 in the two register sets
@@ -1215,13 +1236,13 @@ __global__ __launch_bounds__(512) void gemm_ppd_mixed(GemmArgs a) {
   }
 }
 
-template <int BM, int BN, int BK>
+template <int BM, int BN, int BK, bool F16>
 __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM * BK + BK * BN)];
   const int tiles_m = (int)((a.M + BM - 1) / BM);
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  pp_body<BM, BN, BK, BN>(a, (int64_t)ty * BM, (int64_t)tx * BN, smem);
+  pp_body<BM, BN, BK, BN, F16>(a, (int64_t)ty * BM, (int64_t)tx * BN, smem);
 }
 
 // Two column widths in one launch: columns [0, n_split) in 256 x 256 blocks
@@ -1230,7 +1251,7 @@ __global__ __launch_bounds__(512) void gemm_pp(GemmArgs a) {
 // where 256-wide blocks alone leave the last round partly idle (2048 x 14336:
 // 448 blocks of 256 x 256 take two rounds on 256 CUs; 256 blocks of
 // 256 x 256 and 256 of 256 x 192 take 1.75 rounds of work).
-template <int BK>
+template <int BK, bool F16>
 __global__ __launch_bounds__(512) void gemm_pp_mixed(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (256 * BK + BK * 256)];
   const int tiles_m = (int)((a.M + 255) / 256);
@@ -1238,11 +1259,11 @@ __global__ __launch_bounds__(512) void gemm_pp_mixed(GemmArgs a) {
   int ty, tx;
   if ((int)blockIdx.x < nb1) {
     grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
-    pp_body<256, 256, BK, 256>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
+    pp_body<256, 256, BK, 256, F16>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
   } else {
     const int tn2 = (int)((a.N - a.n_split + 191) / 192);
     grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
-    pp_body<256, 256, BK, 192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
+    pp_body<256, 256, BK, 192, F16>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
   }
 }
 
@@ -1409,7 +1430,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 // When the column tiles split evenly over the eight XCDs (workgroup w runs
 // on XCD w mod 8), each XCD takes a contiguous range of them, so that tiles
 // sharing 128-byte B lines share an L2.
-template <int TMS, int BN, int D, int BK>
+template <int TMS, int BN, int D, int BK, bool F16>
 __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
   constexpr int CPR = BK / 8, BM = 16 * TMS, NWC = BN / 16;
   constexpr int ACH = BM * CPR, BCH = BK * (BN / 8), BROW = BN / 8;
@@ -1485,7 +1506,7 @@ __global__ __launch_bounds__(256) void gemm_skinny(GemmArgs a) {
 #pragma unroll
       for (int mi = 0; mi < TMS; ++mi) {
         const shortx8 af = *(const shortx8*)&As[8 * ldsA(16 * mi + (lane & 15), kk / 8 + (lane >> 4))];
-        acc[mi] = mfma16(af, bfr, acc[mi]);
+        acc[mi] = mfma16t<F16>(af, bfr, acc[mi]);
       }
     }
   };
@@ -1578,7 +1599,8 @@ __global__ __launch_bounds__(256) void splitk_combine(CombineArgs a) {
 template <int MR, int CPT>
 static void launch_scalar_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + 256 * CPT - 1) / (256 * CPT)), (unsigned)((a.M + MR - 1) / MR), (unsigned)a.S);
-  hipLaunchKernelGGL((gemm_scalar<MR, CPT>), grid, dim3(256), 0, st, a);
+  if (a.in_f16) hipLaunchKernelGGL((gemm_scalar<MR, CPT, true>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gemm_scalar<MR, CPT, false>), grid, dim3(256), 0, st, a);
 }
 
 hipError_t launch_gemm_scalar(const GemmArgs& a, hipStream_t st) {
@@ -1621,21 +1643,28 @@ template <int BM, int BN, int WM, int WN, int BK, bool TWO>
 static hipError_t launch_v3_t(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
   dim3 grid((unsigned)(tm * tn), 1, (unsigned)a.S);
-  if constexpr (TWO) hipLaunchKernelGGL((gemm_v3x2<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((gemm_v3<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
+  if (a.in_f16) {
+    if constexpr (TWO) hipLaunchKernelGGL((gemm_v3x2<BM, BN, WM, WN, BK, true>), grid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((gemm_v3<BM, BN, WM, WN, BK, true>), grid, dim3(256), 0, st, a);
+  } else {
+    if constexpr (TWO) hipLaunchKernelGGL((gemm_v3x2<BM, BN, WM, WN, BK, false>), grid, dim3(256), 0, st, a);
+    else hipLaunchKernelGGL((gemm_v3<BM, BN, WM, WN, BK, false>), grid, dim3(256), 0, st, a);
+  }
   return hipGetLastError();
 }
 
 template <int BM, int BN, int BK>
 static hipError_t launch_pp_t(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + BM - 1) / BM, tn = (a.N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_pp<BM, BN, BK>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  if (a.in_f16) hipLaunchKernelGGL((gemm_pp<BM, BN, BK, true>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  else hipLaunchKernelGGL((gemm_pp<BM, BN, BK, false>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_pp_mixed(const GemmArgs& a, hipStream_t st) {
   const int64_t tm = (a.M + 255) / 256, tn = a.n_split / 256 + (a.N - a.n_split + 191) / 192;
-  hipLaunchKernelGGL((gemm_pp_mixed<32>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  if (a.in_f16) hipLaunchKernelGGL((gemm_pp_mixed<32, true>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
+  else hipLaunchKernelGGL((gemm_pp_mixed<32, false>), dim3((unsigned)(tm * tn), 1, (unsigned)a.S), dim3(512), 0, st, a);
   return hipGetLastError();
 }
 
@@ -1836,7 +1865,8 @@ hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tm, int tn, int slots, 
 template <int TMS, int BN, int D, int BK>
 static hipError_t launch_skinny_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + BN - 1) / BN), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
-  hipLaunchKernelGGL((gemm_skinny<TMS, BN, D, BK>), grid, dim3(256), 0, st, a);
+  if (a.in_f16) hipLaunchKernelGGL((gemm_skinny<TMS, BN, D, BK, true>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gemm_skinny<TMS, BN, D, BK, false>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 

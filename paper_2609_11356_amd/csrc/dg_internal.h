@@ -30,6 +30,7 @@ struct GemmArgs {
   int32_t order;                 // block order of the v3 kernels (speed only)
   int64_t split_w;               // strided split: dealt tile width (0: contiguous parts)
   int64_t n_split;               // mixed-width ping-pong: first column of the 192-wide blocks
+  int32_t in_f16;                // operands A and B are binary16 (else bfloat16)
   float* colsum_part;            // set (single part, 256-row blocks): column sums of each 256-row
                                  // run of C, [ceil(M / 256)][N], folded in the epilogue
 };

@@ -37,7 +37,7 @@ class dg_desc_params(ctypes.Structure):
         (n, ctypes.c_int32) for n in ("tile_combine", "split_combine", "tail", "fma", "partial_dtype",
                                       "merge_dtype", "out_dtype", "epilogue", "epi_round", "leaf_w",
                                       "reduce_op", "split_layout", "split_tile", "leaf_layout",
-                                      "lane_fold", "norm_round")]
+                                      "lane_fold", "norm_round", "in_dtype")]
 
 
 class dg_knobs(ctypes.Structure):
@@ -100,13 +100,13 @@ class Desc:
     "strided": leaf_w lanes each taking every leaf_w-th element), lane_fold
     ("up" | "down": the butterfly's offsets counting up or down), norm_round
     ("final" | "pre_weight": dg_rmsnorm rounds the normalised value to bf16
-    before the weight)."""
+    before the weight), in_dtype ("bf16" | "f16": the GEMM operands)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
                     epilogue="none", epi_round="final", leaf_w=64, reduce="sum",
                     split_layout="contiguous", split_tile=0, leaf_layout="contiguous", lane_fold="up",
-                    norm_round="final")
+                    norm_round="final", in_dtype="bf16")
 
     def __init__(self, **fields):
         unknown = set(fields) - set(self.DEFAULTS) - {"model"}
@@ -144,6 +144,7 @@ class Desc:
         p.leaf_layout = {"contiguous": 0, "strided": 1}[f["leaf_layout"]]
         p.lane_fold = {"up": 0, "down": 1}[f["lane_fold"]]
         p.norm_round = {"final": 0, "pre_weight": 1}[f["norm_round"]]
+        p.in_dtype = {"bf16": 0, "f16": 1}[f["in_dtype"]]
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:
@@ -189,7 +190,8 @@ def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knob
     the GPU (or raw device addresses with M, N, K given)."""
     import torch
     if isinstance(A, torch.Tensor):
-        assert A.dtype == torch.bfloat16 and B.dtype == torch.bfloat16, "A and B must be bf16"
+        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
+        assert A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in
         assert A.is_contiguous() and B.is_contiguous() and C.is_contiguous(), "row-major tensors"
         assert A.is_cuda and B.is_cuda and C.is_cuda, "device tensors"
         M, K = A.shape

@@ -48,6 +48,22 @@ def spread_bf16(seed: int, shape, emin: int = -30, emax: int = 30) -> np.ndarray
     return ((sign << 15) | ((e + 127) << 7) | frac).astype(np.uint16)
 
 
+def normal_f16(seed: int, shape, scale: float = 1.0) -> np.ndarray:
+    """N(0, scale^2) draws as IEEE binary16 bits (numpy's nearest-even conversion)."""
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal(shape) * scale).astype(np.float16).view(np.uint16)
+
+
+def spread_f16(seed: int, shape, emin: int = -14, emax: int = 14) -> np.ndarray:
+    """Binary16 bits with uniform exponent fields in [emin, emax] (normal
+    range), random fraction and sign."""
+    rng = np.random.default_rng(seed)
+    e = rng.integers(emin, emax + 1, size=shape, dtype=np.int64)
+    frac = rng.integers(0, 1024, size=shape, dtype=np.int64)
+    sign = rng.integers(0, 2, size=shape, dtype=np.int64)
+    return ((sign << 15) | ((e + 15) << 10) | frac).astype(np.uint16)
+
+
 def lognormal_f32(seed: int, shape, sigma: float = 2.0) -> np.ndarray:
     rng = np.random.default_rng(seed)
     mag = np.exp(sigma * rng.standard_normal(shape))

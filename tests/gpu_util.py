@@ -8,6 +8,11 @@ def dev_bf16(bits):
     return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)).view(torch.bfloat16).cuda()
 
 
+def dev_f16(bits):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(bits, dtype=np.uint16).view(np.int16)).view(torch.float16).cuda()
+
+
 def dev_f32(x):
     import torch
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).cuda()

@@ -165,6 +165,13 @@ def test_argument_errors_need_no_gpu(dg):
                dg.dg_knobs(8, 16, 16, 0, 0, 5, 256, 0), dg.dg_knobs(8, 48, 16, 0, 0, 0, 0, 0)):
         assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
+    # binary16 operands: not on the tiled, direct-to-LDS or four-wave kernels
+    hd = dg.Desc(in_dtype="f16")
+    for k in (2, 7, 8, 10):
+        kn = dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 0)
+        assert lib.dg_gemm_knobs(hd.handle, 16, 16, None, 16, 8, 304, 8, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED
+    assert "/in-f16" in hd.signature() and "/in-f16" not in d.signature()
     # a strided split runs on the generic kernel or on kernel 4 with one dealt tile per slab
     sd = dg.Desc(split_k=4, split_layout="strided", split_tile=64)
     for kn in (dg.dg_knobs(3, 0, 0, 0, 0, 0, 0), dg.dg_knobs(5, 0, 0, 0, 0, 0, 0),
