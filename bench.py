@@ -283,6 +283,29 @@ def main():
                               % (dd["split_k"], dd.get("tile_combine", "carry")),
                       "us_median": round(med * 1e3, 2), "GB/s": round(by / (med * 1e-3) / 1e9, 1)}
 
+    # ----------------- binary16 operands: the fused MLP on the fp16 instruction
+    desc_h16 = dict(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", in_dtype="f16")
+    D_h16 = dg.Desc(**desc_h16)
+    A_h16 = inputs.normal_f16(5, (2048, 4096))
+    B_h16 = inputs.normal_f16(6, (4096, 14336), 0.02)
+    to_f16 = lambda b: torch.from_numpy(b.view(np.int16)).view(torch.float16).to(dev)
+    dA_h16, dB_h16 = to_f16(A_h16), to_f16(B_h16)
+    C_h16 = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
+    for i in range(args.warmup):
+        dg.dg_gemm(D_h16, dA_h16, dB_h16, dbias, C_h16, stream=sptr)
+    ts = []
+    for i in range(args.steps):
+        a, b = ev(), ev()
+        a.record(stream)
+        dg.dg_gemm(D_h16, dA_h16, dB_h16, dbias, C_h16, stream=sptr)
+        b.record(stream)
+        torch.cuda.synchronize()
+        ts.append(a.elapsed_time(b))
+    med = float(np.median(ts))
+    f16_mlp = {"desc": "binary16 A and B, bf16 bias, bias+SiLU, bf16 out (fp16 MFMA, same chunk order)",
+               "us_median": round(med * 1e3, 2),
+               "TFLOP/s": round(2 * 2048 * 14336 * 4096 / (med * 1e-3) / 1e12, 2)}
+
     # ------------------------------- GEMM with a column-sum epilogue (fp32 out)
     desc_cs = dict(mma="16x16x32", tile_k=64)
     D_cs = dg.Desc(**desc_cs)
@@ -522,6 +545,9 @@ def main():
         ii = rng.integers(0, A_h.shape[0], 300)
         jj = rng.integers(0, B_h.shape[1], 300)
         tally(host(C_)[ii, jj], oracle.gemm_at(dd, A_h, B_h, None, ii, jj))
+    ii = rng.integers(0, 2048, 300)
+    jj = rng.integers(0, 14336, 300)
+    tally(host(C_h16)[ii, jj], oracle.gemm_at(desc_h16, A_h16, B_h16, bias_mlp, ii, jj))
     Ccs = C_cs.cpu().numpy()
     want_cs = oracle.colsum(Ccs)
     checked += want_cs.size
@@ -583,6 +609,7 @@ def main():
         "rowsum": rs,
         "gemm_colsum": colsum,
         "scalar_path": scal,
+        "f16_mlp": f16_mlp,
         "free_order": free,
         "hipblaslt_order": vendor,
         "bit_match": {"checked": checked, "matched": matched,
