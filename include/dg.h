@@ -207,10 +207,14 @@ typedef struct {
                       a ring of depth (0 = 8) LDS slots filled by direct-to-LDS
                       loads (tile_m 0 = 16, tile_n 0 = 16, slab_k 0 = 256),
                       9 the scalar-FMA kernel, the only one for DG_MMA_SCALAR_FMA
-                      descriptors (no other knob) */
+                      descriptors (no other knob), 10 four waves with 128-row
+                      sub-tiles, 256 x 256 blocks on the first split_n columns
+                      and 256 x 192 blocks on the rest.  Binary16 operands
+                      (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
+                      and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
-  int32_t order;   /* kernels 3 and 5: block order: 0 library's choice, 1 row-major
+  int32_t order;   /* kernels 3, 5, 6, 7, 10: block order: 0 library's choice, 1 row-major
                       (consecutive workgroups share an A panel), 2 groups of
                       eight block rows walked column by column, 3 as 2 with
                       each of the eight XCDs given a contiguous range */
@@ -220,9 +224,9 @@ typedef struct {
   int32_t slab_k;  /* kernel 4: k per slab (0 = 64; 64, 128 or 256).  Kernel 4
                       builds a fixed list of (tile_m, tile_n, depth, slab_k);
                       others return DG_ERR_UNSUPPORTED */
-  int32_t split_n; /* kernels 6, 7: columns computed in 256-wide blocks, a multiple of
-                      256 in [0, N] (0 = library's choice, which may be 0: all
-                      blocks 192 wide); tile_m, tile_n must be 0 */
+  int32_t split_n; /* kernels 6, 7, 10: columns computed in 256-wide blocks, a multiple
+                      of 256 in [0, N] (0 = library's choice, which may be 0:
+                      all blocks 192 wide); tile_m, tile_n must be 0 */
 } dg_knobs;
 
 /* dg_gemm with explicit speed knobs (NULL = dg_gemm).  A knob combination

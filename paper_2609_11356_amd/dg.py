@@ -185,9 +185,10 @@ def _ptr(t):
 
 
 def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knobs=None):
-    """C = epilogue(A . B) in desc's order.  A (M,K) and B (K,N) bf16, bias (N,)
-    bf16 or None, C (M,N) of the descriptor's output type, all contiguous on
-    the GPU (or raw device addresses with M, N, K given)."""
+    """C = epilogue(A . B) in desc's order.  A (M,K) and B (K,N) bf16 (float16
+    when the descriptor's in_dtype is "f16"), bias (N,) bf16 or None, C (M,N)
+    of the descriptor's output type, all contiguous on the GPU (or raw device
+    addresses with M, N, K given)."""
     import torch
     if isinstance(A, torch.Tensor):
         want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
@@ -249,6 +250,8 @@ def dg_gemm_colsum(desc: Desc, A, B, bias, C, colsum, M=None, N=None, K=None, st
     """dg_gemm, then colsum[j] = the balanced tree down column j of C (fp32)."""
     import torch
     if isinstance(A, torch.Tensor):
+        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
+        assert A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in
         M, K = A.shape
         N = B.shape[1]
         assert colsum.dtype == torch.float32 and colsum.is_cuda and colsum.numel() == N

@@ -106,3 +106,28 @@ def test_f16_mlp_shape_sampled_and_batch_invariant(dg):
     for m in (1, 37, 512):
         Cm = run(dg, desc, A[:m].copy(), B, bias)
         assert np.array_equal(Cm[0], C[0]), m
+
+
+def test_f16_column_sums_and_strided_split(dg):
+    """Binary16 operands through dg_gemm_colsum (the epilogue-folded runs on
+    the 256-row-block kernel, fp32 out) and through a strided split on the
+    few-row kernel."""
+    import torch
+    desc = dict(tile_k=64, in_dtype="f16")
+    M, N, K = 1000, 12288, 128
+    A = inputs.normal_f16(21, (M, K))
+    B = inputs.normal_f16(22, (K, N), 0.5)
+    d = dg.Desc(**desc)
+    C = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    cs = torch.full((N,), float("nan"), dtype=torch.float32, device="cuda")
+    dg.dg_gemm_colsum(d, dev_f16(A), dev_f16(B), None, C, cs)
+    torch.cuda.synchronize()
+    Ch = host_bits(C)
+    assert_bits_equal(cs.cpu().numpy(), oracle.colsum(Ch), "f16 colsum")
+    rng = np.random.default_rng(4)
+    ii, jj = rng.integers(0, M, 200), rng.integers(0, N, 200)
+    assert_bits_equal(Ch[ii, jj], oracle.gemm_at(desc, A, B, None, ii, jj), "f16 colsum C")
+    sdesc = dict(tile_k=64, split_k=4, split_layout="strided", split_tile=64, split_combine="tree", in_dtype="f16")
+    A = inputs.normal_f16(23, (7, 4096))
+    B = inputs.normal_f16(24, (4096, 520), 0.1)
+    assert_bits_equal(run(dg, sdesc, A, B), oracle.gemm(sdesc, A, B), "f16 strided split")
