@@ -312,7 +312,9 @@ const char* dg_strerror(dg_status s);
 
 /* Library version (major * 10000 + minor * 100 + patch).  0.2.0 (200) added
  * dg_desc_params.leaf_layout / lane_fold and dg_knobs.split_n: a caller
- * built against an earlier header must not pass its dg_knobs to this one. */
+ * built against an earlier header must not pass its dg_knobs to this one.
+ * 0.3.0 (300) added dg_desc_params.in_dtype (a smaller struct_size is
+ * rejected) and knob kernel 10. */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

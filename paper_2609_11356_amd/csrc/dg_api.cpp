@@ -184,7 +184,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 200; }
+int32_t dg_version(void) { return 300; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {

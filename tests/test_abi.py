@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 200
+    assert dg.dg_version() == 300
     for s in range(7):
         assert dg.dg_strerror(s)
 
