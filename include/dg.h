@@ -208,8 +208,9 @@ typedef struct {
                       loads (tile_m 0 = 16, tile_n 0 = 16, slab_k 0 = 256),
                       9 the scalar-FMA kernel, the only one for DG_MMA_SCALAR_FMA
                       descriptors (no other knob), 10 four waves with 128-row
-                      sub-tiles, 256 x 256 blocks on the first split_n columns
-                      and 256 x 192 blocks on the rest.  Binary16 operands
+                      sub-tiles and direct-to-LDS loads into a four-slot ring,
+                      256 x 256 blocks on the first split_n columns and
+                      256 x 192 blocks on the rest.  Binary16 operands
                       (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
                       and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */

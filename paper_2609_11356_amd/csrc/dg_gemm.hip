@@ -1271,28 +1271,42 @@ __global__ __launch_bounds__(512) void gemm_pp_mixed(GemmArgs a) {
 //
 // One wave per SIMD, each owning a 128 x (BNC/2) sub-tile of the 256 x BNC
 // block with its accumulators (up to 256 registers) in the accumulation
-// register file.  Against the eight-wave ping-pong this reads a third fewer
-// fragment bytes from LDS per MFMA (each A fragment is read by two waves,
-// not four).  The wave overlaps its own MFMAs with its LDS and global work;
-// in iteration s, between the MFMAs of slab s (fragments in register set
-// s % 2):
-//   * the fragments of slab s+1 are read from LDS buffer (s+1) % 2 into the
-//     other set;
-//   * slab s+2 is written from global-load register set s % 2 into LDS
-//     buffer s % 2 (which held slab s, read during iteration s-1);
-//   * the loads of slab s+4 are issued into that register set;
-// and one barrier closes the iteration.  Same chunk order as every tiled
-// kernel (16x16x32 MFMA chain, 8-k chunks from the part start).
+// register file, tied to the MFMAs through inline assembly.  Against the
+// eight-wave ping-pong this reads a third fewer fragment bytes from LDS per
+// MFMA (each A fragment is read by two waves, not four).  The slabs move by
+// direct-to-LDS loads (lane l's 16 bytes land at the instruction's LDS base
+// + 16 l; each lane fetches the chunk that belongs at its position under the
+// swizzle) into a ring of NS slots, D = NS - 1 slabs ahead: per 32-k slab
+// each wave issues eight such loads and no LDS write (a register-staged
+// version issued eight global loads and eight LDS writes and ran ~6 %
+// slower).  Iteration s: MFMAs of slab s, fragments of slab s+1 read from
+// slot (s+1) % NS, loads of slab s+D into slot (s+D) % NS (whose slab s-1 was
+// consumed in iteration s-1), then a wait until the wave's loads of slab s+2
+// have landed, and one barrier.
+constexpr int W4D_SLOT = 256 * 32 + 32 * 256;   // bf16 elements per slot
+__shared__ __attribute__((aligned(1024))) uint16_t w4d_s0[W4D_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t w4d_s1[W4D_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t w4d_s2[W4D_SLOT];
+__shared__ __attribute__((aligned(1024))) uint16_t w4d_s3[W4D_SLOT];
+
+template <int S>
+__device__ __forceinline__ uint16_t* w4d_slot() {
+  if constexpr (S == 0) return w4d_s0;
+  else if constexpr (S == 1) return w4d_s1;
+  else if constexpr (S == 2) return w4d_s2;
+  else return w4d_s3;
+}
+
 template <int BNC>
-__device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j0, uint16_t* smem) {
-  constexpr int BM = 256, BN = 256, BK = 32, CPR = BK / 8, BROW = BN / 8;
+__device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t j0) {
+  constexpr int NS = 4;   // four separate LDS arrays, so that the compiler tells the slots apart
+  constexpr int BM = 256, BN = 256, BK = 32, CPR = BK / 8, BROW = BN / 8, D = NS - 1;
   constexpr int WTM = 128, WTN = BNC / 2, TM = WTM / 16, TN = WTN / 16;
-  constexpr int NA = BM * CPR / 256, NB = BK * BROW / 256, NL = NA + NB;
-  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN;
-  static_assert(BNC <= BN && BNC % 32 == 0 && NL == TM && TN <= TM, "one load slot per MFMA group");
-  uint16_t* As0 = smem;
-  uint16_t* Bs0 = smem + 2 * A_ELEMS;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int A_ELEMS = BM * BK, B_ELEMS = BK * BN, SLOT = A_ELEMS + B_ELEMS;
+  constexpr int NIA = A_ELEMS * 2 / 1024 / 4, NIB = B_ELEMS * 2 / 1024 / 4, NI = NIA + NIB;   // per wave
+  static_assert(BNC <= BN && BNC % 32 == 0 && TN <= TM && D >= 2 && NI == TM, "one load per MFMA group");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
@@ -1300,42 +1314,43 @@ __device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / 4) % CPR)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
+  // load t of the wave: A run r = NIA wave + t (16 rows of 64 bytes), B run
+  // r = NIB wave + (t - NIA) (2 k-rows of 512 bytes)
   constexpr uint32_t OOB = 0x80000000u;
+  uint32_t off[NI];
+  int kc[NI];
+#pragma unroll
+  for (int t = 0; t < NIA; ++t) {
+    const int row = (NIA * wave + t) * 16 + lane / 4, pc = lane % 4;
+    const int c = pc ^ ((row / 4) % CPR);
+    off[t] = (i0 + row < a.M) ? (uint32_t)((row * a.K + 8 * c) * 2) : OOB;
+    kc[t] = 8 * c;
+  }
+#pragma unroll
+  for (int u = 0; u < NIB; ++u) {
+    const int kr = (NIB * wave + u) * 2 + lane / 32, pc = lane % 32;
+    const int c = pc ^ ((kr & 3) << 1) ^ (((kr >> 3) & 1) << 3);
+    off[NIA + u] = (8 * c < BNC && j0 + 8 * c < a.N) ? (uint32_t)((kr * a.N + j0 + 8 * c) * 2) : OOB;
+    kc[NIA + u] = kr;
+  }
   const int64_t recA = (a.M - i0) * a.K * 2, recB = (a.K - k0) * a.N * 2;
   const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
   const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.B + k0 * a.N), (short)0, (int)(recB < 0x7fffffff ? recB : 0x7fffffff), 0x00020000);
-  // load t < NA: A row tid / 4 + 64 t, chunk tid % 4; load NA + t: B k-row
-  // tid / 32 + 8 t, chunk tid % 32.  Rows 64 apart (A) keep the chunk
-  // swizzle, k-rows 8 apart flip bit 3 of it (B).
-  const int rowA = tid / CPR, cA = tid % CPR, krB = tid / BROW, cB = tid % BROW;
-  const uint32_t offA = (uint32_t)((rowA * a.K + 8 * cA) * 2), strideA = (uint32_t)(64 * a.K * 2);
-  const bool colok = 8 * cB < BNC && j0 + 8 * cB < a.N;
-  const uint32_t offB = colok ? (uint32_t)((krB * a.N + j0 + 8 * cB) * 2) : OOB, strideB = (uint32_t)(8 * a.N * 2);
-  const int ldA0 = ldsA(rowA, cA), ldB0 = ldsB(krB, cB), ldB1 = ldsB(krB + 8, cB);
-  u32x4 g[2][NL];
-  auto gload1 = [&](int sl, auto T, u32x4& dst) {
+  // load t of slab sl into slot `slot`; past the part end: zeros, slab offset 0
+  auto dma1 = [&](int sl_in, auto SL, auto T) {
     constexpr int t = decltype(T)::value;
-    const int64_t ks = k0 + (int64_t)sl * BK, lim = k1 - ks;
-    if constexpr (t < NA) {
-      const uint32_t o = (8 * cA < lim && i0 + rowA + 64 * t < a.M) ? offA + t * strideA : OOB;
-      dst = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, o, (int)(ks * 2), 0));
-    } else {
-      constexpr int u = t - NA;
-      const uint32_t o = (krB + 8 * u < lim && colok) ? offB + u * strideB : OOB;
-      dst = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, o, (int)((ks - k0) * a.N * 2), 0));
-    }
-  };
-  // chunk t of a slab into LDS buffer buf
-  auto lstore1 = [&](int buf, auto T, const u32x4& v) {
-    constexpr int t = decltype(T)::value;
-    if constexpr (t < NA) {
-      *(u32x4*)&As0[buf * A_ELEMS + 8 * ldA0 + 64 * BK * t] = v;
-    } else {
-      constexpr int u = t - NA;
-      if (BNC == BN || colok) *(u32x4*)&Bs0[buf * B_ELEMS + 8 * (u & 1 ? ldB1 : ldB0) + 8 * BN * (u & ~1)] = v;
-    }
+    const bool past = sl_in >= nslab;
+    const int sl = past ? 0 : sl_in;
+    const int64_t ks = k0 + (int64_t)sl * BK, lim = past ? 0 : k1 - ks;
+    uint16_t* base = w4d_slot<decltype(SL)::value>();
+    if constexpr (t < NIA)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(base + (NIA * wave + t) * 512), 16,
+                                               kc[t] < lim ? off[t] : OOB, (int)(ks * 2), 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(base + A_ELEMS + (NIB * wave + t - NIA) * 512), 16,
+                                               kc[t] < lim ? off[t] : OOB, (int)((ks - k0) * a.N * 2), 0, 0);
   };
 
   floatx4 acc[TM][TN];
@@ -1344,12 +1359,12 @@ __device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
   shortx8 fa[2][TM], fb[2][TN];
-  auto rdA = [&](int buf, int mi, shortx8& f) {
+  auto rdA = [&](auto SL, int mi, shortx8& f) {
     const int row = wm * WTM + 16 * mi + (lane & 15);
-    f = *(const shortx8*)&As0[buf * A_ELEMS + 8 * ldsA(row, lane >> 4)];
+    f = *(const shortx8*)&w4d_slot<decltype(SL)::value>()[8 * ldsA(row, lane >> 4)];
   };
-  auto rdB = [&](int buf, int ni, shortx8& f) {
-    const uint16_t* Bs = Bs0 + buf * B_ELEMS;
+  auto rdB = [&](auto SL, int ni, shortx8& f) {
+    const uint16_t* Bs = w4d_slot<decltype(SL)::value>() + A_ELEMS;
     const int i = lane & 15, gq = lane >> 4;
     const int n = wn * WTN + 16 * ni + 4 * (i & 3);
     const int kr0 = 8 * gq + (i >> 2), kr1 = kr0 + 4;
@@ -1358,46 +1373,50 @@ __device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j
     f = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
 
-  // prologue: slab 0 in buffer 0 and read into fragment set 0, slab 1 in
-  // buffer 1, slabs 2 and 3 in the global-load sets
-  static_for<0, NL>([&](auto t) { gload1(0, t, g[0][t]); });
-  static_for<0, NL>([&](auto t) { gload1(1, t, g[1][t]); });
-  static_for<0, NL>([&](auto t) { lstore1(0, t, g[0][t]); });
-  static_for<0, NL>([&](auto t) { gload1(2, t, g[0][t]); });
-  static_for<0, NL>([&](auto t) { lstore1(1, t, g[1][t]); });
-  static_for<0, NL>([&](auto t) { gload1(3, t, g[1][t]); });
-  __syncthreads();
+  // prologue: slabs 0 .. D-1 issued, 0 and 1 landed (all waves), slab 0's
+  // fragments read
+  static_for<0, D>([&](auto x) { static_for<0, NI>([&](auto t) { dma1(x, x, t); }); });
+  __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 2) * NI));
+  barrier_nofence();
+  constexpr std::integral_constant<int, 0> S0{};
 #pragma unroll
-  for (int mi = 0; mi < TM; ++mi) rdA(0, mi, fa[0][mi]);
+  for (int mi = 0; mi < TM; ++mi) rdA(S0, mi, fa[0][mi]);
 #pragma unroll
-  for (int ni = 0; ni < TN; ++ni) rdB(0, ni, fb[0][ni]);
-  __syncthreads();
+  for (int ni = 0; ni < TN; ++ni) rdB(S0, ni, fb[0][ni]);
+  lds_wait();
+  barrier_nofence();
 
-  auto step = [&](int sl, auto CUR) {
-    constexpr int cur = decltype(CUR)::value, nxt = cur ^ 1;
+  auto step = [&](int sl, auto X) {
+    constexpr int x = decltype(X)::value, cur = x & 1, nxt = cur ^ 1;
+    constexpr std::integral_constant<int, (x + 1) % NS> rslot{};
+    constexpr std::integral_constant<int, (x + D) % NS> wslot{};
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, TM>([&](auto mi) {
 #pragma unroll
       for (int ni = 0; ni < TN; ++ni) mfma16_tied(acc[mi][ni], fa[cur][mi], fb[cur][ni]);
       __builtin_amdgcn_sched_barrier(0);
-      rdA(nxt, mi, fa[nxt][mi]);
-      if constexpr (mi < TN) rdB(nxt, mi, fb[nxt][mi]);
-      lstore1(cur, mi, g[cur][mi]);
-      gload1(sl + 4, mi, g[cur][mi]);
+      rdA(rslot, mi, fa[nxt][mi]);
+      if constexpr (mi < TN) rdB(rslot, mi, fb[nxt][mi]);
+      dma1(sl + D, wslot, mi);
       __builtin_amdgcn_sched_barrier(0);
     });
-    __syncthreads();
+    lds_wait();
+    __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 2) * NI));   // the wave's loads of slab sl+2 landed
+    barrier_nofence();
   };
-  for (int sl = 0; sl < nslab; sl += 2) {
-    step(sl, std::integral_constant<int, 0>{});
-    step(sl + 1, std::integral_constant<int, 1>{});
-  }
+  for (int sl = 0; sl < nslab; sl += NS)
+    static_for<0, NS>([&](auto x) { step(sl + x, x); });
   mfma_drain();
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));   // nothing lands in the staging area later
+  barrier_nofence();
 
+  // epilogue: wave w stages through slot w; the bias sits in slot 0 after
+  // wave 0's area
   constexpr int CSP = WTN + 4;
-  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
-  float* bsh = reinterpret_cast<float*>(smem) + 4 * 16 * CSP;
-  static_assert((4 * 16 * CSP + BNC) * 4 <= 2 * (A_ELEMS + B_ELEMS) * 2, "epilogue staging fits");
+  static_assert((16 * CSP + BNC) * 4 <= SLOT * 2, "epilogue staging fits");
+  uint16_t* sb = wave == 0 ? w4d_s0 : wave == 1 ? w4d_s1 : wave == 2 ? w4d_s2 : w4d_s3;
+  float* cs = reinterpret_cast<float*>(sb);
+  float* bsh = reinterpret_cast<float*>(w4d_s0) + 16 * CSP;
   stage_bias(a, j0, BNC, bsh);
   __syncthreads();
   wave_epilogue<TM, TN>(a, s, i0 + wm * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
@@ -1405,17 +1424,16 @@ __device__ __forceinline__ void w4_body(const GemmArgs& a, int64_t i0, int64_t j
 
 // Columns [0, n_split) in 256 x 256 blocks, the rest in 256 x 192 blocks.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_w4_mixed(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (256 * 32 + 32 * 256)];
   const int tiles_m = (int)((a.M + 255) / 256);
   const int tn1 = (int)((a.n_split + 255) / 256), nb1 = tiles_m * tn1;
   int ty, tx;
   if ((int)blockIdx.x < nb1) {
     grouped_tile(blockIdx.x, tiles_m, tn1, a.order, &ty, &tx);
-    w4_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256, smem);
+    w4d_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256);
   } else {
     const int tn2 = a.N > a.n_split ? (int)((a.N - a.n_split + 191) / 192) : 0;
     grouped_tile(blockIdx.x - nb1, tiles_m, tn2, a.order, &ty, &tx);
-    w4_body<192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192, smem);
+    w4d_body<192>(a, (int64_t)ty * 256, a.n_split + (int64_t)tx * 192);
   }
 }
 
