@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import os
+import re
 import subprocess
 import sys
 
@@ -16,7 +17,25 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
          "-ffp-contract=off", "-fno-fast-math",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-         "-Wall", "-Wno-unused-command-line-argument"]
+         "-Wall", "-Wno-unused-command-line-argument",
+         "-Rpass-analysis=kernel-resource-usage"]
+
+
+def spilling_kernels(remarks: str) -> list[str]:
+    """Kernels whose resource-usage remark reports spilled VGPRs.
+
+    No kernel here is meant to spill: the spill code of a kernel that did was
+    seen to drop part of a spilled 16-byte register, so a spill fails the build.
+    """
+    bad, name = [], None
+    for line in remarks.splitlines():
+        if "Function Name:" in line:
+            name = line.split("Function Name:")[1].split()[0]
+        elif "VGPRs Spill:" in line and name is not None:
+            n = int(line.split("VGPRs Spill:")[1].split()[0])
+            if n:
+                bad.append("%s (%d VGPRs)" % (name, n))
+    return bad
 
 
 def build(verbose: bool = False) -> str:
@@ -24,10 +43,17 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp%d" % os.getpid()
     cmd = [HIPCC] + FLAGS + ["-o", tmp] + srcs
     r = subprocess.run(cmd, capture_output=True, text=True)
-    out = "\n".join(l for l in (r.stdout + r.stderr).splitlines()
-                    if "packed-fp32-ops" not in l and l.strip())
+    text = r.stdout + r.stderr
+    # the resource remarks (and their source-context lines) are read, not shown
+    out = "\n".join(l for l in text.splitlines()
+                    if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l
+                    and not re.match(r"^\s*\d*\s*\|", l) and l.strip())
     if r.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + out)
+    spills = spilling_kernels(text)
+    if spills:
+        os.unlink(tmp)
+        raise RuntimeError("kernels spill registers: " + ", ".join(spills))
     if verbose and out:
         print(out, file=sys.stderr)
     os.replace(tmp, LIB)

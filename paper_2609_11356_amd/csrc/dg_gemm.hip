@@ -48,6 +48,22 @@ __device__ __forceinline__ const u32x4* chunk_or_zero(bool ok, const uint16_t* p
   return ok ? reinterpret_cast<const u32x4*>(p) : &g_zero16[0];
 }
 
+// LDS layout of A slabs ([row][k], CPR 16-byte chunks per row): chunk c of
+// row r sits at position c ^ swz_a<CPR>(r).  A fragment read takes one chunk
+// of 16 consecutive rows; with 64-byte rows (CPR 4) the swizzle gives every
+// 8 consecutive rows distinct 16-byte slots of a 128-byte bank window and
+// every 16 rows distinct slots of a 256-byte one (with 128-byte rows, CPR 8,
+// likewise one row per 128 bytes), so the read has no bank conflict whether
+// the LDS serves 8 or 16 lanes per pass.  Measured on the MLP kernel: bank
+// conflict cycles fell from 1.7e7 to 4.6e5 and the kernel's cycles by 9 %
+// against the earlier swizzle c ^ ((r / 4) mod 4).
+template <int CPR>
+__device__ __forceinline__ int swz_a(int row) {
+  static_assert(CPR == 4 || CPR == 8, "64- or 128-byte rows");
+  constexpr int sh = CPR == 4 ? 1 : 0;
+  return ((row >> sh) ^ (row >> (sh + 1))) & (CPR - 1);
+}
+
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
 // that register arrays indexed by I stay in registers.
 template <int B, int E, typename F>
@@ -684,14 +700,13 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + V3_BK - 1) / V3_BK);
 
-  // A chunk (row, c): LDS chunk row*CPR + (c ^ ((row / (16/CPR)) % CPR)), CPR = chunks per
-  // row -- sixteen consecutive rows at one logical chunk land on sixteen
-  // different 16-byte bank groups.
+  // A chunk (row, c): LDS chunk row*CPR + (c ^ swz_a<CPR>(row)), CPR = chunks per
+  // row (conflict-free fragment reads, as the swizzle's own comment says).
   // B chunk (k, c): LDS chunk k*BROW + (c ^ ((k & 3) << 1)) -- the four rows a
   // transpose read touches land on four different 32-byte bank groups.
   constexpr int CPR = V3_BK / 8;
   static_assert(CPR == 4 || CPR == 8, "BK 32 or 64");
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / (16 / CPR)) % CPR)); };
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1)); };
 
   u32x4 r0a[ACH_T], r0b[BCH_T], r1a[ACH_T], r1b[BCH_T];
@@ -882,9 +897,9 @@ __device__ __forceinline__ void pp_body(const GemmArgs& a, int64_t i0, int64_t j
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
-  // A: chunk c of row r at c ^ ((r / (16 / CPR)) % CPR); B: chunk c of
+  // A: chunk c of row r at c ^ swz_a<CPR>(r); B: chunk c of
   // k-row k at c ^ 2 (k % 4) ^ 8 ((k / 8) % 2)
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / (16 / CPR)) % CPR)); };
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
   constexpr uint32_t OOB = 0x80000000u;
@@ -1094,7 +1109,7 @@ __device__ __forceinline__ void ppd_body(const GemmArgs& a, int64_t i0, int64_t 
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / 4) % CPR)); };
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
   auto ldsB = [](int k, int c) { return k * (BN / 8) + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
   constexpr uint32_t OOB = 0x80000000u;
@@ -1111,7 +1126,7 @@ __device__ __forceinline__ void ppd_body(const GemmArgs& a, int64_t i0, int64_t 
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int r = grp * 128 + (wn * 2 + i) * 16 + lane / 4, pc = lane & 3;
-    const int c = pc ^ ((r / 4) % CPR);
+    const int c = pc ^ swz_a<CPR>(r);
     offA[i] = (i0 + r < a.M) ? (uint32_t)((r * a.K + 8 * c) * 2) : OOB;
     kcA[i] = 8 * c;
     dA[i] = (grp * 128 + (wn * 2 + i) * 16) * BK;           // element offset of the 1 KB run
@@ -1311,7 +1326,7 @@ __device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t 
   const int s = blockIdx.z;
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
-  auto ldsA = [](int row, int c) { return row * CPR + (c ^ ((row / 4) % CPR)); };
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
   auto ldsB = [](int k, int c) { return k * BROW + (c ^ ((k & 3) << 1) ^ (((k >> 3) & 1) << 3)); };
 
   // load t of the wave: A run r = NIA wave + t (16 rows of 64 bytes), B run
@@ -1322,7 +1337,7 @@ __device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t 
 #pragma unroll
   for (int t = 0; t < NIA; ++t) {
     const int row = (NIA * wave + t) * 16 + lane / 4, pc = lane % 4;
-    const int c = pc ^ ((row / 4) % CPR);
+    const int c = pc ^ swz_a<CPR>(row);
     off[t] = (i0 + row < a.M) ? (uint32_t)((row * a.K + 8 * c) * 2) : OOB;
     kc[t] = 8 * c;
   }
@@ -1920,7 +1935,12 @@ hipError_t launch_gemm_skinny(const GemmArgs& a, int tm, int tn, int depth, int 
 
 bool v3_supported(int tm, int tn, int occ) {
   if (occ == 2) return (tm == 128 && tn == 128) || (tm == 64 && tn == 128) || (tm == 32 && tn == 128);
-  return (tm == 256 && tn == 256) || (tm == 256 && tn == 128) || (tm == 128 && tn == 256) ||
+  // No 256 x 256 block: its 256 accumulator registers and 64 ring registers per
+  // lane leave the fragments no room, and the register spills that shape needs
+  // were compiled into code that dropped the fourth dword of a spilled
+  // 16-byte load (wrong bits in the block's last 64 rows).  Every shape kept
+  // here compiles without spills.
+  return (tm == 256 && tn == 128) || (tm == 128 && tn == 256) ||
          (tm == 128 && tn == 128) || (tm == 64 && tn == 128) || (tm == 32 && tn == 256) ||
          (tm == 32 && tn == 128);
 }
@@ -1932,7 +1952,6 @@ hipError_t launch_gemm_v3(const GemmArgs& a, int tm, int tn, int occ, hipStream_
     if (tm == 32 && tn == 128) return launch_v3_t<32, 128, 1, 4, 64, true>(a, st);
     return hipErrorInvalidValue;
   }
-  if (tm == 256 && tn == 256) return launch_v3_t<256, 256, 2, 2, 32, false>(a, st);
   if (tm == 256 && tn == 128) return launch_v3_t<256, 128, 2, 2, 32, false>(a, st);
   if (tm == 128 && tn == 256) return launch_v3_t<128, 256, 2, 2, 32, false>(a, st);
   if (tm == 128 && tn == 128) return launch_v3_t<128, 128, 2, 2, 64, false>(a, st);

@@ -150,6 +150,8 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(3, 0, 0, 0, 0, 0, 128)        # slab_k is a kernel-4 knob
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(3, 256, 256, 0, 0, 0)         # kernel 3 has no 256 x 256 block
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
     # kernels 6, 7 and 10 take no tile shape; split_n is a multiple of 256 within N, and only for them
     for k in (6, 7, 10):
         for kn in (dg.dg_knobs(k, 256, 256, 0, 0, 0, 0, 0), dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 100),
@@ -212,3 +214,19 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
     assert lib.dg_rowsum(d.handle, 16, None, 4, 5, None) == dg.DG_ERR_INVALID
     assert lib.dg_rowsum(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
+
+
+def test_build_rejects_register_spills():
+    """The build fails when a kernel's resource remark reports spilled VGPRs."""
+    from paper_2609_11356_amd import build
+    remarks = "\n".join([
+        "a.hip:1:1: remark: Function Name: _Zk1 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:1:1: remark:     SGPRs Spill: 2 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:1:1: remark:     VGPRs Spill: 0 [-Rpass-analysis=kernel-resource-usage]",
+        "   12 | __global__ void k1() {",
+        "      | ^",
+        "a.hip:9:1: remark: Function Name: _Zk2 [-Rpass-analysis=kernel-resource-usage]",
+        "a.hip:9:1: remark:     VGPRs Spill: 154 [-Rpass-analysis=kernel-resource-usage]",
+    ])
+    assert build.spilling_kernels(remarks) == ["_Zk2 (154 VGPRs)"]
+    assert build.spilling_kernels(remarks.replace("154", "0")) == []

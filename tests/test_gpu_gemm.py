@@ -139,7 +139,7 @@ KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, ti
          dict(kernel=2, tile_m=32, tile_n=128), dict(kernel=2, tile_m=64, tile_n=128),
          dict(kernel=2, tile_m=128, tile_n=128), dict(kernel=2, tile_m=256, tile_n=256),
          dict(kernel=2, tile_m=256, tile_n=128), dict(kernel=2, tile_m=128, tile_n=256),
-         dict(kernel=3, tile_m=256, tile_n=256), dict(kernel=3, tile_m=256, tile_n=128),
+         dict(kernel=3, tile_m=256, tile_n=128),
          dict(kernel=3, tile_m=128, tile_n=256), dict(kernel=3, tile_m=128, tile_n=128),
          dict(kernel=3, tile_m=64, tile_n=128), dict(kernel=3, tile_m=32, tile_n=256),
          dict(kernel=3, tile_m=32, tile_n=128), dict(kernel=3, tile_m=128, tile_n=128, occupancy=2, order=2),
