@@ -213,7 +213,8 @@ typedef struct {
                       256 x 192 blocks on the rest.  Binary16 operands
                       (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
                       and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED */
-  int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256 */
+  int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256
+                      (kernel 3: no 256 x 256 block) */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
   int32_t order;   /* kernels 3, 5, 6, 7, 10: block order: 0 library's choice, 1 row-major
                       (consecutive workgroups share an A panel), 2 groups of
