@@ -105,8 +105,8 @@ def profile_only(args, torch, dg, inputs, d_bf16):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=30)
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
