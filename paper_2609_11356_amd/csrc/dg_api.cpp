@@ -172,7 +172,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
     if (S * ((N + 63) / 64) >= 256) return {4, 16, 64, 0, 0, 4, 64};
     return {4, 16, M <= 16 ? 16 : 32, 0, 0, 2, 256};
   }
-  if (M <= 128) return {4, 64, 32, 0, 0, 2, 128};
+  if (M <= 128) return {4, 32, 64, 0, 0, 2, 256};
   const int64_t tiles256 = S * ((M + 255) / 256) * ((N + 255) / 256);
   const int64_t tiles128 = S * ((M + 127) / 128) * ((N + 127) / 128);
   if (tiles256 >= 192) return {5, 256, 256, 1, 0, 0, 0};
