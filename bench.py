@@ -84,6 +84,26 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", epi_round="final")
         run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr)
         what = "fused MLP GEMM 2048x14336x4096"
+    elif args.only in ("gemv", "decode"):
+        # the few-row launches of the step, weights rotated through copies
+        # totalling twice the MALL so that every launch streams B from HBM
+        if args.only == "gemv":
+            A, B = inputs.sweep_activations(1, rows=4096)[:1], inputs.sweep_weight(2)
+            D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16")
+            what = "sweep GEMM M=1: 1x4096 by 4096x4096"
+        else:
+            A, B = inputs.decode()
+            D = dg.Desc(mma="16x16x32", tile_k=64, split_k=8, split_combine="seq", out="bf16")
+            what = "split-K decode 8x14336 by 14336x4096, S=8, chain merge"
+        dA = d_bf16(A)
+        dBs = [d_bf16(B)]
+        dBs += [dBs[0].clone() for _ in range(max(1, -(-2 * MALL_BYTES // B.nbytes)) - 1)]
+        C = torch.empty((A.shape[0], B.shape[1]), dtype=torch.bfloat16, device=dev)
+        it = [0]
+
+        def run():
+            dg.dg_gemm(D, dA, dBs[it[0] % len(dBs)], None, C, stream=sptr)
+            it[0] += 1
     else:
         src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)   # 1 GiB
         dst = torch.empty_like(src)
@@ -110,9 +130,10 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
-    ap.add_argument("--only", choices=("mlp", "copy"), default=None,
-                    help="profiling runs: launch only the fused MLP GEMM, or only a plain "
-                         "1 GiB device copy (the calibration kernel for HBM byte counters)")
+    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode"), default=None,
+                    help="profiling runs: launch only the fused MLP GEMM, the M=1 sweep GEMM, "
+                         "the split-K decode, or a plain 1 GiB device copy (the calibration "
+                         "kernel for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
