@@ -126,3 +126,24 @@ def test_rowsum_strided_independent_of_row_count(dg):
         a = run(dg, desc, X)
         b = run(dg, desc, X[:37].copy())
         assert np.array_equal(a[:37].view(np.uint32), b.view(np.uint32)), W
+
+
+@pytest.mark.parametrize("seed", range(64))
+def test_rowsum_random_descriptor(dg, seed):
+    """Seeded random descriptors (leaf width and layout, the fold direction of
+    strided lanes, SUM or SUMSQ under either fma rule) on ragged row and
+    column counts, every row compared with the oracle."""
+    rng = np.random.default_rng(70_000 + seed)
+    desc = {}
+    if rng.random() < 0.5:
+        desc.update(leaf_layout="strided", leaf_w=int(rng.choice([1, 2, 8, 32, 64, 128, 256])),
+                    lane_fold=str(rng.choice(["up", "down"])))
+    else:
+        desc["leaf_w"] = int(rng.choice([1, 3, 16, 64, 100, 257]))
+    if rng.random() < 0.5:
+        desc.update(reduce="sumsq", fma=int(rng.integers(2)))
+    rows = int(rng.choice([1, 5, 64, 300]))
+    cols = int(rng.choice([0, 1, 31, 64, 255, 1000, 4099, 9000]))
+    X = inputs.lognormal_f32(90_000 + seed, (rows, cols))
+    print("seed %d rows %d cols %d desc %s" % (seed, rows, cols, desc), flush=True)
+    assert_bits_equal(run(dg, desc, X), oracle.rowsum(desc, X), "rowsum %s %dx%d" % (desc, rows, cols))
