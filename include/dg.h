@@ -73,9 +73,10 @@ enum { DG_NORM_FINAL = 0, DG_NORM_PRE_WEIGHT = 1 };      /* RMS-norm rounding po
 enum { DG_IN_BF16 = 0, DG_IN_F16 = 1 };                  /* GEMM operand format */
 
 #define DG_MAX_SPLIT 64
+#define DG_SIGNATURE_MAX 2048
 
-/* The order fields, and nothing else (Sec. 3.2.2; Sec. 4: "a frozen record
- * holding every one of those factors").  No speed knob appears here. */
+/* The order fields, and nothing else (Sec. 3.2.2; Sec. 4 keeps a reconstructed
+ * order as a frozen record of all of its factors).  No speed knob appears here. */
 typedef struct {
   uint32_t struct_size;   /* sizeof(dg_desc_params), for ABI versioning */
   int32_t mma;            /* DG_MMA_*: the instruction group */
@@ -154,13 +155,21 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out);
  * unaffected: launches copy what they need. */
 void dg_desc_destroy(dg_desc* d);
 
-/* Canonical text of the order a descriptor fixes, NUL-terminated into buf
- * (capacity n).  Descriptors with equal signatures give equal bits; fields
- * that cannot change bits (the instruction shape when fma = 1) are
- * normalised away.  DG_ERR_INVALID if buf is too small. */
+/* Canonical text of the order a descriptor fixes (Sec. 4: the reconstructed
+ * order is kept as a frozen record of every factor), NUL-terminated into buf
+ * (capacity n).  Every field that can change a bit is written in full,
+ * explicit cuts included, so descriptors with equal signatures give equal
+ * bits; fields that cannot change bits (the instruction shape when fma = 1)
+ * are normalised away.  The text is at most DG_SIGNATURE_MAX bytes with its
+ * terminating NUL.  DG_ERR_INVALID if d or buf is NULL or buf is too small
+ * (nothing is written then). */
 dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n);
 
-/* C = epilogue(A . B) in the descriptor's order.
+/* C = epilogue(A . B) in the descriptor's order: per output, the K axis cut
+ * into parts, each part into tiles and instruction groups, the groups folded
+ * into an accumulator (Sec. 3.2.1), the tiles and parts combined as the
+ * descriptor says, the parts merged at merge_dtype (Sec. 3.2.2), then the
+ * epilogue at its fixed rounding points (Sec. 1).
  *   A: device, M x K row-major;  B: device, K x N row-major; both bf16, or
  *   binary16 when in_dtype = DG_IN_F16;
  *   bias: device, N bf16, required iff the epilogue uses it (else ignored);
@@ -248,7 +257,6 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
 dg_status dg_rowsum(const dg_desc* d, const float* X, float* out, int64_t rows,
                     int64_t cols, void* stream);
 
-/* Static text for a status code. */
 /* Root-mean-square normalisation of each row, on the row's sum of squares
  * in the descriptor's order (exactly the value dg_rowsum returns for the
  * descriptor with reduce_op DG_OP_SUMSQ: leaf_w, leaf_layout, lane_fold and
@@ -310,6 +318,8 @@ dg_status dg_layernorm(const dg_desc* d, const float* X, const void* w, const vo
 dg_status dg_softmax(const dg_desc* d, const float* X, void* Y, int64_t rows, int64_t cols,
                      void* stream);
 
+/* Static text for a status code (never NULL; unknown codes give
+ * "unknown status"). */
 const char* dg_strerror(dg_status s);
 
 /* Library version (major * 10000 + minor * 100 + patch).  0.2.0 (200) added

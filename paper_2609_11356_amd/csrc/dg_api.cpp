@@ -7,6 +7,7 @@
 #include <map>
 #include <mutex>
 #include <new>
+#include <string>
 #include <utility>
 
 #include "dg_internal.h"
@@ -36,41 +37,44 @@ dg_status plan_cuts(const dg_desc* d, int64_t K, int64_t* cuts) {
   return DG_OK;
 }
 
-void make_signature(dg_desc* d) {
+// Canonical text of the descriptor's order.  Every field that can change a
+// bit appears in full (all explicit cuts included), so equal texts mean equal
+// descriptors up to fields that cannot change bits.  Returns false if the text
+// does not fit d->sig (it always fits: 63 cuts of at most 20 characters and
+// the fixed fields stay far below its size), and create then refuses.
+bool make_signature(dg_desc* d) {
   const dg_desc_params& p = d->p;
   // fma = 1 folds the same 8-k chunks whatever the instruction's K
   // on the scalar path a bf16 product is exact, so fma cannot change bits
-  char grp[32];
   const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
-  if (scalar) std::snprintf(grp, sizeof grp, "scalar-fma");
-  else if (p.fma) std::snprintf(grp, sizeof grp, "chunk8");
-  else std::snprintf(grp, sizeof grp, "group%d", d->group);
-  int n = std::snprintf(d->sig, sizeof d->sig,
+  std::string grp = scalar ? "scalar-fma" : p.fma ? "chunk8" : "group" + std::to_string(d->group);
+  char base[512];
+  int n = std::snprintf(base, sizeof base,
                         "gfx950-bf16-%s/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
                         "out-%s/epi%d/%s/leaf%d/%s",
-                        scalar ? "fma" : "mfma", grp, scalar ? 1 : p.fma, p.tile_k,
+                        scalar ? "fma" : "mfma", grp.c_str(), scalar ? 1 : p.fma, p.tile_k,
                         p.tile_combine == DG_CARRY ? "carry" : p.tile_combine == DG_SEQ ? "seq" : "tree",
                         p.split_k, p.tail == DG_TAIL_FIRST ? "tail-first" : "tail-last",
                         p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
                         p.merge_dtype ? "bf16" : "f32", p.out_dtype ? "bf16" : "f32", p.epilogue,
                         p.epi_round ? "pre-act" : "final", p.leaf_w, p.reduce_op ? "sumsq" : "sum");
+  if (n <= 0 || n >= (int)sizeof base) return false;
+  std::string s(base);
   // the row reduction's leaf layout and lane fold, when not the defaults (one
   // lane has nothing to fold)
-  if (p.leaf_layout == DG_LEAF_STRIDED && n > 0 && n < (int)sizeof d->sig)
-    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/leaf-strided%s",
-                       p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
-  if (p.norm_round == DG_NORM_PRE_WEIGHT && n > 0 && n < (int)sizeof d->sig)
-    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/norm-pre-weight");
-  if (p.in_dtype == DG_IN_F16 && n > 0 && n < (int)sizeof d->sig)
-    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/in-f16");
+  if (p.leaf_layout == DG_LEAF_STRIDED)
+    s += std::string("/leaf-strided") + (p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
+  if (p.norm_round == DG_NORM_PRE_WEIGHT) s += "/norm-pre-weight";
+  if (p.in_dtype == DG_IN_F16) s += "/in-f16";
   // one strided part is the whole axis, as one contiguous part is
-  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && n > 0 && n < (int)sizeof d->sig)
-    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/strided:%d", p.split_tile);
-  if (p.n_cuts && n > 0 && n < (int)sizeof d->sig) {
-    n += std::snprintf(d->sig + n, sizeof d->sig - n, "/cuts");
-    for (int i = 0; i < p.n_cuts && n > 0 && n < (int)sizeof d->sig; ++i)
-      n += std::snprintf(d->sig + n, sizeof d->sig - n, ":%lld", (long long)d->cuts[i]);
+  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1) s += "/strided:" + std::to_string(p.split_tile);
+  if (p.n_cuts) {
+    s += "/cuts";
+    for (int i = 0; i < p.n_cuts; ++i) s += ":" + std::to_string((long long)d->cuts[i]);
   }
+  if (s.size() + 1 > sizeof d->sig) return false;
+  std::memcpy(d->sig, s.c_str(), s.size() + 1);
+  return true;
 }
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
@@ -250,7 +254,10 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   for (int i = 0; i < p->n_cuts; ++i) d->cuts[i] = p->k_cuts[i];
   d->p.k_cuts = p->n_cuts ? d->cuts : nullptr;
   d->group = group;
-  make_signature(d);
+  if (!make_signature(d)) {
+    delete d;
+    return DG_ERR_UNSUPPORTED;
+  }
   *out = d;
   return DG_OK;
 }

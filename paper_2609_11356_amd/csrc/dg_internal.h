@@ -10,7 +10,7 @@ struct dg_desc {
   dg_desc_params p;            // validated copy; p.k_cuts points into cuts[]
   int64_t cuts[DG_MAX_SPLIT];  // explicit interior cuts (n_cuts of them)
   int group;                   // products per instruction group (32 or 16)
-  char sig[512];               // canonical order text
+  char sig[2048];              // canonical order text (every cut written out)
 };
 
 namespace dg {

@@ -22,6 +22,7 @@ EPILOGUE = {"none": 0, "bias": 1, "bias_silu": 2}
 EPI_ROUND = {"final": 0, "pre_act": 1}
 REDUCE = {"sum": 0, "sumsq": 1}
 MAX_SPLIT = 64
+SIGNATURE_MAX = 2048
 
 
 class DgError(RuntimeError):
@@ -152,7 +153,7 @@ class Desc:
         self.handle = h
 
     def signature(self) -> str:
-        buf = ctypes.create_string_buffer(1024)
+        buf = ctypes.create_string_buffer(SIGNATURE_MAX)
         st = lib().dg_desc_signature(self.handle, buf, len(buf))
         if st != DG_OK:
             raise DgError(st, "dg_desc_signature")
@@ -184,25 +185,66 @@ def _ptr(t):
     return int(t.data_ptr())
 
 
+def _need(cond, msg):
+    """Refuse a call before anything reaches the library (kept under python -O)."""
+    if not cond:
+        raise ValueError(msg)
+
+
+def _out_dtype(desc):
+    import torch
+    return torch.bfloat16 if desc.fields["out"] == "bf16" else torch.float32
+
+
+def _on_device(*ts):
+    _need(all(t.is_cuda for t in ts if t is not None), "tensors must be on the GPU")
+
+
+def _check_gemm(desc, A, B, bias, C):
+    """Shapes, dtypes and layout of a GEMM call; returns (M, N, K)."""
+    import torch
+    want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
+    _need(A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in)
+    _need(A.dim() == 2 and B.dim() == 2 and C.dim() == 2, "A, B and C must be matrices")
+    M, K = A.shape
+    K2, N = B.shape
+    _need(K2 == K, "inner dimensions differ (%d, %d)" % (K, K2))
+    _need(tuple(C.shape) == (M, N), "C must be %d x %d" % (M, N))
+    _need(C.dtype == _out_dtype(desc), "C dtype must match the descriptor's output type")
+    _need(A.is_contiguous() and B.is_contiguous() and C.is_contiguous(), "A, B and C must be row-major")
+    if desc.fields["epilogue"] != "none":
+        _need(bias is not None, "the descriptor's epilogue needs a bias")
+    if bias is not None:
+        _need(bias.dtype == torch.bfloat16 and bias.numel() == N and bias.is_contiguous(),
+              "bias must be %d contiguous bf16 values" % N)
+    _on_device(A, B, C, bias)
+    return M, N, K
+
+
+def _check_rows(desc, X, Y, *vecs):
+    """An fp32 row-major X, a Y of X's shape and the descriptor's output type,
+    and optional bf16 per-column vectors; returns (rows, cols)."""
+    import torch
+    _need(X.dtype == torch.float32 and X.dim() == 2, "X must be an fp32 matrix")
+    _need(tuple(Y.shape) == tuple(X.shape), "Y must have X's shape")
+    _need(Y.dtype == _out_dtype(desc), "Y dtype must match the descriptor's output type")
+    _need(X.is_contiguous() and Y.is_contiguous(), "X and Y must be row-major")
+    for t in vecs:
+        _need(t is None or (t.dtype == torch.bfloat16 and t.is_contiguous() and t.numel() == X.shape[1]),
+              "weight and bias must be %d contiguous bf16 values" % X.shape[1])
+    _on_device(X, Y, *vecs)
+    return X.shape
+
+
 def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knobs=None):
     """C = epilogue(A . B) in desc's order.  A (M,K) and B (K,N) bf16 (float16
     when the descriptor's in_dtype is "f16"), bias (N,) bf16 or None, C (M,N)
     of the descriptor's output type, all contiguous on the GPU (or raw device
-    addresses with M, N, K given)."""
+    addresses with M, N, K given).  Inconsistent tensors raise ValueError
+    before the library is called."""
     import torch
     if isinstance(A, torch.Tensor):
-        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
-        assert A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in
-        assert A.is_contiguous() and B.is_contiguous() and C.is_contiguous(), "row-major tensors"
-        assert A.is_cuda and B.is_cuda and C.is_cuda, "device tensors"
-        M, K = A.shape
-        K2, N = B.shape
-        assert K2 == K, "inner dimensions differ"
-        assert tuple(C.shape) == (M, N), "C shape"
-        want = torch.bfloat16 if desc.fields["out"] == "bf16" else torch.float32
-        assert C.dtype == want, "C dtype must match the descriptor's output type"
-        if bias is not None:
-            assert bias.dtype == torch.bfloat16 and bias.numel() == N and bias.is_contiguous()
+        M, N, K = _check_gemm(desc, A, B, bias, C)
     kp = None
     if knobs is not None:
         kp = dg_knobs(int(knobs.get("kernel", 0)), int(knobs.get("tile_m", 0)), int(knobs.get("tile_n", 0)),
@@ -221,10 +263,11 @@ def dg_rowsum(desc: Desc, X, out, rows=None, cols=None, stream=None):
     """out[r] = balanced-tree reduction of row r of X (fp32, row-major)."""
     import torch
     if isinstance(X, torch.Tensor):
-        assert X.dtype == torch.float32 and out.dtype == torch.float32
-        assert X.is_contiguous() and out.is_contiguous() and X.is_cuda and out.is_cuda
+        _need(X.dtype == torch.float32 and out.dtype == torch.float32 and X.dim() == 2, "X and out must be fp32")
         rows, cols = X.shape
-        assert out.numel() == rows
+        _need(out.numel() == rows, "out must hold one value per row")
+        _need(X.is_contiguous() and out.is_contiguous(), "X and out must be contiguous")
+        _on_device(X, out)
     st = lib().dg_rowsum(desc.handle, _ptr(X), _ptr(out), rows, cols, _stream(stream))
     if st != DG_OK:
         raise DgError(st, "dg_rowsum")
@@ -236,10 +279,7 @@ def dg_rmsnorm(desc: Desc, X, w, eps, Y, rows=None, cols=None, stream=None):
     None), in the descriptor's order (its reduce must be "sumsq")."""
     import torch
     if isinstance(X, torch.Tensor):
-        assert X.dtype == torch.float32 and X.is_contiguous() and X.is_cuda
-        assert Y.is_contiguous() and Y.is_cuda and Y.shape == X.shape
-        assert w is None or (w.dtype == torch.bfloat16 and w.is_contiguous() and w.numel() == X.shape[1])
-        rows, cols = X.shape
+        rows, cols = _check_rows(desc, X, Y, w)
     st = lib().dg_rmsnorm(desc.handle, _ptr(X), _ptr(w), ctypes.c_float(eps), _ptr(Y), rows, cols, _stream(stream))
     if st != DG_OK:
         raise DgError(st, "dg_rmsnorm")
@@ -250,12 +290,10 @@ def dg_gemm_colsum(desc: Desc, A, B, bias, C, colsum, M=None, N=None, K=None, st
     """dg_gemm, then colsum[j] = the balanced tree down column j of C (fp32)."""
     import torch
     if isinstance(A, torch.Tensor):
-        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
-        assert A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in
-        M, K = A.shape
-        N = B.shape[1]
-        assert colsum.dtype == torch.float32 and colsum.is_cuda and colsum.numel() == N
-        assert tuple(C.shape) == (M, N) and C.is_contiguous() and C.is_cuda
+        M, N, K = _check_gemm(desc, A, B, bias, C)
+        _need(colsum.dtype == torch.float32 and colsum.numel() == N and colsum.is_contiguous(),
+              "colsum must be %d contiguous fp32 values" % N)
+        _on_device(colsum)
     st = lib().dg_gemm_colsum(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), _ptr(colsum), M, N, K,
                               _stream(stream))
     if st != DG_OK:
@@ -268,11 +306,7 @@ def dg_layernorm(desc: Desc, X, w, b, eps, Y, rows=None, cols=None, stream=None)
     descriptor's order, then the bf16 weight and bias (each may be None)."""
     import torch
     if isinstance(X, torch.Tensor):
-        assert X.dtype == torch.float32 and X.is_contiguous() and X.is_cuda
-        assert Y.is_contiguous() and Y.is_cuda and Y.shape == X.shape
-        for t in (w, b):
-            assert t is None or (t.dtype == torch.bfloat16 and t.is_contiguous() and t.numel() == X.shape[1])
-        rows, cols = X.shape
+        rows, cols = _check_rows(desc, X, Y, w, b)
     st = lib().dg_layernorm(desc.handle, _ptr(X), _ptr(w), _ptr(b), ctypes.c_float(eps), _ptr(Y), rows, cols,
                             _stream(stream))
     if st != DG_OK:
@@ -285,9 +319,7 @@ def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
     order (its reduce must be "sum")."""
     import torch
     if isinstance(X, torch.Tensor):
-        assert X.dtype == torch.float32 and X.is_contiguous() and X.is_cuda
-        assert Y.is_contiguous() and Y.is_cuda and Y.shape == X.shape
-        rows, cols = X.shape
+        rows, cols = _check_rows(desc, X, Y)
     st = lib().dg_softmax(desc.handle, _ptr(X), _ptr(Y), rows, cols, _stream(stream))
     if st != DG_OK:
         raise DgError(st, "dg_softmax")

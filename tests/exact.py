@@ -41,6 +41,13 @@ def rn32(q: Fraction) -> np.float32:
     return np.float32(float(r))
 
 
+def rnbf(q: Fraction) -> Fraction:
+    """RNE of q to bfloat16 (8 significant bits, binary32's exponent range,
+    gradual underflow) as an exact rational; None for an overflow."""
+    r = rn_binary(q, 8, -126)
+    return None if abs(r) >= Fraction(2) ** 128 else r
+
+
 def f(x) -> Fraction:
     return Fraction(float(x))
 

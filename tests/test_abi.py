@@ -114,6 +114,75 @@ def test_signature_canonical(dg):
     assert dg.Desc(norm_round="pre_weight").signature().endswith("norm-pre-weight")
 
 
+def test_signature_writes_every_cut(dg):
+    """Sixty-four parts with explicit cuts that differ only in the last one
+    give different signatures (the text is never cut short), and a buffer one
+    byte too small is refused without being written."""
+    cuts = [1000 * (i + 1) for i in range(63)]
+    other = cuts[:-1] + [cuts[-1] + 1]
+    a = dg.Desc(split_k=64, tile_k=64, k_cuts=cuts).signature()
+    b = dg.Desc(split_k=64, tile_k=64, k_cuts=other).signature()
+    assert a != b
+    assert a.endswith(":" + str(cuts[-1])) and b.endswith(":" + str(other[-1]))
+    assert a.count(":") == 63 and len(a) + 1 <= dg.SIGNATURE_MAX
+    # the widest fields and cuts still fit
+    big = [2 ** 62 - 63 + i for i in range(63)]
+    w = dg.Desc(split_k=64, tile_k=2 ** 30, k_cuts=big, tile_combine="tree", split_combine="tree",
+                tail="first", partial="bf16", merge="bf16", out="bf16", epilogue="bias_silu",
+                epi_round="pre_act", leaf_w=256, reduce="sumsq", leaf_layout="strided", lane_fold="down",
+                norm_round="pre_weight", in_dtype="f16").signature()
+    assert w.endswith(":" + str(big[-1])) and len(w) + 1 <= dg.SIGNATURE_MAX
+    lib = dg.lib()
+    d = dg.Desc(split_k=64, tile_k=64, k_cuts=cuts)
+    buf = ctypes.create_string_buffer(b"x" * len(a), len(a) + 1)
+    assert lib.dg_desc_signature(d.handle, buf, len(a)) == dg.DG_ERR_INVALID
+    assert buf.value == b"x" * len(a)
+    assert lib.dg_desc_signature(d.handle, buf, len(a) + 1) == dg.DG_OK and buf.value.decode() == a
+
+
+def test_binding_refuses_inconsistent_tensors(dg):
+    """The binding checks shapes, dtypes and layout with ValueError (not
+    assert, so python -O keeps them) before the library is called; CPU
+    tensors reach these checks first, so no GPU is needed."""
+    import torch
+    bf, f32 = torch.bfloat16, torch.float32
+    A, B = torch.zeros(8, 16, dtype=bf), torch.zeros(16, 24, dtype=bf)
+    cases = [
+        (dg.dg_gemm, (dg.Desc(), A, B, None, torch.zeros(8, 24, dtype=bf))),            # C dtype
+        (dg.dg_gemm, (dg.Desc(), A, torch.zeros(12, 24, dtype=bf), None, torch.zeros(8, 24))),
+        (dg.dg_gemm, (dg.Desc(), A.float(), B, None, torch.zeros(8, 24))),
+        (dg.dg_gemm, (dg.Desc(), A, B.t(), None, torch.zeros(8, 16))),                    # shape
+        (dg.dg_gemm, (dg.Desc(), A, B.t().contiguous().t(), None, torch.zeros(8, 24))),   # layout
+        (dg.dg_gemm, (dg.Desc(epilogue="bias"), A, B, None, torch.zeros(8, 24))),         # bias missing
+        (dg.dg_gemm, (dg.Desc(epilogue="bias"), A, B, torch.zeros(23, dtype=bf), torch.zeros(8, 24))),
+        (dg.dg_gemm_colsum, (dg.Desc(), A, torch.zeros(12, 24, dtype=bf), None, torch.zeros(8, 24),
+                             torch.zeros(24))),
+        (dg.dg_gemm_colsum, (dg.Desc(), A, B, None, torch.zeros(8, 24, dtype=bf), torch.zeros(24))),
+        (dg.dg_gemm_colsum, (dg.Desc(), A, B, None, torch.zeros(8, 24), torch.zeros(23))),
+        (dg.dg_gemm_colsum, (dg.Desc(epilogue="bias_silu"), A, B, None, torch.zeros(8, 24), torch.zeros(24))),
+        (dg.dg_rmsnorm, (dg.Desc(reduce="sumsq"), torch.zeros(4, 8), None, 1e-6,
+                         torch.zeros(4, 8, dtype=bf))),                                    # Y dtype
+        (dg.dg_rmsnorm, (dg.Desc(reduce="sumsq", out="bf16"), torch.zeros(4, 8), None, 1e-6,
+                         torch.zeros(4, 8))),
+        (dg.dg_rmsnorm, (dg.Desc(reduce="sumsq"), torch.zeros(4, 8), torch.zeros(7, dtype=bf), 1e-6,
+                         torch.zeros(4, 8))),
+        (dg.dg_softmax, (dg.Desc(), torch.zeros(4, 8), torch.zeros(4, 8, dtype=bf))),
+        (dg.dg_softmax, (dg.Desc(), torch.zeros(4, 8), torch.zeros(4, 9))),
+        (dg.dg_layernorm, (dg.Desc(), torch.zeros(4, 8), None, None, 1e-6, torch.zeros(4, 8, dtype=bf))),
+        (dg.dg_layernorm, (dg.Desc(), torch.zeros(4, 8), None, torch.zeros(8), 1e-6, torch.zeros(4, 8))),
+        (dg.dg_rowsum, (dg.Desc(), torch.zeros(4, 8), torch.zeros(3))),
+        (dg.dg_rowsum, (dg.Desc(), torch.zeros(4, 8, dtype=torch.float64), torch.zeros(4))),
+    ]
+    for fn, args in cases:
+        with pytest.raises(ValueError):
+            fn(*args)
+    # consistent CPU tensors pass the shape checks and stop at the device check
+    with pytest.raises(ValueError, match="GPU"):
+        dg.dg_gemm(dg.Desc(), A, B, None, torch.zeros(8, 24))
+    with pytest.raises(ValueError, match="GPU"):
+        dg.dg_softmax(dg.Desc(), torch.zeros(4, 8), torch.zeros(4, 8))
+
+
 def test_argument_errors_need_no_gpu(dg):
     # Every call below must be rejected before any launch: the pointers are
     # not device addresses.  Run where no GPU is visible, so that a

@@ -16,7 +16,7 @@ import pytest
 
 import oracle
 from paper_2609_11356_amd import inputs
-from tests.exact import bf, f, rn32, rn32_sqrt
+from tests.exact import bf, f, rn32, rn32_sqrt, rnbf
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 ONE = np.uint16(0x3F80)
@@ -1001,6 +1001,96 @@ def test_scalar_chained_chunks_match_rationals(S, T, tc, sc):
         for j in range(3):
             want = _chained_chunks_rational(A[i], B[:, j], S, T, tc, sc)
             assert C[i, j].view(np.uint32) == np.float32(want).view(np.uint32), (i, j)
+
+
+# ------------------------------------- parts and merges at bf16 (Sec. 3.2.2)
+#
+# partial_dtype: a finished part is stored at bf16; merge_dtype: the running
+# merge sum is held at bf16, so every merge addition is rounded to bf16.  For
+# two bf16 addends RNbf(RN32(x + y)) = RNbf(x + y) (a sum whose addends are
+# more than 16 binades apart lies far from any bf16 midpoint), so the walk
+# below rounds each merge's exact sum straight to bf16.
+
+
+def _split_bf16_rational(a, b, S, split_combine, partial_bf16, merge_bf16):
+    """Split-K over the scalar instruction written out in exact rationals:
+    parts of span ceil(K/S) (tile_k = 1), each an FMA chain from +0 (one
+    binary32 rounding per product), each part value rounded to bf16 when
+    partial_bf16, the parts chained or met in the balanced tree with every
+    merge addition rounded to bf16 when merge_bf16 (else to binary32)."""
+    K = len(a)
+    span = -(-K // S)
+    parts = []
+    for s in range(S):
+        acc = Fraction(0)
+        for k in range(s * span, min((s + 1) * span, K)):
+            acc = f(rn32(acc + bf(a[k]) * bf(b[k])))
+        parts.append(rnbf(acc) if partial_bf16 else acc)
+    add = (lambda x, y: rnbf(x + y)) if merge_bf16 else (lambda x, y: f(rn32(x + y)))
+    if split_combine == "seq":
+        y = parts[0]
+        for v in parts[1:]:
+            y = add(y, v)
+        return y
+    while len(parts) > 1:
+        nxt = [add(parts[2 * i], parts[2 * i + 1]) for i in range(len(parts) // 2)]
+        if len(parts) % 2:
+            nxt.append(parts[-1])
+        parts = nxt
+    return parts[0]
+
+
+@pytest.mark.parametrize("S,sc,partial,merge", [(4, "seq", "bf16", "bf16"), (4, "tree", "bf16", "bf16"),
+                                                (5, "seq", "bf16", "f32"), (7, "tree", "bf16", "bf16"),
+                                                (8, "tree", "bf16", "f32"), (3, "seq", "f32", "f32")])
+def test_bf16_parts_and_merges_match_rationals(S, sc, partial, merge):
+    """Parts and merges at bf16 against the exact-rational walk, on normal
+    and exponent-spread operands (the scalar instruction, so the parts are
+    plain FMA chains)."""
+    K = 210
+    for A, B in ((bits(np.random.default_rng(41).standard_normal((3, K))),
+                  bits(np.random.default_rng(42).standard_normal((K, 4)))),
+                 (inputs.spread_bf16(43, (3, K)), inputs.spread_bf16(44, (K, 4)))):
+        d = dict(mma="scalar", tile_k=1, split_k=S, split_combine=sc, partial=partial, merge=merge)
+        C = oracle.gemm(d, A, B)
+        for i in range(3):
+            for j in range(4):
+                want = _split_bf16_rational(A[i], B[:, j], S, sc, partial == "bf16", merge == "bf16")
+                assert C[i, j].view(np.uint32) == np.float32(float(want)).view(np.uint32), (i, j)
+
+
+def test_bf16_parts_and_merges_hand_examples():
+    """Cases worked by hand where the bf16 rounding of a part or of a merge
+    decides the result (bf16 keeps 8 significant bits: 1 + 2^-8 is a tie and
+    goes to 1, 1 + 2^-7 is exact)."""
+    one = dict(mma="scalar", tile_k=1)
+    # four parts of one product each: 1, 2^-8, 2^-8, 2^-8
+    A = bits([[1.0, 2.0 ** -8, 2.0 ** -8, 2.0 ** -8]])
+    B = bits(np.ones((4, 1)))
+    want = {("seq", "f32"): 1 + 3 * 2.0 ** -8,     # binary32 holds the sum
+            ("tree", "f32"): 1 + 3 * 2.0 ** -8,
+            ("seq", "bf16"): 1.0,                  # (1 + 2^-8) ties to 1, twice
+            ("tree", "bf16"): 1 + 2.0 ** -7}       # 1 + 2^-8 -> 1; 2^-8 + 2^-8 = 2^-7; 1 + 2^-7 exact
+    for (sc, merge), v in want.items():
+        C = oracle.gemm(dict(one, split_k=4, split_combine=sc, partial="bf16", merge=merge), A, B)
+        assert C[0, 0] == np.float32(v), (sc, merge, C[0, 0])
+    # two parts: (1 + 2^-7)^2 = 1 + 2^-6 + 2^-14 and 2^-9
+    A = bits([[1 + 2.0 ** -7, 1.0]])
+    B = bits([[1 + 2.0 ** -7], [2.0 ** -9]])
+    cases = {("f32", "f32"): 1 + 2.0 ** -6 + 2.0 ** -9 + 2.0 ** -14,
+             ("bf16", "f32"): 1 + 2.0 ** -6 + 2.0 ** -9,   # the part loses its 2^-14
+             ("bf16", "bf16"): 1 + 2.0 ** -6}              # and the merge its 2^-9
+    for (partial, merge), v in cases.items():
+        C = oracle.gemm(dict(one, split_k=2, partial=partial, merge=merge), A, B)
+        assert C[0, 0] == np.float32(v), (partial, merge, C[0, 0])
+    # the gfx950 instruction path takes the same part and merge roundings
+    g = dict(model="gfx950", mma="16x16x32", tile_k=32, split_k=2, partial="bf16", merge="bf16")
+    A = np.zeros((1, 64), dtype=np.uint16)
+    B = np.zeros((64, 1), dtype=np.uint16)
+    A[0, 0], B[0, 0] = bits(1 + 2.0 ** -7), bits(1 + 2.0 ** -7)
+    A[0, 32], B[32, 0] = bits(1.0), bits(2.0 ** -9)
+    assert oracle.gemm(g, A, B)[0, 0] == np.float32(1 + 2.0 ** -6)
+    assert oracle.gemm(dict(g, merge="f32"), A, B)[0, 0] == np.float32(1 + 2.0 ** -6 + 2.0 ** -9)
 
 
 # ------------------------------------------------- binary16 operands

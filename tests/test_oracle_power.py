@@ -70,6 +70,14 @@ MUTANTS = {
     "exp polynomial one term short": ("  p = fmaf(p, r, (float)(1.0 / 720.0));\n", ""),
     "sign of a product lost": ("int sign = (a[t] >> 15) ^ (b[t] >> 15);\n    if (op_isnan(a[t], f16)",
                                "int sign = 0;\n    if (op_isnan(a[t], f16)"),
+    "part stored without its bf16 rounding": ("pvals[s] = p->partial_bf16 ? rnbf(v) : v;", "pvals[s] = v;"),
+    "chained merge without its bf16 rounding": (
+        "for (int k = 1; k < n; ++k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }",
+        "for (int k = 1; k < n; ++k) { s = s + v[k]; }"),
+    "tree merge without its bf16 rounding": ("t[k] = bf16_round ? rnbf(s) : s;", "t[k] = s;"),
+    "merge rounded to bf16 only at the end": (
+        "for (int k = 1; k < n; ++k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }",
+        "for (int k = 1; k < n; ++k) { s = s + v[k]; }\n  if (bf16_round) s = rnbf(s);"),
     "binary16 exponent bias off by one": ("eb = f16 ? 5 : 8, bias = f16 ? 15 : 127;",
                                           "eb = f16 ? 5 : 8, bias = f16 ? 14 : 127;"),
     "binary16 product scale off by one": ("const int fb2 = 2 * op_frac(f16);",
@@ -104,6 +112,8 @@ CHECKS = [
     lambda: pins.test_softmax_steps_and_rounding_points(),
     lambda: pins.test_layernorm_closed_forms(),
     lambda: pins.test_layernorm_steps_and_rounding_points(),
+    lambda: pins.test_bf16_parts_and_merges_hand_examples(),
+    lambda: pins.test_bf16_parts_and_merges_match_rationals(4, "tree", "bf16", "bf16"),
     lambda: pins.test_f16_decoding_matches_numpy_on_every_pattern(),
     lambda: pins.test_f16_exact_dot_is_the_rational_sum_rounded_once(),
     lambda: pins.test_f16_chunk_model_hand_examples(),
