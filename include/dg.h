@@ -46,7 +46,9 @@ typedef enum {
   DG_ERR_SHAPE = 3,       /* sizes inconsistent with the descriptor's plan */
   DG_ERR_ALIGN = 4,       /* a device pointer not aligned to its element size */
   DG_ERR_NOMEM = 5,       /* split-K workspace allocation failed */
-  DG_ERR_HIP = 6          /* a HIP runtime call or kernel launch failed */
+  DG_ERR_HIP = 6,         /* a HIP runtime call or kernel launch failed */
+  DG_ERR_SCRATCH = 7      /* dg_gemm_noalloc: S * M * N partials exceed its
+                             fixed scratch (DG_NOALLOC_SCRATCH_BYTES) */
 } dg_status;
 
 /* Matrix instruction whose group the descriptor names (Sec. 3.2.1:
@@ -74,6 +76,7 @@ enum { DG_IN_BF16 = 0, DG_IN_F16 = 1 };                  /* GEMM operand format 
 
 #define DG_MAX_SPLIT 64
 #define DG_SIGNATURE_MAX 2048
+#define DG_NOALLOC_SCRATCH_BYTES (16u << 20) /* dg_gemm_noalloc's fixed split-K scratch */
 
 /* The order fields, and nothing else (Sec. 3.2.2; Sec. 4 keeps a reconstructed
  * order as a frozen record of all of its factors).  No speed knob appears here. */
@@ -183,6 +186,23 @@ dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n);
  * DG_ERR_NOMEM if that workspace cannot grow. */
 dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias,
                   void* C, int64_t M, int64_t N, int64_t K, void* stream);
+
+/* dg_gemm for callers that cannot allocate device memory (code under HIP
+ * graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same kernels and the same bits as dg_gemm, but split-K partials
+ * (S > 1) go to a fixed array of DG_NOALLOC_SCRATCH_BYTES (16 MiB) that the
+ * library holds on each device it runs on until the process ends, instead of
+ * the workspace dg_gemm grows.  The call allocates and frees nothing (no
+ * hipMalloc, no hipFree, no allocating library routine); the caller passes
+ * inputs and outputs as for dg_gemm.  DG_ERR_SCRATCH, before any launch, if
+ * S * M * N * 4 bytes exceed the array (S = 1 uses no scratch).  Every call on
+ * a device shares that device's one array, which keeps the last call's
+ * partials: calls that overlap in time on one device (other streams, other
+ * host threads) race and give undefined results; calls ordered on one stream
+ * are safe.  Every partial a call reads was written by the same call, so
+ * nothing needs clearing.  Errors otherwise as dg_gemm. */
+dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const void* bias,
+                          void* C, int64_t M, int64_t N, int64_t K, void* stream);
 
 /* dg_gemm followed by the column sums of its output, an epilogue reduction
  * (the paper times a GEMM whose epilogue emits a column sum, Sec. 7):
@@ -326,7 +346,8 @@ const char* dg_strerror(dg_status s);
  * dg_desc_params.leaf_layout / lane_fold and dg_knobs.split_n: a caller
  * built against an earlier header must not pass its dg_knobs to this one.
  * 0.3.0 (300) added dg_desc_params.in_dtype (a smaller struct_size is
- * rejected) and knob kernel 10. */
+ * rejected) and knob kernel 10.  0.4.0 (400) added dg_gemm_noalloc and
+ * DG_ERR_SCRATCH. */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

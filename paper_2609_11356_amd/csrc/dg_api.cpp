@@ -188,7 +188,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 300; }
+int32_t dg_version(void) { return 400; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {
@@ -199,6 +199,7 @@ const char* dg_strerror(dg_status s) {
     case DG_ERR_ALIGN: return "misaligned pointer";
     case DG_ERR_NOMEM: return "workspace allocation failed";
     case DG_ERR_HIP: return "HIP runtime error";
+    case DG_ERR_SCRATCH: return "split-K partials exceed the fixed scratch of the no-allocation entry point";
   }
   return "unknown status";
 }
@@ -277,7 +278,7 @@ dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n) {
 // whether it did.
 static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
                            int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream,
-                           float* colsum_part, bool* fused) {
+                           float* colsum_part, bool* fused, bool noalloc = false) {
   if (fused) *fused = false;
   if (!d) return DG_ERR_INVALID;
   if (M < 0 || N < 0 || K < 0) return DG_ERR_SHAPE;
@@ -358,8 +359,16 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   hipStream_t st = (hipStream_t)stream;
   if (a.S > 1) {
     void* ws = nullptr;
-    dg_status s = get_workspace(st, (size_t)a.S * (size_t)M * (size_t)N * sizeof(float), &ws);
-    if (s != DG_OK) return s;
+    const size_t bytes = (size_t)a.S * (size_t)M * (size_t)N * sizeof(float);
+    if (noalloc) {
+      // the fixed per-device array; nothing is allocated
+      if ((uint64_t)a.S * (uint64_t)M * (uint64_t)N > DG_NOALLOC_SCRATCH_BYTES / sizeof(float))
+        return DG_ERR_SCRATCH;
+      if (dg::noalloc_scratch(&ws) != hipSuccess) return DG_ERR_HIP;
+    } else {
+      dg_status s = get_workspace(st, bytes, &ws);
+      if (s != DG_OK) return s;
+    }
     a.ws = (float*)ws;
   }
 
@@ -510,6 +519,11 @@ dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const vo
 dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
                   int64_t M, int64_t N, int64_t K, void* stream) {
   return dg_gemm_knobs(d, A, B, bias, C, M, N, K, nullptr, stream);
+}
+
+dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
+                          int64_t M, int64_t N, int64_t K, void* stream) {
+  return gemm_impl(d, A, B, bias, C, M, N, K, nullptr, stream, nullptr, nullptr, true);
 }
 
 dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,

@@ -26,12 +26,38 @@
 //   splitk_combine   S fp32 partials -> chain or balanced tree at the merge
 //                    precision -> epilogue (no atomics: the second kernel on
 //                    the same stream).
+#include <mutex>
 #include <type_traits>
 
 #include "dg_device.h"
 #include "dg_internal.h"
 
+// Split-K partials of dg_gemm_noalloc: a fixed array, one copy per device,
+// held until the process ends.  Host code never uses this name as an address
+// (on the host it only stands for the symbol); it asks the runtime for each
+// device's copy once (noalloc_scratch) and passes that pointer to the kernels.
+static __device__ __align__(256) float scratch[DG_NOALLOC_SCRATCH_BYTES / sizeof(float)];
+
 namespace dg {
+
+hipError_t noalloc_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
+}
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short shortx8 __attribute__((ext_vector_type(8)));

@@ -73,6 +73,11 @@ struct ColsumArgs {
   int32_t out_bf16;
 };
 
+// This device's copy of the fixed split-K scratch array of dg_gemm_noalloc
+// (DG_NOALLOC_SCRATCH_BYTES), looked up once per device with that device
+// current; never allocates.
+hipError_t noalloc_scratch(void** out);
+
 // launchers (return hipSuccess or the launch error)
 hipError_t launch_gemm_generic(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_scalar(const GemmArgs& a, hipStream_t s);   // groups of one (scalar FMA)

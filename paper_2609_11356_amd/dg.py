@@ -13,7 +13,7 @@ import os
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdg.so")
 
-DG_OK, DG_ERR_INVALID, DG_ERR_UNSUPPORTED, DG_ERR_SHAPE, DG_ERR_ALIGN, DG_ERR_NOMEM, DG_ERR_HIP = range(7)
+DG_OK, DG_ERR_INVALID, DG_ERR_UNSUPPORTED, DG_ERR_SHAPE, DG_ERR_ALIGN, DG_ERR_NOMEM, DG_ERR_HIP, DG_ERR_SCRATCH = range(8)
 MMA = {"16x16x32": 1, "32x32x16": 2, "scalar": 3}
 COMBINE = {"carry": 0, "seq": 1, "tree": 2}
 TAIL = {"last": 0, "first": 1}
@@ -23,6 +23,7 @@ EPI_ROUND = {"final": 0, "pre_act": 1}
 REDUCE = {"sum": 0, "sumsq": 1}
 MAX_SPLIT = 64
 SIGNATURE_MAX = 2048
+NOALLOC_SCRATCH_BYTES = 16 << 20
 
 
 class DgError(RuntimeError):
@@ -64,6 +65,7 @@ def lib():
         L.dg_desc_destroy.restype = None
         L.dg_desc_signature.argtypes = [vp, ctypes.c_char_p, ctypes.c_size_t]
         L.dg_gemm.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
+        L.dg_gemm_noalloc.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_gemm_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
         L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
         L.dg_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
@@ -73,8 +75,8 @@ def lib():
         L.dg_strerror.argtypes = [ctypes.c_int]
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
-        for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm",
-                  "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
+        for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc", "dg_gemm_knobs",
+                  "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -259,6 +261,19 @@ def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knob
     return C
 
 
+def dg_gemm_noalloc(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None):
+    """dg_gemm through the entry point that allocates nothing: split-K
+    partials go to the library's fixed per-device scratch (at most
+    NOALLOC_SCRATCH_BYTES); calls that overlap on one device race."""
+    import torch
+    if isinstance(A, torch.Tensor):
+        M, N, K = _check_gemm(desc, A, B, bias, C)
+    st = lib().dg_gemm_noalloc(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_gemm_noalloc")
+    return C
+
+
 def dg_rowsum(desc: Desc, X, out, rows=None, cols=None, stream=None):
     """out[r] = balanced-tree reduction of row r of X (fp32, row-major)."""
     import torch
@@ -328,6 +343,6 @@ def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
 
 def exported_symbols():
     """Names of the entry points include/dg.h declares."""
-    return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_knobs",
-            "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
+    return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc",
+            "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
             "dg_version"]

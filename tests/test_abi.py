@@ -34,8 +34,8 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 300
-    for s in range(7):
+    assert dg.dg_version() == 400
+    for s in range(8):
         assert dg.dg_strerror(s)
 
 
@@ -210,6 +210,15 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_gemm(c.handle, 16, 16, None, 16, 8, 8, 256, None) == dg.DG_ERR_SHAPE
     k0 = dg.Desc(split_k=2)
     assert lib.dg_gemm(k0.handle, 16, 16, None, 16, 8, 8, 0, None) == dg.DG_ERR_SHAPE
+    # the no-allocation entry point: partials beyond its fixed scratch are
+    # refused before any HIP call; its other checks are dg_gemm's
+    s8 = dg.Desc(split_k=8, tile_k=64)
+    assert lib.dg_gemm_noalloc(s8.handle, 16, 16, None, 16, 128, 8192, 4096, None) == dg.DG_ERR_SCRATCH
+    assert 8 * 128 * 8192 * 4 > dg.NOALLOC_SCRATCH_BYTES
+    assert lib.dg_gemm_noalloc(s8.handle, 16, 16, None, 16, 0, 8192, 4096, None) == dg.DG_OK
+    assert lib.dg_gemm_noalloc(s8.handle, 16, 16, None, 16, 8, 8, 100, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_gemm_noalloc(d.handle, 17, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_gemm_noalloc(None, 16, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_INVALID
     # knobs the build lacks
     kn = dg.dg_knobs(2, 48, 128, 0, 0, 0)
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
