@@ -111,6 +111,8 @@ def _bind(path):
     L.dgo_exp.restype = f32
     L.dgo_silu.argtypes = [f32]
     L.dgo_silu.restype = f32
+    L.dgo_exp_silu_range.argtypes = [ctypes.c_uint64, i64, vp, vp, i32]
+    L.dgo_exp_silu_range.restype = None
     L.dgo_plan_cuts.argtypes = [P, i64, vp]
     for f in ("dgo_gemm", "dgo_gemm_at", "dgo_rowsum", "dgo_plan_cuts"):
         getattr(L, f).restype = i32
@@ -353,3 +355,11 @@ def exp(x):
 
 def silu(x):
     return np.float32(lib().dgo_silu(float(x)))
+
+
+def exp_silu_range(start, count, nthreads=None):
+    """(exp, silu) of the binary32 values with bit patterns start .. start+count-1."""
+    e = np.empty(count, dtype=np.float32)
+    s = np.empty(count, dtype=np.float32)
+    lib().dgo_exp_silu_range(int(start), int(count), e.ctypes.data, s.ctypes.data, nthreads or os.cpu_count())
+    return e, s

@@ -525,6 +525,18 @@ float dgo_silu(float z) {
   return z / (1.0f + e);
 }
 
+/* dgo_exp and dgo_silu of the binary32 values whose bit patterns are
+ * start .. start + count - 1 (for exhaustive comparisons). */
+void dgo_exp_silu_range(uint64_t start, int64_t count, float* e, float* s, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+  for (int64_t i = 0; i < count; ++i) {
+    float x = u2f((uint32_t)(start + (uint64_t)i));
+    e[i] = dgo_exp(x);
+    s[i] = dgo_silu(x);
+  }
+}
+
 /* ------------------------------------------------------------- GEMM */
 
 /* One output (i, j) of the descriptor's order.  a = row i of A (K values),

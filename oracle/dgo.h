@@ -6,7 +6,7 @@
  * baseline do.  It shares no source with the GPU path.
  *
  * What it computes (paper: "Taming Bitwise Behavior in GPU Kernels with
- * Tensor Core", Sec. 3 "Understand the bit behavior under GPU parallelism"):
+ * Tensor Core", Sec. 3, the bit behaviour of parallel reductions):
  *
  *   A reduction is a dependence tree of binary32 additions; two kernels owe
  *   each other the same bits when their trees are equivalent up to swapping
@@ -16,7 +16,7 @@
  *   the group width, whether the accumulator joins that rounding
  *   (use_fast_accum), where the short K turn falls (k_loop_step), the split-K
  *   cut points, how tiles and parts are combined and at which precision
- *   (partial_dtype / merge_dtype) (Sec. 3.2.2, "The algorithm families").
+ *   (partial_dtype / merge_dtype) (Sec. 3.2.2, the families of GEMM orders).
  *
  * The oracle evaluates exactly that order, one output at a time, with every
  * rounding explicit: exact group sums in a wide fixed-point accumulator,
@@ -176,6 +176,8 @@ float dgo_f16_to_f32(uint16_t h);   /* exact */
 /* Epilogue functions: the exp and SiLU the descriptor's epilogue uses. */
 float dgo_exp(float x);
 float dgo_silu(float z);
+/* e[i] = dgo_exp(x), s[i] = dgo_silu(x) for the binary32 x with bits start + i. */
+void dgo_exp_silu_range(uint64_t start, int64_t count, float* e, float* s, int nthreads);
 
 /* Cut plan for (K, params): writes S+1 cut points to cuts (caller provides
  * split_k + 1 slots).  Returns 0 or a status. */

@@ -1,18 +1,26 @@
-"""Build the MFMA probe kernel (test infrastructure) with hipcc."""
+"""Build the probe kernels (test infrastructure) with hipcc: raw MFMAs, and
+the library's device exp / SiLU over ranges of binary32 inputs."""
 import os
 import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libmfma_probe.so")
+MATH_LIB = os.path.join(HERE, "libmath_probe.so")
 
 
-def build():
-    tmp = LIB + ".tmp%d" % os.getpid()
+def _hipcc(src, lib, extra=()):
+    tmp = lib + ".tmp%d" % os.getpid()
     cmd = [os.environ.get("HIPCC", "/opt/rocm/bin/hipcc"), "--offload-arch=gfx950", "-O2", "-fPIC", "-shared",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-o", tmp, os.path.join(HERE, "mfma_probe.hip")]
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", *extra,
+           "-o", tmp, os.path.join(HERE, src)]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode:
         raise RuntimeError(r.stdout + r.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build():
+    # the math probe is compiled as the library is (no contraction, no fast math)
+    _hipcc("math_probe.hip", MATH_LIB, ("-O3", "-ffp-contract=off", "-fno-fast-math"))
+    return _hipcc("mfma_probe.hip", LIB)

@@ -95,17 +95,23 @@ def test_descriptor_matrix_ragged(dg, di, shape):
     exponent-spread operands."""
     desc = DESCS[di]
     M, N, K = shape
-    if desc.get("k_cuts") and not (desc["k_cuts"][-1] < K):
-        pytest.skip("cuts outside K")
-    S = desc.get("split_k", 1)
-    span = -(-K // S)
-    span = -(-span // desc["tile_k"]) * desc["tile_k"]
-    if S > 1 and not desc.get("k_cuts") and (S - 1) * span >= K:
-        pytest.skip("plan leaves a part empty")
     rng_seed = 100 * di + M
     A = inputs.normal_bf16(rng_seed, (M, K))
     B = inputs.normal_bf16(rng_seed + 1, (K, N), 0.05)
     bias = inputs.normal_bf16(rng_seed + 2, (N,), 0.5)
+    S = desc.get("split_k", 1)
+    span = -(-K // S)
+    span = -(-span // desc["tile_k"]) * desc["tile_k"]
+    cuts_outside = bool(desc.get("k_cuts")) and not desc["k_cuts"][-1] < K
+    empty_part = S > 1 and not desc.get("k_cuts") and (S - 1) * span >= K
+    if cuts_outside or empty_part:
+        # a plan the descriptor cannot make for this K: both sides refuse it
+        with pytest.raises(dg.DgError) as e:
+            run(dg, desc, A, B, bias)
+        assert e.value.status == dg.DG_ERR_SHAPE
+        with pytest.raises(oracle.OracleError):
+            oracle.gemm(desc, A, B, bias)
+        return
     check_full(dg, desc, A, B, bias, what="%s %s normal" % (desc, shape))
     As = inputs.spread_bf16(rng_seed + 3, (M, K))
     Bs = inputs.spread_bf16(rng_seed + 4, (K, N))
@@ -271,13 +277,18 @@ def test_splitk_decode(dg, combine, out):
     A, B = inputs.decode()
     desc = dict(mma="16x16x32", tile_k=64, split_k=8, split_combine=combine, out=out)
     got = run(dg, desc, A, B)
-    rng = np.random.default_rng(6)
-    ii = rng.integers(0, 8, 2000)
-    jj = rng.integers(0, 4096, 2000)
-    want = oracle.gemm_at(desc, A, B, None, ii, jj)
-    if out == "bf16":
-        want = inputs.f32_to_bf16_bits(want)
-    assert_bits_equal(got[ii, jj], want, "decode %s %s" % (combine, out))
+    # every one of the 32768 outputs
+    assert_bits_equal(got, oracle.gemm(desc, A, B), "decode %s %s" % (combine, out))
+
+
+def test_splitk_decode_spread(dg):
+    """The decode shape on exponent-spread operands (where a regrouping of
+    the parts or of the chunks flips output bits), every output."""
+    A = inputs.spread_bf16(31, (8, 14336))
+    B = inputs.spread_bf16(32, (14336, 4096))
+    for combine in ("seq", "tree"):
+        desc = dict(mma="16x16x32", tile_k=64, split_k=8, split_combine=combine, out="bf16")
+        assert_bits_equal(run(dg, desc, A, B), oracle.gemm(desc, A, B), "decode spread %s" % combine)
 
 
 @pytest.mark.parametrize("epi_round", ["final", "pre_act"])
@@ -295,6 +306,32 @@ def test_fused_mlp(dg, epi_round):
     # and the full first rows
     want_rows = oracle.gemm(desc, A[:2], B, bias)
     assert_bits_equal(got[:2], want_rows, "mlp rows 0-1")
+
+
+def test_full_size_spread_draws(dg):
+    """One exponent-spread draw at the fused-MLP shape and at the sweep's
+    M = 4096 shape, compared with the oracle on sampled outputs and whole
+    rows (narrow exponents can hide a regrouping; spread ones do not)."""
+    rng = np.random.default_rng(8)
+    A = inputs.spread_bf16(51, (2048, 4096))
+    B = inputs.spread_bf16(52, (4096, 14336))
+    bias = inputs.spread_bf16(53, (14336,))
+    desc = dict(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu")
+    got = run(dg, desc, A, B, bias)
+    ii = rng.integers(0, 2048, 2500)
+    jj = rng.integers(0, 14336, 2500)
+    want = inputs.f32_to_bf16_bits(oracle.gemm_at(desc, A, B, bias, ii, jj))
+    assert_bits_equal(got[ii, jj], want, "mlp spread sampled")
+    assert_bits_equal(got[[0, 1337, 2047]], oracle.gemm(desc, A[[0, 1337, 2047]], B, bias), "mlp spread rows")
+    A = inputs.spread_bf16(54, (4096, 4096))
+    B = inputs.spread_bf16(55, (4096, 4096))
+    desc = dict(mma="16x16x32", tile_k=64, out="bf16")
+    got = run(dg, desc, A, B)
+    ii = rng.integers(0, 4096, 3000)
+    jj = rng.integers(0, 4096, 3000)
+    want = inputs.f32_to_bf16_bits(oracle.gemm_at(desc, A, B, None, ii, jj))
+    assert_bits_equal(got[ii, jj], want, "sweep M=4096 spread sampled")
+    assert_bits_equal(got[[5, 4095]], oracle.gemm(desc, A[[5, 4095]], B), "sweep M=4096 spread rows")
 
 
 def test_error_bound_vs_fp64(dg):

@@ -4,10 +4,13 @@ Each case draws, from its own seed, a descriptor (instruction group, tile
 length, split count and merge, tile combine, short-tile position, the fma
 rule, partial / merge / output types, epilogue and rounding point, operand
 format), a ragged shape, inputs from the seeded generators, and one of the
-speed knobs the knob test uses.  A knob the drawn descriptor or shape cannot
-run on is refused with DG_ERR_UNSUPPORTED; the case then runs the library's
-own choice, so that every case compares all of its outputs with the oracle,
-bit for bit.  A draw whose K the descriptor's cut plan cannot split is one
+speed knobs the knob test uses, among those the descriptor admits (the tiled
+MFMA kernels take a carried accumulator with the fused rule; binary16
+operands are not taken by the tiled, direct-to-LDS and four-wave kernels; the
+scalar instruction runs on its own kernel).  A knob the drawn shape still
+cannot run on is refused with DG_ERR_UNSUPPORTED; the case then runs the
+library's own choice, so that every case compares all of its outputs with the
+oracle, bit for bit, and the last test requires that most drawn knobs ran.  A draw whose K the descriptor's cut plan cannot split is one
 the oracle refuses; the library must then refuse it as well (DG_ERR_SHAPE).
 Most draws keep to what the tiled MFMA kernels accept (the 16x16x32 group, a
 carried accumulator, the fused rule, K a multiple of 8) so that the knobs
@@ -80,8 +83,19 @@ def draw(seed):
         A = inputs.normal_bf16(2 * seed, (M, K))
         B = inputs.normal_bf16(2 * seed + 1, (K, N), 0.05)
     bias = inputs.normal_bf16(7 * seed + 3, (N,), 1.0) if epi != "none" else None
-    knobs = KNOBS[int(rng.integers(len(KNOBS)))] if rng.random() < 0.8 else None
+    if mma == "scalar":
+        pool = [dict(kernel=9)]
+    elif not tiled:
+        pool = [dict(kernel=1)]
+    elif f16:
+        pool = [k for k in KNOBS if k is not None and k["kernel"] not in (2, 7, 8, 10)]
+    else:
+        pool = [k for k in KNOBS if k is not None]
+    knobs = pool[int(rng.integers(len(pool)))] if rng.random() < 0.8 else None
     return desc, A, B, bias, knobs, f16
+
+
+KNOB_RUNS = {"ran": 0, "refused": 0}
 
 
 @pytest.mark.parametrize("seed", range(192))
@@ -110,8 +124,20 @@ def test_random_descriptor_and_knob(dg, seed):
         return
     try:
         dg.dg_gemm(d, dA, dB, db, C, knobs=knobs)
+        if knobs is not None:
+            KNOB_RUNS["ran"] += 1
     except dg.DgError as ex:
         assert ex.status == dg.DG_ERR_UNSUPPORTED, ex
+        KNOB_RUNS["refused"] += 1
         dg.dg_gemm(d, dA, dB, db, C)
     torch.cuda.synchronize()
     assert_bits_equal(host_bits(C), want, "seed %d %s %s" % (seed, desc, knobs))
+
+
+def test_drawn_knobs_mostly_ran(dg):
+    """The speed-knob coverage is measured: of the drawn knobs, at least 85 %
+    ran as drawn (the rest hit a shape limit and ran the library's choice)."""
+    n = KNOB_RUNS["ran"] + KNOB_RUNS["refused"]
+    if n < 100:
+        pytest.skip("needs the whole seed range in this session (%d knob cases ran)" % n)
+    assert KNOB_RUNS["ran"] >= 0.85 * n, KNOB_RUNS
