@@ -51,6 +51,11 @@ class _Params(ctypes.Structure):
             "split_strided", "split_tile", "leaf_strided", "fold_down", "norm_pre_round", "in_f16")]
 
 
+class _AttnParams(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("key_block", "causal", "q_block", "block_sum", "pv_fma", "l_fma",
+                                              "final_recip", "out_bf16", "model")]
+
+
 _lib = None
 
 
@@ -111,6 +116,15 @@ def _bind(path):
     L.dgo_exp.restype = f32
     L.dgo_silu.argtypes = [f32]
     L.dgo_silu.restype = f32
+    PA = ctypes.POINTER(_AttnParams)
+    L.dgo_attention.argtypes = [PA, vp, vp, vp, vp, i64, i64, i64, i64, f32, i32]
+    L.dgo_attention.restype = i32
+    L.dgo_attention_rows.argtypes = [PA, vp, vp, vp, i64, i64, i64, i64, f32, vp, vp, i64, vp, i32]
+    L.dgo_attention_rows.restype = i32
+    L.dgo_exp2.argtypes = [f32]
+    L.dgo_exp2.restype = f32
+    L.dgo_exp2_range.argtypes = [ctypes.c_uint64, i64, vp, i32]
+    L.dgo_exp2_range.restype = None
     L.dgo_exp_silu_range.argtypes = [ctypes.c_uint64, i64, vp, vp, i32]
     L.dgo_exp_silu_range.restype = None
     L.dgo_plan_cuts.argtypes = [P, i64, vp]
@@ -363,3 +377,74 @@ def exp_silu_range(start, count, nthreads=None):
     s = np.empty(count, dtype=np.float32)
     lib().dgo_exp_silu_range(int(start), int(count), e.ctypes.data, s.ctypes.data, nthreads or os.cpu_count())
     return e, s
+
+
+# ------------------------------------------------------------------ attention
+
+ATTN_DEFAULTS = dict(model="gfx950", key_block=64, causal=0, q_block=64, block_sum="tree", pv_fma=1, l_fma=0,
+                     final="div", out="bf16")
+
+
+def attn_params(desc):
+    """Map an attention descriptor dict (fields as the library's binding
+    names them) to the oracle's struct."""
+    f = dict(ATTN_DEFAULTS)
+    unknown = set(desc) - set(f)
+    if unknown:
+        raise ValueError("unknown attention fields %s" % sorted(unknown))
+    f.update(desc)
+    p = _AttnParams()
+    p.key_block = int(f["key_block"])
+    p.causal = int(bool(f["causal"]))
+    p.q_block = int(f["q_block"])
+    p.block_sum = COMBINE[f["block_sum"]]
+    p.pv_fma = int(f["pv_fma"])
+    p.l_fma = int(f["l_fma"])
+    p.final_recip = {"div": 0, "recip": 1}[f["final"]]
+    p.out_bf16 = int(f["out"] == "bf16")
+    p.model = {"exact": MODEL_EXACT, "gfx950": MODEL_GFX950}[f["model"]]
+    return p
+
+
+def attention(desc, Q, K, V, qk_scale, nthreads=None):
+    """O = attention in the descriptor's order.  Q (H, Lq, d), K and V (H, Lk,
+    d) as bf16 bit patterns; returns (H, Lq, d) float32 or bf16 bits."""
+    Q, K, V = _u16(Q), _u16(K), _u16(V)
+    H, Lq, d = Q.shape
+    Lk = K.shape[1]
+    assert K.shape == (H, Lk, d) and V.shape == (H, Lk, d)
+    p = attn_params(desc)
+    out = np.zeros((H, Lq, d), dtype=np.uint16 if p.out_bf16 else np.float32)
+    st = lib().dgo_attention(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), out.ctypes.data, H, Lq, Lk, d,
+                             float(qk_scale), nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_attention status %d" % st)
+    return out
+
+
+def attention_rows(desc, Q, K, V, qk_scale, hh, ii, nthreads=None):
+    """Rows (hh[r], ii[r]) of the same attention as float32 (bf16 widened)."""
+    Q, K, V = _u16(Q), _u16(K), _u16(V)
+    H, Lq, d = Q.shape
+    Lk = K.shape[1]
+    hh = np.ascontiguousarray(hh, dtype=np.int64)
+    ii = np.ascontiguousarray(ii, dtype=np.int64)
+    out = np.zeros((len(hh), d), dtype=np.float32)
+    p = attn_params(desc)
+    st = lib().dgo_attention_rows(ctypes.byref(p), _ptr(Q), _ptr(K), _ptr(V), H, Lq, Lk, d, float(qk_scale),
+                                  hh.ctypes.data, ii.ctypes.data, len(hh), out.ctypes.data,
+                                  nthreads or os.cpu_count())
+    if st:
+        raise OracleError("dgo_attention_rows status %d" % st)
+    return out
+
+
+def exp2(x):
+    return np.float32(lib().dgo_exp2(float(x)))
+
+
+def exp2_range(start, count, nthreads=None):
+    """dgo_exp2 of the binary32 values with bit patterns start .. start+count-1."""
+    out = np.empty(count, dtype=np.float32)
+    lib().dgo_exp2_range(int(start), int(count), out.ctypes.data, nthreads or os.cpu_count())
+    return out

@@ -893,3 +893,207 @@ int dgo_rmsnorm(const dgo_params* p, const float* X, const uint16_t* w, float ep
   }
   return 0;
 }
+
+/* ------------------------------------------------------------ attention */
+
+/* 2^x in binary32 by a fixed sequence of steps (our own, written from the
+ * Taylor series of e^(f ln 2)): n = rint(x); f = x - n, exact, |f| <= 1/2;
+ * 2^f by the degree-7 polynomial sum_k c_k f^k with c_k = RN32((ln 2)^k / k!)
+ * in Horner form, one fused multiply-add per step; then the exact scaling by
+ * 2^n in two power-of-two factors, so that only the last multiply can round
+ * (into the subnormal range or to infinity).  At or above 128 the result is
+ * +inf, below -151 it is +0 (2^-151 rounds to zero). */
+#define LN2_D 0.69314718055994530942
+float dgo_exp2(float x) {
+  if (x != x) return x + x;
+  if (x >= 128.0f) return INFINITY;
+  if (x < -151.0f) return 0.0f;
+  const float c7 = (float)(LN2_D * LN2_D * LN2_D * LN2_D * LN2_D * LN2_D * LN2_D / 5040.0);
+  const float c6 = (float)(LN2_D * LN2_D * LN2_D * LN2_D * LN2_D * LN2_D / 720.0);
+  const float c5 = (float)(LN2_D * LN2_D * LN2_D * LN2_D * LN2_D / 120.0);
+  const float c4 = (float)(LN2_D * LN2_D * LN2_D * LN2_D / 24.0);
+  const float c3 = (float)(LN2_D * LN2_D * LN2_D / 6.0);
+  const float c2 = (float)(LN2_D * LN2_D / 2.0);
+  const float c1 = (float)LN2_D;
+  float n = rintf(x);
+  float f = x - n;
+  float p = c7;
+  p = fmaf(p, f, c6);
+  p = fmaf(p, f, c5);
+  p = fmaf(p, f, c4);
+  p = fmaf(p, f, c3);
+  p = fmaf(p, f, c2);
+  p = fmaf(p, f, c1);
+  p = fmaf(p, f, 1.0f);
+  int ni = (int)n;
+  int n1 = ni / 2, n2 = ni - ni / 2;
+  float s1 = u2f((uint32_t)(n1 + 127) << 23);
+  float s2 = u2f((uint32_t)(n2 + 127) << 23);
+  return (p * s1) * s2;
+}
+
+void dgo_exp2_range(uint64_t start, int64_t count, float* out, int nthreads) {
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+  for (int64_t i = 0; i < count; ++i) out[i] = dgo_exp2(u2f((uint32_t)(start + (uint64_t)i)));
+}
+
+/* The offset a causal mask adds to a score above the diagonal before the
+ * block maximum (App. F): large enough that its probability underflows. */
+#define ATTN_MASK_OFFSET (-1.0e6f)
+
+/* The key blocks row i walks (App. F, the recurrence and the causal split):
+ * unmasked, [0, Lk) cut into blocks of w from key 0 (the last one shorter);
+ * causal (Lq = Lk), with q0 = (i / BM) BM and q1 = min(q0 + BM, Lk), first
+ * [0, q0) cut into blocks of w from key 0 (the last one ending at q0), then
+ * [q0, q1) cut into blocks of w from q0 (the last one ending at q1), the
+ * keys of that second stage above the diagonal (t > i) masked.  Writes the
+ * block bounds (begin, end, masked-stage flag) and returns their count. */
+static int64_t attn_blocks(const dgo_attn_params* p, int64_t i, int64_t Lk, int64_t* kb, int64_t* ke,
+                           int* stage2) {
+  const int64_t w = p->key_block;
+  int64_t n = 0;
+  if (!p->causal) {
+    for (int64_t t = 0; t < Lk; t += w) {
+      kb[n] = t; ke[n] = t + w < Lk ? t + w : Lk; stage2[n] = 0; ++n;
+    }
+    return n;
+  }
+  const int64_t q0 = i / p->q_block * p->q_block;
+  const int64_t q1 = q0 + p->q_block < Lk ? q0 + p->q_block : Lk;
+  for (int64_t t = 0; t < q0; t += w) {
+    kb[n] = t; ke[n] = t + w < q0 ? t + w : q0; stage2[n] = 0; ++n;
+  }
+  for (int64_t t = q0; t < q1; t += w) {
+    kb[n] = t; ke[n] = t + w < q1 ? t + w : q1; stage2[n] = 1; ++n;
+  }
+  return n;
+}
+
+/* One query row of one head: out[c], c < d, as binary32 values (the output
+ * type's rounding applied by the caller).  The two matrix multiplications
+ * fold their products in groups of 32 (the 16x16x32 instruction) under the
+ * chosen model: the score from +0 with the accumulator carried over the head
+ * dimension; the block's P.V with the rescaled output row as the accumulator
+ * (pv_fma) or from +0 and then added. */
+static void attn_row(const dgo_attn_params* p, const uint16_t* q, const uint16_t* K, const uint16_t* V,
+                     int64_t i, int64_t Lk, int64_t d, float qk_scale, float* O, float* s, float* pr,
+                     uint16_t* pb, uint16_t* abuf, uint16_t* bbuf, int64_t* kb, int64_t* ke, int* st2,
+                     float* out) {
+  const int64_t nb = attn_blocks(p, i, Lk, kb, ke, st2);
+  float m = -INFINITY, l = 0.0f;
+  for (int64_t c = 0; c < d; ++c) O[c] = 0.0f;
+  for (int64_t b = 0; b < nb; ++b) {
+    const int64_t n = ke[b] - kb[b];
+    /* scores of the block's keys, scaled (log2 e folded into qk_scale) */
+    float bm = -INFINITY;
+    for (int64_t u = 0; u < n; ++u) {
+      const int64_t t = kb[b] + u;
+      float acc = 0.0f;
+      for (int64_t c0 = 0; c0 < d; c0 += 32) {
+        int g = (int)(d - c0 < 32 ? d - c0 : 32);
+        acc = group_update_fmt(0, p->model, acc, q + c0, K + t * d + c0, g, 32, 1);
+      }
+      float v = acc * qk_scale;
+      if (st2[b] && t > i) v = v + ATTN_MASK_OFFSET;
+      s[u] = v;
+      if (v > bm) bm = v;
+    }
+    const float mn = m > bm ? m : bm;
+    const float alpha = dgo_exp2(m - mn);
+    for (int64_t u = 0; u < n; ++u) {
+      pr[u] = dgo_exp2(s[u] - mn);
+      pb[u] = dgo_f32_to_bf16(pr[u]);   /* narrowed before it meets V */
+    }
+    const float rs = p->block_sum == DGO_TREE ? dgo_tree(pr, (int)n, 0) : chain(pr, (int)n, 0);
+    l = p->l_fma ? fmaf(alpha, l, rs) : alpha * l + rs;
+    for (int64_t c = 0; c < d; ++c) {
+      const float base = alpha * O[c];
+      float acc = p->pv_fma ? base : 0.0f;
+      for (int64_t u0 = 0; u0 < n; u0 += 32) {
+        int g = (int)(n - u0 < 32 ? n - u0 : 32);
+        for (int u = 0; u < g; ++u) {
+          abuf[u] = pb[u0 + u];
+          bbuf[u] = V[(kb[b] + u0 + u) * d + c];
+        }
+        acc = group_update_fmt(0, p->model, acc, abuf, bbuf, g, 32, 1);
+      }
+      O[c] = p->pv_fma ? acc : base + acc;
+    }
+    m = mn;
+  }
+  if (p->final_recip) {
+    const float r = 1.0f / l;
+    for (int64_t c = 0; c < d; ++c) out[c] = O[c] * r;
+  } else {
+    for (int64_t c = 0; c < d; ++c) out[c] = O[c] / l;
+  }
+}
+
+static int attn_check(const dgo_attn_params* p, int64_t H, int64_t Lq, int64_t Lk, int64_t d) {
+  if (p->key_block < 1 || (p->causal && p->q_block < 1)) return 1;
+  if (p->block_sum != DGO_SEQ && p->block_sum != DGO_TREE) return 1;
+  if (p->model != DGO_MODEL_EXACT && p->model != DGO_MODEL_GFX950) return 1;
+  if (H < 0 || Lq < 0 || d < 1 || Lk < 1) return 3;
+  if (p->causal && Lq != Lk) return 3;
+  return 0;
+}
+
+#define ATTN_SCRATCH(Lk, d)                                                              \
+  float* O_ = (float*)malloc(sizeof(float) * (size_t)(d));                               \
+  float* s_ = (float*)malloc(sizeof(float) * (size_t)(Lk));                              \
+  float* pr_ = (float*)malloc(sizeof(float) * (size_t)(Lk));                             \
+  uint16_t* pb_ = (uint16_t*)malloc(sizeof(uint16_t) * (size_t)(Lk));                    \
+  uint16_t ab_[32], bb_[32];                                                             \
+  int64_t* kb_ = (int64_t*)malloc(sizeof(int64_t) * (size_t)(Lk + 2));                   \
+  int64_t* ke_ = (int64_t*)malloc(sizeof(int64_t) * (size_t)(Lk + 2));                   \
+  int* st_ = (int*)malloc(sizeof(int) * (size_t)(Lk + 2));                               \
+  float* row_ = (float*)malloc(sizeof(float) * (size_t)(d))
+#define ATTN_SCRATCH_FREE() free(O_); free(s_); free(pr_); free(pb_); free(kb_); free(ke_); free(st_); free(row_)
+
+int dgo_attention(const dgo_attn_params* p, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                  void* O, int64_t H, int64_t Lq, int64_t Lk, int64_t d, float qk_scale, int nthreads) {
+  int st = attn_check(p, H, Lq, Lk, d);
+  if (st) return st;
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    ATTN_SCRATCH(Lk, d);
+#pragma omp for schedule(dynamic, 4) collapse(2)
+    for (int64_t h = 0; h < H; ++h)
+      for (int64_t i = 0; i < Lq; ++i) {
+        attn_row(p, Q + (h * Lq + i) * d, K + h * Lk * d, V + h * Lk * d, i, Lk, d, qk_scale, O_, s_, pr_,
+                 pb_, ab_, bb_, kb_, ke_, st_, row_);
+        for (int64_t c = 0; c < d; ++c) {
+          const int64_t o = (h * Lq + i) * d + c;
+          if (p->out_bf16) ((uint16_t*)O)[o] = dgo_f32_to_bf16(row_[c]);
+          else ((float*)O)[o] = row_[c];
+        }
+      }
+    ATTN_SCRATCH_FREE();
+  }
+  return 0;
+}
+
+int dgo_attention_rows(const dgo_attn_params* p, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                       int64_t H, int64_t Lq, int64_t Lk, int64_t d, float qk_scale, const int64_t* hh,
+                       const int64_t* ii, int64_t n, float* out, int nthreads) {
+  int st = attn_check(p, H, Lq, Lk, d);
+  if (st) return st;
+  for (int64_t r = 0; r < n; ++r)
+    if (hh[r] < 0 || hh[r] >= H || ii[r] < 0 || ii[r] >= Lq) return 1;
+  if (nthreads < 1) nthreads = 1;
+#pragma omp parallel num_threads(nthreads)
+  {
+    ATTN_SCRATCH(Lk, d);
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n; ++r) {
+      const int64_t h = hh[r], i = ii[r];
+      attn_row(p, Q + (h * Lq + i) * d, K + h * Lk * d, V + h * Lk * d, i, Lk, d, qk_scale, O_, s_, pr_, pb_,
+               ab_, bb_, kb_, ke_, st_, row_);
+      for (int64_t c = 0; c < d; ++c) out[r * d + c] = p->out_bf16 ? rnbf(row_[c]) : row_[c];
+    }
+    ATTN_SCRATCH_FREE();
+  }
+  return 0;
+}

@@ -179,6 +179,52 @@ float dgo_silu(float z);
 /* e[i] = dgo_exp(x), s[i] = dgo_silu(x) for the binary32 x with bits start + i. */
 void dgo_exp_silu_range(uint64_t start, int64_t count, float* e, float* s, int nthreads);
 
+/* ---------------------------------------------------------------- attention
+ *
+ * The reduction order of one attention head (App. F): per query row i, the
+ * keys are walked in blocks; the kernel carries a running maximum m, a
+ * denominator l and an output row O (binary32).  At block j (keys kb..ke-1):
+ *   s_t   = RN32(score_t * qk_scale), score_t = q_i . k_t by the first matrix
+ *           multiplication (groups of 32 over the head dimension from +0,
+ *           accumulator carried); a masked key adds ATTN_MASK_OFFSET (-1e6);
+ *   mn    = max(m, max_t s_t)            (exact);
+ *   alpha = exp2(RN32(m - mn)),  p_t = exp2(RN32(s_t - mn))  (dgo_exp2);
+ *   rs    = the block's p_t summed by block_sum: chain in key order, or the
+ *           balanced tree over the block's positions in key order;
+ *   l     = fma(alpha, l, rs)  (l_fma)  or  RN32(RN32(alpha l) + rs);
+ *   O_c   = the block's P.V over its keys in groups of 32 from the block
+ *           start, p narrowed to bf16, with RN32(alpha O_c) as the
+ *           accumulator (pv_fma) or from +0 and then added to RN32(alpha O_c);
+ *   m     = mn;
+ * starting from m = -inf, l = +0, O = +0; finally out_c = RN_out(O_c / l)
+ * or, with final_recip, RN_out(O_c * RN32(1 / l)).  The blocks: see
+ * attn_blocks in dgo.c (unmasked: width key_block from key 0; causal: the
+ * split at the multiples of q_block). */
+typedef struct {
+  int32_t key_block;     /* w, keys per block (BLOCK_N) */
+  int32_t causal;        /* 1: key t visible to query i iff t <= i (Lq = Lk) */
+  int32_t q_block;       /* BLOCK_M: where the masked stage starts (causal only) */
+  int32_t block_sum;     /* DGO_SEQ or DGO_TREE */
+  int32_t pv_fma;        /* 1: rescaled output row is the P.V accumulator */
+  int32_t l_fma;         /* 1: the denominator update is one fused multiply-add */
+  int32_t final_recip;   /* 0: out = O / l;  1: out = O * (1 / l) */
+  int32_t out_bf16;      /* output stored as bf16 */
+  int32_t model;         /* DGO_MODEL_* for both matrix multiplications */
+} dgo_attn_params;
+
+/* Q: H x Lq x d, K and V: H x Lk x d, bf16 row-major; O: H x Lq x d (fp32
+ * values or bf16 bits).  Status 1: invalid parameters; 3: shapes (Lk = 0,
+ * d = 0, or a causal mask with Lq != Lk). */
+int dgo_attention(const dgo_attn_params* p, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                  void* O, int64_t H, int64_t Lq, int64_t Lk, int64_t d, float qk_scale, int nthreads);
+/* Selected rows (hh[r], ii[r]): out[r * d + c] as binary32 (bf16 outputs widened). */
+int dgo_attention_rows(const dgo_attn_params* p, const uint16_t* Q, const uint16_t* K, const uint16_t* V,
+                       int64_t H, int64_t Lq, int64_t Lk, int64_t d, float qk_scale, const int64_t* hh,
+                       const int64_t* ii, int64_t n, float* out, int nthreads);
+/* 2^x by the library's fixed steps (see dgo.c), and over a range of bit patterns. */
+float dgo_exp2(float x);
+void dgo_exp2_range(uint64_t start, int64_t count, float* out, int nthreads);
+
 /* Cut plan for (K, params): writes S+1 cut points to cuts (caller provides
  * split_k + 1 slots).  Returns 0 or a status. */
 int dgo_plan_cuts(const dgo_params* p, int64_t K, int64_t* cuts);

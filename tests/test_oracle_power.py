@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
+from tests import test_oracle_attention as attn
 from tests import test_oracle_pins as pins
 
 HERE = os.path.dirname(os.path.abspath(oracle.__file__))
@@ -78,6 +79,26 @@ MUTANTS = {
     "merge rounded to bf16 only at the end": (
         "for (int k = 1; k < n; ++k) { s = s + v[k]; if (bf16_round) s = rnbf(s); }",
         "for (int k = 1; k < n; ++k) { s = s + v[k]; }\n  if (bf16_round) s = rnbf(s);"),
+    "attention rescale skipped": ("const float alpha = dgo_exp2(m - mn);",
+                                  "const float alpha = m == -INFINITY ? 0.0f : 1.0f;"),
+    "attention key block one wider": ("const int64_t w = p->key_block;\n  int64_t n = 0;",
+                                      "const int64_t w = p->key_block + 1;\n  int64_t n = 0;"),
+    "attention probabilities truncated to bf16": ("pb[u] = dgo_f32_to_bf16(pr[u]);",
+                                                  "pb[u] = (uint16_t)(f2u(pr[u]) >> 16);"),
+    "attention denominator fma ignored": ("l = p->l_fma ? fmaf(alpha, l, rs) : alpha * l + rs;",
+                                          "l = alpha * l + rs;"),
+    "attention final reciprocal ignored": ("if (p->final_recip) {\n    const float r = 1.0f / l;",
+                                           "if (0) {\n    const float r = 1.0f / l;"),
+    "attention causal split on the key grid": ("const int64_t q0 = i / p->q_block * p->q_block;",
+                                               "const int64_t q0 = i / p->key_block * p->key_block;"),
+    "attention mask offset left out": ("if (st2[b] && t > i) v = v + ATTN_MASK_OFFSET;", "if (0) v = v;"),
+    "attention block sum always a chain": (
+        "const float rs = p->block_sum == DGO_TREE ? dgo_tree(pr, (int)n, 0) : chain(pr, (int)n, 0);",
+        "const float rs = chain(pr, (int)n, 0);"),
+    "attention P.V restarts from zero": ("float acc = p->pv_fma ? base : 0.0f;", "float acc = 0.0f;"),
+    "attention score scaled before the dot product ends": ("float v = acc * qk_scale;",
+                                                           "float v = acc * qk_scale * 1.0000001f;"),
+    "exp2 polynomial one term short": ("  p = fmaf(p, f, c6);\n", ""),
     "binary16 exponent bias off by one": ("eb = f16 ? 5 : 8, bias = f16 ? 15 : 127;",
                                           "eb = f16 ? 5 : 8, bias = f16 ? 14 : 127;"),
     "binary16 product scale off by one": ("const int fb2 = 2 * op_frac(f16);",
@@ -115,6 +136,12 @@ CHECKS = [
     lambda: pins.test_bf16_parts_and_merges_hand_examples(),
     lambda: pins.test_bf16_parts_and_merges_match_rationals(4, "tree", "bf16", "bf16"),
     lambda: pins.test_f16_decoding_matches_numpy_on_every_pattern(),
+    lambda: attn.test_exp2_exact_points_and_edges(),
+    lambda: attn.test_exp2_accuracy_dense_sweep(),
+    lambda: [attn.test_recurrence_matches_rationals(di) for di in (0, 21, 45, 66, 93, 120)],
+    lambda: [attn.test_equal_scores_give_the_mean_of_the_visible_values(di) for di in (0, 44, 92)],
+    lambda: [attn.test_one_dominant_key_returns_its_value_row(di) for di in (1, 53, 93)],
+    lambda: attn.test_query_block_enters_only_causal_answers_off_the_key_grid(),
     lambda: pins.test_f16_exact_dot_is_the_rational_sum_rounded_once(),
     lambda: pins.test_f16_chunk_model_hand_examples(),
     lambda: pins.test_f16_chunk_model_equals_exact_when_window_holds_everything(),
