@@ -338,6 +338,74 @@ dg_status dg_layernorm(const dg_desc* d, const float* X, const void* w, const vo
 dg_status dg_softmax(const dg_desc* d, const float* X, void* Y, int64_t rows, int64_t cols,
                      void* stream);
 
+/* ------------------------------------------------------------- attention
+ *
+ * The reduction order of one attention head (App. F).  Per query row the
+ * keys are walked in blocks; the row carries a running maximum m, a
+ * denominator l and an output row O in binary32, starting from m = -inf,
+ * l = +0, O = +0.  At a block of keys kb .. ke-1:
+ *   s_t   = RN32(score_t * qk_scale), score_t = q . k_t over the head
+ *           dimension in groups of 32 (the 16x16x32 instruction, chunks of 8
+ *           in increasing order) from +0; under a causal mask a key above the
+ *           diagonal in the masked stage gets s_t (+) -1e6 (its probability
+ *           underflows to zero);
+ *   mn    = max(m, max_t s_t);  alpha = exp2(m - mn);  p_t = exp2(s_t - mn),
+ *           exp2 the library's own binary32 base-two exponential (Cody-Waite
+ *           style split x = n + f, degree-7 polynomial for 2^f, exact scaling);
+ *           the caller folds log2 e into qk_scale;
+ *   rs    = the block's p_t summed in the order block_sum names: DG_SEQ, a
+ *           chain in key order, or DG_TREE, the balanced tree over the
+ *           block's positions in key order;
+ *   l     = RN32(alpha l) (+) rs, or fma(alpha, l, rs) when l_fma;
+ *   O_c   = P~ . V over the block's keys in groups of 32 from the block start,
+ *           P~ = p narrowed to p_dtype before it meets V, with RN32(alpha O_c)
+ *           as the accumulator (pv_fma) or from +0 and then added to it;
+ *   m     = mn.
+ * The answer is O_c / l per element, or O_c * RN32(1 / l) (final), rounded
+ * to out_dtype.  The blocks: unmasked, width key_block from key 0 (the last
+ * one shorter); causal (key t visible to query i iff t <= i, Lq = Lk), with
+ * q0 = (i / q_block) q_block and q1 = min(q0 + q_block, Lk): [0, q0) cut into
+ * blocks of key_block from key 0, the last ending at q0, then [q0, q1) cut
+ * into blocks of key_block from q0, the last ending at q1, in which the keys
+ * above the diagonal are masked.  So q_block (BLOCK_M) takes part in a
+ * causal answer whenever it is not a multiple of key_block. */
+enum { DG_ATTN_DIV = 0, DG_ATTN_RECIP = 1 };
+
+typedef struct {
+  uint32_t struct_size;   /* sizeof(dg_attn_params) */
+  int32_t key_block;      /* w, keys per block (BLOCK_N), >= 1 */
+  int32_t causal;         /* 0: no mask; 1: causal (Lq = Lk) */
+  int32_t q_block;        /* BLOCK_M, >= 1: where the masked stage starts (causal) */
+  int32_t block_sum;      /* DG_SEQ or DG_TREE: the row sum of a block's probabilities */
+  int32_t p_dtype;        /* DG_BF16: the type the probabilities are narrowed to */
+  int32_t pv_fma;         /* 1: the rescaled output row is the P.V accumulator */
+  int32_t l_fma;          /* 1: the denominator update is one fused multiply-add */
+  int32_t final_div;      /* DG_ATTN_DIV: O / l;  DG_ATTN_RECIP: O * (1 / l) */
+  int32_t out_dtype;      /* DG_F32 or DG_BF16 */
+} dg_attn_params;
+
+typedef struct dg_attn_desc dg_attn_desc; /* opaque, immutable */
+
+/* Validate p and build an attention descriptor (free with
+ * dg_attn_desc_destroy).  DG_ERR_INVALID for NULL arguments, a small
+ * struct_size or a field out of range; DG_ERR_UNSUPPORTED for an order this
+ * build cannot run: key_block other than 32, 64 or 128, p_dtype other than
+ * bf16, or a causal q_block that is not a multiple of 16. */
+dg_status dg_attn_desc_create(const dg_attn_params* p, dg_attn_desc** out);
+void dg_attn_desc_destroy(dg_attn_desc* d);
+
+/* O = attention(Q, K, V) in the descriptor's order, for H independent heads.
+ *   Q: device, H x Lq x d bf16;  K, V: device, H x Lk x d bf16;  O: device,
+ *   H x Lq x d of out_dtype (written, never read); all row-major and 16-byte
+ *   aligned.  d is 64 or 128.  qk_scale multiplies each score (fold log2 e
+ *   and 1 / sqrt(d) into it).
+ * H = 0 or Lq = 0 is a no-op.  DG_ERR_SHAPE for Lk < 1, H > 65535, or a
+ * causal descriptor with Lq != Lk; DG_ERR_UNSUPPORTED for another d;
+ * DG_ERR_ALIGN for a pointer not 16-byte aligned.  One launch on stream; no
+ * workspace. */
+dg_status dg_attention(const dg_attn_desc* d, const void* Q, const void* K, const void* V, void* O,
+                       int64_t H, int64_t Lq, int64_t Lk, int64_t dim, float qk_scale, void* stream);
+
 /* Static text for a status code (never NULL; unknown codes give
  * "unknown status"). */
 const char* dg_strerror(dg_status s);
@@ -347,7 +415,7 @@ const char* dg_strerror(dg_status s);
  * built against an earlier header must not pass its dg_knobs to this one.
  * 0.3.0 (300) added dg_desc_params.in_dtype (a smaller struct_size is
  * rejected) and knob kernel 10.  0.4.0 (400) added dg_gemm_noalloc and
- * DG_ERR_SCRATCH. */
+ * DG_ERR_SCRATCH, and the attention descriptor and dg_attention. */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

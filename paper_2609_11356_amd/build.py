@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdg.so")
-SOURCES = ["dg_api.cpp", "dg_gemm.hip", "dg_rowsum.hip"]
+SOURCES = ["dg_api.cpp", "dg_gemm.hip", "dg_rowsum.hip", "dg_attn.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -ffp-contract=off: no multiply-add is fused unless the source spells it out.

@@ -733,4 +733,62 @@ dg_status dg_rmsnorm(const dg_desc* d, const float* X, const void* w, float eps,
   return DG_OK;
 }
 
+dg_status dg_attn_desc_create(const dg_attn_params* p, dg_attn_desc** out) {
+  if (!p || !out) return DG_ERR_INVALID;
+  *out = nullptr;
+  if (p->struct_size < sizeof(dg_attn_params)) return DG_ERR_INVALID;
+  if (p->key_block < 1 || !in(p->causal, 0, 1) || (p->causal && p->q_block < 1)) return DG_ERR_INVALID;
+  if (p->block_sum != DG_SEQ && p->block_sum != DG_TREE) return DG_ERR_INVALID;
+  if (!in(p->p_dtype, DG_F32, DG_BF16) || !in(p->pv_fma, 0, 1) || !in(p->l_fma, 0, 1)) return DG_ERR_INVALID;
+  if (!in(p->final_div, DG_ATTN_DIV, DG_ATTN_RECIP) || !in(p->out_dtype, DG_F32, DG_BF16)) return DG_ERR_INVALID;
+  // the bf16 instruction takes the probabilities at bf16; the kernel's blocks
+  // are whole 32-key instruction steps; a workgroup's 16-row waves share one split
+  if (p->p_dtype != DG_BF16) return DG_ERR_UNSUPPORTED;
+  if (p->key_block != 32 && p->key_block != 64 && p->key_block != 128) return DG_ERR_UNSUPPORTED;
+  if (p->causal && p->q_block % 16 != 0) return DG_ERR_UNSUPPORTED;
+  dg_attn_desc* d = new (std::nothrow) dg_attn_desc;
+  if (!d) return DG_ERR_NOMEM;
+  d->p = *p;
+  d->p.struct_size = sizeof(dg_attn_params);
+  if (!d->p.causal) d->p.q_block = 0;   // not part of an unmasked order
+  *out = d;
+  return DG_OK;
+}
+
+void dg_attn_desc_destroy(dg_attn_desc* d) { delete d; }
+
+dg_status dg_attention(const dg_attn_desc* d, const void* Q, const void* K, const void* V, void* O, int64_t H,
+                       int64_t Lq, int64_t Lk, int64_t dim, float qk_scale, void* stream) {
+  if (!d) return DG_ERR_INVALID;
+  if (H < 0 || Lq < 0 || Lk < 0 || dim < 0) return DG_ERR_SHAPE;
+  if (!dg::attn_supported(dim, d->p.key_block)) return DG_ERR_UNSUPPORTED;
+  if (H == 0 || Lq == 0) return DG_OK;
+  if (Lk < 1 || H > 65535 || (d->p.causal && Lq != Lk)) return DG_ERR_SHAPE;
+  if ((Lq + 15) / 16 > 0x7fffffff) return DG_ERR_SHAPE;
+  if (!Q || !K || !V || !O) return DG_ERR_INVALID;
+  if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16)) return DG_ERR_ALIGN;
+  dg::AttnArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.Q = (const uint16_t*)Q;
+  a.K = (const uint16_t*)K;
+  a.V = (const uint16_t*)V;
+  a.O = O;
+  a.H = H;
+  a.Lq = Lq;
+  a.Lk = Lk;
+  a.qk_scale = qk_scale;
+  a.causal = d->p.causal;
+  a.q_block = d->p.q_block;
+  a.block_tree = d->p.block_sum == DG_TREE;
+  a.pv_fma = d->p.pv_fma;
+  a.l_fma = d->p.l_fma;
+  a.final_recip = d->p.final_div == DG_ATTN_RECIP;
+  a.out_bf16 = d->p.out_dtype == DG_BF16;
+  // four waves (64 rows) per workgroup when the causal split allows it
+  int nw = 4;
+  while (a.causal && a.q_block % (16 * nw) != 0) nw /= 2;
+  if (dg::launch_attention(a, dim, d->p.key_block, nw, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
+  return DG_OK;
+}
+
 }  // extern "C"

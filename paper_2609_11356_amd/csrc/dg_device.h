@@ -71,6 +71,31 @@ __device__ __forceinline__ float exp_f32(float x_in) {
   return x_in != x_in ? x_in + x_in : e;
 }
 
+// 2^x in binary32 by a fixed sequence of steps (the base-two exponential of
+// the attention recurrence, whose score scale carries log2 e):
+//   n  = rint(x),  f = x - n          (exact, |f| <= 1/2)
+//   p  = sum_{k=0..7} c_k f^k,  c_k = RN32((ln 2)^k / k!)   (Horner, fma)
+//   2^x = p * 2^n                       (one rounding: the scaling is exact
+//                                        but for the last step)
+// on x clamped into [-151, 128] (x itself inside): at the clamp ends the
+// steps give 0 (2^-151 rounds to zero) and +inf by themselves; a NaN is
+// selected at the end, so there are no branches.
+__device__ __forceinline__ float exp2_f32(float x_in) {
+  const float x = __builtin_fminf(__builtin_fmaxf(x_in, -151.0f), 128.0f);
+  const float n = __builtin_rintf(x);
+  const float f = x - n;
+  float p = 0x1.ffcbfcp-17f;                  // (ln 2)^7 / 7!
+  p = __builtin_fmaf(p, f, 0x1.430912p-13f);  // (ln 2)^6 / 6!
+  p = __builtin_fmaf(p, f, 0x1.5d87fep-10f);  // (ln 2)^5 / 5!
+  p = __builtin_fmaf(p, f, 0x1.3b2ab6p-7f);   // (ln 2)^4 / 4!
+  p = __builtin_fmaf(p, f, 0x1.c6b08ep-5f);   // (ln 2)^3 / 3!
+  p = __builtin_fmaf(p, f, 0x1.ebfbep-3f);    // (ln 2)^2 / 2!
+  p = __builtin_fmaf(p, f, 0x1.62e43p-1f);    // ln 2
+  p = __builtin_fmaf(p, f, 1.0f);
+  const float e = __builtin_ldexpf(p, (int)n);
+  return x_in != x_in ? x_in + x_in : e;
+}
+
 // SiLU z * sigmoid(z) = z / (1 + exp(-z)), correctly rounded division.
 __device__ __forceinline__ float silu_f32(float z) {
   float e = exp_f32(-z);

@@ -13,6 +13,10 @@ struct dg_desc {
   char sig[2048];              // canonical order text (every cut written out)
 };
 
+struct dg_attn_desc {
+  dg_attn_params p;            // validated copy
+};
+
 namespace dg {
 
 // Everything a GEMM launch needs, passed by value as the kernel argument.
@@ -72,6 +76,21 @@ struct ColsumArgs {
   int64_t M, N;
   int32_t out_bf16;
 };
+
+struct AttnArgs {
+  const uint16_t* Q;             // H x Lq x d bf16
+  const uint16_t* K;             // H x Lk x d bf16
+  const uint16_t* V;             // H x Lk x d bf16
+  void* O;                       // H x Lq x d, fp32 or bf16
+  int64_t H, Lq, Lk;
+  float qk_scale;
+  int32_t causal, q_block;
+  int32_t block_tree, pv_fma, l_fma, final_recip, out_bf16;
+};
+
+bool attn_supported(int64_t d, int key_block);
+// nw: waves (16 query rows each) per workgroup, 1, 2 or 4
+hipError_t launch_attention(const AttnArgs& a, int64_t d, int key_block, int nw, hipStream_t s);
 
 // This device's copy of the fixed split-K scratch array of dg_gemm_noalloc
 // (DG_NOALLOC_SCRATCH_BYTES), looked up once per device with that device

@@ -48,6 +48,12 @@ class dg_knobs(ctypes.Structure):
                 ("slab_k", ctypes.c_int32), ("split_n", ctypes.c_int32)]
 
 
+class dg_attn_params(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_uint32)] + [
+        (n, ctypes.c_int32) for n in ("key_block", "causal", "q_block", "block_sum", "p_dtype", "pv_fma", "l_fma",
+                                      "final_div", "out_dtype")]
+
+
 _lib = None
 
 
@@ -72,6 +78,12 @@ def lib():
         L.dg_softmax.argtypes = [vp, vp, vp, i64, i64, vp]
         L.dg_layernorm.argtypes = [vp, vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_gemm_colsum.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp]
+        L.dg_attn_desc_create.argtypes = [ctypes.POINTER(dg_attn_params), ctypes.POINTER(vp)]
+        L.dg_attn_desc_create.restype = ctypes.c_int
+        L.dg_attn_desc_destroy.argtypes = [vp]
+        L.dg_attn_desc_destroy.restype = None
+        L.dg_attention.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, i64, ctypes.c_float, vp]
+        L.dg_attention.restype = ctypes.c_int
         L.dg_strerror.argtypes = [ctypes.c_int]
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
@@ -341,8 +353,73 @@ def dg_softmax(desc: Desc, X, Y, rows=None, cols=None, stream=None):
     return Y
 
 
+class AttnDesc:
+    """An immutable attention descriptor (dg_attn_desc_create /
+    dg_attn_desc_destroy).  Fields: key_block (BLOCK_N), causal (0/1), q_block
+    (BLOCK_M, causal only), block_sum ("seq" | "tree"), p_dtype ("bf16"),
+    pv_fma (0/1), l_fma (0/1), final ("div" | "recip"), out ("f32" | "bf16")."""
+
+    DEFAULTS = dict(key_block=64, causal=0, q_block=64, block_sum="tree", p_dtype="bf16", pv_fma=1, l_fma=0,
+                    final="div", out="bf16")
+
+    def __init__(self, **fields):
+        unknown = set(fields) - set(self.DEFAULTS) - {"model"}
+        if unknown:
+            raise ValueError("unknown attention fields: %s" % sorted(unknown))
+        if fields.get("model", "gfx950") != "gfx950":
+            raise ValueError("libdg realises the gfx950 MFMA arithmetic only")
+        f = dict(self.DEFAULTS)
+        f.update({k: v for k, v in fields.items() if k != "model"})
+        self.fields = f
+        p = dg_attn_params()
+        p.struct_size = ctypes.sizeof(dg_attn_params)
+        p.key_block = int(f["key_block"])
+        p.causal = int(f["causal"])
+        p.q_block = int(f["q_block"])
+        p.block_sum = COMBINE[f["block_sum"]]
+        p.p_dtype = DTYPE[f["p_dtype"]]
+        p.pv_fma = int(f["pv_fma"])
+        p.l_fma = int(f["l_fma"])
+        p.final_div = {"div": 0, "recip": 1}[f["final"]]
+        p.out_dtype = DTYPE[f["out"]]
+        h = ctypes.c_void_p()
+        st = lib().dg_attn_desc_create(ctypes.byref(p), ctypes.byref(h))
+        if st != DG_OK:
+            raise DgError(st, "dg_attn_desc_create")
+        self.handle = h
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h and _lib is not None:
+            _lib.dg_attn_desc_destroy(h)
+            self.handle = None
+
+
+def dg_attention(desc: AttnDesc, Q, K, V, O, qk_scale, H=None, Lq=None, Lk=None, dim=None, stream=None):
+    """O = attention in the descriptor's order: Q (H, Lq, d), K and V (H, Lk,
+    d) bf16, O (H, Lq, d) of the descriptor's output type, contiguous on the
+    GPU (or raw device addresses with the sizes given)."""
+    import torch
+    if isinstance(Q, torch.Tensor):
+        _need(Q.dtype == torch.bfloat16 and K.dtype == torch.bfloat16 and V.dtype == torch.bfloat16,
+              "Q, K and V must be bf16")
+        _need(Q.dim() == 3 and K.dim() == 3 and V.dim() == 3 and O.dim() == 3, "Q, K, V and O are (H, L, d)")
+        H, Lq, dim = Q.shape
+        Lk = K.shape[1]
+        _need(tuple(K.shape) == (H, Lk, dim) and tuple(V.shape) == (H, Lk, dim), "K and V must be (H, Lk, d)")
+        _need(tuple(O.shape) == (H, Lq, dim), "O must be (H, Lq, d)")
+        _need(O.dtype == _out_dtype(desc), "O dtype must match the descriptor's output type")
+        _need(all(t.is_contiguous() for t in (Q, K, V, O)), "Q, K, V and O must be contiguous")
+        _on_device(Q, K, V, O)
+    st = lib().dg_attention(desc.handle, _ptr(Q), _ptr(K), _ptr(V), _ptr(O), H, Lq, Lk, dim,
+                            ctypes.c_float(qk_scale), _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_attention")
+    return O
+
+
 def exported_symbols():
     """Names of the entry points include/dg.h declares."""
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc",
             "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
-            "dg_version"]
+            "dg_version", "dg_attn_desc_create", "dg_attn_desc_destroy", "dg_attention"]

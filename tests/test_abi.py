@@ -140,6 +140,36 @@ def test_signature_writes_every_cut(dg):
     assert lib.dg_desc_signature(d.handle, buf, len(a) + 1) == dg.DG_OK and buf.value.decode() == a
 
 
+def test_attention_descriptor_validation(dg):
+    """Attention descriptors: fields out of range are invalid; orders this
+    build cannot run are unsupported; calls are checked before any launch."""
+    for bad in (dict(key_block=0), dict(causal=2), dict(block_sum="carry"), dict(pv_fma=2), dict(final="half")):
+        with pytest.raises((dg.DgError, KeyError)) as e:
+            dg.AttnDesc(**bad)
+        if isinstance(e.value, dg.DgError):
+            assert e.value.status == dg.DG_ERR_INVALID, bad
+    for bad in (dict(key_block=16), dict(key_block=96), dict(p_dtype="f32"), dict(causal=1, q_block=40)):
+        with pytest.raises(dg.DgError) as e:
+            dg.AttnDesc(**bad)
+        assert e.value.status == dg.DG_ERR_UNSUPPORTED, bad
+    for ok in (dict(key_block=32, causal=1, q_block=48), dict(key_block=128, q_block=1)):
+        dg.AttnDesc(**ok)
+    import torch
+    if torch.cuda.is_available():
+        return
+    lib = dg.lib()
+    a = dg.AttnDesc()
+    c = dg.AttnDesc(causal=1, q_block=64)
+    assert lib.dg_attention(a.handle, 16, 16, 16, 16, 0, 8, 8, 64, 1.0, None) == dg.DG_OK
+    assert lib.dg_attention(a.handle, 16, 16, 16, 16, 2, 8, 0, 64, 1.0, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_attention(a.handle, 16, 16, 16, 16, 2, 8, 8, 96, 1.0, None) == dg.DG_ERR_UNSUPPORTED
+    assert lib.dg_attention(c.handle, 16, 16, 16, 16, 2, 8, 9, 64, 1.0, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_attention(a.handle, 16, 24, 16, 16, 2, 8, 8, 64, 1.0, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_attention(a.handle, None, 16, 16, 16, 2, 8, 8, 64, 1.0, None) == dg.DG_ERR_INVALID
+    assert lib.dg_attention(None, 16, 16, 16, 16, 2, 8, 8, 64, 1.0, None) == dg.DG_ERR_INVALID
+    assert lib.dg_attention(a.handle, 16, 16, 16, 16, 65536, 8, 8, 64, 1.0, None) == dg.DG_ERR_SHAPE
+
+
 def test_binding_refuses_inconsistent_tensors(dg):
     """The binding checks shapes, dtypes and layout with ValueError (not
     assert, so python -O keeps them) before the library is called; CPU

@@ -1,6 +1,6 @@
 """The library's device exp and SiLU (the functions the fused epilogue and
-the softmax kernels call) against the CPU oracle's dgo_exp / dgo_silu on
-every binary32 input, bit for bit (NaNs compared as a class).  The exp is
+the softmax kernels call) and exp2 (the attention kernel's) against the CPU
+oracle's dgo_exp / dgo_silu / dgo_exp2 on every binary32 input, bit for bit (NaNs compared as a class).  The exp is
 the library's own fixed sequence of steps (Cody-Waite reduction, degree-7
 Taylor polynomial, exact power-of-two scaling), so its bits have no external
 reference: the oracle's plain C version of the same steps is what fixes
@@ -27,6 +27,8 @@ def probe():
     L.math_probe_exp_silu.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                       ctypes.c_void_p]
     L.math_probe_exp_silu.restype = ctypes.c_int
+    L.math_probe_exp2.argtypes = [ctypes.c_uint64, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p]
+    L.math_probe_exp2.restype = ctypes.c_int
     return L
 
 
@@ -57,3 +59,22 @@ def test_exp_and_silu_equal_the_oracle_on_every_binary32(probe, quarter):
                                      "device %r, oracle %r" % (name, int((~ok).sum()), start, x, start + i,
                                                                got[i], want[i]))
         print("slab 0x%08x ok" % start, flush=True)
+
+
+@pytest.mark.parametrize("half", range(2))
+def test_exp2_equals_the_oracle_on_every_binary32(probe, half):
+    import torch
+    e_d = torch.empty(SLAB, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    lo = half << 31
+    for start in range(lo, lo + (1 << 31), SLAB):
+        st = probe.math_probe_exp2(start, SLAB, e_d.data_ptr(), stream)
+        assert st == 0, "probe launch failed (%d)" % st
+        got = e_d.cpu().numpy()
+        want = oracle.exp2_range(start, SLAB)
+        ok = _same(got, want)
+        if not ok.all():
+            i = int(np.nonzero(~ok)[0][0])
+            raise AssertionError("exp2 differs on %d inputs of slab 0x%08x; first bits 0x%08x: device %r, oracle %r"
+                                 % (int((~ok).sum()), start, start + i, got[i], want[i]))
+        print("exp2 slab 0x%08x ok" % start, flush=True)
