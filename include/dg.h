@@ -399,8 +399,8 @@ void dg_attn_desc_destroy(dg_attn_desc* d);
  *   H x Lq x d of out_dtype (written, never read); all row-major and 16-byte
  *   aligned.  d is 64 or 128.  qk_scale multiplies each score (fold log2 e
  *   and 1 / sqrt(d) into it).
- * H = 0 or Lq = 0 is a no-op.  DG_ERR_SHAPE for Lk < 1, H > 65535, or a
- * causal descriptor with Lq != Lk; DG_ERR_UNSUPPORTED for another d;
+ * H = 0 or Lq = 0 is a no-op.  DG_ERR_SHAPE for Lk < 1, H > 65535,
+ * Lq > 16 * 65535, or a causal descriptor with Lq != Lk; DG_ERR_UNSUPPORTED for another d;
  * DG_ERR_ALIGN for a pointer not 16-byte aligned.  One launch on stream; no
  * workspace. */
 dg_status dg_attention(const dg_attn_desc* d, const void* Q, const void* K, const void* V, void* O,

@@ -764,7 +764,7 @@ dg_status dg_attention(const dg_attn_desc* d, const void* Q, const void* K, cons
   if (!dg::attn_supported(dim, d->p.key_block)) return DG_ERR_UNSUPPORTED;
   if (H == 0 || Lq == 0) return DG_OK;
   if (Lk < 1 || H > 65535 || (d->p.causal && Lq != Lk)) return DG_ERR_SHAPE;
-  if ((Lq + 15) / 16 > 0x7fffffff) return DG_ERR_SHAPE;
+  if ((Lq + 15) / 16 > 65535) return DG_ERR_SHAPE;
   if (!Q || !K || !V || !O) return DG_ERR_INVALID;
   if (!aligned(Q, 16) || !aligned(K, 16) || !aligned(V, 16) || !aligned(O, 16)) return DG_ERR_ALIGN;
   dg::AttnArgs a;
@@ -784,10 +784,7 @@ dg_status dg_attention(const dg_attn_desc* d, const void* Q, const void* K, cons
   a.l_fma = d->p.l_fma;
   a.final_recip = d->p.final_div == DG_ATTN_RECIP;
   a.out_bf16 = d->p.out_dtype == DG_BF16;
-  // four waves (64 rows) per workgroup when the causal split allows it
-  int nw = 4;
-  while (a.causal && a.q_block % (16 * nw) != 0) nw /= 2;
-  if (dg::launch_attention(a, dim, d->p.key_block, nw, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
+  if (dg::launch_attention(a, dim, d->p.key_block, (hipStream_t)stream) != hipSuccess) return DG_ERR_HIP;
   return DG_OK;
 }
 
