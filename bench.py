@@ -473,6 +473,40 @@ def main():
         rs[name] = {"ms": round(ms, 4), "GB/s": round(by / ms / 1e6, 1),
                     "frac_hbm": round(by / ms / 1e6 / PEAK_HBM_GBS, 4), "what": what}
 
+    # ------------------------------------------------------------ attention
+    # 32 heads x 4096 tokens x 128 (a Llama-style head set), bf16, key
+    # blocks of 64, BLOCK_M 128, the block row sum by the balanced tree; the
+    # free-order reference is torch's scaled_dot_product_attention
+    import math
+    H_at, L_at, d_at = 32, 4096, 128
+    Q_at = inputs.normal_bf16(91, (H_at, L_at, d_at), 1.5)
+    K_at = inputs.normal_bf16(92, (H_at, L_at, d_at), 1.5)
+    V_at = inputs.normal_bf16(93, (H_at, L_at, d_at))
+    dQ_at, dK_at, dV_at = d_bf16(Q_at), d_bf16(K_at), d_bf16(V_at)
+    qs_at = float(np.float32(math.log2(math.e) / math.sqrt(d_at)))
+    O_at = {c: torch.empty((H_at, L_at, d_at), dtype=torch.bfloat16, device=dev) for c in (0, 1)}
+    desc_at = {c: dict(key_block=64, causal=c, q_block=128, block_sum="tree", out="bf16") for c in (0, 1)}
+    attn = {}
+    for c in (0, 1):
+        Da = dg.AttnDesc(**desc_at[c])
+        run_dg = lambda i, Da=Da, c=c: dg.dg_attention(Da, dQ_at, dK_at, dV_at, O_at[c], qs_at, stream=sptr)
+        q4, k4, v4 = dQ_at.unsqueeze(0), dK_at.unsqueeze(0), dV_at.unsqueeze(0)
+        run_free = lambda i, c=c: torch.nn.functional.scaled_dot_product_attention(q4, k4, v4, is_causal=bool(c))
+        try:
+            t_dg, t_free = paired(run_dg, run_free, max(5, reps // 2))
+        except Exception as exc:  # the reference never conditions the library's row
+            t_dg, t_free = timeit(run_dg, max(5, reps // 2)), float("nan")
+            attn["free_error"] = repr(exc)
+        run_dg(0)
+        fl = 4 * H_at * L_at * L_at * d_at * (0.5 if c else 1.0)
+        attn["causal" if c else "unmasked"] = {
+            "ms": round(t_dg, 4), "TFLOP/s": round(fl / t_dg / 1e9, 1),
+            "frac_mfma_peak": round(fl / t_dg / 1e9 / PEAK_BF16_TFLOPS, 4),
+            "sdpa_ms": round(t_free, 4), "cost_vs_sdpa": round(t_dg / t_free, 3)}
+    attn["what"] = ("dg_attention 32 heads x 4096 x 128, key blocks of 64, BLOCK_M 128, tree block sums, "
+                    "bf16; FLOPs 4 H L^2 d (half under the causal mask); reference "
+                    "torch scaled_dot_product_attention (free order), timed in alternating blocks")
+
     # ---------------------------------------------- free-order references
     # Each reference runs in alternating blocks with the dg launch it is
     # compared with (same inputs, same clock state); cost = t_dg / t_free.
@@ -608,6 +642,13 @@ def main():
     got_ln = host(Y_ln)[rr]
     checked += want_ln.size
     matched += int(np.sum(got_ln == want_ln))
+    for c in (0, 1):
+        hh = rng.integers(0, H_at, 8)
+        ii = rng.integers(0, L_at, 8)
+        want_at = inputs.f32_to_bf16_bits(oracle.attention_rows(desc_at[c], Q_at, K_at, V_at, qs_at, hh, ii))
+        got_at = host(O_at[c])[hh, ii]
+        checked += want_at.size
+        matched += int(np.sum(got_at == want_at))
 
     clock.stop()
 
@@ -665,6 +706,7 @@ def main():
         "scalar_path": scal,
         "tile_tree_and_fma0": tree_rows,
         "f16_mlp": f16_mlp,
+        "attention": attn,
         "free_order": free,
         "hipblaslt_order": vendor,
         "bit_match": {"checked": checked, "matched": matched,

@@ -49,6 +49,21 @@ __device__ __forceinline__ float butterfly_partner(float x) {
   else return __shfl_xor(x, 32, 64);
 }
 
+// The exact partner lane ^ M (M a power of two below 64), for butterflies
+// whose steps meet lanes that still hold different values (the count-down
+// order, whose first step pairs lanes 32 apart): xor 1 and 2 by quad_perm,
+// xor 8 by row_ror:8 (a rotation by half of a 16-lane row), xor 4 and 16 by
+// ds_swizzle's xor mode (within 32-lane groups), xor 32 by ds_bpermute.
+template <int M>
+__device__ __forceinline__ float xor_partner(float x) {
+  if constexpr (M == 1) return dpp_f32<kDppXor1>(x);
+  else if constexpr (M == 2) return dpp_f32<kDppXor2>(x);
+  else if constexpr (M == 4) return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x101F));
+  else if constexpr (M == 8) return dpp_f32<0x128>(x);   // row_ror:8
+  else if constexpr (M == 16) return __builtin_bit_cast(float, __builtin_amdgcn_ds_swizzle(__builtin_bit_cast(int, x), 0x401F));
+  else return __shfl_xor(x, 32, 64);
+}
+
 // Sum over groups of 2^K consecutive lanes, the count-up tree in lane order;
 // every lane of a group ends with its group's root.
 template <int K>

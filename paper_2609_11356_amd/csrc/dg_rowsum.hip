@@ -7,7 +7,8 @@
 // tree over the leaves padded on the right with -0 to a power of two (-0 is
 // the exact identity of binary32 addition), and the perfect tree over 64
 // lanes holding leaves 0..63 in lane order is the count-up xor butterfly
-// (offsets 1, 2, 4, .., 32).  So one wave reduces a row in passes of 64
+// (offsets 1, 2, 4, .., 32), whose lane steps are DPP and swizzle
+// permutations (dg_lanes.h).  So one wave reduces a row in passes of 64
 // leaves: every lane folds one leaf, the butterfly gives the pass root, and
 // the pass roots are combined by the same tree through a binary-counter
 // stack (lane k of the wave holds level k).
@@ -19,6 +20,7 @@
 // elements are folded straight from global memory.
 #include "dg_device.h"
 #include "dg_internal.h"
+#include "dg_lanes.h"
 
 namespace dg {
 
@@ -40,10 +42,32 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_wave_barrier();
 }
 
-__device__ __forceinline__ float butterfly(float v) {
+__device__ __forceinline__ float butterfly(float v) { return tree_sum_lanes<6>(v); }
+
+// log2 of a power of two up to 64
+template <int G>
+constexpr int lg2() {
+  return G <= 1 ? 0 : 1 + lg2<G / 2>();
+}
+
+// One step of a count-down butterfly over an array of per-lane values: each
+// value meets its exact partner lane ^ M.
+template <int M, int N>
+__device__ __forceinline__ void down_step(float* s) {
 #pragma unroll
-  for (int m = 1; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
-  return v;
+  for (int u = 0; u < N; ++u) s[u] = s[u] + xor_partner<M>(s[u]);
+}
+
+// The count-down butterfly's lane steps over groups of G lanes: offsets
+// G / 2, ..., 2, 1.
+template <int G, int N>
+__device__ __forceinline__ void down_lanes(float* s) {
+  if constexpr (G >= 64) down_step<32, N>(s);
+  if constexpr (G >= 32) down_step<16, N>(s);
+  if constexpr (G >= 16) down_step<8, N>(s);
+  if constexpr (G >= 8) down_step<4, N>(s);
+  if constexpr (G >= 4) down_step<2, N>(s);
+  if constexpr (G >= 2) down_step<1, N>(s);
 }
 
 // Staged path (leaf_w <= 64, 16-byte aligned rows): a pass's 64 leaves are
@@ -232,13 +256,9 @@ __global__ __launch_bounds__(256) void rowsum_strided(RowsumArgs a) {
 #pragma unroll
       for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
     r = s[0];
-#pragma unroll
-    for (int m = 1; m < G; m <<= 1) r = r + __shfl_xor(r, m, 64);
+    r = tree_sum_lanes<lg2<G>()>(r);
   } else {
-#pragma unroll
-    for (int m = G / 2; m >= 1; m >>= 1)
-#pragma unroll
-      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], m, 64);
+    down_lanes<G, LPL>(s);
 #pragma unroll
     for (int h = LPL / 2; h >= 1; h >>= 1)
 #pragma unroll
@@ -425,13 +445,9 @@ __global__ __launch_bounds__(256) void rmsnorm_strided_fused(RowsumArgs ra, Norm
 #pragma unroll
       for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
     r = s[0];
-#pragma unroll
-    for (int m = 1; m < 64; m <<= 1) r = r + __shfl_xor(r, m, 64);
+    r = tree_sum_lanes<6>(r);
   } else {
-#pragma unroll
-    for (int m = 32; m >= 1; m >>= 1)
-#pragma unroll
-      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], m, 64);
+    down_lanes<64, LPL>(s);
 #pragma unroll
     for (int h = LPL / 2; h >= 1; h >>= 1)
 #pragma unroll
@@ -542,14 +558,9 @@ __device__ __forceinline__ float lanes_meet(float (&s)[LPL]) {
 #pragma unroll
       for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
     float r = s[0];
-#pragma unroll
-    for (int k = 1; k < 64; k <<= 1) r = r + __shfl_xor(r, k, 64);
-    return r;
+    return tree_sum_lanes<6>(r);
   } else {
-#pragma unroll
-    for (int k = 32; k >= 1; k >>= 1)
-#pragma unroll
-      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], k, 64);
+    down_lanes<64, LPL>(s);
 #pragma unroll
     for (int h = LPL / 2; h >= 1; h >>= 1)
 #pragma unroll
@@ -877,8 +888,12 @@ __global__ __launch_bounds__(256) void softmax_strided_fused(RowsumArgs ra, Norm
 #pragma unroll
   for (int u = 0; u < LPL; ++u)
     if (has[u]) m = max_nan(m, v[NST][u]);
-#pragma unroll
-  for (int k = 1; k < 64; k <<= 1) m = max_nan(m, __shfl_xor(m, k, 64));
+  m = max_nan(m, butterfly_partner<0>(m));
+  m = max_nan(m, butterfly_partner<1>(m));
+  m = max_nan(m, butterfly_partner<2>(m));
+  m = max_nan(m, butterfly_partner<3>(m));
+  m = max_nan(m, butterfly_partner<4>(m));
+  m = max_nan(m, butterfly_partner<5>(m));
 #pragma unroll
   for (int t = 0; t < NST; ++t)
     if (t < nfull)
@@ -905,13 +920,9 @@ __global__ __launch_bounds__(256) void softmax_strided_fused(RowsumArgs ra, Norm
 #pragma unroll
       for (int u = 0; u < LPL; u += 2 * h) s[u] = s[u] + s[u + h];
     r = s[0];
-#pragma unroll
-    for (int k = 1; k < 64; k <<= 1) r = r + __shfl_xor(r, k, 64);
+    r = tree_sum_lanes<6>(r);
   } else {
-#pragma unroll
-    for (int k = 32; k >= 1; k >>= 1)
-#pragma unroll
-      for (int u = 0; u < LPL; ++u) s[u] = s[u] + __shfl_xor(s[u], k, 64);
+    down_lanes<64, LPL>(s);
 #pragma unroll
     for (int h = LPL / 2; h >= 1; h >>= 1)
 #pragma unroll
@@ -976,8 +987,12 @@ __global__ __launch_bounds__(256) void softmax_exp(NormArgs a) {
   const float* x = a.X + row * cols;
   float m = -__builtin_inff();
   for (int64_t j = threadIdx.x; j < cols; j += 256) m = max_nan(m, x[j]);
-#pragma unroll
-  for (int k = 1; k < 64; k <<= 1) m = max_nan(m, __shfl_xor(m, k, 64));
+  m = max_nan(m, butterfly_partner<0>(m));
+  m = max_nan(m, butterfly_partner<1>(m));
+  m = max_nan(m, butterfly_partner<2>(m));
+  m = max_nan(m, butterfly_partner<3>(m));
+  m = max_nan(m, butterfly_partner<4>(m));
+  m = max_nan(m, butterfly_partner<5>(m));
   if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
   __syncthreads();
   m = max_nan(max_nan(wm[0], wm[1]), max_nan(wm[2], wm[3]));
