@@ -89,8 +89,7 @@ struct AttnArgs {
 };
 
 bool attn_supported(int64_t d, int key_block);
-// nw: waves (16 query rows each) per workgroup, 1, 2 or 4
-hipError_t launch_attention(const AttnArgs& a, int64_t d, int key_block, int nw, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int64_t d, int key_block, hipStream_t s);
 
 // This device's copy of the fixed split-K scratch array of dg_gemm_noalloc
 // (DG_NOALLOC_SCRATCH_BYTES), looked up once per device with that device
