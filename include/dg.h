@@ -204,6 +204,38 @@ dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bi
 dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const void* bias,
                           void* C, int64_t M, int64_t N, int64_t K, void* stream);
 
+/* Packed B for few-row GEMMs (a layout for the memory system; the order,
+ * and so every bit, is the descriptor's, as Sec. 5.2 has it for layouts
+ * under a pinned order).  Every 32 x 16 block of B (32 consecutive k of 16
+ * consecutive columns) is one contiguous 1 KB run holding, for l = 0 .. 63
+ * in turn, the 8 values B[k0 + 8 (l / 16) + e][n0 + l % 16], e = 0 .. 7 --
+ * the B operand layout of the 16x16x32 MFMA -- and the runs are ordered by
+ * column panel (n0 / 16), then by k block (k0 / 32).  Columns past N and k
+ * past K are zeros.  The element type is not read (bf16 or binary16 alike).
+ * dg_packed_b_bytes gives the size: ceil(N / 16) * ceil(K / 32) * 1024
+ * bytes (0 for K = 0 or N = 0; SIZE_MAX for a negative size). */
+size_t dg_packed_b_bytes(int64_t K, int64_t N);
+
+/* Write the packed form of B (device, K x N row-major 16-bit elements) into
+ * Bp (device, dg_packed_b_bytes(K, N) bytes, 16-byte aligned), on stream.
+ * DG_ERR_SHAPE for a negative size; DG_ERR_ALIGN if B is not 2-byte or Bp
+ * not 16-byte aligned; DG_ERR_INVALID for a NULL pointer with a non-empty
+ * size.  One launch, no workspace. */
+dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream);
+
+/* dg_gemm with B in the packed form (Bp from dg_pack_b for the same K, N):
+ * the same order and the same bits as dg_gemm on the row-major B, on a
+ * kernel that streams each 1 KB run with one coalesced load (one wave per
+ * 16 columns, split-K part and up to 64 rows of A).  For few-row products:
+ * M <= 64.  Descriptors: carried accumulator (tile_combine CARRY), fma 1,
+ * no leading short tile; contiguous parts whose interior cut points are
+ * multiples of 32, or strided parts dealing tiles of 32 * 2^j k.
+ * DG_ERR_UNSUPPORTED for anything else (M > 64 included), DG_ERR_ALIGN if Bp
+ * is not 16-byte aligned; errors otherwise as dg_gemm, and split-K uses the
+ * same workspace. */
+dg_status dg_gemm_packed(const dg_desc* d, const void* A, const void* Bp, const void* bias,
+                         void* C, int64_t M, int64_t N, int64_t K, void* stream);
+
 /* dg_gemm followed by the column sums of its output, an epilogue reduction
  * (the paper times a GEMM whose epilogue emits a column sum, Sec. 7):
  * colsum[j] = the balanced tree over the rows of column j in order (count
@@ -239,7 +271,10 @@ typedef struct {
                       descriptors (no other knob), 10 four waves with 128-row
                       sub-tiles and direct-to-LDS loads into a four-slot ring,
                       256 x 256 blocks on the first split_n columns and
-                      256 x 192 blocks on the rest.  Binary16 operands
+                      256 x 192 blocks on the rest, 11 the packed-B kernel
+                      (dg_gemm_packed only, which runs nothing else; tile_m
+                      0, 16, 32 or 64 rows per wave, depth its ring of k
+                      blocks).  Binary16 operands
                       (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
                       and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256
@@ -251,7 +286,9 @@ typedef struct {
                       each of the eight XCDs given a contiguous range */
   int32_t occupancy; /* kernel 3: 0 library's choice, 1 or 2 workgroups per CU */
   int32_t depth;   /* kernel 4: slabs of loads kept in flight (0 = 4; 2, 4 or 8);
-                      kernel 8: LDS ring slots */
+                      kernel 8: LDS ring slots; kernel 11: k blocks in flight
+                      (16-row waves 8, 16, 24, 32; 32-row 8, 12, 16; 64-row
+                      6, 10; with A rows not 16-byte aligned 4, 2, 1) */
   int32_t slab_k;  /* kernel 4: k per slab (0 = 64; 64, 128 or 256).  Kernel 4
                       builds a fixed list of (tile_m, tile_n, depth, slab_k);
                       others return DG_ERR_UNSUPPORTED */
@@ -265,6 +302,12 @@ typedef struct {
 dg_status dg_gemm_knobs(const dg_desc* d, const void* A, const void* B, const void* bias,
                         void* C, int64_t M, int64_t N, int64_t K,
                         const dg_knobs* knobs, void* stream);
+
+/* dg_gemm_packed with explicit speed knobs (kernel 0 or 11, tile_m, depth;
+ * every other knob 0). */
+dg_status dg_gemm_packed_knobs(const dg_desc* d, const void* A, const void* Bp, const void* bias,
+                               void* C, int64_t M, int64_t N, int64_t K,
+                               const dg_knobs* knobs, void* stream);
 
 /* out[r] = balanced-tree reduction of row r of X (Sec. 3.1, Sec. 5.1):
  * leaves of leaf_w consecutive elements folded in index order (SUM: s = x0,
@@ -415,7 +458,9 @@ const char* dg_strerror(dg_status s);
  * built against an earlier header must not pass its dg_knobs to this one.
  * 0.3.0 (300) added dg_desc_params.in_dtype (a smaller struct_size is
  * rejected) and knob kernel 10.  0.4.0 (400) added dg_gemm_noalloc and
- * DG_ERR_SCRATCH, and the attention descriptor and dg_attention. */
+ * DG_ERR_SCRATCH, and the attention descriptor and dg_attention.  0.5.0
+ * (500) added the packed B form (dg_packed_b_bytes, dg_pack_b,
+ * dg_gemm_packed, dg_gemm_packed_knobs) and knob kernel 11. */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

@@ -9,7 +9,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdg.so")
-SOURCES = ["dg_api.cpp", "dg_gemm.hip", "dg_rowsum.hip", "dg_attn.hip"]
+SOURCES = ["dg_api.cpp", "dg_gemm.hip", "dg_panel.hip", "dg_rowsum.hip", "dg_attn.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 # -ffp-contract=off: no multiply-add is fused unless the source spells it out.
@@ -38,17 +38,36 @@ def spilling_kernels(remarks: str) -> list[str]:
     return bad
 
 
+def _compile(src: str, obj: str) -> tuple[int, str]:
+    flags = [f for f in FLAGS if f != "-shared"]
+    r = subprocess.run([HIPCC] + flags + ["-c", "-o", obj, src], capture_output=True, text=True)
+    return r.returncode, r.stdout + r.stderr
+
+
 def build(verbose: bool = False) -> str:
+    """Compile every source to an object in parallel, then link them."""
+    from concurrent.futures import ThreadPoolExecutor
     srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    objdir = os.path.join(HERE, "_build")
+    os.makedirs(objdir, exist_ok=True)
+    objs = [os.path.join(objdir, os.path.basename(s) + ".%d.o" % os.getpid()) for s in srcs]
+    with ThreadPoolExecutor(max_workers=min(len(srcs), os.cpu_count() or 1)) as ex:
+        results = list(ex.map(lambda so: _compile(*so), zip(srcs, objs)))
+    text = "\n".join(t for _, t in results)
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-o", tmp] + srcs
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    text = r.stdout + r.stderr
+    rc = max(r for r, _ in results)
+    if rc == 0:
+        r = subprocess.run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp] + objs,
+                           capture_output=True, text=True)
+        rc, text = r.returncode, text + r.stdout + r.stderr
+    for o in objs:
+        if os.path.exists(o):
+            os.unlink(o)
     # the resource remarks (and their source-context lines) are read, not shown
     out = "\n".join(l for l in text.splitlines()
                     if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l
                     and not re.match(r"^\s*\d*\s*\|", l) and l.strip())
-    if r.returncode != 0:
+    if rc != 0:
         raise RuntimeError("hipcc failed:\n" + out)
     spills = spilling_kernels(text)
     if spills:

@@ -188,7 +188,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 400; }
+int32_t dg_version(void) { return 500; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {
@@ -278,7 +278,7 @@ dg_status dg_desc_signature(const dg_desc* d, char* buf, size_t n) {
 // whether it did.
 static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
                            int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream,
-                           float* colsum_part, bool* fused, bool noalloc = false) {
+                           float* colsum_part, bool* fused, bool noalloc = false, bool packed = false) {
   if (fused) *fused = false;
   if (!d) return DG_ERR_INVALID;
   if (M < 0 || N < 0 || K < 0) return DG_ERR_SHAPE;
@@ -289,7 +289,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 10) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 11) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  // packed B runs on kernel 11 only, and kernel 11 runs nothing else
+  if (packed ? (kern != 0 && kern != 11) : kern == 11) return DG_ERR_UNSUPPORTED;
+  if (packed) kern = 11;
   // the scalar instruction runs on kernel 9 only, and kernel 9 runs nothing else
   const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
   if (scalar ? (kern != 0 && kern != 9) : kern == 9) return DG_ERR_UNSUPPORTED;
@@ -303,16 +306,18 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern != 6 && kern != 7 && kern != 10 && split_n) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && occ) return DG_ERR_UNSUPPORTED;
   if (kern == 5 && (tm || tn) && !dg::wide_supported(tm, tn)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && kern != 8 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
+  if (kern != 4 && kern != 8 && kern != 11 && (depth || slab_k)) return DG_ERR_UNSUPPORTED;
+  if (kern == 11 && (slab_k || tn || order || occ || split_n || !(tm == 0 || tm == 16 || tm == 32 || tm == 64)))
+    return DG_ERR_UNSUPPORTED;
   if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth, slab_k)) return DG_ERR_UNSUPPORTED;
   if (kern == 8 && !dg::skinny_dma_supported(tm ? tm : 16, tn ? tn : 16, depth ? depth : 8, slab_k ? slab_k : 256))
     return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && kern != 5 && kern != 8 && (tm || tn) &&
+  if (kern != 4 && kern != 5 && kern != 8 && kern != 11 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
   // A strided split runs on the generic kernel or on the few-row kernel with
   // one dealt tile per slab.
-  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 && kern != 9 &&
+  if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1 && kern != 0 && kern != 1 && kern != 9 && kern != 11 &&
       !((kern == 4 || kern == 8) && slab_k == p.split_tile))
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
@@ -356,6 +361,29 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   a.in_f16 = f16;
   if ((M + 15) / 16 > 65535 || (N + 15) / 16 > (int64_t)1 << 31) return DG_ERR_SHAPE;
 
+  // The packed-B kernel (dg_panel.hip): one accumulator carried through the
+  // part's 32-k blocks, parts starting on a block, dealt tiles of 2^j blocks.
+  int panel_tms = 0, panel_depth = 0;
+  bool panel_avec = false;
+  if (packed) {
+    if (scalar || p.tile_combine != DG_CARRY || p.fma != 1 || p.tail == DG_TAIL_FIRST || M > 64)
+      return DG_ERR_UNSUPPORTED;
+    if (strided) {
+      const int64_t wf = p.split_tile / 32;
+      if (p.split_tile % 32 || (wf & (wf - 1))) return DG_ERR_UNSUPPORTED;
+    } else {
+      for (int s = 1; s < a.S; ++s)
+        if (a.cuts[s] % 32) return DG_ERR_UNSUPPORTED;
+    }
+    if (!aligned(B, 16)) return DG_ERR_ALIGN;
+    // every buffer offset (the packed B, A's rows) stays in 31 bits
+    if (dg_packed_b_bytes(K, N) > 0x7fffffff || M * K * 2 > 0x7fffffff) return DG_ERR_UNSUPPORTED;
+    panel_tms = tm ? tm / 16 : (M <= 16 ? 1 : M <= 32 ? 2 : 4);
+    panel_avec = K % 8 == 0 && aligned(A, 16);
+    panel_depth = depth ? depth : dg::panel_default_depth(panel_tms, panel_avec);
+    if (!dg::panel_supported(panel_tms, panel_depth, panel_avec)) return DG_ERR_UNSUPPORTED;
+  }
+
   hipStream_t st = (hipStream_t)stream;
   if (a.S > 1) {
     void* ws = nullptr;
@@ -385,7 +413,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     tiled_ok = false;
     kern = 9;
   }
-  if (kern >= 2 && kern != 9 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern >= 2 && kern != 9 && kern != 11 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (strided && kern == 0) {
     const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
     const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
@@ -424,7 +452,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     *fused = true;
   }
   hipError_t e;
-  if (kern == 9) {
+  if (kern == 11) {
+    e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
+  } else if (kern == 9) {
     if ((M + 3) / 4 > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
     e = dg::launch_gemm_scalar(a, st);
   } else if (kern == 8) {
@@ -524,6 +554,35 @@ dg_status dg_gemm(const dg_desc* d, const void* A, const void* B, const void* bi
 dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,
                           int64_t M, int64_t N, int64_t K, void* stream) {
   return gemm_impl(d, A, B, bias, C, M, N, K, nullptr, stream, nullptr, nullptr, true);
+}
+
+size_t dg_packed_b_bytes(int64_t K, int64_t N) {
+  if (K < 0 || N < 0) return SIZE_MAX;
+  const uint64_t panels = (uint64_t)(N + 15) / 16, blocks = (uint64_t)(K + 31) / 32;
+  if (panels && blocks > (SIZE_MAX / 1024) / panels) return SIZE_MAX;
+  return (size_t)(panels * blocks * 1024);
+}
+
+dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream) {
+  if (K < 0 || N < 0) return DG_ERR_SHAPE;
+  if (K == 0 || N == 0) return DG_OK;
+  if (!B || !Bp) return DG_ERR_INVALID;
+  if (!aligned(B, 2) || !aligned(Bp, 16)) return DG_ERR_ALIGN;
+  if (dg_packed_b_bytes(K, N) == SIZE_MAX || (N + 15) / 16 * ((K + 31) / 32) > ((int64_t)1 << 31) * 4)
+    return DG_ERR_SHAPE;
+  if (dg::launch_pack_b((const uint16_t*)B, (uint16_t*)Bp, K, N, (hipStream_t)stream) != hipSuccess)
+    return DG_ERR_HIP;
+  return DG_OK;
+}
+
+dg_status dg_gemm_packed_knobs(const dg_desc* d, const void* A, const void* Bp, const void* bias, void* C,
+                               int64_t M, int64_t N, int64_t K, const dg_knobs* knobs, void* stream) {
+  return gemm_impl(d, A, Bp, bias, C, M, N, K, knobs, stream, nullptr, nullptr, false, true);
+}
+
+dg_status dg_gemm_packed(const dg_desc* d, const void* A, const void* Bp, const void* bias, void* C,
+                         int64_t M, int64_t N, int64_t K, void* stream) {
+  return dg_gemm_packed_knobs(d, A, Bp, bias, C, M, N, K, nullptr, stream);
 }
 
 dg_status dg_gemm_colsum(const dg_desc* d, const void* A, const void* B, const void* bias, void* C,

@@ -113,6 +113,13 @@ hipError_t launch_gemm_w4(const GemmArgs& a, hipStream_t st);
 hipError_t launch_gemm_skinny(const GemmArgs& a, int tile_m, int tile_n, int depth, int slab_k, hipStream_t s);
 bool skinny_supported(int tile_m, int tile_n, int depth, int slab_k);
 hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tile_m, int tile_n, int slots, int slab_k, hipStream_t s);
+// packed B (dg_panel.hip): the layout writer, and the few-row kernel on it
+// (tms 16-row A tiles per wave, a ring of depth k blocks; avec: A rows read
+// as 16-byte runs, else element by element)
+hipError_t launch_pack_b(const uint16_t* B, uint16_t* Bp, int64_t K, int64_t N, hipStream_t s);
+hipError_t launch_gemm_panel(const GemmArgs& a, int tms, int depth, bool avec, hipStream_t s);
+bool panel_supported(int tms, int depth, bool avec);
+int panel_default_depth(int tms, bool avec);
 bool skinny_dma_supported(int tile_m, int tile_n, int slots, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);

@@ -73,6 +73,11 @@ def lib():
         L.dg_gemm.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_gemm_noalloc.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_gemm_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
+        L.dg_packed_b_bytes.argtypes = [i64, i64]
+        L.dg_packed_b_bytes.restype = ctypes.c_size_t
+        L.dg_pack_b.argtypes = [vp, vp, i64, i64, vp]
+        L.dg_gemm_packed.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
+        L.dg_gemm_packed_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
         L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
         L.dg_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_float, vp, i64, i64, vp]
         L.dg_softmax.argtypes = [vp, vp, vp, i64, i64, vp]
@@ -88,7 +93,7 @@ def lib():
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
         for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc", "dg_gemm_knobs",
-                  "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
+                  "dg_pack_b", "dg_gemm_packed", "dg_gemm_packed_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -259,17 +264,86 @@ def dg_gemm(desc: Desc, A, B, bias, C, M=None, N=None, K=None, stream=None, knob
     import torch
     if isinstance(A, torch.Tensor):
         M, N, K = _check_gemm(desc, A, B, bias, C)
-    kp = None
     if knobs is not None:
-        kp = dg_knobs(int(knobs.get("kernel", 0)), int(knobs.get("tile_m", 0)), int(knobs.get("tile_n", 0)),
-                      int(knobs.get("order", 0)), int(knobs.get("occupancy", 0)), int(knobs.get("depth", 0)),
-                      int(knobs.get("slab_k", 0)), int(knobs.get("split_n", 0)))
+        kp = _knobs(knobs)
         st = lib().dg_gemm_knobs(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K,
                                  ctypes.byref(kp), _stream(stream))
     else:
         st = lib().dg_gemm(desc.handle, _ptr(A), _ptr(B), _ptr(bias), _ptr(C), M, N, K, _stream(stream))
     if st != DG_OK:
         raise DgError(st, "dg_gemm")
+    return C
+
+
+def _knobs(knobs):
+    return dg_knobs(int(knobs.get("kernel", 0)), int(knobs.get("tile_m", 0)), int(knobs.get("tile_n", 0)),
+                    int(knobs.get("order", 0)), int(knobs.get("occupancy", 0)), int(knobs.get("depth", 0)),
+                    int(knobs.get("slab_k", 0)), int(knobs.get("split_n", 0)))
+
+
+def dg_packed_b_bytes(K: int, N: int) -> int:
+    """Bytes of the packed form of a K x N matrix: ceil(N/16) ceil(K/32) 1 KB."""
+    return int(lib().dg_packed_b_bytes(int(K), int(N)))
+
+
+class PackedB:
+    """B (K x N, bf16 or float16) in the packed form dg_gemm_packed reads:
+    every 32 x 16 block one 1 KB run in the 16x16x32 MFMA's B operand layout,
+    runs by column panel then k block.  data is a uint8 device tensor."""
+
+    def __init__(self, data, K: int, N: int, dtype):
+        self.data, self.K, self.N, self.dtype = data, int(K), int(N), dtype
+
+
+def dg_pack_b(B, out=None, stream=None) -> PackedB:
+    """The packed form of B (K, N) (contiguous, on the GPU), into out (a
+    uint8 device tensor of dg_packed_b_bytes(K, N) bytes) or a new one."""
+    import torch
+    _need(B.dim() == 2 and B.is_contiguous() and B.dtype in (torch.bfloat16, torch.float16),
+          "B must be a contiguous bf16 or float16 matrix")
+    _on_device(B)
+    K, N = B.shape
+    n = dg_packed_b_bytes(K, N)
+    if out is None:
+        out = torch.empty(max(n, 16), dtype=torch.uint8, device=B.device)
+    _need(out.dtype == torch.uint8 and out.numel() >= n and out.is_contiguous(), "out must hold %d bytes" % n)
+    st = lib().dg_pack_b(_ptr(B), _ptr(out), K, N, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_pack_b")
+    return PackedB(out, K, N, B.dtype)
+
+
+def dg_gemm_packed(desc: Desc, A, Bp, bias, C, M=None, N=None, K=None, stream=None, knobs=None):
+    """dg_gemm with B packed by dg_pack_b (the same bits); Bp a PackedB, or a
+    raw device address with M, N, K given."""
+    import torch
+    if isinstance(A, torch.Tensor):
+        _need(isinstance(Bp, PackedB), "Bp must come from dg_pack_b")
+        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
+        _need(A.dtype == want_in and Bp.dtype == want_in, "A and B must be %s" % want_in)
+        _need(A.dim() == 2 and C.dim() == 2 and A.is_contiguous() and C.is_contiguous(), "A and C must be row-major")
+        M, K = A.shape
+        N = Bp.N
+        _need(Bp.K == K, "inner dimensions differ (%d, %d)" % (K, Bp.K))
+        _need(tuple(C.shape) == (M, N), "C must be %d x %d" % (M, N))
+        _need(C.dtype == _out_dtype(desc), "C dtype must match the descriptor's output type")
+        if desc.fields["epilogue"] != "none":
+            _need(bias is not None, "the descriptor's epilogue needs a bias")
+        if bias is not None:
+            _need(bias.dtype == torch.bfloat16 and bias.numel() == N and bias.is_contiguous(),
+                  "bias must be %d contiguous bf16 values" % N)
+        _on_device(A, C, bias, Bp.data)
+        bptr = _ptr(Bp.data)
+    else:
+        bptr = _ptr(Bp)
+    if knobs is not None:
+        kp = _knobs(knobs)
+        st = lib().dg_gemm_packed_knobs(desc.handle, _ptr(A), bptr, _ptr(bias), _ptr(C), M, N, K,
+                                        ctypes.byref(kp), _stream(stream))
+    else:
+        st = lib().dg_gemm_packed(desc.handle, _ptr(A), bptr, _ptr(bias), _ptr(C), M, N, K, _stream(stream))
+    if st != DG_OK:
+        raise DgError(st, "dg_gemm_packed")
     return C
 
 
@@ -422,4 +496,5 @@ def exported_symbols():
     """Names of the entry points include/dg.h declares."""
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc",
             "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
-            "dg_version", "dg_attn_desc_create", "dg_attn_desc_destroy", "dg_attention"]
+            "dg_version", "dg_attn_desc_create", "dg_attn_desc_destroy", "dg_attention",
+            "dg_packed_b_bytes", "dg_pack_b", "dg_gemm_packed", "dg_gemm_packed_knobs"]

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 400
+    assert dg.dg_version() == 500
     for s in range(8):
         assert dg.dg_strerror(s)
 
@@ -322,6 +322,45 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
     assert lib.dg_rowsum(d.handle, 16, None, 4, 5, None) == dg.DG_ERR_INVALID
     assert lib.dg_rowsum(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
+
+
+def test_packed_b_size_and_refusals_need_no_gpu(dg):
+    """The packed form's size, and dg_pack_b / dg_gemm_packed refusing what
+    they do not take before any launch (host integers as pointers)."""
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("runs without a GPU: the calls pass host integers as pointers")
+    lib = dg.lib()
+    assert dg.dg_packed_b_bytes(0, 16) == 0 and dg.dg_packed_b_bytes(32, 0) == 0
+    assert dg.dg_packed_b_bytes(32, 16) == 1024
+    assert dg.dg_packed_b_bytes(33, 17) == 2 * 2 * 1024
+    assert dg.dg_packed_b_bytes(4096, 4096) == 4096 * 4096 * 2      # whole blocks: no padding
+    assert dg.dg_packed_b_bytes(-1, 16) == 2 ** 64 - 1
+    assert dg.dg_packed_b_bytes(1 << 62, 1 << 62) == 2 ** 64 - 1    # overflow
+    assert lib.dg_pack_b(16, 16, -1, 8, None) == dg.DG_ERR_SHAPE
+    assert lib.dg_pack_b(16, 16, 0, 8, None) == dg.DG_OK
+    assert lib.dg_pack_b(None, 16, 8, 8, None) == dg.DG_ERR_INVALID
+    assert lib.dg_pack_b(17, 16, 8, 8, None) == dg.DG_ERR_ALIGN
+    assert lib.dg_pack_b(16, 8, 8, 8, None) == dg.DG_ERR_ALIGN       # Bp needs 16 bytes
+    d = dg.Desc()
+    ok = dict(A=16, B=16, C=16)
+    gp = lambda desc, M, N, K, A=16, B=16, C=16: lib.dg_gemm_packed(desc.handle, A, B, None, C, M, N, K, None)
+    assert gp(d, 0, 8, 8) == dg.DG_OK
+    assert gp(d, 65, 8, 8) == dg.DG_ERR_UNSUPPORTED                 # few rows only
+    assert gp(d, 8, 8, 8, B=8) == dg.DG_ERR_ALIGN
+    assert gp(d, 8, 8, 8, A=None) == dg.DG_ERR_INVALID
+    for bad in (dict(tile_combine="tree", tile_k=64), dict(fma=0), dict(tail="first", tile_k=64),
+                dict(split_k=2, k_cuts=[48]), dict(split_k=4, split_layout="strided", split_tile=96, tile_k=32),
+                dict(mma="scalar")):
+        assert gp(dg.Desc(**bad), 8, 64, 256) == dg.DG_ERR_UNSUPPORTED, bad
+    kn = dg.dg_knobs(4, 16, 64, 0, 0, 4, 64)       # a row-major kernel on packed B
+    assert lib.dg_gemm_packed_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == \
+        dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(11, 16, 0, 0, 0, 7)           # a ring depth the build lacks
+    assert lib.dg_gemm_packed_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == \
+        dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(11, 0, 0, 0, 0, 0)            # kernel 11 only reads packed B
+    assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
 
 
 def test_build_rejects_register_spills():
