@@ -38,8 +38,11 @@ MALL_BYTES = 256 << 20
 MLP_KERNEL = ("dg::gemm_pp_mixed<32> (eight-wave ping-pong, fused bias+SiLU epilogue; 256 blocks of 256x256 "
               "then 256 of 256x192)")
 # the workload the value is quoted on (at most 120 characters)
-WORKLOAD = ("GEMM suite: sweep N=K=4096 M=1,7,32,128,1024,4096; decode 8x4096x14336 S=8 seq+tree; "
-            "SiLU MLP 2048x14336x4096")
+WORKLOAD = ("GEMM suite: N=K=4096 M=1,7,32,128,1024,4096; decode 8x4096x14336 S=8 seq+tree; "
+            "SiLU MLP 2048x14336x4096; packed B M<=32")
+# rows with at most this many rows of A read the weight in the packed form
+# (dg_pack_b, done once before timing); the same bits as the row-major call
+PACKED_MAX_M = 64
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_pp_mlp_hbm_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_11356_amd", "csrc", "dg_gemm.hip")
 
@@ -144,10 +147,10 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         def run():
             dg.dg_gemm(D, dA, dBs[it[0] % len(dBs)], None, C, stream=sptr)
             it[0] += 1
-    elif args.only in ("gemv", "decode"):
+    elif args.only in ("gemv", "decode", "gemv_packed", "decode_packed"):
         # the few-row launches of the step, weights rotated through copies
         # totalling twice the MALL so that every launch streams B from HBM
-        if args.only == "gemv":
+        if args.only.startswith("gemv"):
             A, B = inputs.sweep_activations(1, rows=4096)[:1], inputs.sweep_weight(2)
             D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16")
             what = "sweep GEMM M=1: 1x4096 by 4096x4096"
@@ -160,10 +163,18 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         dBs += [dBs[0].clone() for _ in range(max(1, -(-2 * MALL_BYTES // B.nbytes)) - 1)]
         C = torch.empty((A.shape[0], B.shape[1]), dtype=torch.bfloat16, device=dev)
         it = [0]
+        if args.only.endswith("_packed"):
+            dPs = [dg.dg_pack_b(b) for b in dBs]
+            del dBs
+            what += ", packed weight"
 
-        def run():
-            dg.dg_gemm(D, dA, dBs[it[0] % len(dBs)], None, C, stream=sptr)
-            it[0] += 1
+            def run():
+                dg.dg_gemm_packed(D, dA, dPs[it[0] % len(dPs)], None, C, stream=sptr)
+                it[0] += 1
+        else:
+            def run():
+                dg.dg_gemm(D, dA, dBs[it[0] % len(dBs)], None, C, stream=sptr)
+                it[0] += 1
     else:
         src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)   # 1 GiB
         dst = torch.empty_like(src)
@@ -193,11 +204,13 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
-    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode", "sweep128", "sweep1024", "sweep4096"),
+    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode", "gemv_packed", "decode_packed", "sweep128",
+                                        "sweep1024", "sweep4096"),
                     default=None,
                     help="profiling runs: launch only the fused MLP GEMM, the M=1 sweep GEMM, "
-                         "the split-K decode, one sweep GEMM (M=128, 1024, 4096), or a plain 1 GiB "
-                         "device copy (the calibration kernel for HBM byte counters)")
+                         "the split-K decode (each on the row-major or the packed weight), one sweep "
+                         "GEMM (M=128, 1024, 4096), or a plain 1 GiB device copy (the calibration "
+                         "kernel for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -235,6 +248,11 @@ def main():
     dA_sw = d_bf16(A_sw)
     dA_sw_M = {M: dA_sw[:M].contiguous() for M in inputs.SWEEP_M}
     dB_dec = copies(d_bf16(B_dec), B_dec.nbytes)
+    # the packed form of every weight copy, written once (a weight's layout is
+    # chosen at load time; the order, and so every bit, is the descriptor's)
+    dP_sw = [dg.dg_pack_b(b) for b in dB_sw]
+    dP_dec = [dg.dg_pack_b(b) for b in dB_dec]
+    torch.cuda.synchronize()
     dA_dec = d_bf16(A_dec)
     dB_mlp = copies(d_bf16(B_mlp), B_mlp.nbytes)
     dA_mlp = d_bf16(A_mlp)
@@ -291,18 +309,24 @@ def main():
                   2 * (8 * 14336 + 14336 * 4096 + 8 * 4096) + 2 * 4 * 8 * 8 * 4096) for c in ("seq", "tree")]
     launches += [("mlp", "mlp", 2 * 2048 * 14336 * 4096, 2 * (2048 * 4096 + 4096 * 14336 + 14336 + 2048 * 14336))]
 
+    def sweep_launch(M, i):
+        if M <= PACKED_MAX_M:
+            dg.dg_gemm_packed(D_sw, dA_sw_M[M], dP_sw[i % len(dP_sw)], None, C_sw[M], stream=sptr)
+        else:
+            dg.dg_gemm(D_sw, dA_sw_M[M], dB_sw[i % len(dB_sw)], None, C_sw[M], stream=sptr)
+
     def step(i, record):
         e = [ev() for _ in range(len(launches) + 1)] if record else None
         if record:
             e[0].record(stream)
         n = 0
         for M in inputs.SWEEP_M:
-            dg.dg_gemm(D_sw, dA_sw_M[M], dB_sw[i % len(dB_sw)], None, C_sw[M], stream=sptr)
+            sweep_launch(M, i)
             n += 1
             if record:
                 e[n].record(stream)
         for u, c in enumerate(("seq", "tree")):
-            dg.dg_gemm(D_dec[c], dA_dec, dB_dec[(2 * i + u) % len(dB_dec)], None, C_dec[c], stream=sptr)
+            dg.dg_gemm_packed(D_dec[c], dA_dec, dP_dec[(2 * i + u) % len(dP_dec)], None, C_dec[c], stream=sptr)
             n += 1
             if record:
                 e[n].record(stream)
@@ -473,6 +497,23 @@ def main():
         rs[name] = {"ms": round(ms, 4), "GB/s": round(by / ms / 1e6, 1),
                     "frac_hbm": round(by / ms / 1e6 / PEAK_HBM_GBS, 4), "what": what}
 
+    # ------------------------- few-row launches: packed weight against row-major
+    few = {}
+    few_cases = [("sweep_M%d" % M, D_sw, dA_sw_M[M], dP_sw, dB_sw, C_sw[M]) for M in inputs.SWEEP_M
+                 if M <= PACKED_MAX_M]
+    few_cases += [("decode_" + c, D_dec[c], dA_dec, dP_dec, dB_dec, C_dec[c]) for c in ("seq", "tree")]
+    for name, Dv, A_, Pl, Bl, C_ in few_cases:
+        t_p, t_r = paired(lambda i, Dv=Dv, A_=A_, Pl=Pl, C_=C_: dg.dg_gemm_packed(Dv, A_, Pl[i % len(Pl)], None, C_,
+                                                                                   stream=sptr),
+                          lambda i, Dv=Dv, A_=A_, Bl=Bl, C_=C_: dg.dg_gemm(Dv, A_, Bl[i % len(Bl)], None, C_,
+                                                                            stream=sptr), reps)
+        by = Bl[0].numel() * 2
+        few[name] = {"packed_us": round(1e3 * t_p, 2), "row_major_us": round(1e3 * t_r, 2),
+                     "speedup": round(t_r / t_p, 3), "packed_GB/s": round(by / (t_p * 1e-3) / 1e9, 1)}
+    few["what"] = ("dg_gemm_packed on the packed weight (dg_pack_b) against dg_gemm on the row-major one, "
+                   "same descriptor and bits, alternating blocks; GB/s counts the weight's bytes")
+    # the launches above leave C as the step wrote it (same bits either way)
+
     # ------------------------------------------------------------ attention
     # 32 heads x 4096 tokens x 128 (a Llama-style head set), bf16, key
     # blocks of 64, BLOCK_M 128, the block row sum by the balanced tree; the
@@ -512,12 +553,11 @@ def main():
     # compared with (same inputs, same clock state); cost = t_dg / t_free.
     free = {}
     try:
-        sw_dg = lambda M: (lambda i: dg.dg_gemm(D_sw, dA_sw_M[M], dB_sw[i % len(dB_sw)], None, C_sw[M],
-                                                 stream=sptr))
+        sw_dg = lambda M: (lambda i: sweep_launch(M, i))
         sw_free = lambda M: (lambda i: torch.matmul(dA_sw_M[M], dB_sw[i % len(dB_sw)]))
         by_M = {M: paired(sw_dg(M), sw_free(M), reps) for M in inputs.SWEEP_M}
-        t_dec = paired(lambda i: dg.dg_gemm(D_dec["seq"], dA_dec, dB_dec[i % len(dB_dec)], None, C_dec["seq"],
-                                            stream=sptr),
+        t_dec = paired(lambda i: dg.dg_gemm_packed(D_dec["seq"], dA_dec, dP_dec[i % len(dP_dec)], None,
+                                                   C_dec["seq"], stream=sptr),
                        lambda i: torch.matmul(dA_dec, dB_dec[i % len(dB_dec)]), reps)
         t_mlp = paired(lambda i: dg.dg_gemm(D_mlp, dA_mlp, dB_mlp[i % len(dB_mlp)], dbias, C_mlp, stream=sptr),
                        lambda i: torch.nn.functional.silu(torch.matmul(dA_mlp, dB_mlp[i % len(dB_mlp)]) + dbias),
@@ -554,22 +594,29 @@ def main():
     try:
         strided = {w: dict(mma="16x16x32", tile_k=64, split_k=4, split_layout="strided", split_tile=w,
                            out="bf16") for w in (64, 128)}
-        cases = [("sweep_M%d" % M, dA_sw_M[M], dB_sw, strided[64]) for M in (1, 7, 32)]
-        cases.append(("decode", dA_dec, dB_dec, strided[128]))
-        for name, A_, Bl, desc in cases:
+        cases = [("sweep_M%d" % M, dA_sw_M[M], dB_sw, dP_sw, strided[64]) for M in (1, 7, 32)]
+        cases.append(("decode", dA_dec, dB_dec, dP_dec, strided[128]))
+        for name, A_, Bl, Pl, desc in cases:
             Dv = dg.Desc(**desc)
             C_ = torch.empty((A_.shape[0], Bl[0].shape[1]), dtype=torch.bfloat16, device=dev)
+            Cp = torch.empty_like(C_)
             for i in range(args.warmup):
                 dg.dg_gemm(Dv, A_, Bl[i % len(Bl)], None, C_, stream=sptr)
+                dg.dg_gemm_packed(Dv, A_, Pl[i % len(Pl)], None, Cp, stream=sptr)
             t_dg = timeit(lambda i: dg.dg_gemm(Dv, A_, Bl[i % len(Bl)], None, C_, stream=sptr), args.steps)
+            t_dp = timeit(lambda i: dg.dg_gemm_packed(Dv, A_, Pl[i % len(Pl)], None, Cp, stream=sptr), args.steps)
             t_hb = timeit(lambda i: torch.matmul(A_, Bl[i % len(Bl)]), args.steps)
             dg.dg_gemm(Dv, A_, Bl[0], None, C_, stream=sptr)
+            dg.dg_gemm_packed(Dv, A_, Pl[0], None, Cp, stream=sptr)
             ref = torch.matmul(A_, Bl[0])
             torch.cuda.synchronize()
             mism = int((C_.view(torch.int16) != ref.view(torch.int16)).sum().item())
+            mism_p = int((Cp.view(torch.int16) != ref.view(torch.int16)).sum().item())
             vendor[name] = {"desc": "strided split S=4, %d-k tiles" % desc["split_tile"],
-                            "dg_us": round(1e3 * t_dg, 2), "hipblaslt_us": round(1e3 * t_hb, 2),
-                            "mismatching_outputs": mism, "outputs": int(ref.numel())}
+                            "dg_us": round(1e3 * t_dg, 2), "dg_packed_us": round(1e3 * t_dp, 2),
+                            "hipblaslt_us": round(1e3 * t_hb, 2),
+                            "mismatching_outputs": mism, "mismatching_outputs_packed": mism_p,
+                            "outputs": int(ref.numel())}
         for name, A_, Bl in (("sweep_M4096", dA_sw_M[4096], dB_sw), ("mlp_no_epilogue", dA_mlp, dB_mlp)):
             Dv = dg.Desc(mma="16x16x32", tile_k=64, out="bf16")
             C_ = torch.empty((A_.shape[0], Bl[0].shape[1]), dtype=torch.bfloat16, device=dev)
@@ -709,6 +756,7 @@ def main():
         "attention": attn,
         "free_order": free,
         "hipblaslt_order": vendor,
+        "few_row_packed": few,
         "bit_match": {"checked": checked, "matched": matched,
                       "pct": round(100.0 * matched / max(checked, 1), 4),
                       "batch_invariant_row0": inv_ok},

@@ -359,6 +359,9 @@ def test_packed_b_size_and_refusals_need_no_gpu(dg):
     kn = dg.dg_knobs(11, 16, 0, 0, 0, 7)           # a ring depth the build lacks
     assert lib.dg_gemm_packed_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == \
         dg.DG_ERR_UNSUPPORTED
+    kn = dg.dg_knobs(11, 0, 0, 1, 0, 0)            # no block order on kernel 11
+    assert lib.dg_gemm_packed_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == \
+        dg.DG_ERR_UNSUPPORTED
     kn = dg.dg_knobs(11, 0, 0, 0, 0, 0)            # kernel 11 only reads packed B
     assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 8, 8, 8, ctypes.byref(kn), None) == dg.DG_ERR_UNSUPPORTED
 
