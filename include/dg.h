@@ -72,7 +72,7 @@ enum { DG_SPLIT_CONTIGUOUS = 0, DG_SPLIT_STRIDED = 1 };  /* layout of the split 
 enum { DG_LEAF_CONTIGUOUS = 0, DG_LEAF_STRIDED = 1 };    /* row-reduction leaf layout */
 enum { DG_FOLD_UP = 0, DG_FOLD_DOWN = 1 };               /* how the leaves meet */
 enum { DG_NORM_FINAL = 0, DG_NORM_PRE_WEIGHT = 1 };      /* RMS-norm rounding point */
-enum { DG_IN_BF16 = 0, DG_IN_F16 = 1 };                  /* GEMM operand format */
+enum { DG_IN_BF16 = 0, DG_IN_F16 = 1, DG_IN_BF16_E4M3 = 2 }; /* GEMM operand format */
 
 #define DG_MAX_SPLIT 64
 #define DG_SIGNATURE_MAX 2048
@@ -142,7 +142,16 @@ typedef struct {
                              instruction of the same shape, whose chunks follow
                              the same rules with binary16 exponents (a product
                              of two binary16 values is exact in binary32, so the
-                             scalar path is unchanged).  The bias stays bf16. */
+                             scalar path is unchanged).  DG_IN_BF16_E4M3: A
+                             bf16, B one byte per element in the OCP 8-bit
+                             e4m3 format (bias 7, no infinities, S.1111.111
+                             NaN), each value widened exactly to bf16 (every
+                             e4m3 value is one) and folded by the bf16
+                             instruction: the order and bits of a bf16 GEMM on
+                             the widened B.  The fp8 instructions themselves
+                             fold differently and are not used.  An e4m3 B is
+                             taken by the MFMA descriptors only (not
+                             DG_MMA_SCALAR_FMA).  The bias stays bf16. */
 } dg_desc_params;
 
 typedef struct dg_desc dg_desc; /* opaque, immutable */
@@ -216,6 +225,15 @@ dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const 
  * bytes (0 for K = 0 or N = 0; SIZE_MAX for a negative size). */
 size_t dg_packed_b_bytes(int64_t K, int64_t N);
 
+/* The packed form of an e4m3 B (DG_IN_BF16_E4M3): the same blocks and run
+ * order, one byte per element, so every 32 x 16 block is a 512-byte run
+ * (for l = 0 .. 63 in turn the 8 bytes B[k0 + 8 (l / 16) + e][n0 + l % 16]).
+ * dg_packed_b8_bytes: ceil(N / 16) * ceil(K / 32) * 512 (SIZE_MAX as
+ * dg_packed_b_bytes); dg_pack_b8 writes it from a row-major K x N byte
+ * matrix, with the errors of dg_pack_b (B needs no alignment). */
+size_t dg_packed_b8_bytes(int64_t K, int64_t N);
+dg_status dg_pack_b8(const void* B, void* Bp, int64_t K, int64_t N, void* stream);
+
 /* Write the packed form of B (device, K x N row-major 16-bit elements) into
  * Bp (device, dg_packed_b_bytes(K, N) bytes, 16-byte aligned), on stream.
  * DG_ERR_SHAPE for a negative size; DG_ERR_ALIGN if B is not 2-byte or Bp
@@ -223,7 +241,8 @@ size_t dg_packed_b_bytes(int64_t K, int64_t N);
  * size.  One launch, no workspace. */
 dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream);
 
-/* dg_gemm with B in the packed form (Bp from dg_pack_b for the same K, N):
+/* dg_gemm with B in the packed form (Bp from dg_pack_b for the same K, N, or
+ * dg_pack_b8 for a DG_IN_BF16_E4M3 descriptor):
  * the same order and the same bits as dg_gemm on the row-major B, on a
  * kernel that streams each 1 KB run with one coalesced load (one wave per
  * 16 columns, split-K part and up to 64 rows of A).  For few-row products:
@@ -276,7 +295,9 @@ typedef struct {
                       0, 16, 32 or 64 rows per wave, depth its ring of k
                       blocks).  Binary16 operands
                       (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
-                      and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED */
+                      and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED.
+                      An e4m3 B (DG_IN_BF16_E4M3) runs on kernel 1 (row-major)
+                      and kernel 11 (packed) */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256
                       (kernel 3: no 256 x 256 block) */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */
@@ -460,7 +481,8 @@ const char* dg_strerror(dg_status s);
  * rejected) and knob kernel 10.  0.4.0 (400) added dg_gemm_noalloc and
  * DG_ERR_SCRATCH, and the attention descriptor and dg_attention.  0.5.0
  * (500) added the packed B form (dg_packed_b_bytes, dg_pack_b,
- * dg_gemm_packed, dg_gemm_packed_knobs) and knob kernel 11. */
+ * dg_gemm_packed, dg_gemm_packed_knobs), knob kernel 11, and e4m3 weights
+ * (DG_IN_BF16_E4M3, dg_packed_b8_bytes, dg_pack_b8). */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

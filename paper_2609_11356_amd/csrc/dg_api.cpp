@@ -66,6 +66,7 @@ bool make_signature(dg_desc* d) {
     s += std::string("/leaf-strided") + (p.lane_fold == DG_FOLD_DOWN && p.leaf_w > 1 ? "/fold-down" : "");
   if (p.norm_round == DG_NORM_PRE_WEIGHT) s += "/norm-pre-weight";
   if (p.in_dtype == DG_IN_F16) s += "/in-f16";
+  if (p.in_dtype == DG_IN_BF16_E4M3) s += "/in-bf16xe4m3";
   // one strided part is the whole axis, as one contiguous part is
   if (p.split_layout == DG_SPLIT_STRIDED && p.split_k > 1) s += "/strided:" + std::to_string(p.split_tile);
   if (p.n_cuts) {
@@ -179,7 +180,9 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
   if (M <= 128) return {4, 32, 64, 0, 0, 2, 256};
   const int64_t tiles256 = S * ((M + 255) / 256) * ((N + 255) / 256);
   const int64_t tiles128 = S * ((M + 127) / 128) * ((N + 127) / 128);
-  if (tiles256 >= 192) return {5, 256, 256, 1, 0, 0, 0};
+  // 256 x 256 blocks, each XCD given a contiguous range of them (2-3 % over
+  // row-major order at 4096 x 4096 x 4096 on MI355X)
+  if (tiles256 >= 192) return {5, 256, 256, 3, 0, 0, 0};
   if (tiles128 >= 128) return {5, 128, 128, 3, 0, 0, 0};
   return {3, 64, 128, 3, 2, 0, 0};
 }
@@ -232,7 +235,8 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   if (!in(p->leaf_layout, DG_LEAF_CONTIGUOUS, DG_LEAF_STRIDED) || !in(p->lane_fold, DG_FOLD_UP, DG_FOLD_DOWN))
     return DG_ERR_INVALID;
   if (!in(p->norm_round, DG_NORM_FINAL, DG_NORM_PRE_WEIGHT)) return DG_ERR_INVALID;
-  if (!in(p->in_dtype, DG_IN_BF16, DG_IN_F16)) return DG_ERR_INVALID;
+  if (!in(p->in_dtype, DG_IN_BF16, DG_IN_BF16_E4M3)) return DG_ERR_INVALID;
+  if (p->in_dtype == DG_IN_BF16_E4M3 && p->mma == DG_MMA_SCALAR_FMA) return DG_ERR_UNSUPPORTED;
   if (p->split_layout == DG_SPLIT_STRIDED) {
     if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
       return DG_ERR_INVALID;
@@ -300,6 +304,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   // binary16 operands: the generic, v3, few-row, ping-pong and scalar kernels
   const bool f16 = p.in_dtype == DG_IN_F16;
   if (f16 && (kern == 2 || kern == 7 || kern == 8 || kern == 10)) return DG_ERR_UNSUPPORTED;
+  // an e4m3 B: the generic kernel (row-major) and the packed kernel only
+  const bool b8 = p.in_dtype == DG_IN_BF16_E4M3;
+  if (b8 && !packed && kern == 0) kern = 1;
+  if (b8 && kern != 1 && kern != 11) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
     return DG_ERR_UNSUPPORTED;
@@ -322,7 +330,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
   if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
-  if (!aligned(A, 2) || !aligned(B, 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
+  if (!aligned(A, 2) || !aligned(B, b8 ? 1 : 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
       (need_bias && !aligned(bias, 2)))
     return DG_ERR_ALIGN;
   if (K == 0 && p.split_k > 1) return DG_ERR_SHAPE;
@@ -359,6 +367,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   a.epilogue = p.epilogue;
   a.pre_act = p.epi_round == DG_ROUND_PRE_ACT;
   a.in_f16 = f16;
+  a.b_e4m3 = b8;
   if ((M + 15) / 16 > 65535 || (N + 15) / 16 > (int64_t)1 << 31) return DG_ERR_SHAPE;
 
   // The packed-B kernel (dg_panel.hip): one accumulator carried through the
@@ -377,7 +386,8 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     }
     if (!aligned(B, 16)) return DG_ERR_ALIGN;
     // every buffer offset (the packed B, A's rows) stays in 31 bits
-    if (dg_packed_b_bytes(K, N) > 0x7fffffff || M * K * 2 > 0x7fffffff) return DG_ERR_UNSUPPORTED;
+    if ((b8 ? dg_packed_b8_bytes(K, N) : dg_packed_b_bytes(K, N)) > 0x7fffffff || M * K * 2 > 0x7fffffff)
+      return DG_ERR_UNSUPPORTED;
     panel_tms = tm ? tm / 16 : (M <= 16 ? 1 : M <= 32 ? 2 : 4);
     panel_avec = K % 8 == 0 && aligned(A, 16);
     panel_depth = depth ? depth : dg::panel_default_depth(panel_tms, panel_avec);
@@ -434,8 +444,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     if (c.kern == 5 && c.tm == 256 && c.tn == 256) {
       const int64_t sp = mixed_split(M, N, a.S, cu_count());
       if (sp >= 0) {
+        // the width mix keeps row-major block order (measured best for it)
         c.kern = 6;
         c.tm = c.tn = 0;
+        c.order = 1;
         split_n = sp;
       }
     }
@@ -571,6 +583,23 @@ dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream)
   if (dg_packed_b_bytes(K, N) == SIZE_MAX || (N + 15) / 16 * ((K + 31) / 32) > ((int64_t)1 << 31) * 4)
     return DG_ERR_SHAPE;
   if (dg::launch_pack_b((const uint16_t*)B, (uint16_t*)Bp, K, N, (hipStream_t)stream) != hipSuccess)
+    return DG_ERR_HIP;
+  return DG_OK;
+}
+
+size_t dg_packed_b8_bytes(int64_t K, int64_t N) {
+  const size_t b = dg_packed_b_bytes(K, N);
+  return b == SIZE_MAX ? SIZE_MAX : b / 2;
+}
+
+dg_status dg_pack_b8(const void* B, void* Bp, int64_t K, int64_t N, void* stream) {
+  if (K < 0 || N < 0) return DG_ERR_SHAPE;
+  if (K == 0 || N == 0) return DG_OK;
+  if (!B || !Bp) return DG_ERR_INVALID;
+  if (!aligned(Bp, 16)) return DG_ERR_ALIGN;
+  if (dg_packed_b_bytes(K, N) == SIZE_MAX || (N + 15) / 16 * ((K + 31) / 32) > ((int64_t)1 << 31) * 4)
+    return DG_ERR_SHAPE;
+  if (dg::launch_pack_b8((const uint8_t*)B, (uint8_t*)Bp, K, N, (hipStream_t)stream) != hipSuccess)
     return DG_ERR_HIP;
   return DG_OK;
 }

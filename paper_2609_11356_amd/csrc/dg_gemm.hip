@@ -405,7 +405,10 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
         const int64_t k = gs + kb + e;
         const bool ok = k < ge;
         av[e] = (ok && arow < a.M) ? (short)a.A[arow * a.K + k] : (short)0;
-        bv[e] = (ok && bcol < a.N) ? (short)a.B[k * a.N + bcol] : (short)0;
+        if (a.b_e4m3)
+          bv[e] = (ok && bcol < a.N) ? (short)e4m3_bf16(((const uint8_t*)a.B)[k * a.N + bcol]) : (short)0;
+        else
+          bv[e] = (ok && bcol < a.N) ? (short)a.B[k * a.N + bcol] : (short)0;
       }
       if (a.fma) {
         v = a.in_f16 ? mfma16h(av, bv, v) : mfma16(av, bv, v);

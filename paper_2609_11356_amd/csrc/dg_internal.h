@@ -35,6 +35,7 @@ struct GemmArgs {
   int64_t split_w;               // strided split: dealt tile width (0: contiguous parts)
   int64_t n_split;               // mixed-width ping-pong: first column of the 192-wide blocks
   int32_t in_f16;                // operands A and B are binary16 (else bfloat16)
+  int32_t b_e4m3;                // B holds one OCP e4m3 byte per element (A bf16)
   float* colsum_part;            // set (single part, 256-row blocks): column sums of each 256-row
                                  // run of C, [ceil(M / 256)][N], folded in the epilogue
 };
@@ -117,6 +118,7 @@ hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tile_m, int tile_n, int
 // (tms 16-row A tiles per wave, a ring of depth k blocks; avec: A rows read
 // as 16-byte runs, else element by element)
 hipError_t launch_pack_b(const uint16_t* B, uint16_t* Bp, int64_t K, int64_t N, hipStream_t s);
+hipError_t launch_pack_b8(const uint8_t* B, uint8_t* Bp, int64_t K, int64_t N, hipStream_t s);
 hipError_t launch_gemm_panel(const GemmArgs& a, int tms, int depth, bool avec, hipStream_t s);
 bool panel_supported(int tms, int depth, bool avec);
 int panel_default_depth(int tms, bool avec);

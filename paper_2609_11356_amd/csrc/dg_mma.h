@@ -15,6 +15,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef short shortx8 __attribute__((ext_vector_type(8)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Compile-time loop: f(std::integral_constant<int, I>) for I in [B, E), so
 // that register arrays indexed by I stay in registers.
@@ -62,6 +63,18 @@ __device__ __forceinline__ void finish(const GemmArgs& a, int s, int64_t i, int6
   }
   if (a.out_bf16) ((uint16_t*)a.C)[i * a.N + j] = f32_bf16(z);
   else ((float*)a.C)[i * a.N + j] = z;
+}
+
+// OCP e4m3 byte(s) widened to bf16 by the part's own conversion (exact:
+// every e4m3 value, subnormals and signed zeros included, is a bf16 value;
+// NaN stays NaN), the pair in bytes 2h and 2h + 1 of x.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+template <bool HI>
+__device__ __forceinline__ uint32_t e4m3x2_bf16x2(uint32_t x) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)x, 1.0f, HI));
+}
+__device__ __forceinline__ uint16_t e4m3_bf16(uint8_t b) {
+  return (uint16_t)(e4m3x2_bf16x2<false>(b) & 0xffffu);
 }
 
 // s_waitcnt immediate waiting for at most n outstanding vector-memory

@@ -23,6 +23,12 @@
 // cuts on multiples of 32), a strided part the blocks of its dealt tiles
 // (width a multiple of 32).  Blocks past the part's end hold zeros, whose
 // chunks leave the accumulators unchanged.
+//
+// An e4m3 B (one byte per element) packs the same way into 512-byte runs
+// (8 bytes per lane); the wave widens each lane's 8 values to bf16 with the
+// part's conversion instruction (exact) just before the bf16 instruction, so
+// the order and bits are those of the bf16 GEMM on the widened B, with half
+// the bytes streamed.
 #include <type_traits>
 
 #include "dg_device.h"
@@ -57,8 +63,12 @@ __device__ __forceinline__ u32x4 load_a_elems(__amdgpu_buffer_rsrc_t r, int64_t 
 
 }  // namespace
 
-template <int TMS, int D, bool AVEC, bool STRIDED, bool F16>
+// BT: the B operand, 0 bf16, 1 binary16 (A binary16 too), 2 OCP e4m3 bytes
+// (512-byte runs, widened to bf16 before the instruction)
+template <int TMS, int D, bool AVEC, bool STRIDED, int BT>
 __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
+  constexpr bool F16 = BT == 1;
+  constexpr int RUN = BT == 2 ? 512 : 1024;   // bytes of one block's run
   const int lane = threadIdx.x;
   const int64_t panel = blockIdx.x;
   const int64_t i0 = (int64_t)blockIdx.y * 16 * TMS, j0 = panel * 16;
@@ -76,7 +86,7 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
     fb0 = (int)(a.cuts[s] / 32);
     nf = (int)((a.cuts[s + 1] + 31) / 32) - fb0;
   }
-  const int64_t recA = (a.M - i0) * a.K * 2, recB = ((a.N + 15) / 16) * (int64_t)KB * 1024;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = ((a.N + 15) / 16) * (int64_t)KB * RUN;
   const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
   // the panel's runs: a base moved to the panel, the block in the scalar offset
@@ -85,7 +95,7 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
   // lane constants: B's run slot; A's row run (out of range past M), and the
   // first block whose 8 k of this lane lie at or past K (only the last block
   // when K % 32 != 0).  A block's offset goes in the scalar buffer offset.
-  const uint32_t vb = (uint32_t)(panel * KB * 1024) + (uint32_t)lane * 16u;
+  const uint32_t vb = (uint32_t)(panel * KB * RUN) + (uint32_t)lane * (RUN / 64);
   const int flim = (K - kl + 31) / 32;
   uint32_t va[TMS];
 #pragma unroll
@@ -102,12 +112,18 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
     if constexpr (STRIDED) return ((s + a.S * (q >> lgw)) << lgw) + (q & ((1 << lgw) - 1));
     else return fb0 + q;
   };
-  u32x4 rb[D], ra[D][TMS];
+  // B's ring: 16 bytes (bf16, binary16) or 8 bytes (e4m3) per lane and block
+  using BReg = std::conditional_t<BT == 2, u32x2, u32x4>;
+  BReg rb[D];
+  u32x4 ra[D][TMS];
   auto load = [&](int u, int q) {
     const int f = block_of(q);
     const bool ok = q < nfe && (!STRIDED || f < KB);
     const int so = ok ? f : 0;
-    rb[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, ok ? vb : kOOB, so * 1024, 0));
+    if constexpr (BT == 2)
+      rb[u] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rB, ok ? vb : kOOB, so * RUN, 0));
+    else
+      rb[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, ok ? vb : kOOB, so * RUN, 0));
 #pragma unroll
     for (int mi = 0; mi < TMS; ++mi) {
       if constexpr (AVEC) {
@@ -135,9 +151,15 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
       // this block's loads are the oldest D - 1 + 1 groups in flight
       if constexpr (AVEC) __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 1) * (1 + TMS)));
       if (q < nf) {
+        u32x4 bw;
+        if constexpr (BT == 2)
+          bw = u32x4{e4m3x2_bf16x2<false>(rb[u][0]), e4m3x2_bf16x2<true>(rb[u][0]),
+                     e4m3x2_bf16x2<false>(rb[u][1]), e4m3x2_bf16x2<true>(rb[u][1])};
+        else
+          bw = rb[u];
 #pragma unroll
         for (int mi = 0; mi < TMS; ++mi)
-          acc[mi] = mfma16t<F16>(__builtin_bit_cast(shortx8, ra[u][mi]), __builtin_bit_cast(shortx8, rb[u]), acc[mi]);
+          acc[mi] = mfma16t<F16>(__builtin_bit_cast(shortx8, ra[u][mi]), __builtin_bit_cast(shortx8, bw), acc[mi]);
       }
       load(u, q + D);
       __builtin_amdgcn_sched_barrier(0);
@@ -172,6 +194,37 @@ __global__ __launch_bounds__(256) void pack_b(const uint16_t* __restrict__ B, ui
   *(u32x4*)&Bp[t * 8] = u32x4{w[0], w[1], w[2], w[3]};
 }
 
+// The same for one-byte elements: 8 bytes per lane, 512-byte runs.
+__global__ __launch_bounds__(256) void pack_b8(const uint8_t* __restrict__ B, uint8_t* __restrict__ Bp, int64_t K,
+                                               int64_t N, int64_t runs) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= runs * 64) return;
+  const int64_t run = t / 64, KB = (K + 31) / 32;
+  const int l = (int)(t % 64);
+  const int64_t p = run / KB, f = run % KB;
+  const int64_t n = p * 16 + (l & 15), k0 = f * 32 + 8 * (l >> 4);
+  uint32_t w[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint32_t v = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t k = k0 + 4 * h + e;
+      v |= (uint32_t)((n < N && k < K) ? B[k * N + n] : 0) << (8 * e);
+    }
+    w[h] = v;
+  }
+  *(u32x2*)&Bp[t * 8] = u32x2{w[0], w[1]};
+}
+
+hipError_t launch_pack_b8(const uint8_t* B, uint8_t* Bp, int64_t K, int64_t N, hipStream_t st) {
+  const int64_t runs = ((N + 15) / 16) * ((K + 31) / 32);
+  const int64_t blocks = (runs * 64 + 255) / 256;
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_b8, dim3((unsigned)blocks), dim3(256), 0, st, B, Bp, K, N, runs);
+  return hipGetLastError();
+}
+
 hipError_t launch_pack_b(const uint16_t* B, uint16_t* Bp, int64_t K, int64_t N, hipStream_t st) {
   const int64_t runs = ((N + 15) / 16) * ((K + 31) / 32);
   const int64_t blocks = (runs * 64 + 255) / 256;
@@ -184,13 +237,15 @@ template <int TMS, int D, bool AVEC>
 static hipError_t launch_panel_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + 15) / 16), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
   const bool strided = a.split_w != 0;
-  if (a.in_f16) {
-    if (strided) hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, true, true>), grid, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, false, true>), grid, dim3(64), 0, st, a);
-  } else {
-    if (strided) hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, true, false>), grid, dim3(64), 0, st, a);
-    else hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, false, false>), grid, dim3(64), 0, st, a);
-  }
+  const int bt = a.b_e4m3 ? 2 : a.in_f16 ? 1 : 0;
+  auto go = [&](auto BT_) {
+    constexpr int BT = decltype(BT_)::value;
+    if (strided) hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, true, BT>), grid, dim3(64), 0, st, a);
+    else hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, false, BT>), grid, dim3(64), 0, st, a);
+  };
+  if (bt == 2) go(std::integral_constant<int, 2>{});
+  else if (bt == 1) go(std::integral_constant<int, 1>{});
+  else go(std::integral_constant<int, 0>{});
   return hipGetLastError();
 }
 

@@ -76,6 +76,9 @@ def lib():
         L.dg_packed_b_bytes.argtypes = [i64, i64]
         L.dg_packed_b_bytes.restype = ctypes.c_size_t
         L.dg_pack_b.argtypes = [vp, vp, i64, i64, vp]
+        L.dg_packed_b8_bytes.argtypes = [i64, i64]
+        L.dg_packed_b8_bytes.restype = ctypes.c_size_t
+        L.dg_pack_b8.argtypes = [vp, vp, i64, i64, vp]
         L.dg_gemm_packed.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, vp]
         L.dg_gemm_packed_knobs.argtypes = [vp, vp, vp, vp, vp, i64, i64, i64, ctypes.POINTER(dg_knobs), vp]
         L.dg_rowsum.argtypes = [vp, vp, vp, i64, i64, vp]
@@ -93,7 +96,7 @@ def lib():
         L.dg_strerror.restype = ctypes.c_char_p
         L.dg_version.restype = ctypes.c_int32
         for f in ("dg_desc_create", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc", "dg_gemm_knobs",
-                  "dg_pack_b", "dg_gemm_packed", "dg_gemm_packed_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
+                  "dg_pack_b", "dg_pack_b8", "dg_gemm_packed", "dg_gemm_packed_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -120,7 +123,8 @@ class Desc:
     "strided": leaf_w lanes each taking every leaf_w-th element), lane_fold
     ("up" | "down": the butterfly's offsets counting up or down), norm_round
     ("final" | "pre_weight": dg_rmsnorm rounds the normalised value to bf16
-    before the weight), in_dtype ("bf16" | "f16": the GEMM operands)."""
+    before the weight), in_dtype ("bf16" | "f16" | "bf16_e4m3": the GEMM
+    operands; "bf16_e4m3" is a bf16 A with a B of OCP e4m3 bytes)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
@@ -164,7 +168,7 @@ class Desc:
         p.leaf_layout = {"contiguous": 0, "strided": 1}[f["leaf_layout"]]
         p.lane_fold = {"up": 0, "down": 1}[f["lane_fold"]]
         p.norm_round = {"final": 0, "pre_weight": 1}[f["norm_round"]]
-        p.in_dtype = {"bf16": 0, "f16": 1}[f["in_dtype"]]
+        p.in_dtype = {"bf16": 0, "f16": 1, "bf16_e4m3": 2}[f["in_dtype"]]
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:
@@ -219,11 +223,23 @@ def _on_device(*ts):
     _need(all(t.is_cuda for t in ts if t is not None), "tensors must be on the GPU")
 
 
+def _in_dtypes(desc):
+    """The torch dtypes A and B must have under desc (an e4m3 B as raw bytes
+    or torch's float8_e4m3fn)."""
+    import torch
+    f = desc.fields["in_dtype"]
+    if f == "f16":
+        return (torch.float16,), (torch.float16,)
+    if f == "bf16_e4m3":
+        return (torch.bfloat16,), (torch.uint8, getattr(torch, "float8_e4m3fn", torch.uint8))
+    return (torch.bfloat16,), (torch.bfloat16,)
+
+
 def _check_gemm(desc, A, B, bias, C):
     """Shapes, dtypes and layout of a GEMM call; returns (M, N, K)."""
     import torch
-    want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
-    _need(A.dtype == want_in and B.dtype == want_in, "A and B must be %s" % want_in)
+    want_a, want_b = _in_dtypes(desc)
+    _need(A.dtype in want_a and B.dtype in want_b, "A must be %s and B %s" % (want_a[0], want_b[0]))
     _need(A.dim() == 2 and B.dim() == 2 and C.dim() == 2, "A, B and C must be matrices")
     M, K = A.shape
     K2, N = B.shape
@@ -287,30 +303,40 @@ def dg_packed_b_bytes(K: int, N: int) -> int:
 
 
 class PackedB:
-    """B (K x N, bf16 or float16) in the packed form dg_gemm_packed reads:
-    every 32 x 16 block one 1 KB run in the 16x16x32 MFMA's B operand layout,
-    runs by column panel then k block.  data is a uint8 device tensor."""
+    """B (K x N, bf16 or float16, or e4m3 bytes) in the packed form
+    dg_gemm_packed reads: every 32 x 16 block one run (1 KB, or 512 bytes
+    for e4m3) in the 16x16x32 MFMA's B operand layout, runs by column panel
+    then k block.  data is a uint8 device tensor; dtype the element type."""
 
     def __init__(self, data, K: int, N: int, dtype):
         self.data, self.K, self.N, self.dtype = data, int(K), int(N), dtype
 
 
+def dg_packed_b8_bytes(K: int, N: int) -> int:
+    """Bytes of the packed form of a K x N e4m3 matrix: ceil(N/16) ceil(K/32) 512."""
+    return int(lib().dg_packed_b8_bytes(int(K), int(N)))
+
+
 def dg_pack_b(B, out=None, stream=None) -> PackedB:
-    """The packed form of B (K, N) (contiguous, on the GPU), into out (a
-    uint8 device tensor of dg_packed_b_bytes(K, N) bytes) or a new one."""
+    """The packed form of B (K, N) (contiguous, on the GPU: bf16 or float16,
+    or e4m3 as uint8 / float8_e4m3fn), into out (a uint8 device tensor of
+    dg_packed_b_bytes(K, N), or dg_packed_b8_bytes for e4m3, bytes) or a
+    new one."""
     import torch
-    _need(B.dim() == 2 and B.is_contiguous() and B.dtype in (torch.bfloat16, torch.float16),
-          "B must be a contiguous bf16 or float16 matrix")
+    b8 = B.dtype in (torch.uint8, getattr(torch, "float8_e4m3fn", torch.uint8))
+    _need(B.dim() == 2 and B.is_contiguous() and (b8 or B.dtype in (torch.bfloat16, torch.float16)),
+          "B must be a contiguous bf16, float16 or e4m3 matrix")
     _on_device(B)
     K, N = B.shape
-    n = dg_packed_b_bytes(K, N)
+    n = dg_packed_b8_bytes(K, N) if b8 else dg_packed_b_bytes(K, N)
     if out is None:
         out = torch.empty(max(n, 16), dtype=torch.uint8, device=B.device)
     _need(out.dtype == torch.uint8 and out.numel() >= n and out.is_contiguous(), "out must hold %d bytes" % n)
-    st = lib().dg_pack_b(_ptr(B), _ptr(out), K, N, _stream(stream))
+    fn = lib().dg_pack_b8 if b8 else lib().dg_pack_b
+    st = fn(_ptr(B), _ptr(out), K, N, _stream(stream))
     if st != DG_OK:
-        raise DgError(st, "dg_pack_b")
-    return PackedB(out, K, N, B.dtype)
+        raise DgError(st, "dg_pack_b8" if b8 else "dg_pack_b")
+    return PackedB(out, K, N, torch.uint8 if b8 else B.dtype)
 
 
 def dg_gemm_packed(desc: Desc, A, Bp, bias, C, M=None, N=None, K=None, stream=None, knobs=None):
@@ -319,8 +345,8 @@ def dg_gemm_packed(desc: Desc, A, Bp, bias, C, M=None, N=None, K=None, stream=No
     import torch
     if isinstance(A, torch.Tensor):
         _need(isinstance(Bp, PackedB), "Bp must come from dg_pack_b")
-        want_in = torch.float16 if desc.fields["in_dtype"] == "f16" else torch.bfloat16
-        _need(A.dtype == want_in and Bp.dtype == want_in, "A and B must be %s" % want_in)
+        want_a, want_b = _in_dtypes(desc)
+        _need(A.dtype in want_a and Bp.dtype in want_b, "A must be %s and B %s" % (want_a[0], want_b[0]))
         _need(A.dim() == 2 and C.dim() == 2 and A.is_contiguous() and C.is_contiguous(), "A and C must be row-major")
         M, K = A.shape
         N = Bp.N
@@ -497,4 +523,5 @@ def exported_symbols():
     return ["dg_desc_create", "dg_desc_destroy", "dg_desc_signature", "dg_gemm", "dg_gemm_noalloc",
             "dg_gemm_knobs", "dg_rowsum", "dg_rmsnorm", "dg_softmax", "dg_layernorm", "dg_gemm_colsum", "dg_strerror",
             "dg_version", "dg_attn_desc_create", "dg_attn_desc_destroy", "dg_attention",
-            "dg_packed_b_bytes", "dg_pack_b", "dg_gemm_packed", "dg_gemm_packed_knobs"]
+            "dg_packed_b_bytes", "dg_pack_b", "dg_gemm_packed", "dg_gemm_packed_knobs", "dg_packed_b8_bytes",
+            "dg_pack_b8"]

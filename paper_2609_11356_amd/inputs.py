@@ -64,6 +64,31 @@ def spread_f16(seed: int, shape, emin: int = -14, emax: int = 14) -> np.ndarray:
     return ((sign << 15) | ((e + 15) << 10) | frac).astype(np.uint16)
 
 
+def e4m3_uniform(seed: int, shape) -> np.ndarray:
+    """OCP e4m3 codes (uint8) drawn uniformly over the 254 non-NaN codes:
+    both zeros, every subnormal and normal, up to +-448."""
+    rng = np.random.default_rng(seed)
+    c = rng.integers(0, 254, size=shape).astype(np.uint8)
+    # skip 0x7F (and, shifted by one more, 0xFF): codes 0..126 -> 0x00..0x7E,
+    # 127..253 -> 0x80..0xFE
+    return np.where(c >= 127, c + 1, c).astype(np.uint8)
+
+
+def e4m3_weights(seed: int, shape, e_mid: float = 6.0, e_sd: float = 1.5) -> np.ndarray:
+    """OCP e4m3 codes shaped like quantised weights: a random sign, a
+    mantissa field uniform over 0..7, and an exponent field drawn around
+    e_mid (values near 2^(e_mid - 7)), clipped to 0..15; NaN codes redrawn
+    as the largest finite magnitude."""
+    rng = np.random.default_rng(seed)
+    e = np.clip(np.rint(rng.normal(e_mid, e_sd, size=shape)), 0, 15).astype(np.uint8)
+    m = rng.integers(0, 8, size=shape).astype(np.uint8)
+    sgn = rng.integers(0, 2, size=shape).astype(np.uint8)
+    c = (sgn << 7) | (e << 3) | m
+    nan = (c & 0x7F) == 0x7F
+    c[nan] = c[nan] - 1
+    return c.astype(np.uint8)
+
+
 def lognormal_f32(seed: int, shape, sigma: float = 2.0) -> np.ndarray:
     rng = np.random.default_rng(seed)
     mag = np.exp(sigma * rng.standard_normal(shape))
