@@ -49,12 +49,24 @@ __global__ __launch_bounds__(64) void probe32h(const shortx8* A, const shortx8* 
                                                 __builtin_bit_cast(f16x8, B[i]), C[i], 0, 0, 0);
 }
 
+// The fp8 instruction of the same shape (OCP e4m3 operands, 8 bytes per lane:
+// lane l holds A[l%16][8(l/16)+e], B[8(l/16)+e][l%16], byte e).
+__global__ __launch_bounds__(64) void probe16f8(const long* A, const long* B, const floatx4* C, floatx4* D,
+                                                int ncases) {
+  const int c = blockIdx.x, l = threadIdx.x;
+  if (c >= ncases) return;
+  const size_t i = (size_t)c * 64 + l;
+  D[i] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8(A[i], B[i], C[i], 0, 0, 0);
+}
+
 // instr 0: 16x16x32 bf16 (4 accumulator floats per lane), 1: 32x32x16 bf16
-// (16); 2 and 3: the same shapes with fp16 operands.
+// (16); 2 and 3: the same shapes with fp16 operands; 4: 16x16x32 with e4m3
+// operands (8 bytes per lane, not 16).
 // All pointers are device pointers sized for ncases.
 extern "C" int mfma_probe(int instr, int ncases, const void* A, const void* B, const void* C,
                           void* D, void* stream) {
   if (ncases <= 0) return 0;
+  (void)hipGetLastError();   // an error left by an earlier call is not this launch's
   hipStream_t s = (hipStream_t)stream;
   if (instr == 0)
     hipLaunchKernelGGL(probe16, dim3(ncases), dim3(64), 0, s, (const shortx8*)A, (const shortx8*)B,
@@ -68,7 +80,11 @@ extern "C" int mfma_probe(int instr, int ncases, const void* A, const void* B, c
   else if (instr == 3)
     hipLaunchKernelGGL(probe32h, dim3(ncases), dim3(64), 0, s, (const shortx8*)A, (const shortx8*)B,
                        (const floatx16*)C, (floatx16*)D, ncases);
+  else if (instr == 4)
+    hipLaunchKernelGGL(probe16f8, dim3(ncases), dim3(64), 0, s, (const long*)A, (const long*)B,
+                       (const floatx4*)C, (floatx4*)D, ncases);
   else
     return -1;
-  return hipGetLastError() == hipSuccess ? 0 : -2;
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : -1000 - (int)e;   // -1000 - the HIP error code
 }
