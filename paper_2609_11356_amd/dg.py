@@ -61,6 +61,10 @@ def lib():
     """The loaded libdg.so (raises if it has not been built)."""
     global _lib
     if _lib is None:
+        # torch's HIP runtime first: libdg.so then binds to the runtime already
+        # in the process instead of loading a second one beside it (two
+        # runtimes in one process do not share the device)
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise RuntimeError("libdg.so is not built (run __graft_entry__.build() or "
                                "python -m paper_2609_11356_amd.build)")
