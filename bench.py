@@ -425,17 +425,21 @@ def main():
                               % (dd["split_k"], dd.get("tile_combine", "carry")),
                       "us_per_launch": round(med * 1e3, 2), "GB/s": round(by / (med * 1e-3) / 1e9, 1)}
 
-    # ------- a tile-tree descriptor and one without fma at an LLM shape (sweep M = 1024)
+    # ------- tile-tree and tile-chain descriptors and fma = 0 at an LLM shape
+    # (sweep M = 1024; the tiled tile-combine kernel), beside the carried chain
     tree_rows = {}
     for name, dd in (("tile_tree_M1024", dict(mma="16x16x32", tile_k=256, tile_combine="tree", out="bf16")),
+                     ("tile_tree64_M1024", dict(mma="16x16x32", tile_k=64, tile_combine="tree", out="bf16")),
+                     ("tile_chain_M1024", dict(mma="16x16x32", tile_k=128, tile_combine="seq", out="bf16")),
                      ("fma0_M1024", dict(mma="16x16x32", tile_k=64, fma=0, out="bf16"))):
         Dv = dg.Desc(**dd)
         C_ = torch.empty((1024, 4096), dtype=torch.bfloat16, device=dev)
         run = lambda i, Dv=Dv, C_=C_: dg.dg_gemm(Dv, dA_sw_M[1024], dB_sw[i % len(dB_sw)], None, C_, stream=sptr)
         run(0)
-        med = timeit(run, max(3, reps // 4))
-        tree_rows[name] = {"desc": dd, "us_per_launch": round(med * 1e3, 2),
-                           "TFLOP/s": round(2 * 1024 * 4096 * 4096 / (med * 1e-3) / 1e12, 2)}
+        med = timeit(run, reps)
+        tf = 2 * 1024 * 4096 * 4096 / (med * 1e-3) / 1e12
+        tree_rows[name] = {"desc": dd, "us_per_launch": round(med * 1e3, 2), "TFLOP/s": round(tf, 2),
+                           "frac_mfma_peak": round(tf / 2500.0, 4)}
         scal_out[name] = (dd, C_)
 
     # ----------------- binary16 operands: the fused MLP on the fp16 instruction

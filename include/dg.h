@@ -293,9 +293,17 @@ typedef struct {
                       256 x 192 blocks on the rest, 11 the packed-B kernel
                       (dg_gemm_packed only, which runs nothing else; tile_m
                       0, 16, 32 or 64 rows per wave, depth its ring of k
-                      blocks).  Binary16 operands
-                      (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6
-                      and 9; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED.
+                      blocks), 12 the tile-combine kernel: tile_combine
+                      DG_SEQ or DG_TREE, or fma = 0, on 128 x 64 blocks of
+                      four waves (no other knob; the library's choice for
+                      those descriptors when K and N are multiples of 8, the
+                      operands 16-byte aligned, every part's tile boundaries
+                      on 32-k steps from its start, fma = 0 only with the
+                      16x16x32 instruction, a tree part at most 128 tiles;
+                      otherwise DG_ERR_UNSUPPORTED, and kernel 0 runs the
+                      generic kernel 1).  Binary16 operands
+                      (in_dtype = DG_IN_F16) run on kernels 0, 1, 3, 4, 5, 6,
+                      9 and 12; kernels 2, 7, 8 and 10 return DG_ERR_UNSUPPORTED.
                       An e4m3 B (DG_IN_BF16_E4M3) runs on kernel 1 (row-major)
                       and kernel 11 (packed) */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256
@@ -482,7 +490,8 @@ const char* dg_strerror(dg_status s);
  * DG_ERR_SCRATCH, and the attention descriptor and dg_attention.  0.5.0
  * (500) added the packed B form (dg_packed_b_bytes, dg_pack_b,
  * dg_gemm_packed, dg_gemm_packed_knobs), knob kernel 11, and e4m3 weights
- * (DG_IN_BF16_E4M3, dg_packed_b8_bytes, dg_pack_b8). */
+ * (DG_IN_BF16_E4M3, dg_packed_b8_bytes, dg_pack_b8).  0.5.1 (501) added knob
+ * kernel 12 (tile chain and tree, fma = 0, on a tiled kernel). */
 int32_t dg_version(void);
 
 #ifdef __cplusplus

@@ -2,6 +2,7 @@
 // selection (speed only, never order), split-K workspace, error mapping.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -191,7 +192,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 500; }
+int32_t dg_version(void) { return 501; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {
@@ -293,7 +294,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 11) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 12) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   // packed B runs on kernel 11 only, and kernel 11 runs nothing else
   if (packed ? (kern != 0 && kern != 11) : kern == 11) return DG_ERR_UNSUPPORTED;
   if (packed) kern = 11;
@@ -320,6 +321,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern == 4 && !dg::skinny_supported(tm ? tm : 16, tn ? tn : 64, depth, slab_k)) return DG_ERR_UNSUPPORTED;
   if (kern == 8 && !dg::skinny_dma_supported(tm ? tm : 16, tn ? tn : 16, depth ? depth : 8, slab_k ? slab_k : 256))
     return DG_ERR_UNSUPPORTED;
+  if (kern == 12 && (tm || tn)) return DG_ERR_UNSUPPORTED;
   if (kern != 4 && kern != 5 && kern != 8 && kern != 11 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
@@ -419,11 +421,30 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     int64_t len = a.cuts[s + 1] - a.cuts[s];
     if (a.tail_first && (len % p.tile_k) % 8) tiled_ok = false;
   }
+  // The tile-combine kernel (tile chain or tree, or fma = 0, on the tiled
+  // layout): the tiled layout's alignment, every tile boundary of every part
+  // on a 32-k step from the part start, and for the tree at most 128 tiles
+  // per part (its stack lives in registers).
+  const bool gen = p.tile_combine != DG_CARRY || p.fma == 0;
+  bool tc_ok = gen && !scalar && !strided && !b8 && (p.fma == 1 || d->group == 32) && p.tile_k % 32 == 0 &&
+               K % 8 == 0 && N % 8 == 0 && aligned(A, 16) && aligned(B, 16) && aligned(C, 16) &&
+               (!need_bias || aligned(bias, 16));
+  int64_t max_tiles = 0;
+  for (int s = 0; s < a.S && tc_ok; ++s) {
+    const int64_t len = a.cuts[s + 1] - a.cuts[s];
+    if (a.cuts[s] % 8 || (a.tail_first && (len % p.tile_k) % 32)) tc_ok = false;
+    max_tiles = std::max<int64_t>(max_tiles, (len + p.tile_k - 1) / p.tile_k);
+  }
+  int tc_levels = 2;
+  while (tc_levels < 7 && max_tiles > ((int64_t)1 << tc_levels)) ++tc_levels;
+  if (p.tile_combine == DG_TREE && max_tiles > 128) tc_ok = false;
   if (scalar) {
     tiled_ok = false;
     kern = 9;
   }
-  if (kern >= 2 && kern != 9 && kern != 11 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern == 12 && !tc_ok) return DG_ERR_UNSUPPORTED;
+  if (kern == 0 && !tiled_ok && tc_ok) kern = 12;
+  if (kern >= 2 && kern != 9 && kern != 11 && kern != 12 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (strided && kern == 0) {
     const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
     const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
@@ -466,6 +487,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   hipError_t e;
   if (kern == 11) {
     e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
+  } else if (kern == 12) {
+    if (((M + 127) / 128) * ((N + 63) / 64) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = 1;
+    e = dg::launch_gemm_tc(a, tc_levels, st);
   } else if (kern == 9) {
     if ((M + 3) / 4 > 65535 || (N + 255) / 256 > 0x7fffffff) return DG_ERR_SHAPE;
     e = dg::launch_gemm_scalar(a, st);

@@ -659,9 +659,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 typedef short shortx4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) shortx4* lds_s4;
 
-template <int BM, int BN, int WM, int WN, int V3_BK, bool F16>
+// The same pipeline serves the descriptors whose accumulator is not one
+// carried chain (tile_combine chain or tree, or fma = 0) when every tile
+// boundary lies on a 32-k step from the part start: COMB is the tile
+// combine, FMA0 that each 32-k instruction starts from zero and its result
+// is added to the tile's accumulator (v = v + w, one binary32 addition per
+// element), L the levels of the tile tree's binary-counter stack, held in
+// registers.  The part's last tile stays in the accumulator (its folded
+// value is the lowest entry of the final fold) and needs no level of its
+// own, so L levels hold a part of up to 2^L tiles.  Steps past the part end are skipped, so they close no tile and
+// add nothing.
+template <int BM, int BN, int WM, int WN, int V3_BK, bool F16, int COMB = DG_CARRY, bool FMA0 = false, int L = 1>
 __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j0) {
   static_assert(WM * WN == 4, "four waves");
+  constexpr bool GEN = COMB != DG_CARRY || FMA0;   // not one carried chain
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 16, TN = WTN / 16;
   constexpr int ACH = BM * (V3_BK / 8);        // 16-byte chunks per A slab
@@ -727,7 +738,62 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int buf) {
+  // tile combine state (GEN only): the open tile's accumulator is acc; the
+  // chain's running sum or the tree's stack hold the closed tiles
+  constexpr int NL = COMB == DG_TREE ? L : COMB == DG_SEQ ? 1 : 0;
+  floatx4 stk[NL > 0 ? NL : 1][TM][TN];
+  uint32_t count = 0;                                  // tiles closed
+  int64_t tile_end = k1;                               // end of the open tile
+  if constexpr (GEN) {
+    const int64_t len = k1 - k0, tk = a.tile_k;
+    const int64_t first = (a.tail_first && len % tk) ? len % tk : tk;
+    tile_end = k0 + (first < len ? first : len);
+  }
+  const floatx4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  auto close_tile = [&](bool last) {
+    if constexpr (COMB == DG_SEQ) {
+      if (count == 0) {
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < TN; ++ni) stk[0][mi][ni] = acc[mi][ni];
+      } else {
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < TN; ++ni) stk[0][mi][ni] = stk[0][mi][ni] + acc[mi][ni];
+      }
+    } else if constexpr (COMB == DG_TREE) {
+      // binary counter: fold the levels whose bit is set, park at the first clear one
+      bool parked = false;
+      static_for<0, NL>([&](auto lv) {
+        constexpr int LV = decltype(lv)::value;
+        if (!parked) {
+          if ((count >> LV) & 1u) {
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+              for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = stk[LV][mi][ni] + acc[mi][ni];
+          } else {
+#pragma unroll
+            for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+              for (int ni = 0; ni < TN; ++ni) stk[LV][mi][ni] = acc[mi][ni];
+            parked = true;
+          }
+        }
+      });
+    }
+    ++count;
+    if (COMB == DG_SEQ || !last) {
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = zero4;
+    }
+  };
+
+  auto compute = [&](int buf, int sl) {
     const uint16_t* As = As0 + buf * A_ELEMS;
     const uint16_t* Bs = Bs0 + buf * B_ELEMS;
 #pragma unroll
@@ -749,10 +815,33 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
             (lds_s4)(&Bs[8 * ldsB(kr1, n / 8) + (n & 7)]));
         bfr[ni] = shortx8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
       }
+      if constexpr (!GEN) {
 #pragma unroll
-      for (int mi = 0; mi < TM; ++mi)
+        for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16t<F16>(af[mi], bfr[ni], acc[mi][ni]);
+          for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma16t<F16>(af[mi], bfr[ni], acc[mi][ni]);
+      } else {
+        const int64_t kpos = k0 + (int64_t)sl * V3_BK + kk;   // this 32-k step (uniform)
+        if (kpos < k1) {
+#pragma unroll
+          for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < TN; ++ni) {
+              if constexpr (FMA0) {
+                const floatx4 w = mfma16t<F16>(af[mi], bfr[ni], zero4);
+                acc[mi][ni] = acc[mi][ni] + w;
+              } else {
+                acc[mi][ni] = mfma16t<F16>(af[mi], bfr[ni], acc[mi][ni]);
+              }
+            }
+          if constexpr (COMB != DG_CARRY) {
+            if (kpos + 32 >= tile_end) {
+              close_tile(tile_end >= k1);
+              tile_end = tile_end + a.tile_k < k1 ? tile_end + a.tile_k : k1;
+            }
+          }
+        }
+      }
     }
   };
 
@@ -766,13 +855,37 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
   for (int sl = 0; sl < nslab; sl += 2) {
     // even slab sl in buffer 0, its successor's registers in set 1
     gload(sl + 2, r0a, r0b);
-    compute(0);
+    compute(0, sl);
     lstore(1, r1a, r1b);
     __syncthreads();
     gload(sl + 3, r1a, r1b);
-    if (sl + 1 < nslab) compute(1);
+    if (sl + 1 < nslab) compute(1, sl + 1);
     lstore(0, r0a, r0b);
     __syncthreads();
+  }
+  // the part's value: the chain's sum, or the tree's stack folded low to high
+  if constexpr (COMB == DG_SEQ) {
+    if (count) {
+#pragma unroll
+      for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = stk[0][mi][ni];
+    }
+  } else if constexpr (COMB == DG_TREE) {
+    // acc holds the last tile's folded value, the entry of level ctz(count);
+    // the set levels above it meet it in increasing order
+    if (count) {
+      const int low = __builtin_ctz(count);
+      static_for<0, NL>([&](auto lv) {
+        constexpr int LV = decltype(lv)::value;
+        if (LV > low && ((count >> LV) & 1u)) {
+#pragma unroll
+          for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = stk[LV][mi][ni] + acc[mi][ni];
+        }
+      });
+    }
   }
 
   float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
@@ -821,6 +934,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
   v3_body<BM, BN, WM, WN, BK, F16>(a, (int64_t)ty * BM, (int64_t)tx * BN);
+}
+
+// Tile-combine descriptors (chain or tree, or fma = 0) on the v3 pipeline:
+// 128 x 128 blocks of four 64 x 64 waves, 32-k slabs, one wave per SIMD.
+// The tree's stack takes L x 64 registers per lane at that shape; from four
+// levels on the blocks are 128 x 64 (waves of 64 x 32), which halves it.
+template <int COMB, int L>
+constexpr int tc_bn() { return 64; }
+template <int COMB, bool FMA0, int L>
+constexpr int tc_bk() { return 32; }
+template <int COMB, int L>
+constexpr int tc_occ() { return COMB == DG_TREE && L >= 5 ? 1 : 2; }
+
+template <int COMB, bool FMA0, int L, bool F16>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(tc_occ<COMB, L>(), tc_occ<COMB, L>()))) void gemm_tc(GemmArgs a) {
+  constexpr int BN = tc_bn<COMB, L>();
+  const int tiles_m = (int)((a.M + 127) / 128);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  v3_body<128, BN, 2, 2, tc_bk<COMB, FMA0, L>(), F16, COMB, FMA0, L>(a, (int64_t)ty * 128, (int64_t)tx * BN);
 }
 
 template <int BM, int BN, int WM, int WN, int BK, bool F16>
@@ -1936,6 +2069,32 @@ hipError_t launch_gemm_v3(const GemmArgs& a, int tm, int tn, int occ, hipStream_
   if (tm == 32 && tn == 256) return launch_v3_t<32, 256, 1, 4, 64, false>(a, st);
   if (tm == 32 && tn == 128) return launch_v3_t<32, 128, 1, 4, 64, false>(a, st);
   return hipErrorInvalidValue;
+}
+
+template <int COMB, bool FMA0, int L>
+static hipError_t launch_tc_t(const GemmArgs& a, hipStream_t st) {
+  constexpr int BN = tc_bn<COMB, L>();
+  const int64_t tm = (a.M + 127) / 128, tn = (a.N + BN - 1) / BN;
+  dim3 grid((unsigned)(tm * tn), 1, (unsigned)a.S);
+  if (a.in_f16) hipLaunchKernelGGL((gemm_tc<COMB, FMA0, L, true>), grid, dim3(256), 0, st, a);
+  else hipLaunchKernelGGL((gemm_tc<COMB, FMA0, L, false>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_tc(const GemmArgs& a, int levels, hipStream_t st) {
+  const bool fma0 = a.fma == 0;
+  if (a.tile_combine == DG_CARRY) return fma0 ? launch_tc_t<DG_CARRY, true, 1>(a, st) : hipErrorInvalidValue;
+  if (a.tile_combine == DG_SEQ) return fma0 ? launch_tc_t<DG_SEQ, true, 1>(a, st) : launch_tc_t<DG_SEQ, false, 1>(a, st);
+  if (a.tile_combine != DG_TREE) return hipErrorInvalidValue;
+  switch (levels) {
+    case 2: return fma0 ? launch_tc_t<DG_TREE, true, 2>(a, st) : launch_tc_t<DG_TREE, false, 2>(a, st);
+    case 3: return fma0 ? launch_tc_t<DG_TREE, true, 3>(a, st) : launch_tc_t<DG_TREE, false, 3>(a, st);
+    case 4: return fma0 ? launch_tc_t<DG_TREE, true, 4>(a, st) : launch_tc_t<DG_TREE, false, 4>(a, st);
+    case 5: return fma0 ? launch_tc_t<DG_TREE, true, 5>(a, st) : launch_tc_t<DG_TREE, false, 5>(a, st);
+    case 6: return fma0 ? launch_tc_t<DG_TREE, true, 6>(a, st) : launch_tc_t<DG_TREE, false, 6>(a, st);
+    case 7: return fma0 ? launch_tc_t<DG_TREE, true, 7>(a, st) : launch_tc_t<DG_TREE, false, 7>(a, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 bool tiled_supported(int tm, int tn) {

@@ -104,6 +104,9 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tile_m, int tile_n, hipStrea
 bool tiled_supported(int tile_m, int tile_n);
 hipError_t launch_gemm_v3(const GemmArgs& a, int tile_m, int tile_n, int occupancy, hipStream_t s);
 bool v3_supported(int tile_m, int tile_n, int occupancy);
+// tile chain or tree, or fma = 0, on 128 x 64 tiled blocks (levels: the
+// tree's stack depth, 2..7; each part at most 2^levels tiles)
+hipError_t launch_gemm_tc(const GemmArgs& a, int levels, hipStream_t s);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)

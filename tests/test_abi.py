@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 500
+    assert dg.dg_version() == 501
     for s in range(8):
         assert dg.dg_strerror(s)
 
@@ -288,6 +288,23 @@ def test_argument_errors_need_no_gpu(dg):
                dg.dg_knobs(4, 16, 32, 0, 0, 4, 128)):
         assert lib.dg_gemm_knobs(sd.handle, 16, 16, None, 16, 8, 8, 64, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
+    # kernel 12 (tile chain or tree, or fma = 0, on the tiled layout): no
+    # other knob, no carried chain, no strided split, scalar path or e4m3 B,
+    # tile boundaries on 32-k steps, at most 128 tiles per tree part
+    tree = dg.Desc(tile_k=64, tile_combine="tree")
+    k12 = dg.dg_knobs(12, 0, 0, 0, 0, 0, 0, 0)
+    for desc, K in [(d, 512), (sd, 512), (sc, 512), (dg.Desc(tile_k=64, in_dtype="bf16_e4m3", fma=0), 512),
+                    (dg.Desc(tile_k=32, tile_combine="tree"), 8192), (dg.Desc(tile_k=64, tile_combine="seq",
+                                                                              tail="first"), 1000),
+                    (dg.Desc(mma="32x32x16", tile_k=64, fma=0), 512)]:
+        assert lib.dg_gemm_knobs(desc.handle, 16, 16, None, 16, 8, 64, K, ctypes.byref(k12), None) == \
+            dg.DG_ERR_UNSUPPORTED, desc.signature()
+    for kn in (dg.dg_knobs(12, 128, 128, 0, 0, 0, 0, 0), dg.dg_knobs(12, 0, 0, 1, 0, 0, 0, 0),
+               dg.dg_knobs(12, 0, 0, 0, 0, 4, 0, 0), dg.dg_knobs(13, 0, 0, 0, 0, 0, 0, 0)):
+        assert lib.dg_gemm_knobs(tree.handle, 16, 16, None, 16, 8, 64, 512, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED
+    assert lib.dg_gemm_knobs(tree.handle, 16, 16, None, 16, 8, 60, 512, ctypes.byref(k12), None) == \
+        dg.DG_ERR_UNSUPPORTED                                            # N % 8
     # RMS normalisation: the descriptor must name the sum of squares
     q = dg.Desc(reduce="sumsq")
     assert lib.dg_rmsnorm(d.handle, 16, None, 0.0, 16, 4, 5, None) == dg.DG_ERR_INVALID
