@@ -73,6 +73,13 @@ def build(verbose: bool = False) -> str:
     if spills:
         os.unlink(tmp)
         raise RuntimeError("kernels spill registers: " + ", ".join(spills))
+    # a kernel template whose host-side stub was not emitted links silently
+    # and fails only when the library is loaded
+    nm = subprocess.run(["nm", "--undefined-only", tmp], capture_output=True, text=True)
+    stubs = [l.split()[-1] for l in nm.stdout.splitlines() if "__device_stub__" in l]
+    if nm.returncode == 0 and stubs:
+        os.unlink(tmp)
+        raise RuntimeError("kernel stubs missing from the library: " + ", ".join(stubs[:4]))
     if verbose and out:
         print(out, file=sys.stderr)
     os.replace(tmp, LIB)
