@@ -549,7 +549,7 @@ def main():
             fp8[name] = {"us_per_launch": round(1e3 * t, 2),
                          "GB/s": round(B8.nbytes / (t * 1e-3) / 1e9, 1),
                          "bf16_packed_us": few.get(name, {}).get("packed_us")}
-        fp8["what"] = ("bf16 activations, OCP e4m3 weights (packed, 512-byte runs) widened exactly to bf16 in "
+        fp8["what"] = ("bf16 activations, OCP e4m3 weights (packed, 1 KB runs of 64 k) widened exactly to bf16 in "
                        "registers and folded by the bf16 instruction (the bf16 order on the widened values); "
                        "GB/s counts the weight's bytes (half of bf16's)")
     except Exception as exc:  # reported, never hidden

@@ -225,12 +225,15 @@ dg_status dg_gemm_noalloc(const dg_desc* d, const void* A, const void* B, const 
  * bytes (0 for K = 0 or N = 0; SIZE_MAX for a negative size). */
 size_t dg_packed_b_bytes(int64_t K, int64_t N);
 
-/* The packed form of an e4m3 B (DG_IN_BF16_E4M3): the same blocks and run
- * order, one byte per element, so every 32 x 16 block is a 512-byte run
- * (for l = 0 .. 63 in turn the 8 bytes B[k0 + 8 (l / 16) + e][n0 + l % 16]).
- * dg_packed_b8_bytes: ceil(N / 16) * ceil(K / 32) * 512 (SIZE_MAX as
- * dg_packed_b_bytes); dg_pack_b8 writes it from a row-major K x N byte
- * matrix, with the errors of dg_pack_b (B needs no alignment). */
+/* The packed form of an e4m3 B (DG_IN_BF16_E4M3), one byte per element:
+ * every 64 x 16 block (two 32-k blocks) is one 1 KB run, for l = 0 .. 63 in
+ * turn the 8 bytes B[k0 + 8 (l / 16) + e][n0 + l % 16] of the first block
+ * and then the 8 of the second (k0 + 32), so one 16-byte load per lane
+ * brings a lane its operands of both blocks; runs by column panel, then by
+ * k0 / 64; zeros past N and K.  dg_packed_b8_bytes: ceil(N / 16) *
+ * ceil(K / 64) * 1024 (SIZE_MAX as dg_packed_b_bytes); dg_pack_b8 writes it
+ * from a row-major K x N byte matrix, with the errors of dg_pack_b (B needs
+ * no alignment). */
 size_t dg_packed_b8_bytes(int64_t K, int64_t N);
 dg_status dg_pack_b8(const void* B, void* Bp, int64_t K, int64_t N, void* stream);
 
@@ -248,7 +251,8 @@ dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream)
  * 16 columns, split-K part and up to 64 rows of A).  For few-row products:
  * M <= 64.  Descriptors: carried accumulator (tile_combine CARRY), fma 1,
  * no leading short tile; contiguous parts whose interior cut points are
- * multiples of 32, or strided parts dealing tiles of 32 * 2^j k.
+ * multiples of 32 (64 for an e4m3 B), or strided parts dealing tiles of
+ * 32 * 2^j k (64 * 2^j for an e4m3 B).
  * DG_ERR_UNSUPPORTED for anything else (M > 64 included), DG_ERR_ALIGN if Bp
  * is not 16-byte aligned; errors otherwise as dg_gemm, and split-K uses the
  * same workspace. */

@@ -379,12 +379,14 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (packed) {
     if (scalar || p.tile_combine != DG_CARRY || p.fma != 1 || p.tail == DG_TAIL_FIRST || M > 64)
       return DG_ERR_UNSUPPORTED;
+    // runs of 32 k (bf16, binary16) or 64 k (e4m3): parts start on a run
+    const int64_t run_k = b8 ? 64 : 32;
     if (strided) {
-      const int64_t wf = p.split_tile / 32;
-      if (p.split_tile % 32 || (wf & (wf - 1))) return DG_ERR_UNSUPPORTED;
+      const int64_t wf = p.split_tile / run_k;
+      if (p.split_tile % run_k || (wf & (wf - 1))) return DG_ERR_UNSUPPORTED;
     } else {
       for (int s = 1; s < a.S; ++s)
-        if (a.cuts[s] % 32) return DG_ERR_UNSUPPORTED;
+        if (a.cuts[s] % run_k) return DG_ERR_UNSUPPORTED;
     }
     if (!aligned(B, 16)) return DG_ERR_ALIGN;
     // every buffer offset (the packed B, A's rows) stays in 31 bits
@@ -392,8 +394,8 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
       return DG_ERR_UNSUPPORTED;
     panel_tms = tm ? tm / 16 : (M <= 16 ? 1 : M <= 32 ? 2 : 4);
     panel_avec = K % 8 == 0 && aligned(A, 16);
-    panel_depth = depth ? depth : dg::panel_default_depth(panel_tms, panel_avec);
-    if (!dg::panel_supported(panel_tms, panel_depth, panel_avec)) return DG_ERR_UNSUPPORTED;
+    panel_depth = depth ? depth : dg::panel_default_depth(panel_tms, panel_avec, b8);
+    if (!dg::panel_supported(panel_tms, panel_depth, panel_avec, b8)) return DG_ERR_UNSUPPORTED;
   }
 
   hipStream_t st = (hipStream_t)stream;
@@ -613,8 +615,10 @@ dg_status dg_pack_b(const void* B, void* Bp, int64_t K, int64_t N, void* stream)
 }
 
 size_t dg_packed_b8_bytes(int64_t K, int64_t N) {
-  const size_t b = dg_packed_b_bytes(K, N);
-  return b == SIZE_MAX ? SIZE_MAX : b / 2;
+  if (K < 0 || N < 0) return SIZE_MAX;
+  const uint64_t panels = (uint64_t)(N + 15) / 16, runs = (uint64_t)(K + 63) / 64;
+  if (panels && runs > (SIZE_MAX / 1024) / panels) return SIZE_MAX;
+  return (size_t)(panels * runs * 1024);
 }
 
 dg_status dg_pack_b8(const void* B, void* Bp, int64_t K, int64_t N, void* stream) {
@@ -622,7 +626,7 @@ dg_status dg_pack_b8(const void* B, void* Bp, int64_t K, int64_t N, void* stream
   if (K == 0 || N == 0) return DG_OK;
   if (!B || !Bp) return DG_ERR_INVALID;
   if (!aligned(Bp, 16)) return DG_ERR_ALIGN;
-  if (dg_packed_b_bytes(K, N) == SIZE_MAX || (N + 15) / 16 * ((K + 31) / 32) > ((int64_t)1 << 31) * 4)
+  if (dg_packed_b8_bytes(K, N) == SIZE_MAX || (N + 15) / 16 * ((K + 63) / 64) > ((int64_t)1 << 31) * 4)
     return DG_ERR_SHAPE;
   if (dg::launch_pack_b8((const uint8_t*)B, (uint8_t*)Bp, K, N, (hipStream_t)stream) != hipSuccess)
     return DG_ERR_HIP;

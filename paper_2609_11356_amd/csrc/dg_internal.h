@@ -123,8 +123,8 @@ hipError_t launch_gemm_skinny_dma(const GemmArgs& a, int tile_m, int tile_n, int
 hipError_t launch_pack_b(const uint16_t* B, uint16_t* Bp, int64_t K, int64_t N, hipStream_t s);
 hipError_t launch_pack_b8(const uint8_t* B, uint8_t* Bp, int64_t K, int64_t N, hipStream_t s);
 hipError_t launch_gemm_panel(const GemmArgs& a, int tms, int depth, bool avec, hipStream_t s);
-bool panel_supported(int tms, int depth, bool avec);
-int panel_default_depth(int tms, bool avec);
+bool panel_supported(int tms, int depth, bool avec, bool b8);
+int panel_default_depth(int tms, bool avec, bool b8);
 bool skinny_dma_supported(int tile_m, int tile_n, int slots, int slab_k);
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_rowsum(const RowsumArgs& a, hipStream_t s);

@@ -24,11 +24,14 @@
 // (width a multiple of 32).  Blocks past the part's end hold zeros, whose
 // chunks leave the accumulators unchanged.
 //
-// An e4m3 B (one byte per element) packs the same way into 512-byte runs
-// (8 bytes per lane); the wave widens each lane's 8 values to bf16 with the
-// part's conversion instruction (exact) just before the bf16 instruction, so
-// the order and bits are those of the bf16 GEMM on the widened B, with half
-// the bytes streamed.
+// An e4m3 B (one byte per element) packs two k blocks per 1 KB run: lane
+// l's 16 bytes are its 8 k of the first block, then its 8 k of the second,
+// so each load still moves 1 KB (a 512-byte run per block measured slower
+// than bf16 at one row: the loads, not the bytes, set the pace) and e4m3
+// parts start on 64-k runs.  The wave widens each block's 8 values to bf16
+// with the part's conversion instruction (exact) just before the bf16
+// instruction, so the order and bits are those of the bf16 GEMM on the
+// widened B, with half the bytes streamed.
 #include <type_traits>
 
 #include "dg_device.h"
@@ -40,10 +43,6 @@ namespace dg {
 namespace {
 
 constexpr uint32_t kOOB = 0x80000000u;   // a buffer offset past any record: reads zero
-
-__device__ __forceinline__ u32x4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
 
 // 8 values of one A row from k on, each checked against K (rows whose 16-byte
 // runs are not 16-byte aligned: K % 8 != 0 or A itself unaligned).
@@ -64,38 +63,45 @@ __device__ __forceinline__ u32x4 load_a_elems(__amdgpu_buffer_rsrc_t r, int64_t 
 }  // namespace
 
 // BT: the B operand, 0 bf16, 1 binary16 (A binary16 too), 2 OCP e4m3 bytes
-// (512-byte runs, widened to bf16 before the instruction)
+// (1 KB runs of two blocks, widened to bf16 before the instruction).  The
+// ring holds D runs (BPR blocks each) with the A fragments of their blocks.
 template <int TMS, int D, bool AVEC, bool STRIDED, int BT>
 __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
   constexpr bool F16 = BT == 1;
-  constexpr int RUN = BT == 2 ? 512 : 1024;   // bytes of one block's run
+  constexpr int BPR = BT == 2 ? 2 : 1;         // k blocks per 1 KB run
+  constexpr int RUN = 1024;
+  static_assert(!AVEC || (D - 1) * (1 + BPR * TMS) <= 63, "the ring's waits fit the load counter");
   const int lane = threadIdx.x;
   const int64_t panel = blockIdx.x;
   const int64_t i0 = (int64_t)blockIdx.y * 16 * TMS, j0 = panel * 16;
   const int s = blockIdx.z;
   // every k block index and byte offset fits 31 bits (the host keeps the
   // packed B under 2 GiB and A's rows under 2 GiB)
-  const int KB = (int)((a.K + 31) / 32), K = (int)a.K;
-  // blocks of part s: contiguous from fb0, or dealt tiles of 2^lgw blocks
-  int nf = 0, fb0 = 0, lgw = 0;
+  const int KR = (int)((a.K + 32 * BPR - 1) / (32 * BPR)), K = (int)a.K;
+  // blocks (nf) and runs (nr) of part s: contiguous from run r0 (the host
+  // puts interior cuts on run boundaries), or dealt tiles of 2^lgw blocks
+  // (2^lgr runs)
+  int nf = 0, r0 = 0, lgr = 0;
   if constexpr (STRIDED) {
-    lgw = __builtin_ctz((unsigned)(a.split_w / 32));
+    const int lgw = __builtin_ctz((unsigned)(a.split_w / 32));
+    lgr = lgw - (BPR == 2 ? 1 : 0);
     const int w = (int)a.split_w, ntile = (K + w - 1) / w;
     nf = ntile > s ? ((ntile - s + a.S - 1) / a.S) << lgw : 0;
   } else if (a.cuts[s + 1] > a.cuts[s]) {
-    fb0 = (int)(a.cuts[s] / 32);
-    nf = (int)((a.cuts[s + 1] + 31) / 32) - fb0;
+    r0 = (int)(a.cuts[s] / (32 * BPR));
+    nf = (int)((a.cuts[s + 1] + 31) / 32) - BPR * r0;
   }
-  const int64_t recA = (a.M - i0) * a.K * 2, recB = ((a.N + 15) / 16) * (int64_t)KB * RUN;
+  const int nr = (nf + BPR - 1) / BPR;
+  const int64_t recA = (a.M - i0) * a.K * 2, recB = ((a.N + 15) / 16) * (int64_t)KR * RUN;
   const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(a.A + i0 * a.K), (short)0, (int)(recA < 0x7fffffff ? recA : 0x7fffffff), 0x00020000);
-  // the panel's runs: a base moved to the panel, the block in the scalar offset
+  // the panel's runs: a base moved to the panel, the run in the scalar offset
   const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc((void*)a.B, (short)0, (int)recB, 0x00020000);
   const int kl = 8 * (lane >> 4);   // the lane's first k within a block
   // lane constants: B's run slot; A's row run (out of range past M), and the
   // first block whose 8 k of this lane lie at or past K (only the last block
   // when K % 32 != 0).  A block's offset goes in the scalar buffer offset.
-  const uint32_t vb = (uint32_t)(panel * KB * RUN) + (uint32_t)lane * (RUN / 64);
+  const uint32_t vb = (uint32_t)(panel * KR * RUN) + (uint32_t)lane * 16;
   const int flim = (K - kl + 31) / 32;
   uint32_t va[TMS];
 #pragma unroll
@@ -103,35 +109,35 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
     const int row = 16 * mi + (lane & 15);
     va[mi] = (i0 + row < a.M) ? (uint32_t)((row * K + kl) * 2) : kOOB;
   }
-  // blocks q < nfe are real (a strided part's last dealt tile may run past
-  // K's last block: those blocks read as zeros)
-  const int nfe = STRIDED ? nf : (nf < KB - fb0 ? nf : KB - fb0);
+  // runs g < nre are real (a strided part's last dealt tile may run past
+  // K's last run: those runs read as zeros)
+  const int nre = STRIDED ? nr : (nr < KR - r0 ? nr : KR - r0);
 
-  // block q of the part -> global k block
-  auto block_of = [&](int q) -> int {
-    if constexpr (STRIDED) return ((s + a.S * (q >> lgw)) << lgw) + (q & ((1 << lgw) - 1));
-    else return fb0 + q;
+  // run g of the part -> global run
+  auto run_of = [&](int g) -> int {
+    if constexpr (STRIDED) return ((s + a.S * (g >> lgr)) << lgr) + (g & ((1 << lgr) - 1));
+    else return r0 + g;
   };
-  // B's ring: 16 bytes (bf16, binary16) or 8 bytes (e4m3) per lane and block
-  using BReg = std::conditional_t<BT == 2, u32x2, u32x4>;
-  BReg rb[D];
-  u32x4 ra[D][TMS];
-  auto load = [&](int u, int q) {
-    const int f = block_of(q);
-    const bool ok = q < nfe && (!STRIDED || f < KB);
-    const int so = ok ? f : 0;
-    if constexpr (BT == 2)
-      rb[u] = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rB, ok ? vb : kOOB, so * RUN, 0));
-    else
-      rb[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, ok ? vb : kOOB, so * RUN, 0));
+  // the ring: one run of B (16 bytes per lane) and the A fragments of its blocks
+  u32x4 rb[D];
+  u32x4 ra[D][BPR][TMS];
+  auto load = [&](int u, int g) {
+    const int R = run_of(g);
+    const bool ok = g < nre && (!STRIDED || R < KR);
+    const int so = ok ? R : 0;
+    rb[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rB, ok ? vb : kOOB, so * RUN, 0));
 #pragma unroll
-    for (int mi = 0; mi < TMS; ++mi) {
-      if constexpr (AVEC) {
-        ra[u][mi] = __builtin_bit_cast(
-            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, (ok && f < flim) ? va[mi] : kOOB, so * 64, 0));
-      } else {
-        const int row = 16 * mi + (lane & 15);
-        ra[u][mi] = load_a_elems(rA, (int64_t)row * a.K, (int64_t)f * 32 + kl, a.K, ok && i0 + row < a.M);
+    for (int h = 0; h < BPR; ++h) {
+      const int f = BPR * so + h;
+#pragma unroll
+      for (int mi = 0; mi < TMS; ++mi) {
+        if constexpr (AVEC) {
+          ra[u][h][mi] = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rA, (ok && f < flim) ? va[mi] : kOOB, f * 64, 0));
+        } else {
+          const int row = 16 * mi + (lane & 15);
+          ra[u][h][mi] = load_a_elems(rA, (int64_t)row * a.K, (int64_t)f * 32 + kl, a.K, ok && i0 + row < a.M);
+        }
       }
     }
   };
@@ -140,28 +146,32 @@ __global__ __launch_bounds__(64) void gemm_panel(GemmArgs a) {
 #pragma unroll
   for (int mi = 0; mi < TMS; ++mi) acc[mi] = floatx4{0.f, 0.f, 0.f, 0.f};
   // The loads stay in ring order (no scheduling across the barriers): the
-  // waits count on block q's loads being older than those of q + 1.
+  // waits count on run g's loads being older than those of g + 1.
   static_for<0, D>([&](auto u) {
     load(u, u);
     __builtin_amdgcn_sched_barrier(0);
   });
-  for (int base = 0; base < nf; base += D) {
+  for (int base = 0; base < nr; base += D) {
     static_for<0, D>([&](auto u) {
-      const int q = base + u;
-      // this block's loads are the oldest D - 1 + 1 groups in flight
-      if constexpr (AVEC) __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 1) * (1 + TMS)));
-      if (q < nf) {
-        u32x4 bw;
-        if constexpr (BT == 2)
-          bw = u32x4{e4m3x2_bf16x2<false>(rb[u][0]), e4m3x2_bf16x2<true>(rb[u][0]),
-                     e4m3x2_bf16x2<false>(rb[u][1]), e4m3x2_bf16x2<true>(rb[u][1])};
-        else
-          bw = rb[u];
+      const int g = base + u;
+      // this run's loads are the oldest of D groups in flight
+      if constexpr (AVEC) __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 1) * (1 + BPR * TMS)));
 #pragma unroll
-        for (int mi = 0; mi < TMS; ++mi)
-          acc[mi] = mfma16t<F16>(__builtin_bit_cast(shortx8, ra[u][mi]), __builtin_bit_cast(shortx8, bw), acc[mi]);
+      for (int h = 0; h < BPR; ++h) {
+        if (BPR * g + h < nf) {
+          u32x4 bw;
+          if constexpr (BT == 2)
+            bw = u32x4{e4m3x2_bf16x2<false>(rb[u][2 * h]), e4m3x2_bf16x2<true>(rb[u][2 * h]),
+                       e4m3x2_bf16x2<false>(rb[u][2 * h + 1]), e4m3x2_bf16x2<true>(rb[u][2 * h + 1])};
+          else
+            bw = rb[u];
+#pragma unroll
+          for (int mi = 0; mi < TMS; ++mi)
+            acc[mi] = mfma16t<F16>(__builtin_bit_cast(shortx8, ra[u][h][mi]), __builtin_bit_cast(shortx8, bw),
+                                   acc[mi]);
+        }
       }
-      load(u, q + D);
+      load(u, g + D);
       __builtin_amdgcn_sched_barrier(0);
     });
   }
@@ -194,31 +204,34 @@ __global__ __launch_bounds__(256) void pack_b(const uint16_t* __restrict__ B, ui
   *(u32x4*)&Bp[t * 8] = u32x4{w[0], w[1], w[2], w[3]};
 }
 
-// The same for one-byte elements: 8 bytes per lane, 512-byte runs.
+// One-byte elements: every 64 x 16 block (two k blocks) is one 1 KB run, lane
+// l's 16 bytes holding its 8 k of the first block, then its 8 k of the
+// second: thread t writes lane l = t % 64 of run t / 64 (panel p = run / KR,
+// run r = run % KR of the panel).
 __global__ __launch_bounds__(256) void pack_b8(const uint8_t* __restrict__ B, uint8_t* __restrict__ Bp, int64_t K,
                                                int64_t N, int64_t runs) {
   const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (t >= runs * 64) return;
-  const int64_t run = t / 64, KB = (K + 31) / 32;
+  const int64_t run = t / 64, KR = (K + 63) / 64;
   const int l = (int)(t % 64);
-  const int64_t p = run / KB, f = run % KB;
-  const int64_t n = p * 16 + (l & 15), k0 = f * 32 + 8 * (l >> 4);
-  uint32_t w[2];
+  const int64_t p = run / KR, r = run % KR;
+  const int64_t n = p * 16 + (l & 15), k0 = r * 64 + 8 * (l >> 4);
+  uint32_t w[4];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {
+  for (int q = 0; q < 4; ++q) {
     uint32_t v = 0;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const int64_t k = k0 + 4 * h + e;
+      const int64_t k = k0 + 32 * (q >> 1) + 4 * (q & 1) + e;
       v |= (uint32_t)((n < N && k < K) ? B[k * N + n] : 0) << (8 * e);
     }
-    w[h] = v;
+    w[q] = v;
   }
-  *(u32x2*)&Bp[t * 8] = u32x2{w[0], w[1]};
+  *(u32x4*)&Bp[t * 16] = u32x4{w[0], w[1], w[2], w[3]};
 }
 
 hipError_t launch_pack_b8(const uint8_t* B, uint8_t* Bp, int64_t K, int64_t N, hipStream_t st) {
-  const int64_t runs = ((N + 15) / 16) * ((K + 31) / 32);
+  const int64_t runs = ((N + 15) / 16) * ((K + 63) / 64);
   const int64_t blocks = (runs * 64 + 255) / 256;
   if (blocks == 0) return hipSuccess;
   hipLaunchKernelGGL(pack_b8, dim3((unsigned)blocks), dim3(256), 0, st, B, Bp, K, N, runs);
@@ -233,6 +246,10 @@ hipError_t launch_pack_b(const uint16_t* B, uint16_t* Bp, int64_t K, int64_t N, 
   return hipGetLastError();
 }
 
+// an e4m3 ring of D runs holds 2 D TMS A fragments (16 bytes per lane each),
+// and its waits count up to (D - 1)(1 + 2 TMS) loads (the counter holds 63)
+constexpr bool panel_b8_fits(int tms, int d) { return 2 * d * tms <= 48 && (d - 1) * (1 + 2 * tms) <= 63; }
+
 template <int TMS, int D, bool AVEC>
 static hipError_t launch_panel_t(const GemmArgs& a, hipStream_t st) {
   dim3 grid((unsigned)((a.N + 15) / 16), (unsigned)((a.M + 16 * TMS - 1) / (16 * TMS)), (unsigned)a.S);
@@ -243,7 +260,11 @@ static hipError_t launch_panel_t(const GemmArgs& a, hipStream_t st) {
     if (strided) hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, true, BT>), grid, dim3(64), 0, st, a);
     else hipLaunchKernelGGL((gemm_panel<TMS, D, AVEC, false, BT>), grid, dim3(64), 0, st, a);
   };
-  if (bt == 2) go(std::integral_constant<int, 2>{});
+  if (bt == 2) {
+    // two blocks per run: the rings whose A fragments fit the registers
+    if constexpr (panel_b8_fits(TMS, D)) go(std::integral_constant<int, 2>{});
+    else return hipErrorInvalidValue;
+  }
   else if (bt == 1) go(std::integral_constant<int, 1>{});
   else go(std::integral_constant<int, 0>{});
   return hipGetLastError();
@@ -255,13 +276,16 @@ static hipError_t launch_panel_t(const GemmArgs& a, hipStream_t st) {
   X(1, 8) X(1, 16) X(1, 24) X(1, 32) X(2, 8) X(2, 12) X(2, 16) X(4, 6) X(4, 10)
 #define DG_PANEL_ELEM_LIST(X) X(1, 4) X(2, 2) X(4, 1)
 
-// Ring depths measured best on MI355X (4096 x 4096 B, M = 1, 7, 32, 64)
-int panel_default_depth(int tms, bool avec) {
+// Ring depths measured best on MI355X (4096 x 4096 B, M = 1, 7, 32, 64);
+// an e4m3 ring's runs hold two blocks each
+int panel_default_depth(int tms, bool avec, bool b8) {
   if (!avec) return tms == 1 ? 4 : tms == 2 ? 2 : 1;
+  if (b8) return tms == 1 ? 8 : tms == 2 ? 8 : 6;
   return tms == 1 ? 16 : tms == 2 ? 16 : 10;
 }
 
-bool panel_supported(int tms, int depth, bool avec) {
+bool panel_supported(int tms, int depth, bool avec, bool b8) {
+  if (b8 && !panel_b8_fits(tms, depth)) return false;
 #define DG_PANEL_HAS(T_, D_) \
   if (tms == T_ && depth == D_) return true;
   if (avec) {

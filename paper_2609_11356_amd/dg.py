@@ -308,16 +308,16 @@ def dg_packed_b_bytes(K: int, N: int) -> int:
 
 class PackedB:
     """B (K x N, bf16 or float16, or e4m3 bytes) in the packed form
-    dg_gemm_packed reads: every 32 x 16 block one run (1 KB, or 512 bytes
-    for e4m3) in the 16x16x32 MFMA's B operand layout, runs by column panel
-    then k block.  data is a uint8 device tensor; dtype the element type."""
+    dg_gemm_packed reads: every 32 x 16 block (64 x 16 for e4m3) one 1 KB
+    run in the 16x16x32 MFMA's B operand layout, runs by column panel then
+    k.  data is a uint8 device tensor; dtype the element type."""
 
     def __init__(self, data, K: int, N: int, dtype):
         self.data, self.K, self.N, self.dtype = data, int(K), int(N), dtype
 
 
 def dg_packed_b8_bytes(K: int, N: int) -> int:
-    """Bytes of the packed form of a K x N e4m3 matrix: ceil(N/16) ceil(K/32) 512."""
+    """Bytes of the packed form of a K x N e4m3 matrix: ceil(N/16) ceil(K/64) 1024."""
     return int(lib().dg_packed_b8_bytes(int(K), int(N)))
 
 

@@ -44,6 +44,39 @@ def run(dg, desc, A, B8, bias=None, packed=False, knobs=None):
     return host_bits(C)
 
 
+@pytest.mark.parametrize("K,N", [(100, 37), (64, 16), (1000, 160), (31, 5)])
+def test_pack_layout(dg, K, N):
+    """dg_pack_b8 against the layout written out from its definition: every
+    64 x 16 block one 1 KB run, lane l's 8 k of the first 32-k block, then
+    its 8 k of the second."""
+    B8 = inputs.e4m3_uniform(K + N, (K, N))
+    Bp = dg.dg_pack_b(dev_u8(B8))
+    got = Bp.data.cpu().numpy()[:dg.dg_packed_b8_bytes(K, N)]
+    KR, NP = -(-K // 64), -(-N // 16)
+    Bz = np.zeros((KR * 64, NP * 16), np.uint8)
+    Bz[:K, :N] = B8
+    want = np.zeros((NP, KR, 64, 2, 8), np.uint8)
+    for l in range(64):
+        for h in range(2):
+            for e in range(8):
+                want[:, :, l, h, e] = Bz[np.arange(KR)[None, :] * 64 + 32 * h + 8 * (l // 16) + e,
+                                         np.arange(NP)[:, None] * 16 + l % 16]
+    assert np.array_equal(got, want.reshape(-1))
+
+
+def test_packed_refuses_parts_off_the_64k_runs(dg):
+    """e4m3 runs hold 64 k: parts must start on one (bf16's 32-k parts are
+    refused for an e4m3 B)."""
+    A, B8 = inputs.normal_bf16(1, (4, 256)), inputs.e4m3_uniform(2, (256, 32))
+    for desc in (dict(tile_k=32, split_k=2, k_cuts=[96]), dict(tile_k=32, split_k=2, split_layout="strided",
+                                                               split_tile=32)):
+        with pytest.raises(dg.DgError) as e:
+            run(dg, desc, A, B8, packed=True)
+        assert e.value.status == dg.DG_ERR_UNSUPPORTED, desc
+    got = run(dg, dict(tile_k=32, split_k=2, k_cuts=[128]), A, B8, packed=True)
+    assert_bits_equal(got, oracle.gemm(dict(tile_k=32, split_k=2, k_cuts=[128], in_dtype="bf16_e4m3"), A, B8), "cut 128")
+
+
 @pytest.mark.parametrize("packed", [False, True])
 def test_every_code_widens_exactly(dg, packed):
     """Row k0 of B holds the 256 codes (one per column), every other row
@@ -69,6 +102,7 @@ DESCS = [
     dict(tile_k=64, out="bf16", epilogue="bias_silu"),
     dict(tile_k=64, split_k=3, split_combine="tree"),
     dict(tile_k=64, split_k=4, split_layout="strided", split_tile=64, out="bf16"),
+    dict(tile_k=64, split_k=2, split_layout="strided", split_tile=256),
     dict(tile_k=32, tile_combine="tree", fma=0),                 # row-major only
 ]
 

@@ -121,6 +121,8 @@ def test_library_accepts_and_refuses_e4m3_descriptors():
             dg.DG_ERR_UNSUPPORTED, kern
     # a row-major e4m3 B needs no 2-byte alignment; misaligned A is still refused
     assert lib.dg_gemm(d.handle, 17, 16, None, 16, 8, 8, 8, None) == dg.DG_ERR_ALIGN
-    assert dg.dg_packed_b8_bytes(32, 16) == 512 and dg.dg_packed_b8_bytes(33, 17) == 2048
+    assert dg.dg_packed_b8_bytes(32, 16) == 1024 and dg.dg_packed_b8_bytes(64, 16) == 1024
+    assert dg.dg_packed_b8_bytes(33, 17) == 2048 and dg.dg_packed_b8_bytes(65, 17) == 4096
+    assert dg.dg_packed_b8_bytes(-1, 16) == 2 ** 64 - 1
     assert lib.dg_pack_b8(16, 8, 8, 8, None) == dg.DG_ERR_ALIGN        # Bp needs 16 bytes
     assert lib.dg_pack_b8(None, 16, 8, 8, None) == dg.DG_ERR_INVALID
