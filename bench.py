@@ -133,6 +133,15 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", epi_round="final")
         run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr)
         what = "fused MLP GEMM 2048x14336x4096"
+    elif args.only in ("tile_tree", "fma0"):
+        # the tile-combine kernel at the sweep's M = 1024 shape
+        A, B = inputs.sweep_activations(1, rows=4096)[:1024], inputs.sweep_weight(2)
+        dd = dict(tile_k=256, tile_combine="tree") if args.only == "tile_tree" else dict(tile_k=64, fma=0)
+        D = dg.Desc(mma="16x16x32", out="bf16", **dd)
+        what = "sweep GEMM M=1024 with %s" % dd
+        dA, dB = d_bf16(A), d_bf16(B)
+        C = torch.empty((1024, 4096), dtype=torch.bfloat16, device=dev)
+        run = lambda: dg.dg_gemm(D, dA, dB, None, C, stream=sptr)
     elif args.only in ("sweep128", "sweep1024", "sweep4096"):
         M = int(args.only[5:])
         A, B = inputs.sweep_activations(1, rows=4096)[:M], inputs.sweep_weight(2)
@@ -204,12 +213,13 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
-    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode", "gemv_packed", "decode_packed", "sweep128",
-                                        "sweep1024", "sweep4096"),
+    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode", "gemv_packed", "decode_packed", "tile_tree",
+                                       "fma0", "sweep128", "sweep1024", "sweep4096"),
                     default=None,
                     help="profiling runs: launch only the fused MLP GEMM, the M=1 sweep GEMM, "
                          "the split-K decode (each on the row-major or the packed weight), one sweep "
-                         "GEMM (M=128, 1024, 4096), or a plain 1 GiB device copy (the calibration "
+                         "GEMM (M=128, 1024, 4096), the M=1024 sweep GEMM under a tile-tree or fma=0 "
+                         "descriptor, or a plain 1 GiB device copy (the calibration "
                          "kernel for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
