@@ -599,21 +599,24 @@ __device__ __forceinline__ void tiled_body(const GemmArgs& a, int64_t i0, int64_
   // Epilogue through LDS, one 16-row strip of every wave at a time: the
   // accumulators are parked as fp32, then each lane finishes 4 consecutive
   // columns (bias, SiLU, rounding) and stores them with one vector store.
-  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
-  static_assert(4 * 16 * WTN * 4 <= (int)sizeof(smem), "epilogue staging fits");
+  // staging rows of pitch WTN + 4 floats: the four row groups a write
+  // instruction covers (rows 4 apart) start 16 banks apart
+  constexpr int CSP = WTN + 4;
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
+  static_assert(4 * 16 * CSP * 4 <= (int)sizeof(smem), "epilogue staging fits");
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
     __syncthreads();
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * WTN + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
     __syncthreads();
 #pragma unroll 1
     for (int q = lane; q < 16 * WTN / 4; q += 64) {
       const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
       const int64_t i = i0 + wm * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
-      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * WTN + cc]);
+      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
     }
   }
 }
@@ -888,21 +891,24 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
     }
   }
 
-  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * WTN;
-  static_assert(4 * 16 * WTN * 4 <= (int)sizeof(smem), "epilogue staging fits");
+  // staging rows of pitch WTN + 4 floats: the four row groups a write
+  // instruction covers (rows 4 apart) start 16 banks apart
+  constexpr int CSP = WTN + 4;
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
+  static_assert(4 * 16 * CSP * 4 <= (int)sizeof(smem), "epilogue staging fits");
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
     __syncthreads();
 #pragma unroll
     for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * WTN + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
     __syncthreads();
 #pragma unroll 1
     for (int q = lane; q < 16 * WTN / 4; q += 64) {
       const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
       const int64_t i = i0 + wm * WTM + 16 * mi + rr, j = j0 + wn * WTN + cc;
-      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * WTN + cc]);
+      if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
     }
   }
 }
