@@ -127,6 +127,28 @@ def test_all_ones_count(dg, K, S):
     assert np.all(got == K), np.unique(got)
 
 
+@pytest.mark.parametrize("desc", [dict(tile_k=64, split_k=64, split_combine="tree"),
+                                  dict(tile_k=32, split_k=64, split_combine="seq", partial="bf16", merge="bf16",
+                                       out="bf16"),
+                                  dict(tile_k=64, split_k=64, split_layout="strided", split_tile=64,
+                                       split_combine="tree")])
+def test_maximum_split(dg, desc):
+    """The largest split a descriptor holds (64 parts, DG_MAX_SPLIT) on the
+    MFMA path, row-major and packed B, against the oracle on every output."""
+    import torch
+    M, N, K = 5, 40, 4088       # 64 parts of 64 k under the span rule, the last one 56
+    A, B = inputs.spread_bf16(51, (M, K)), inputs.spread_bf16(52, (K, N))
+    want = oracle.gemm(desc, A, B)
+    print("maximum split", desc, flush=True)
+    assert_bits_equal(run(dg, desc, A, B), want, "row-major %s" % desc)
+    if desc.get("split_layout") == "strided" or desc["tile_k"] % 32 == 0:
+        out_bf16 = desc.get("out") == "bf16"
+        C = torch.full((M, N), float("nan"), dtype=torch.bfloat16 if out_bf16 else torch.float32, device="cuda")
+        dg.dg_gemm_packed(dg.Desc(**desc), dev_bf16(A), dg.dg_pack_b(dev_bf16(B)), None, C)
+        torch.cuda.synchronize()
+        assert_bits_equal(host_bits(C), want, "packed %s" % desc)
+
+
 def test_k_zero_gives_epilogue_of_zero(dg):
     import torch
     bias = inputs.normal_bf16(1, (16,), 1.0)
