@@ -131,8 +131,10 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         dA, dB, db = d_bf16(A), d_bf16(B), d_bf16(bias)
         C = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
         D = dg.Desc(mma="16x16x32", tile_k=64, out="bf16", epilogue="bias_silu", epi_round="final")
-        run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr)
-        what = "fused MLP GEMM 2048x14336x4096"
+        # --block-order n: the mixed-width kernel with block order n (speed only)
+        kn = dict(kernel=6, order=args.block_order) if args.block_order else None
+        run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr, knobs=kn)
+        what = "fused MLP GEMM 2048x14336x4096" + (", block order %d" % args.block_order if kn else "")
     elif args.only in ("tile_tree", "fma0"):
         # the tile-combine kernel at the sweep's M = 1024 shape
         A, B = inputs.sweep_activations(1, rows=4096)[:1024], inputs.sweep_weight(2)
@@ -221,6 +223,9 @@ def main():
                          "GEMM (M=128, 1024, 4096), the M=1024 sweep GEMM under a tile-tree or fma=0 "
                          "descriptor, or a plain 1 GiB device copy (the calibration "
                          "kernel for HBM byte counters)")
+    ap.add_argument("--block-order", type=int, choices=(0, 1, 2, 3), default=0,
+                    help="with --only mlp: run the mixed-width kernel with this block order (1 row-major, "
+                         "2 groups of eight block rows, 3 the same with each XCD given a contiguous range)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
