@@ -11,6 +11,7 @@ import pytest
 
 import oracle
 from tests import test_oracle_attention as attn
+from tests import test_oracle_fp8 as fp8
 from tests import test_oracle_pins as pins
 
 HERE = os.path.dirname(os.path.abspath(oracle.__file__))
@@ -99,8 +100,20 @@ MUTANTS = {
     "attention score scaled before the dot product ends": ("float v = acc * qk_scale;",
                                                            "float v = acc * qk_scale * 1.0000001f;"),
     "exp2 polynomial one term short": ("  p = fmaf(p, f, c6);\n", ""),
-    "binary16 exponent bias off by one": ("eb = f16 ? 5 : 8, bias = f16 ? 15 : 127;",
-                                          "eb = f16 ? 5 : 8, bias = f16 ? 14 : 127;"),
+    "binary16 exponent bias off by one": ("bias = f16 == 2 ? 7 : f16 ? 15 : 127;",
+                                          "bias = f16 == 2 ? 7 : f16 ? 14 : 127;"),
+    "e4m3 exponent bias off by one": ("bias = f16 == 2 ? 7 : f16 ? 15 : 127;",
+                                      "bias = f16 == 2 ? 8 : f16 ? 15 : 127;"),
+    "fp8 group grid one bit coarser": ("#define F8_GW 13", "#define F8_GW 12"),
+    "fp8 chunk grid one bit finer": ("#define F8_W 24", "#define F8_W 25"),
+    "fp8 result grid one bit finer": ("#define F8_F 31", "#define F8_F 32"),
+    "fp8 accumulator kept one binade lower": ("#define F8_DROP 25", "#define F8_DROP 26"),
+    "fp8 accumulator never left out": ("    if (xacc_lead >= E - F8_DROP) xacc_add_int(&x, neg, m, e);",
+                                       "    (void)xacc_lead; xacc_add_int(&x, neg, m, e);"),
+    "fp8 chunks of 8 products": ("const int cw = (f16 == 2) ? 16 : 8;", "const int cw = 8;"),
+    "fp8 group sums truncated toward zero": (
+        "return v >= 0 ? (v >> s) : -((-v + ((int64_t)1 << s) - 1) >> s);",
+        "return v >= 0 ? (v >> s) : -((-v) >> s);"),
     "binary16 product scale off by one": ("const int fb2 = 2 * op_frac(f16);",
                                           "const int fb2 = 2 * op_frac(f16) - f16;"),
 }
@@ -145,6 +158,10 @@ CHECKS = [
     lambda: pins.test_f16_exact_dot_is_the_rational_sum_rounded_once(),
     lambda: pins.test_f16_chunk_model_hand_examples(),
     lambda: pins.test_f16_chunk_model_equals_exact_when_window_holds_everything(),
+    lambda: [fp8.test_hand_examples(c) for c in range(len(fp8.HAND))],
+    lambda: [fp8.test_walk_matches_the_placement_rule(r) for r in fp8.WALK_R],
+    lambda: fp8.test_equals_exact_when_the_grids_hold_everything("16x16x32_fp8"),
+    lambda: fp8.test_fma_on_ignores_the_instruction_shape(),
 ]
 
 
