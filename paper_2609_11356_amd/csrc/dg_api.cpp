@@ -47,13 +47,15 @@ bool make_signature(dg_desc* d) {
   const dg_desc_params& p = d->p;
   // fma = 1 folds the same 8-k chunks whatever the instruction's K
   // on the scalar path a bf16 product is exact, so fma cannot change bits
+  // (likewise the same 16-k chunks for the fp8 instructions)
   const bool scalar = p.mma == DG_MMA_SCALAR_FMA;
-  std::string grp = scalar ? "scalar-fma" : p.fma ? "chunk8" : "group" + std::to_string(d->group);
+  const bool f8 = p.in_dtype == DG_IN_E4M3;
+  std::string grp = scalar ? "scalar-fma" : p.fma ? (f8 ? "chunk16" : "chunk8") : "group" + std::to_string(d->group);
   char base[512];
   int n = std::snprintf(base, sizeof base,
-                        "gfx950-bf16-%s/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
+                        "gfx950-%s-%s/%s/fma%d/tile%d/%s/S%d/%s/merge-%s/partial-%s/merge-dt-%s/"
                         "out-%s/epi%d/%s/leaf%d/%s",
-                        scalar ? "fma" : "mfma", grp.c_str(), scalar ? 1 : p.fma, p.tile_k,
+                        f8 ? "e4m3" : "bf16", scalar ? "fma" : "mfma", grp.c_str(), scalar ? 1 : p.fma, p.tile_k,
                         p.tile_combine == DG_CARRY ? "carry" : p.tile_combine == DG_SEQ ? "seq" : "tree",
                         p.split_k, p.tail == DG_TAIL_FIRST ? "tail-first" : "tail-last",
                         p.split_combine == DG_SEQ ? "seq" : "tree", p.partial_dtype ? "bf16" : "f32",
@@ -192,7 +194,7 @@ AutoConfig auto_config(int64_t M, int64_t N, int S) {
 
 extern "C" {
 
-int32_t dg_version(void) { return 501; }
+int32_t dg_version(void) { return 600; }
 
 const char* dg_strerror(dg_status s) {
   switch (s) {
@@ -213,8 +215,10 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   *out = nullptr;
   if (p->struct_size < sizeof(dg_desc_params)) return DG_ERR_INVALID;
   int group;
-  if (p->mma == DG_MMA_16X16X32_BF16) group = 32;
-  else if (p->mma == DG_MMA_32X32X16_BF16) group = 16;
+  if (p->mma == DG_MMA_16X16X32_BF16 || p->mma == DG_MMA_16X16X32_FP8) group = 32;
+  else if (p->mma == DG_MMA_32X32X16_BF16 || p->mma == DG_MMA_32X32X16_FP8) group = 16;
+  else if (p->mma == DG_MMA_16X16X128_F8F6F4) group = 128;
+  else if (p->mma == DG_MMA_32X32X64_F8F6F4) group = 64;
   else if (p->mma == DG_MMA_SCALAR_FMA) group = 1;
   else return DG_ERR_INVALID;
   if (p->tile_k < group || p->tile_k % group != 0 || p->tile_k > (1 << 30)) return DG_ERR_INVALID;
@@ -236,7 +240,9 @@ dg_status dg_desc_create(const dg_desc_params* p, dg_desc** out) {
   if (!in(p->leaf_layout, DG_LEAF_CONTIGUOUS, DG_LEAF_STRIDED) || !in(p->lane_fold, DG_FOLD_UP, DG_FOLD_DOWN))
     return DG_ERR_INVALID;
   if (!in(p->norm_round, DG_NORM_FINAL, DG_NORM_PRE_WEIGHT)) return DG_ERR_INVALID;
-  if (!in(p->in_dtype, DG_IN_BF16, DG_IN_BF16_E4M3)) return DG_ERR_INVALID;
+  if (!in(p->in_dtype, DG_IN_BF16, DG_IN_E4M3)) return DG_ERR_INVALID;
+  // e4m3 x e4m3 goes with an fp8 instruction, and an fp8 instruction with it
+  if ((p->in_dtype == DG_IN_E4M3) != in(p->mma, DG_MMA_16X16X32_FP8, DG_MMA_32X32X64_F8F6F4)) return DG_ERR_INVALID;
   if (p->in_dtype == DG_IN_BF16_E4M3 && p->mma == DG_MMA_SCALAR_FMA) return DG_ERR_UNSUPPORTED;
   if (p->split_layout == DG_SPLIT_STRIDED) {
     if (p->split_tile < p->tile_k || p->split_tile % p->tile_k != 0 || p->split_tile > (1 << 30))
@@ -294,7 +300,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 12) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 13) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   // packed B runs on kernel 11 only, and kernel 11 runs nothing else
   if (packed ? (kern != 0 && kern != 11) : kern == 11) return DG_ERR_UNSUPPORTED;
   if (packed) kern = 11;
@@ -309,6 +315,12 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   const bool b8 = p.in_dtype == DG_IN_BF16_E4M3;
   if (b8 && !packed && kern == 0) kern = 1;
   if (b8 && kern != 1 && kern != 11) return DG_ERR_UNSUPPORTED;
+  // e4m3 x e4m3: the generic kernel (any descriptor) or the fp8 tiled kernel
+  // 13 (a carried accumulator); kernel 13 runs nothing else and takes no knob
+  const bool f8 = p.in_dtype == DG_IN_E4M3;
+  if (f8 && (packed || !(kern == 0 || kern == 1 || kern == 13))) return DG_ERR_UNSUPPORTED;
+  if (!f8 && kern == 13) return DG_ERR_UNSUPPORTED;
+  if (kern == 13 && (tm || tn || order || occ || depth || slab_k || split_n)) return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
     return DG_ERR_UNSUPPORTED;
@@ -332,7 +344,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     return DG_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return DG_OK;
   if (!C || (need_bias && !bias) || (K > 0 && (!A || !B))) return DG_ERR_INVALID;
-  if (!aligned(A, 2) || !aligned(B, b8 ? 1 : 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
+  if (!aligned(A, f8 ? 1 : 2) || !aligned(B, (b8 || f8) ? 1 : 2) || !aligned(C, p.out_dtype == DG_F32 ? 4 : 2) ||
       (need_bias && !aligned(bias, 2)))
     return DG_ERR_ALIGN;
   if (K == 0 && p.split_k > 1) return DG_ERR_SHAPE;
@@ -370,6 +382,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   a.pre_act = p.epi_round == DG_ROUND_PRE_ACT;
   a.in_f16 = f16;
   a.b_e4m3 = b8;
+  a.ab_e4m3 = f8;
   if ((M + 15) / 16 > 65535 || (N + 15) / 16 > (int64_t)1 << 31) return DG_ERR_SHAPE;
 
   // The packed-B kernel (dg_panel.hip): one accumulator carried through the
@@ -398,6 +411,20 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     if (!dg::panel_supported(panel_tms, panel_depth, panel_avec, b8)) return DG_ERR_UNSUPPORTED;
   }
 
+  // The fp8 tiled kernel: a carried accumulator with fma = 1 (the 16-k chunk
+  // chain), 16-byte rows (K, N multiples of 16) and the chunk grid on
+  // multiples of 16 from k = 0 (parts and a leading short tile).
+  // (decided before any workspace is taken)
+  if (f8) {
+    bool f8_ok = p.tile_combine == DG_CARRY && p.fma == 1 && !strided && K % 16 == 0 && N % 16 == 0 &&
+                 aligned(A, 16) && aligned(B, 16) && aligned(C, 16) && (!need_bias || aligned(bias, 16));
+    for (int s = 0; s < a.S && f8_ok; ++s) {
+      const int64_t len = a.cuts[s + 1] - a.cuts[s];
+      if (a.cuts[s] % 16 || (a.tail_first && (len % p.tile_k) % 16)) f8_ok = false;
+    }
+    if (kern == 13 && !f8_ok) return DG_ERR_UNSUPPORTED;
+    if (kern == 0) kern = f8_ok ? 13 : 1;
+  }
   hipStream_t st = (hipStream_t)stream;
   if (a.S > 1) {
     void* ws = nullptr;
@@ -416,7 +443,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
 
   // The tiled kernel needs the chunk grid (8 k from every tile start) to sit
   // on multiples of 8 from k = 0, a carried accumulator, and 16-byte rows.
-  bool tiled_ok = p.tile_combine == DG_CARRY && p.fma == 1 && K % 8 == 0 && N % 8 == 0 &&
+  bool tiled_ok = !f8 && p.tile_combine == DG_CARRY && p.fma == 1 && K % 8 == 0 && N % 8 == 0 &&
                   aligned(A, 16) && aligned(B, 16) && aligned(C, 16) && (!need_bias || aligned(bias, 16));
   for (int s = 0; s < a.S && tiled_ok; ++s) {
     if (a.cuts[s] % 8) tiled_ok = false;
@@ -428,7 +455,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   // on a 32-k step from the part start, and for the tree at most 128 tiles
   // per part (its stack lives in registers).
   const bool gen = p.tile_combine != DG_CARRY || p.fma == 0;
-  bool tc_ok = gen && !scalar && !strided && !b8 && (p.fma == 1 || d->group == 32) && p.tile_k % 32 == 0 &&
+  bool tc_ok = gen && !scalar && !strided && !b8 && !f8 && (p.fma == 1 || d->group == 32) && p.tile_k % 32 == 0 &&
                K % 8 == 0 && N % 8 == 0 && aligned(A, 16) && aligned(B, 16) && aligned(C, 16) &&
                (!need_bias || aligned(bias, 16));
   int64_t max_tiles = 0;
@@ -446,7 +473,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   }
   if (kern == 12 && !tc_ok) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && !tiled_ok && tc_ok) kern = 12;
-  if (kern >= 2 && kern != 9 && kern != 11 && kern != 12 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern >= 2 && kern != 9 && kern != 11 && kern != 12 && kern != 13 && !tiled_ok) return DG_ERR_UNSUPPORTED;
   if (strided && kern == 0) {
     const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
     const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
@@ -489,6 +516,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   hipError_t e;
   if (kern == 11) {
     e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
+  } else if (kern == 13) {
+    if (((M + 127) / 128) * ((N + 127) / 128) > INT32_MAX) return DG_ERR_SHAPE;
+    e = dg::launch_gemm_f8(a, st);
   } else if (kern == 12) {
     if (((M + 127) / 128) * ((N + 63) / 64) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = 1;

@@ -379,6 +379,20 @@ __global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
     }
 }
 
+// The fp8 instructions (OCP e4m3 operands).  16x16x32: lane l holds 8 bytes,
+// k = 8(l/16) + e.  The block-scaled 16x16x128 (format 0 = e4m3 for both
+// operands, E8M0 scales 127 = 1.0): 32 bytes, bytes 0..15 at
+// k = 16(l/16) + e and bytes 16..31 at k = 64 + 16(l/16) + e.  Both fold
+// the same chain of 16-k chunks.
+typedef int intx8 __attribute__((ext_vector_type(8)));
+typedef int intx2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ floatx4 mfma_fp8(uint64_t a, uint64_t b, floatx4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)a, (long)b, c, 0, 0, 0);
+}
+__device__ __forceinline__ floatx4 mfma_fp8x128(const intx8& a, const intx8& b, const floatx4& c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 127, 0, 127);
+}
+
 // ------------------------------------------------------------- generic
 
 __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
@@ -399,6 +413,27 @@ __global__ __launch_bounds__(64) void gemm_generic(GemmArgs a) {
     floatx4 v = (a.tile_combine == DG_CARRY) ? acc : zero;
     for (int64_t gs = ts; gs < te; gs += step) {
       const int64_t ge = (gs + step < te) ? gs + step : te;
+      if (a.ab_e4m3) {
+        // e4m3 x e4m3: the group's 32-k instructions chained from the
+        // accumulator (fma = 1) or from +0 (fma = 0); a 16-k group is one
+        // instruction whose second chunk is empty, which leaves it as it is
+        floatx4 w = a.fma ? v : zero;
+        for (int64_t ss = gs; ss < ge; ss += 32) {
+          uint64_t av8 = 0, bv8 = 0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t k = ss + kb + e;
+            const bool ok = k < ge;
+            const uint64_t x = (ok && arow < a.M) ? ((const uint8_t*)a.A)[arow * a.K + k] : 0;
+            const uint64_t y = (ok && bcol < a.N) ? ((const uint8_t*)a.B)[k * a.N + bcol] : 0;
+            av8 |= x << (8 * e);
+            bv8 |= y << (8 * e);
+          }
+          w = mfma_fp8(av8, bv8, w);
+        }
+        v = a.fma ? w : v + w;
+        continue;
+      }
       shortx8 av, bv;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -911,6 +946,166 @@ __device__ __forceinline__ void v3_body(const GemmArgs& a, int64_t i0, int64_t j
       if (i < a.M && j < a.N) finish4(a, s, i, j, *(const float4*)&cs[rr * CSP + cc]);
     }
   }
+}
+
+// ---------------------------------------------------------- fp8 tiled
+//
+// e4m3 x e4m3 with a carried accumulator and fma = 1: the chain of 16-k
+// chunks from k = 0, which every fp8 instruction folds alike, issued as the
+// block-scaled 16x16x128 (unit scales).  128 x 128 blocks of four 64 x 64
+// waves, 128-k slabs (128-byte rows), the v3 pipeline: global loads two
+// slabs ahead through two register sets, an LDS double buffer, one barrier
+// per slab.
+//   * A slab [row][k]: eight 16-byte chunks per row, chunk c at
+//     c ^ swz_a<8>(row); a lane's operand is chunk l/16 of its row (bytes
+//     0..15) and chunk 4 + l/16 (bytes 16..31): two conflict-free reads;
+//   * B slab [k][n]: BN/16 chunks per row, chunk c of row k at c ^ (k & 7),
+//     so the 8 rows a transposing read covers sit in 8 different 16-byte
+//     slots.  ds_read_b64_tr_b8: lane i of a 16-lane group addresses row
+//     i/2, bytes 8(i%2).. of an 8 x 16 byte block and lane j receives
+//     column j, byte e from row e; four such reads give a lane its 32 bytes
+//     (k = 16(l/16) + 0..7, + 8..15, 64 + 16(l/16) + 0..7, + 8..15);
+//   * every 16-byte chunk is wholly inside or outside the part and the
+//     matrix (K, N and the part starts are multiples of 16), so a load is a
+//     select between a chunk and the zero chunk; a chunk of zero products
+//     leaves the accumulator as it is.
+typedef __attribute__((address_space(3))) intx2* lds_i2;
+
+__device__ __forceinline__ const u32x4* chunk_or_zero8(bool ok, const uint8_t* p) {
+  return ok ? reinterpret_cast<const u32x4*>(p) : &g_zero16[0];
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ void f8_body(const GemmArgs& a, int64_t i0, int64_t j0) {
+  constexpr int WM = 2, WN = 2, WTM = BM / WM, WTN = BN / WN, TM = WTM / 16, TN = WTN / 16;
+  constexpr int BK = 128;                        // k per slab (bytes per A row)
+  constexpr int CPR = BK / 16, BROW = BN / 16;   // 16-byte chunks per A row, per B row
+  constexpr int ACH_T = BM * CPR / 256, BCH_T = BK * BROW / 256;
+  static_assert(BM * CPR % 256 == 0 && BK * BROW % 256 == 0, "whole chunks per thread");
+  constexpr int A_BYTES = BM * BK, B_BYTES = BK * BN;
+  __shared__ __attribute__((aligned(16))) uint8_t smem[2 * (A_BYTES + B_BYTES)];
+  uint8_t* As0 = smem;
+  uint8_t* Bs0 = smem + 2 * A_BYTES;
+  const uint8_t* A8 = (const uint8_t*)a.A;
+  const uint8_t* B8 = (const uint8_t*)a.B;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<8>(row)); };
+  auto ldsB = [](int k, int c) { return k * BROW + (c ^ (k & 7)); };
+
+  u32x4 r0a[ACH_T], r0b[BCH_T], r1a[ACH_T], r1b[BCH_T];
+  auto gload = [&](int sl, u32x4* ra, u32x4* rb) {
+    const int64_t ks = k0 + (int64_t)sl * BK;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t, row = q / CPR, c = q % CPR;
+      const int64_t gi = i0 + row, gk = ks + 16 * c;
+      ra[t] = *chunk_or_zero8((gi < a.M) && (gk < k1), A8 + gi * a.K + gk);
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t, kr = q / BROW, c = q % BROW;
+      const int64_t gk = ks + kr, gn = j0 + 16 * c;
+      rb[t] = *chunk_or_zero8((gk < k1) && (gn < a.N), B8 + gk * a.N + gn);
+    }
+  };
+  auto lstore = [&](int buf, const u32x4* ra, const u32x4* rb) {
+    uint8_t* As = As0 + buf * A_BYTES;
+    uint8_t* Bs = Bs0 + buf * B_BYTES;
+#pragma unroll
+    for (int t = 0; t < ACH_T; ++t) {
+      const int q = tid + 256 * t;
+      *(u32x4*)&As[16 * ldsA(q / CPR, q % CPR)] = ra[t];
+    }
+#pragma unroll
+    for (int t = 0; t < BCH_T; ++t) {
+      const int q = tid + 256 * t;
+      *(u32x4*)&Bs[16 * ldsB(q / BROW, q % BROW)] = rb[t];
+    }
+  };
+
+  floatx4 acc[TM][TN];
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf) {
+    const uint8_t* As = As0 + buf * A_BYTES;
+    const uint8_t* Bs = Bs0 + buf * B_BYTES;
+    const int i = lane & 15, g = lane >> 4;
+    intx8 af[TM], bfr[TN];
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi) {
+      const int row = wm * WTM + 16 * mi + i;
+      const u32x4 lo = *(const u32x4*)&As[16 * ldsA(row, g)];
+      const u32x4 hi = *(const u32x4*)&As[16 * ldsA(row, 4 + g)];
+      af[mi] = intx8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      const int c = (wn * WTN + 16 * ni) / 16;
+      intx2 q[4];
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const int kr = (h < 2 ? 16 * g + 8 * h : 64 + 16 * g + 8 * (h - 2)) + (i >> 1);
+        q[h] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i2)(&Bs[16 * ldsB(kr, c) + 8 * (i & 1)]));
+      }
+      bfr[ni] = intx8{q[0][0], q[0][1], q[1][0], q[1][1], q[2][0], q[2][1], q[3][0], q[3][1]};
+    }
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) acc[mi][ni] = mfma_fp8x128(af[mi], bfr[ni], acc[mi][ni]);
+  };
+
+  // prologue: slabs 0 and 1 in flight, slab 0 in LDS (loads past the part
+  // end read the zero chunk)
+  gload(0, r0a, r0b);
+  gload(1, r1a, r1b);
+  lstore(0, r0a, r0b);
+  __syncthreads();
+  for (int sl = 0; sl < nslab; sl += 2) {
+    gload(sl + 2, r0a, r0b);
+    compute(0);
+    lstore(1, r1a, r1b);
+    __syncthreads();
+    gload(sl + 3, r1a, r1b);
+    if (sl + 1 < nslab) compute(1);
+    lstore(0, r0a, r0b);
+    __syncthreads();
+  }
+
+  // epilogue: each wave stages 16-row bands of its tile through LDS (rows of
+  // pitch WTN + 4 floats) and finishes four consecutive columns per store
+  constexpr int CSP = WTN + 4;
+  float* cs = reinterpret_cast<float*>(smem) + wave * 16 * CSP;
+  static_assert(4 * 16 * CSP * 4 <= (int)sizeof(smem), "epilogue staging fits");
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+    __syncthreads();
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) cs[(4 * (lane >> 4) + r) * CSP + 16 * ni + (lane & 15)] = acc[mi][ni][r];
+    __syncthreads();
+#pragma unroll 1
+    for (int q = lane; q < 16 * WTN / 4; q += 64) {
+      const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+      const int64_t gi = i0 + wm * WTM + 16 * mi + rr, gj = j0 + wn * WTN + cc;
+      if (gi < a.M && gj < a.N) finish4(a, s, gi, gj, *(const float4*)&cs[rr * CSP + cc]);
+    }
+  }
+}
+
+template <int BM, int BN>
+__global__ __launch_bounds__(256) void gemm_f8(GemmArgs a) {
+  const int tiles_n = (int)((a.N + BN - 1) / BN);
+  f8_body<BM, BN>(a, (int64_t)(blockIdx.x / tiles_n) * BM, (int64_t)(blockIdx.x % tiles_n) * BN);
 }
 
 // Block order (speed only).  order 1: row-major, consecutive workgroups share
@@ -2119,6 +2314,12 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) 
   if (tm == 256 && tn == 128) return launch_big_t<256, 128, 2, 2>(a, st);
   if (tm == 128 && tn == 256) return launch_big_t<128, 256, 2, 2>(a, st);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_f8(const GemmArgs& a, hipStream_t st) {
+  const int64_t tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
+  hipLaunchKernelGGL((gemm_f8<128, 128>), dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_splitk_combine(const CombineArgs& a, hipStream_t st) {

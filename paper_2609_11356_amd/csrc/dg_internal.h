@@ -36,6 +36,7 @@ struct GemmArgs {
   int64_t n_split;               // mixed-width ping-pong: first column of the 192-wide blocks
   int32_t in_f16;                // operands A and B are binary16 (else bfloat16)
   int32_t b_e4m3;                // B holds one OCP e4m3 byte per element (A bf16)
+  int32_t ab_e4m3;               // A and B hold OCP e4m3 bytes (the fp8 instructions)
   float* colsum_part;            // set (single part, 256-row blocks): column sums of each 256-row
                                  // run of C, [ceil(M / 256)][N], folded in the epilogue
 };
@@ -107,6 +108,10 @@ bool v3_supported(int tile_m, int tile_n, int occupancy);
 // tile chain or tree, or fma = 0, on 128 x 64 tiled blocks (levels: the
 // tree's stack depth, 2..7; each part at most 2^levels tiles)
 hipError_t launch_gemm_tc(const GemmArgs& a, int levels, hipStream_t s);
+// e4m3 x e4m3 with a carried accumulator and fma = 1 on the block-scaled fp8
+// instruction: 128 x 128 blocks, 128-k slabs (K, N and the part starts
+// multiples of 16; A, B, C 16-byte aligned)
+hipError_t launch_gemm_f8(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)

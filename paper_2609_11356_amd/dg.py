@@ -14,7 +14,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libdg.so")
 
 DG_OK, DG_ERR_INVALID, DG_ERR_UNSUPPORTED, DG_ERR_SHAPE, DG_ERR_ALIGN, DG_ERR_NOMEM, DG_ERR_HIP, DG_ERR_SCRATCH = range(8)
-MMA = {"16x16x32": 1, "32x32x16": 2, "scalar": 3}
+MMA = {"16x16x32": 1, "32x32x16": 2, "scalar": 3,
+       # the fp8 instructions (in_dtype "e4m3"; the f8f6f4 shapes at unit scales)
+       "16x16x32_fp8": 4, "32x32x16_fp8": 5, "16x16x128_f8f6f4": 6, "32x32x64_f8f6f4": 7}
 COMBINE = {"carry": 0, "seq": 1, "tree": 2}
 TAIL = {"last": 0, "first": 1}
 DTYPE = {"f32": 0, "bf16": 1}
@@ -117,7 +119,9 @@ def dg_version() -> int:
 class Desc:
     """An immutable descriptor (dg_desc_create / dg_desc_destroy).
 
-    Fields (strings as in the header's enums): mma ("16x16x32" | "32x32x16"),
+    Fields (strings as in the header's enums): mma ("16x16x32" | "32x32x16" |
+    "scalar", or with e4m3 operands "16x16x32_fp8" | "32x32x16_fp8" |
+    "16x16x128_f8f6f4" | "32x32x64_f8f6f4"),
     tile_k, split_k, k_cuts (None or S-1 ints), tile_combine ("carry" |
     "seq" | "tree"), split_combine ("seq" | "tree"), tail ("last" | "first"),
     fma (0/1), partial / merge / out ("f32" | "bf16"), epilogue ("none" |
@@ -127,8 +131,9 @@ class Desc:
     "strided": leaf_w lanes each taking every leaf_w-th element), lane_fold
     ("up" | "down": the butterfly's offsets counting up or down), norm_round
     ("final" | "pre_weight": dg_rmsnorm rounds the normalised value to bf16
-    before the weight), in_dtype ("bf16" | "f16" | "bf16_e4m3": the GEMM
-    operands; "bf16_e4m3" is a bf16 A with a B of OCP e4m3 bytes)."""
+    before the weight), in_dtype ("bf16" | "f16" | "bf16_e4m3" | "e4m3": the
+    GEMM operands; "bf16_e4m3" is a bf16 A with a B of OCP e4m3 bytes,
+    "e4m3" both A and B OCP e4m3 bytes, folded by an fp8 instruction)."""
 
     DEFAULTS = dict(mma="16x16x32", tile_k=64, split_k=1, k_cuts=None, tile_combine="carry",
                     split_combine="seq", tail="last", fma=1, partial="f32", merge="f32", out="f32",
@@ -172,7 +177,7 @@ class Desc:
         p.leaf_layout = {"contiguous": 0, "strided": 1}[f["leaf_layout"]]
         p.lane_fold = {"up": 0, "down": 1}[f["lane_fold"]]
         p.norm_round = {"final": 0, "pre_weight": 1}[f["norm_round"]]
-        p.in_dtype = {"bf16": 0, "f16": 1, "bf16_e4m3": 2}[f["in_dtype"]]
+        p.in_dtype = {"bf16": 0, "f16": 1, "bf16_e4m3": 2, "e4m3": 3}[f["in_dtype"]]
         h = ctypes.c_void_p()
         st = lib().dg_desc_create(ctypes.byref(p), ctypes.byref(h))
         if st != DG_OK:
@@ -236,6 +241,9 @@ def _in_dtypes(desc):
         return (torch.float16,), (torch.float16,)
     if f == "bf16_e4m3":
         return (torch.bfloat16,), (torch.uint8, getattr(torch, "float8_e4m3fn", torch.uint8))
+    if f == "e4m3":
+        e = (torch.uint8, getattr(torch, "float8_e4m3fn", torch.uint8))
+        return e, e
     return (torch.bfloat16,), (torch.bfloat16,)
 
 

@@ -34,7 +34,7 @@ def test_every_declared_symbol_is_exported(dg):
 
 
 def test_version_and_strerror(dg):
-    assert dg.dg_version() == 501
+    assert dg.dg_version() == 600
     for s in range(8):
         assert dg.dg_strerror(s)
 
@@ -339,6 +339,46 @@ def test_argument_errors_need_no_gpu(dg):
     assert lib.dg_rowsum(d.handle, 16, 18, 4, 5, None) == dg.DG_ERR_ALIGN
     assert lib.dg_rowsum(d.handle, 16, None, 4, 5, None) == dg.DG_ERR_INVALID
     assert lib.dg_rowsum(d.handle, 16, 16, -1, 5, None) == dg.DG_ERR_SHAPE
+
+
+def test_fp8_descriptors_need_no_gpu(dg):
+    """e4m3 x e4m3 pairs with the fp8 instructions only; under fma = 1 the
+    four fp8 shapes share one signature (one chunk chain), under fma = 0
+    each its own group; the kernels that may run it, and kernel 13's
+    conditions, are checked before any launch."""
+    lib = dg.lib()
+    fp8 = ("16x16x32_fp8", "32x32x16_fp8", "16x16x128_f8f6f4", "32x32x64_f8f6f4")
+    for bad in (dict(mma="16x16x32", in_dtype="e4m3"), dict(mma="16x16x32_fp8", tile_k=64),
+                dict(mma="scalar", in_dtype="e4m3"), dict(mma="16x16x128_f8f6f4", tile_k=64, in_dtype="e4m3"),
+                dict(mma="16x16x32_fp8", tile_k=64, in_dtype="bf16_e4m3")):
+        with pytest.raises(dg.DgError) as e:
+            dg.Desc(**bad)
+        assert e.value.status == dg.DG_ERR_INVALID, bad
+    sigs = {dg.Desc(mma=m, tile_k=128, in_dtype="e4m3").signature() for m in fp8}
+    assert len(sigs) == 1 and next(iter(sigs)).startswith("gfx950-e4m3-mfma/chunk16/"), sigs
+    assert len({dg.Desc(mma=m, tile_k=128, in_dtype="e4m3", fma=0).signature() for m in fp8}) == 4
+    d = dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3")
+    for k in (2, 3, 4, 5, 6, 7, 8, 9, 10, 11, 12):
+        kn = dg.dg_knobs(k, 0, 0, 0, 0, 0, 0, 0)
+        assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 16, 64, 512, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED, k
+    k13 = dg.dg_knobs(13, 0, 0, 0, 0, 0, 0, 0)
+    for desc, N, K in [(dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3", fma=0), 64, 512),
+                       (dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3", tile_combine="tree"), 64, 512),
+                       (dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3", split_k=2, split_layout="strided",
+                                split_tile=64), 64, 512),
+                       (dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3", tail="first"), 64, 520),
+                       (dg.Desc(mma="16x16x32_fp8", tile_k=64, in_dtype="e4m3", split_k=2, k_cuts=[72]), 64, 512),
+                       (d, 56, 512), (d, 64, 520)]:
+        assert lib.dg_gemm_knobs(desc.handle, 16, 16, None, 16, 16, N, K, ctypes.byref(k13), None) == \
+            dg.DG_ERR_UNSUPPORTED, (desc.signature(), N, K)
+    for kn in (dg.dg_knobs(13, 128, 128, 0, 0, 0, 0, 0), dg.dg_knobs(13, 0, 0, 1, 0, 0, 0, 0)):
+        assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 16, 64, 512, ctypes.byref(kn), None) == \
+            dg.DG_ERR_UNSUPPORTED
+    # byte operands need no alignment of their own; kernel 13 needs 16-byte rows
+    assert lib.dg_gemm_knobs(d.handle, 17, 16, None, 16, 16, 64, 512, ctypes.byref(k13), None) == \
+        dg.DG_ERR_UNSUPPORTED
+    assert lib.dg_gemm(d.handle, 17, 16, None, 16, 0, 64, 512, None) == dg.DG_OK
 
 
 def test_packed_b_size_and_refusals_need_no_gpu(dg):
