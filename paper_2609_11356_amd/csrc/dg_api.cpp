@@ -320,7 +320,8 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   const bool f8 = p.in_dtype == DG_IN_E4M3;
   if (f8 && (packed || !(kern == 0 || kern == 1 || kern == 13))) return DG_ERR_UNSUPPORTED;
   if (!f8 && kern == 13) return DG_ERR_UNSUPPORTED;
-  if (kern == 13 && (tm || tn || order || occ || depth || slab_k || split_n)) return DG_ERR_UNSUPPORTED;
+  if (kern == 13 && (tn || order || occ || depth || slab_k || split_n || !(tm == 0 || tm == 128 || tm == 256)))
+    return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
     return DG_ERR_UNSUPPORTED;
@@ -334,7 +335,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern == 8 && !dg::skinny_dma_supported(tm ? tm : 16, tn ? tn : 16, depth ? depth : 8, slab_k ? slab_k : 256))
     return DG_ERR_UNSUPPORTED;
   if (kern == 12 && (tm || tn)) return DG_ERR_UNSUPPORTED;
-  if (kern != 4 && kern != 5 && kern != 8 && kern != 11 && (tm || tn) &&
+  if (kern != 4 && kern != 5 && kern != 8 && kern != 11 && kern != 13 && (tm || tn) &&
       !(tm && tn && (kern == 3 ? dg::v3_supported(tm, tn, occ == 2 ? 2 : 1) : dg::tiled_supported(tm, tn))))
     return DG_ERR_UNSUPPORTED;
   // A strided split runs on the generic kernel or on the few-row kernel with
@@ -424,6 +425,13 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     }
     if (kern == 13 && !f8_ok) return DG_ERR_UNSUPPORTED;
     if (kern == 0) kern = f8_ok ? 13 : 1;
+    // 256 x 256 blocks (buffer offsets: M K and K N bytes below 2^31) from
+    // 129 rows on, else 128 x 128
+    if (kern == 13) {
+      const bool big_ok = M * K < 0x7fffffff && K * N < 0x7fffffff;
+      if (tm == 256 && !big_ok) return DG_ERR_UNSUPPORTED;
+      if (!tm) tm = (M > 128 && big_ok) ? 256 : 128;
+    }
   }
   hipStream_t st = (hipStream_t)stream;
   if (a.S > 1) {
@@ -517,8 +525,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern == 11) {
     e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
   } else if (kern == 13) {
-    if (((M + 127) / 128) * ((N + 127) / 128) > INT32_MAX) return DG_ERR_SHAPE;
-    e = dg::launch_gemm_f8(a, st);
+    if (((M + tm - 1) / tm) * ((N + tm - 1) / tm) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = 1;
+    e = dg::launch_gemm_f8(a, tm, st);
   } else if (kern == 12) {
     if (((M + 127) / 128) * ((N + 63) / 64) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = 1;

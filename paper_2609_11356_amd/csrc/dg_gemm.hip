@@ -386,6 +386,7 @@ __global__ __launch_bounds__(256) void gemm_scalar(GemmArgs a) {
 // the same chain of 16-k chunks.
 typedef int intx8 __attribute__((ext_vector_type(8)));
 typedef int intx2 __attribute__((ext_vector_type(2)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
 __device__ __forceinline__ floatx4 mfma_fp8(uint64_t a, uint64_t b, floatx4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)a, (long)b, c, 0, 0, 0);
 }
@@ -1748,6 +1749,208 @@ __device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t 
   wave_epilogue<TM, TN>(a, s, i0 + wm * WTM, j0 + wn * WTN, cs, bsh + wn * WTN, acc);
 }
 
+// e4m3 x e4m3 (carried accumulator, fma = 1) on 256 x 256 blocks of four
+// 128 x 128 waves: the w4d pipeline above with bytes for bf16 elements.
+// The slab is 64 k, so A rows are 64 bytes (the bf16 slab's layout and
+// swizzle) and the instruction is the block-scaled 32x32x64 (unit scales),
+// whose K is the slab: lane l's bytes 0..15 are k = 16(l/32) + e, bytes
+// 16..31 k = 32 + 16(l/32) + e, row (A) or column (B) l % 32; its 16
+// results are rows 8(r/4) + 4(l/32) + r%4 of column l % 32.  B rows are 256
+// bytes, chunk c of row k at c ^ (k & 7) ^ 8 (c & 1), read through
+// ds_read_b64_tr_b8 as in the 128 x 128 kernel: a read pass serves two
+// 16-lane groups, on neighbouring chunks of the same 8 rows, and the odd
+// chunk's rows sit in the other half of the 256-byte row (all 64 banks).
+// Per slab each wave issues four A and four B direct-to-LDS loads (16 rows
+// of A or 4 rows of B per 1 KB run) and 16 MFMAs; the accumulators (256
+// floats) live in the accumulation registers.  The ring has four slots,
+// three slabs ahead, and each slot is two LDS arrays (A, B): the compiler
+// keeps a fragment read apart from the direct-to-LDS loads still in flight
+// only when they touch different arrays (it tracks up to eight), and with
+// one array per slot it made every B-fragment read wait for all of them.
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_a0[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_a1[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_a2[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_a3[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_b0[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_b1[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_b2[16384];
+__shared__ __attribute__((aligned(1024))) uint8_t f8w_b3[16384];
+template <int S>
+__device__ __forceinline__ uint8_t* f8w_aslot() {
+  if constexpr (S == 0) return f8w_a0;
+  else if constexpr (S == 1) return f8w_a1;
+  else if constexpr (S == 2) return f8w_a2;
+  else return f8w_a3;
+}
+template <int S>
+__device__ __forceinline__ uint8_t* f8w_bslot() {
+  if constexpr (S == 0) return f8w_b0;
+  else if constexpr (S == 1) return f8w_b1;
+  else if constexpr (S == 2) return f8w_b2;
+  else return f8w_b3;
+}
+
+template <int X>
+__device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t j0) {
+  constexpr int NS = 4, D = NS - 1;
+  constexpr int BM = 256, BN = 256, BK = 64, CPR = BK / 16, BROW = BN / 16;
+  constexpr int WTM = 128, WTN = 128, TM = WTM / 32, TN = WTN / 32;
+  constexpr int A_BYTES = BM * BK, B_BYTES = BK * BN;
+  constexpr int NIA = A_BYTES / 1024 / 4, NIB = B_BYTES / 1024 / 4, NI = NIA + NIB;   // per wave
+  static_assert(NI == 2 * TM && TM == TN && A_BYTES == 16384 && B_BYTES == 16384, "two loads per MFMA row");
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int s = blockIdx.z;
+  const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
+  const int nslab = (int)((k1 - k0 + BK - 1) / BK);
+  auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
+  auto ldsB = [](int k, int c) { return k * BROW + (c ^ (k & 7) ^ ((c & 1) << 3)); };
+
+  // load t of the wave: A run r = NIA wave + t (rows 16r..), B run
+  // r = NIB wave + (t - NIA) (k rows 4r..); each lane fetches the chunk
+  // that belongs at its LDS position under the swizzle
+  constexpr uint32_t OOB = 0x80000000u;
+  uint32_t off[NI];
+  int kc[NI];
+#pragma unroll
+  for (int t = 0; t < NIA; ++t) {
+    const int row = (NIA * wave + t) * 16 + lane / 4, pc = lane % 4;
+    const int c = pc ^ swz_a<CPR>(row);
+    off[t] = (i0 + row < a.M) ? (uint32_t)(row * a.K + 16 * c) : OOB;
+    kc[t] = 16 * c;
+  }
+#pragma unroll
+  for (int u = 0; u < NIB; ++u) {
+    const int kr = (NIB * wave + u) * 4 + lane / 16, pc = lane % 16;
+    const int c = pc ^ (kr & 7) ^ (((pc ^ kr) & 1) << 3);   // the chunk stored at position pc
+    off[NIA + u] = (j0 + 16 * c < a.N) ? (uint32_t)(kr * a.N + j0 + 16 * c) : OOB;
+    kc[NIA + u] = kr;
+  }
+  const uint8_t* A8 = (const uint8_t*)a.A;
+  const uint8_t* B8 = (const uint8_t*)a.B;
+  const int64_t recA = (a.M - i0) * a.K, recB = (a.K - k0) * a.N;   // below 2^31 (host check)
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void*)(A8 + i0 * a.K), (short)0, (int)recA,
+                                                                      0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc((void*)(B8 + k0 * a.N), (short)0, (int)recB,
+                                                                      0x00020000);
+  auto dma1 = [&](int sl_in, auto SL, auto T) {
+    constexpr int t = decltype(T)::value;
+    const bool past = sl_in >= nslab;
+    const int sl = past ? 0 : sl_in;
+    const int64_t ks = k0 + (int64_t)sl * BK, lim = past ? 0 : k1 - ks;
+    constexpr int sl_ = decltype(SL)::value;
+    if constexpr (t < NIA)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(f8w_aslot<sl_>() + (NIA * wave + t) * 1024), 16,
+                                               kc[t] < lim ? off[t] : OOB, (int)ks, 0, 0);
+    else
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(f8w_bslot<sl_>() + (NIB * wave + t - NIA) * 1024), 16,
+                                               kc[t] < lim ? off[t] : OOB, (int)((ks - k0) * a.N), 0, 0);
+  };
+
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
+  intx8 fa[2][TM], fb[2][TN];
+  auto rdA = [&](auto SL, int mi, intx8& f) {
+    const uint8_t* As = f8w_aslot<decltype(SL)::value>();
+    const int row = wm * WTM + 32 * mi + (lane & 31), h = lane >> 5;
+    const u32x4 lo = *(const u32x4*)&As[16 * ldsA(row, h)];
+    const u32x4 hi = *(const u32x4*)&As[16 * ldsA(row, 2 + h)];
+    f = intx8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  };
+  auto rdB = [&](auto SL, int ni, intx8& f) {
+    const uint8_t* Bs = f8w_bslot<decltype(SL)::value>();
+    const int q = lane >> 4, i = lane & 15, h = q >> 1;
+    const int c = (wn * WTN + 32 * ni + 16 * (q & 1)) / 16;
+    intx2 v[4];
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+      const int kr = (p < 2 ? 16 * h + 8 * p : 32 + 16 * h + 8 * (p - 2)) + (i >> 1);
+      v[p] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i2)(&Bs[16 * ldsB(kr, c) + 8 * (i & 1)]));
+    }
+    f = intx8{v[0][0], v[0][1], v[1][0], v[1][1], v[2][0], v[2][1], v[3][0], v[3][1]};
+  };
+
+  // prologue: slabs 0 .. D-1 issued, 0 and 1 landed (all waves), slab 0's
+  // fragments read
+  static_for<0, D>([&](auto x) { static_for<0, NI>([&](auto t) { dma1(x, x, t); }); });
+  __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 2) * NI));
+  barrier_nofence();
+  constexpr std::integral_constant<int, 0> S0{};
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) rdA(S0, mi, fa[0][mi]);
+#pragma unroll
+  for (int ni = 0; ni < TN; ++ni) rdB(S0, ni, fb[0][ni]);
+  lds_wait();
+  barrier_nofence();
+
+  auto step = [&](int sl, auto X_) {
+    constexpr int x = decltype(X_)::value, cur = x & 1, nxt = cur ^ 1;
+    constexpr std::integral_constant<int, (x + 1) % NS> rslot{};
+    constexpr std::integral_constant<int, (x + D) % NS> wslot{};
+    __builtin_amdgcn_sched_barrier(0);
+    static_for<0, TM>([&](auto mi) {
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni)
+        acc[mi][ni] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[cur][mi], fb[cur][ni], acc[mi][ni],
+                                                                      0, 0, 0, 127, 0, 127);
+      __builtin_amdgcn_sched_barrier(0);
+      rdA(rslot, mi, fa[nxt][mi]);
+      rdB(rslot, mi, fb[nxt][mi]);
+      dma1(sl + D, wslot, std::integral_constant<int, 2 * decltype(mi)::value>{});
+      dma1(sl + D, wslot, std::integral_constant<int, 2 * decltype(mi)::value + 1>{});
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    lds_wait();
+    __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 2) * NI));   // the wave's loads of slab sl+2 landed
+    barrier_nofence();
+  };
+  // slabs past the part end (up to NS - 1 of them) are zero: their chunks
+  // hold no product and leave the accumulators as they are
+  for (int sl = 0; sl < nslab; sl += NS)
+    static_for<0, NS>([&](auto x) { step(sl + x, x); });
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));   // nothing lands in the staging area later
+  __syncthreads();
+
+  // epilogue: wave w stages 16-row halves of its 32-row bands through its
+  // own A array (pitch WTN + 8 floats: the two row sets of one write sit 32
+  // banks apart)
+  constexpr int CSP = WTN + 8;
+  static_assert(16 * CSP * 4 <= 16384, "epilogue staging fits");
+  float* cs = reinterpret_cast<float*>(wave == 0 ? f8w_a0 : wave == 1 ? f8w_a1 : wave == 2 ? f8w_a2 : f8w_a3);
+#pragma unroll
+  for (int mi = 0; mi < TM; ++mi) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+        for (int r = 8 * half; r < 8 * half + 8; ++r)
+          cs[(8 * (r / 4) - 16 * half + 4 * (lane >> 5) + (r & 3)) * CSP + 32 * ni + (lane & 31)] = acc[mi][ni][r];
+      lds_wait();
+#pragma unroll 1
+      for (int q = lane; q < 16 * WTN / 4; q += 64) {
+        const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
+        const int64_t gi = i0 + wm * WTM + 32 * mi + 16 * half + rr, gj = j0 + wn * WTN + cc;
+        if (gi < a.M && gj < a.N) finish4(a, s, gi, gj, *(const float4*)&cs[rr * CSP + cc]);
+      }
+      lds_wait();
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_f8w(GemmArgs a) {
+  const int tiles_m = (int)((a.M + 255) / 256);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  f8w_body<0>(a, (int64_t)ty * 256, (int64_t)tx * 256);
+}
+
 // Columns [0, n_split) in 256 x 256 blocks, the rest in 256 x 192 blocks.
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_w4_mixed(GemmArgs a) {
   const int tiles_m = (int)((a.M + 255) / 256);
@@ -2316,7 +2519,13 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) 
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_gemm_f8(const GemmArgs& a, hipStream_t st) {
+hipError_t launch_gemm_f8(const GemmArgs& a, int tile, hipStream_t st) {
+  if (tile == 256) {
+    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
+    hipLaunchKernelGGL(gemm_f8w, dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
+  if (tile != 128) return hipErrorInvalidValue;
   const int64_t tiles = ((a.M + 127) / 128) * ((a.N + 127) / 128);
   hipLaunchKernelGGL((gemm_f8<128, 128>), dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);
   return hipGetLastError();

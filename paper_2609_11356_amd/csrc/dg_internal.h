@@ -109,9 +109,10 @@ bool v3_supported(int tile_m, int tile_n, int occupancy);
 // tree's stack depth, 2..7; each part at most 2^levels tiles)
 hipError_t launch_gemm_tc(const GemmArgs& a, int levels, hipStream_t s);
 // e4m3 x e4m3 with a carried accumulator and fma = 1 on the block-scaled fp8
-// instruction: 128 x 128 blocks, 128-k slabs (K, N and the part starts
-// multiples of 16; A, B, C 16-byte aligned)
-hipError_t launch_gemm_f8(const GemmArgs& a, hipStream_t s);
+// instructions (K, N and the part starts multiples of 16; A, B, C 16-byte
+// aligned): tile 128, 128 x 128 blocks on 128-k slabs; tile 256, 256 x 256
+// blocks on 64-k slabs loaded direct to LDS (M K and K N below 2^31 bytes)
+hipError_t launch_gemm_f8(const GemmArgs& a, int tile, hipStream_t s);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)

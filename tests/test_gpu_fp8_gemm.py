@@ -109,7 +109,9 @@ def test_matches_oracle(dg, di, shape):
         assert_bits_equal(run(dg, desc, A8, B8, bias), want, "%s %s %s" % (desc, shape, draw))
         assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=1)), want, "generic %s" % desc)
         if tiled:
-            assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=13)), want, "kernel 13 %s" % desc)
+            for tm in (128, 256):
+                assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=13, tile_m=tm)), want,
+                                  "kernel 13 tile %d %s" % (tm, desc))
 
 
 def test_instruction_names_give_the_same_bits_under_fma(dg):
@@ -133,7 +135,8 @@ def test_explicit_cuts_on_and_off_the_16k_grid(dg):
         want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
         assert_bits_equal(run(dg, desc, A8, B8), want, str(cuts))
         if tiled:
-            assert_bits_equal(run(dg, desc, A8, B8, knobs=dict(kernel=13)), want, "kernel 13 %s" % cuts)
+            for tm in (128, 256):
+                assert_bits_equal(run(dg, desc, A8, B8, knobs=dict(kernel=13, tile_m=tm)), want, "kernel 13 %s" % cuts)
         else:
             with pytest.raises(dg.DgError) as e:
                 run(dg, desc, A8, B8, knobs=dict(kernel=13))
@@ -145,7 +148,8 @@ def test_refusals(dg):
     for desc, knobs in [(dict(mma="16x16x32_fp8", tile_k=32, fma=0), dict(kernel=13)),
                         (dict(mma="16x16x32_fp8", tile_k=64, tile_combine="tree"), dict(kernel=13)),
                         (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=3)),
-                        (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=128))]:
+                        (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=64)),
+                        (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=256, tile_n=256))]:
         with pytest.raises(dg.DgError) as e:
             run(dg, desc, A8, B8, knobs=knobs)
         assert e.value.status == dg.DG_ERR_UNSUPPORTED, (desc, knobs)
@@ -170,27 +174,28 @@ def test_special_codes(dg):
     B8[:, 6] = 0x7E
     desc = dict(mma="16x16x128_f8f6f4", tile_k=128)
     want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
-    for kern in (13, 1):
-        got = run(dg, desc, A8, B8, knobs=dict(kernel=kern))
-        assert_bits_equal(got, want, "kernel %d" % kern)
+    for knobs in (dict(kernel=13, tile_m=256), dict(kernel=13, tile_m=128), dict(kernel=1)):
+        got = run(dg, desc, A8, B8, knobs=knobs)
+        assert_bits_equal(got, want, str(knobs))
     assert np.isnan(want[3]).all() and np.isnan(want[:, 5]).all()
     assert np.isfinite(np.delete(np.delete(want, 3, 0), 5, 1)).all()
 
 
-@pytest.mark.parametrize("kern", [13, 1])
-def test_mlp_shape_sampled(dg, kern):
+@pytest.mark.parametrize("knobs", [dict(kernel=13, tile_m=256), dict(kernel=13, tile_m=128), dict(kernel=1)],
+                         ids=["k13-256", "k13-128", "k1"])
+def test_mlp_shape_sampled(dg, knobs):
     """2048 x 14336 x 4096 with the fused bias + SiLU and bf16 output (the
-    bench's fp8 MLP launch on kernel 13, and the generic kernel), sampled
-    outputs against the oracle."""
+    bench's fp8 MLP launch: kernel 13 on 256 x 256 blocks; also its 128 x 128
+    blocks and the generic kernel), sampled outputs against the oracle."""
     M, N, K = 2048, 14336, 4096
     A8 = inputs.e4m3_weights(41, (M, K), e_mid=4.0)
     B8 = inputs.e4m3_weights(42, (K, N))
     bias = inputs.normal_bf16(43, (N,))
     desc = dict(mma="16x16x128_f8f6f4", tile_k=128, out="bf16", epilogue="bias_silu")
-    print("fp8 MLP shape kernel", kern, flush=True)
-    got = run(dg, desc, A8, B8, bias, knobs=dict(kernel=kern))
+    print("fp8 MLP shape", knobs, flush=True)
+    got = run(dg, desc, A8, B8, bias, knobs=knobs)
     rng = np.random.default_rng(12)
     ii = np.concatenate([rng.integers(0, M, 500), [0, M - 1, M - 1]])
     jj = np.concatenate([rng.integers(0, N, 500), [N - 1, 0, N - 1]])
     want = inputs.f32_to_bf16_bits(oracle.gemm_at(dict(desc, in_dtype="e4m3"), A8, B8, bias, ii, jj))
-    assert_bits_equal(got[ii, jj], want, "fp8 MLP kernel %d" % kern)
+    assert_bits_equal(got[ii, jj], want, "fp8 MLP %s" % knobs)
