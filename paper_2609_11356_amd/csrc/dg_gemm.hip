@@ -1762,8 +1762,12 @@ __device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t 
 // chunk's rows sit in the other half of the 256-byte row (all 64 banks).
 // Per slab each wave issues four A and four B direct-to-LDS loads (16 rows
 // of A or 4 rows of B per 1 KB run) and 16 MFMAs; the accumulators (256
-// floats) live in the accumulation registers.  The ring has four slots,
-// three slabs ahead, and each slot is two LDS arrays (A, B): the compiler
+// floats) live in the accumulation registers.  The ring has four slots
+// and runs four slabs ahead: slab s's slot is free once its fragments are
+// in registers (the barrier ending step s - 1), so step s loads slab s + 4
+// into it, and a load has two to three steps to land (fp8 spends half the
+// bf16 kernel's MFMA time on a slab of the same bytes).  Each slot is two
+// LDS arrays (A, B): the compiler
 // keeps a fragment read apart from the direct-to-LDS loads still in flight
 // only when they touch different arrays (it tracks up to eight), and with
 // one array per slot it made every B-fragment read wait for all of them.
@@ -1792,7 +1796,7 @@ __device__ __forceinline__ uint8_t* f8w_bslot() {
 
 template <int X>
 __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t j0) {
-  constexpr int NS = 4, D = NS - 1;
+  constexpr int NS = 4, D = NS;
   constexpr int BM = 256, BN = 256, BK = 64, CPR = BK / 16, BROW = BN / 16;
   constexpr int WTM = 128, WTN = 128, TM = WTM / 32, TN = WTN / 32;
   constexpr int A_BYTES = BM * BK, B_BYTES = BK * BN;
@@ -1917,11 +1921,16 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   __builtin_amdgcn_s_waitcnt(vmcnt_only(0));   // nothing lands in the staging area later
   __syncthreads();
 
-  // epilogue: wave w stages 16-row halves of its 32-row bands through its
-  // own A array (pitch WTN + 8 floats: the two row sets of one write sit 32
-  // banks apart)
+  // epilogue: the block's bias as binary32 in the B array of slot 0; wave
+  // w stages 16-row halves of its 32-row bands through its own A array
+  // (pitch WTN + 8 floats: the two row sets of one write sit 32 banks
+  // apart) and finishes four columns per store, two stores in flight
   constexpr int CSP = WTN + 8;
-  static_assert(16 * CSP * 4 <= 16384, "epilogue staging fits");
+  static_assert(16 * CSP * 4 <= 16384 && BN * 4 <= 16384, "epilogue staging fits");
+  float* bsh = reinterpret_cast<float*>(f8w_b0);
+  stage_bias(a, j0, BN, bsh);
+  __syncthreads();
+  const bool bias = needs_bias(a);
   float* cs = reinterpret_cast<float*>(wave == 0 ? f8w_a0 : wave == 1 ? f8w_a1 : wave == 2 ? f8w_a2 : f8w_a3);
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
@@ -1933,11 +1942,12 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
         for (int r = 8 * half; r < 8 * half + 8; ++r)
           cs[(8 * (r / 4) - 16 * half + 4 * (lane >> 5) + (r & 3)) * CSP + 32 * ni + (lane & 31)] = acc[mi][ni][r];
       lds_wait();
-#pragma unroll 1
+#pragma unroll 2
       for (int q = lane; q < 16 * WTN / 4; q += 64) {
         const int rr = q / (WTN / 4), cc = 4 * (q % (WTN / 4));
         const int64_t gi = i0 + wm * WTM + 32 * mi + 16 * half + rr, gj = j0 + wn * WTN + cc;
-        if (gi < a.M && gj < a.N) finish4(a, s, gi, gj, *(const float4*)&cs[rr * CSP + cc]);
+        const float4 b4 = bias ? *(const float4*)&bsh[wn * WTN + cc] : float4{0.f, 0.f, 0.f, 0.f};
+        if (gi < a.M && gj < a.N) (void)finish4v(a, s, gi, gj, *(const float4*)&cs[rr * CSP + cc], b4);
       }
       lds_wait();
     }
