@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP8_TFLOPS = 5000.0    # MI355X dense fp8 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 MALL_BYTES = 256 << 20
 
@@ -135,6 +136,15 @@ def profile_only(args, torch, dg, inputs, d_bf16):
         kn = dict(kernel=6, order=args.block_order) if args.block_order else None
         run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr, knobs=kn)
         what = "fused MLP GEMM 2048x14336x4096" + (", block order %d" % args.block_order if kn else "")
+    elif args.only == "fp8mlp":
+        # e4m3 x e4m3 at the MLP shape on kernel 13 (the bench's fp8 row)
+        A8, B8, bias = inputs.e4m3_weights(51, (2048, 4096), e_mid=4.0), inputs.e4m3_weights(52, (4096, 14336)), \
+            inputs.mlp()[2]
+        dA, dB, db = torch.from_numpy(A8).to(dev), torch.from_numpy(B8).to(dev), d_bf16(bias)
+        C = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
+        D = dg.Desc(mma="16x16x128_f8f6f4", tile_k=128, in_dtype="e4m3", out="bf16", epilogue="bias_silu")
+        run = lambda: dg.dg_gemm(D, dA, dB, db, C, stream=sptr)
+        what = "fused MLP GEMM 2048x14336x4096, e4m3 x e4m3 on the fp8 instruction"
     elif args.only in ("tile_tree", "fma0"):
         # the tile-combine kernel at the sweep's M = 1024 shape
         A, B = inputs.sweep_activations(1, rows=4096)[:1024], inputs.sweep_weight(2)
@@ -215,7 +225,7 @@ def main():
     ap.add_argument("--cpu-sample", type=int, default=0,
                     help="MLP outputs the CPU oracle computes for the baseline "
                          "(default: 150000 per host core, about 20 s)")
-    ap.add_argument("--only", choices=("mlp", "copy", "gemv", "decode", "gemv_packed", "decode_packed", "tile_tree",
+    ap.add_argument("--only", choices=("mlp", "fp8mlp", "copy", "gemv", "decode", "gemv_packed", "decode_packed", "tile_tree",
                                        "fma0", "sweep128", "sweep1024", "sweep4096"),
                     default=None,
                     help="profiling runs: launch only the fused MLP GEMM, the M=1 sweep GEMM, "
@@ -570,6 +580,56 @@ def main():
     except Exception as exc:  # reported, never hidden
         fp8 = {"error": repr(exc)}
 
+    # -------------- e4m3 x e4m3 on the fp8 instructions: the SiLU MLP shape
+    # (both operands OCP e4m3 codes shaped like quantised tensors; the fp8
+    # 16-k chunk order, kernel 13 on 256 x 256 blocks); the free-order
+    # reference is hipBLASLt's fp8 GEMM (torch._scaled_mm, unit scales, no
+    # epilogue), timed in alternating blocks
+    f8mlp = {}
+    f8mlp_out = {}
+    try:
+        A8_m = inputs.e4m3_weights(51, (2048, 4096), e_mid=4.0)
+        B8_m = inputs.e4m3_weights(52, (4096, 14336))
+        dA8_m = torch.from_numpy(A8_m).to(dev)
+        dB8_m = [torch.from_numpy(B8_m).to(dev)]
+        dB8_m += [dB8_m[0].clone() for _ in range(max(1, -(-2 * MALL_BYTES // B8_m.nbytes)) - 1)]
+        fl8 = 2 * 2048 * 14336 * 4096
+        for name, dd in (("bias_silu", dict(mma="16x16x128_f8f6f4", tile_k=128, in_dtype="e4m3", out="bf16",
+                                             epilogue="bias_silu")),
+                         ("plain", dict(mma="16x16x128_f8f6f4", tile_k=128, in_dtype="e4m3", out="bf16"))):
+            Dv = dg.Desc(**dd)
+            C_ = torch.empty((2048, 14336), dtype=torch.bfloat16, device=dev)
+            bb = dbias if dd.get("epilogue", "none") != "none" else None
+            run = lambda i, Dv=Dv, C_=C_, bb=bb: dg.dg_gemm(Dv, dA8_m, dB8_m[i % len(dB8_m)], bb, C_, stream=sptr)
+            for i in range(args.warmup):
+                run(i)
+            row = {"desc": dd}
+            try:
+                a8 = dA8_m.view(torch.float8_e4m3fn)
+                b8t = [b.view(torch.float8_e4m3fn).t().contiguous().t() for b in dB8_m]
+                one = torch.ones((), device=dev)
+                free8 = lambda i: torch._scaled_mm(a8, b8t[i % len(b8t)], scale_a=one, scale_b=one,
+                                                   out_dtype=torch.bfloat16)
+                t8, tf8 = paired(run, free8, max(5, reps // 2))
+                row["hipblaslt_fp8_us"] = round(tf8 * 1e3, 2)
+                row["cost_vs_hipblaslt_fp8"] = round(t8 / tf8, 3)
+            except Exception as exc:  # the reference never conditions the library's row
+                t8 = timeit(run, reps)
+                row["free_error"] = repr(exc)
+            run(0)
+            torch.cuda.synchronize()
+            row["us_per_launch"] = round(t8 * 1e3, 2)
+            row["TFLOP/s"] = round(fl8 / (t8 * 1e-3) / 1e12, 1)
+            row["frac_fp8_peak"] = round(fl8 / (t8 * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4)
+            f8mlp[name] = row
+            f8mlp_out[name] = (dd, C_)
+        f8mlp["what"] = ("2048 x 14336 x 4096, A and B OCP e4m3, fp8 16-k chunk order (kernel 13: 256 x 256 "
+                         "blocks, block-scaled 32x32x64 at unit scales), bf16 out, with and without the fused "
+                         "bias + SiLU; FLOP 2MNK against the 5.0 PFLOP/s dense fp8 peak; the reference is "
+                         "torch._scaled_mm (hipBLASLt fp8, free order, no epilogue)")
+    except Exception as exc:  # reported, never hidden
+        f8mlp = {"error": repr(exc)}
+
     # ------------------------------------------------------------ attention
     # 32 heads x 4096 tokens x 128 (a Llama-style head set), bf16, key
     # blocks of 64, BLOCK_M 128, the block row sum by the balanced tree; the
@@ -749,6 +809,11 @@ def main():
         ii = rng.integers(0, A_h.shape[0], 300)
         jj = rng.integers(0, 4096, 300)
         tally(host(C_)[ii, jj], oracle.gemm_at(dd, A_h, B8, None, ii, jj))
+    for name, (dd, C_) in f8mlp_out.items():
+        ii = rng.integers(0, 2048, 300)
+        jj = rng.integers(0, 14336, 300)
+        bb = bias_mlp if dd.get("epilogue", "none") != "none" else None
+        tally(host(C_)[ii, jj], oracle.gemm_at(dd, A8_m, B8_m, bb, ii, jj))
     for c in (0, 1):
         hh = rng.integers(0, H_at, 8)
         ii = rng.integers(0, L_at, 8)
@@ -818,6 +883,7 @@ def main():
         "hipblaslt_order": vendor,
         "few_row_packed": few,
         "e4m3_weights": fp8,
+        "fp8_mlp": f8mlp,
         "bit_match": {"checked": checked, "matched": matched,
                       "pct": round(100.0 * matched / max(checked, 1), 4),
                       "batch_invariant_row0": inv_ok},
