@@ -328,8 +328,10 @@ typedef struct {
                       An e4m3 B (DG_IN_BF16_E4M3) runs on kernel 1 (row-major)
                       and kernel 11 (packed).  13 the fp8 kernel, the only one
                       besides kernel 1 for e4m3 x e4m3 (DG_IN_E4M3) and for
-                      nothing else: 128 x 128 blocks of four waves on the
-                      block-scaled 16x16x128 instruction (no other knob;
+                      nothing else: four waves on the block-scaled fp8
+                      instructions, blocks tile_m x tile_n of 128 x 128,
+                      256 x 256 or 256 x 128 (0: 256 x 128 from 129 rows
+                      on, else 128 x 128; no other knob;
                       the library's choice when tile_combine is DG_CARRY,
                       fma = 1, the split contiguous, K and N multiples of
                       16, every part start and leading short tile on a

@@ -83,6 +83,11 @@ bool make_signature(dg_desc* d) {
 
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
 
+// Block width of the fp8 kernel's 256-row blocks (speed only): 256 x 128 blocks
+// run two per CU, so one block's prologue and epilogue overlap the other's
+// main loop (MLP 2048 x 14336 x 4096 with bias + SiLU: 148 against 172 us)
+constexpr int F8_AUTO_TN = 128;
+
 // ------------------------------------------------------------ workspace
 
 struct Workspace {
@@ -320,7 +325,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   const bool f8 = p.in_dtype == DG_IN_E4M3;
   if (f8 && (packed || !(kern == 0 || kern == 1 || kern == 13))) return DG_ERR_UNSUPPORTED;
   if (!f8 && kern == 13) return DG_ERR_UNSUPPORTED;
-  if (kern == 13 && (tn || order || occ || depth || slab_k || split_n || !(tm == 0 || tm == 128 || tm == 256)))
+  // kernel 13 blocks: 128 x 128, 256 x 256 or 256 x 128 (tile_m, tile_n)
+  if (kern == 13 && (order || occ || depth || slab_k || split_n ||
+                     !((tm == 0 && tn == 0) || (tm == 128 && (tn == 0 || tn == 128)) ||
+                       (tm == 256 && (tn == 0 || tn == 128 || tn == 256)))))
     return DG_ERR_UNSUPPORTED;
   if (kern != 3 && kern != 5 && kern != 6 && kern != 7 && kern != 10 && order) return DG_ERR_UNSUPPORTED;
   if ((kern == 6 || kern == 7 || kern == 10) && (tm || tn || split_n < 0 || split_n % 256 || split_n > N))
@@ -425,12 +433,13 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
     }
     if (kern == 13 && !f8_ok) return DG_ERR_UNSUPPORTED;
     if (kern == 0) kern = f8_ok ? 13 : 1;
-    // 256 x 256 blocks (buffer offsets: M K and K N bytes below 2^31) from
+    // 256-row blocks (buffer offsets: M K and K N bytes below 2^31) from
     // 129 rows on, else 128 x 128
     if (kern == 13) {
       const bool big_ok = M * K < 0x7fffffff && K * N < 0x7fffffff;
       if (tm == 256 && !big_ok) return DG_ERR_UNSUPPORTED;
       if (!tm) tm = (M > 128 && big_ok) ? 256 : 128;
+      if (!tn) tn = tm == 256 ? F8_AUTO_TN : 128;
     }
   }
   hipStream_t st = (hipStream_t)stream;
@@ -525,9 +534,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern == 11) {
     e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
   } else if (kern == 13) {
-    if (((M + tm - 1) / tm) * ((N + tm - 1) / tm) > INT32_MAX) return DG_ERR_SHAPE;
+    if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = 1;
-    e = dg::launch_gemm_f8(a, tm, st);
+    e = dg::launch_gemm_f8(a, tm == 256 && tn == 128 ? 256 + 128 : tm, st);
   } else if (kern == 12) {
     if (((M + 127) / 128) * ((N + 63) / 64) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = 1;

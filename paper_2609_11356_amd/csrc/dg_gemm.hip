@@ -1750,7 +1750,8 @@ __device__ __forceinline__ void w4d_body(const GemmArgs& a, int64_t i0, int64_t 
 }
 
 // e4m3 x e4m3 (carried accumulator, fma = 1) on 256 x 256 blocks of four
-// 128 x 128 waves: the w4d pipeline above with bytes for bf16 elements.
+// 128 x 128 waves, or 256 x 128 blocks of four 128 x 64 waves (two blocks
+// per CU): the w4d pipeline above with bytes for bf16 elements.
 // The slab is 64 k, so A rows are 64 bytes (the bf16 slab's layout and
 // swizzle) and the instruction is the block-scaled 32x32x64 (unit scales),
 // whose K is the slab: lane l's bytes 0..15 are k = 16(l/32) + e, bytes
@@ -1786,22 +1787,36 @@ __device__ __forceinline__ uint8_t* f8w_aslot() {
   else if constexpr (S == 2) return f8w_a2;
   else return f8w_a3;
 }
-template <int S>
+// The 256 x 128 blocks' B slots (64 x 128 bytes): a block then takes
+// 72 KB of LDS and registers for two waves per SIMD, so two blocks share a
+// CU and one's prologue and epilogue run beside the other's main loop.
+__shared__ __attribute__((aligned(1024))) uint8_t f8n_b0[8192];
+__shared__ __attribute__((aligned(1024))) uint8_t f8n_b1[8192];
+__shared__ __attribute__((aligned(1024))) uint8_t f8n_b2[8192];
+template <int BN, int S>
 __device__ __forceinline__ uint8_t* f8w_bslot() {
-  if constexpr (S == 0) return f8w_b0;
-  else if constexpr (S == 1) return f8w_b1;
-  else if constexpr (S == 2) return f8w_b2;
-  else return f8w_b3;
+  if constexpr (BN == 128) {
+    if constexpr (S == 0) return f8n_b0;
+    else if constexpr (S == 1) return f8n_b1;
+    else return f8n_b2;
+  } else {
+    if constexpr (S == 0) return f8w_b0;
+    else if constexpr (S == 1) return f8w_b1;
+    else if constexpr (S == 2) return f8w_b2;
+    else return f8w_b3;
+  }
 }
 
-template <int X>
+// BN 256: four slots; BN 128 (waves of 128 x 64): three slots.
+template <int BN>
 __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t j0) {
-  constexpr int NS = 4, D = NS;
-  constexpr int BM = 256, BN = 256, BK = 64, CPR = BK / 16, BROW = BN / 16;
-  constexpr int WTM = 128, WTN = 128, TM = WTM / 32, TN = WTN / 32;
+  constexpr int NS = BN == 256 ? 4 : 3, D = NS;
+  constexpr int BM = 256, BK = 64, CPR = BK / 16, BROW = BN / 16;
+  constexpr int WTM = 128, WTN = BN / 2, TM = WTM / 32, TN = WTN / 32;
   constexpr int A_BYTES = BM * BK, B_BYTES = BK * BN;
   constexpr int NIA = A_BYTES / 1024 / 4, NIB = B_BYTES / 1024 / 4, NI = NIA + NIB;   // per wave
-  static_assert(NI == 2 * TM && TM == TN && A_BYTES == 16384 && B_BYTES == 16384, "two loads per MFMA row");
+  constexpr int BRUN = 1024 / (16 * BROW);                                            // B rows per 1 KB run
+  static_assert((BN == 256 || BN == 128) && TN <= TM && A_BYTES == 16384, "block shapes");
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
@@ -1809,10 +1824,12 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
-  auto ldsB = [](int k, int c) { return k * BROW + (c ^ (k & 7) ^ ((c & 1) << 3)); };
+  // 128-byte B rows: two rows span the 64 banks, so c ^ (k & 7) already
+  // spreads a transposing read's 8 rows and two groups over them
+  auto ldsB = [](int k, int c) { return k * BROW + (c ^ (k & 7) ^ (BROW == 16 ? (c & 1) << 3 : 0)); };
 
   // load t of the wave: A run r = NIA wave + t (rows 16r..), B run
-  // r = NIB wave + (t - NIA) (k rows 4r..); each lane fetches the chunk
+  // r = NIB wave + (t - NIA) (k rows BRUN r..); each lane fetches the chunk
   // that belongs at its LDS position under the swizzle
   constexpr uint32_t OOB = 0x80000000u;
   uint32_t off[NI];
@@ -1826,8 +1843,8 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   }
 #pragma unroll
   for (int u = 0; u < NIB; ++u) {
-    const int kr = (NIB * wave + u) * 4 + lane / 16, pc = lane % 16;
-    const int c = pc ^ (kr & 7) ^ (((pc ^ kr) & 1) << 3);   // the chunk stored at position pc
+    const int kr = (NIB * wave + u) * BRUN + lane / BROW, pc = lane % BROW;
+    const int c = pc ^ (kr & 7) ^ (BROW == 16 ? ((pc ^ kr) & 1) << 3 : 0);   // the chunk stored at position pc
     off[NIA + u] = (j0 + 16 * c < a.N) ? (uint32_t)(kr * a.N + j0 + 16 * c) : OOB;
     kc[NIA + u] = kr;
   }
@@ -1848,7 +1865,7 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(f8w_aslot<sl_>() + (NIA * wave + t) * 1024), 16,
                                                kc[t] < lim ? off[t] : OOB, (int)ks, 0, 0);
     else
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(f8w_bslot<sl_>() + (NIB * wave + t - NIA) * 1024), 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(f8w_bslot<BN, sl_>() + (NIB * wave + t - NIA) * 1024), 16,
                                                kc[t] < lim ? off[t] : OOB, (int)((ks - k0) * a.N), 0, 0);
   };
 
@@ -1868,7 +1885,7 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
     f = intx8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
   };
   auto rdB = [&](auto SL, int ni, intx8& f) {
-    const uint8_t* Bs = f8w_bslot<decltype(SL)::value>();
+    const uint8_t* Bs = f8w_bslot<BN, decltype(SL)::value>();
     const int q = lane >> 4, i = lane & 15, h = q >> 1;
     const int c = (wn * WTN + 32 * ni + 16 * (q & 1)) / 16;
     intx2 v[4];
@@ -1904,20 +1921,30 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
         acc[mi][ni] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[cur][mi], fb[cur][ni], acc[mi][ni],
                                                                       0, 0, 0, 127, 0, 127);
       __builtin_amdgcn_sched_barrier(0);
-      rdA(rslot, mi, fa[nxt][mi]);
-      rdB(rslot, mi, fb[nxt][mi]);
-      dma1(sl + D, wslot, std::integral_constant<int, 2 * decltype(mi)::value>{});
-      dma1(sl + D, wslot, std::integral_constant<int, 2 * decltype(mi)::value + 1>{});
+      constexpr int MI = decltype(mi)::value;
+      rdA(rslot, MI, fa[nxt][MI]);
+      if constexpr (MI < TN) rdB(rslot, MI, fb[nxt][MI]);
+      // the step's NI loads spread over the TM row groups
+      static_for<0, NI>([&](auto t) {
+        if constexpr (decltype(t)::value * TM / NI == MI) dma1(sl + D, wslot, t);
+      });
       __builtin_amdgcn_sched_barrier(0);
     });
     lds_wait();
     __builtin_amdgcn_s_waitcnt(vmcnt_only((D - 2) * NI));   // the wave's loads of slab sl+2 landed
     barrier_nofence();
   };
-  // slabs past the part end (up to NS - 1 of them) are zero: their chunks
-  // hold no product and leave the accumulators as they are
-  for (int sl = 0; sl < nslab; sl += NS)
-    static_for<0, NS>([&](auto x) { step(sl + x, x); });
+  // slot x % NS, fragment set x & 1: the pattern repeats every U slabs.
+  // Whole groups of U run unguarded; the last group stops at the part end
+  // (slabs past it would be zero: no product, accumulators unchanged)
+  constexpr int U = NS % 2 == 0 ? NS : 2 * NS;
+  int sl = 0;
+  for (; sl + U <= nslab; sl += U)
+    static_for<0, U>([&](auto x) { step(sl + x, x); });
+  if (sl < nslab)
+    static_for<0, U>([&](auto x) {
+      if (sl + decltype(x)::value < nslab) step(sl + x, x);
+    });
   __builtin_amdgcn_s_waitcnt(vmcnt_only(0));   // nothing lands in the staging area later
   __syncthreads();
 
@@ -1926,12 +1953,15 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   // (pitch WTN + 8 floats: the two row sets of one write sit 32 banks
   // apart) and finishes four columns per store, two stores in flight
   constexpr int CSP = WTN + 8;
-  static_assert(16 * CSP * 4 <= 16384 && BN * 4 <= 16384, "epilogue staging fits");
-  float* bsh = reinterpret_cast<float*>(f8w_b0);
+  static_assert(16 * CSP * 4 <= 16384 && BN * 4 <= B_BYTES, "epilogue staging fits");
+  float* bsh = reinterpret_cast<float*>(f8w_bslot<BN, 0>());
   stage_bias(a, j0, BN, bsh);
   __syncthreads();
   const bool bias = needs_bias(a);
-  float* cs = reinterpret_cast<float*>(wave == 0 ? f8w_a0 : wave == 1 ? f8w_a1 : wave == 2 ? f8w_a2 : f8w_a3);
+  // (256 x 128 blocks: two waves per A array, 8 KB each, within the ring's three)
+  float* cs = BN == 256 ? reinterpret_cast<float*>(wave == 0 ? f8w_a0 : wave == 1 ? f8w_a1 : wave == 2 ? f8w_a2 : f8w_a3)
+                        : reinterpret_cast<float*>((wave < 2 ? f8w_a0 : f8w_a1) + 8192 * (wave & 1));
+  static_assert(BN == 256 || 16 * CSP * 4 <= 8192, "two staging areas per A array");
 #pragma unroll
   for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
@@ -1958,7 +1988,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int tiles_m = (int)((a.M + 255) / 256);
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
-  f8w_body<0>(a, (int64_t)ty * 256, (int64_t)tx * 256);
+  f8w_body<256>(a, (int64_t)ty * 256, (int64_t)tx * 256);
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_f8n(GemmArgs a) {
+  const int tiles_m = (int)((a.M + 255) / 256);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  f8w_body<128>(a, (int64_t)ty * 256, (int64_t)tx * 128);
 }
 
 // Columns [0, n_split) in 256 x 256 blocks, the rest in 256 x 192 blocks.
@@ -2530,6 +2567,11 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) 
 }
 
 hipError_t launch_gemm_f8(const GemmArgs& a, int tile, hipStream_t st) {
+  if (tile == 256 + 128) {   // 256 x 128 blocks
+    const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 127) / 128);
+    hipLaunchKernelGGL(gemm_f8n, dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
   if (tile == 256) {
     const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 255) / 256);
     hipLaunchKernelGGL(gemm_f8w, dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);

@@ -372,7 +372,8 @@ def test_fp8_descriptors_need_no_gpu(dg):
                        (d, 56, 512), (d, 64, 520)]:
         assert lib.dg_gemm_knobs(desc.handle, 16, 16, None, 16, 16, N, K, ctypes.byref(k13), None) == \
             dg.DG_ERR_UNSUPPORTED, (desc.signature(), N, K)
-    for kn in (dg.dg_knobs(13, 128, 128, 0, 0, 0, 0, 0), dg.dg_knobs(13, 0, 0, 1, 0, 0, 0, 0)):
+    for kn in (dg.dg_knobs(13, 128, 256, 0, 0, 0, 0, 0), dg.dg_knobs(13, 0, 0, 1, 0, 0, 0, 0),
+               dg.dg_knobs(13, 0, 128, 0, 0, 0, 0, 0), dg.dg_knobs(13, 64, 0, 0, 0, 0, 0, 0)):
         assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 16, 64, 512, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
     # byte operands need no alignment of their own; kernel 13 needs 16-byte rows

@@ -109,9 +109,9 @@ def test_matches_oracle(dg, di, shape):
         assert_bits_equal(run(dg, desc, A8, B8, bias), want, "%s %s %s" % (desc, shape, draw))
         assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=1)), want, "generic %s" % desc)
         if tiled:
-            for tm in (128, 256):
-                assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=13, tile_m=tm)), want,
-                                  "kernel 13 tile %d %s" % (tm, desc))
+            for tm, tn in ((128, 128), (256, 256), (256, 128)):
+                assert_bits_equal(run(dg, desc, A8, B8, bias, knobs=dict(kernel=13, tile_m=tm, tile_n=tn)), want,
+                                  "kernel 13 tile %dx%d %s" % (tm, tn, desc))
 
 
 def test_instruction_names_give_the_same_bits_under_fma(dg):
@@ -135,8 +135,9 @@ def test_explicit_cuts_on_and_off_the_16k_grid(dg):
         want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
         assert_bits_equal(run(dg, desc, A8, B8), want, str(cuts))
         if tiled:
-            for tm in (128, 256):
-                assert_bits_equal(run(dg, desc, A8, B8, knobs=dict(kernel=13, tile_m=tm)), want, "kernel 13 %s" % cuts)
+            for tm, tn in ((128, 128), (256, 256), (256, 128)):
+                assert_bits_equal(run(dg, desc, A8, B8, knobs=dict(kernel=13, tile_m=tm, tile_n=tn)), want,
+                                  "kernel 13 %s" % cuts)
         else:
             with pytest.raises(dg.DgError) as e:
                 run(dg, desc, A8, B8, knobs=dict(kernel=13))
@@ -149,7 +150,7 @@ def test_refusals(dg):
                         (dict(mma="16x16x32_fp8", tile_k=64, tile_combine="tree"), dict(kernel=13)),
                         (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=3)),
                         (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=64)),
-                        (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=256, tile_n=256))]:
+                        (dict(mma="16x16x32_fp8", tile_k=64), dict(kernel=13, tile_m=256, tile_n=64))]:
         with pytest.raises(dg.DgError) as e:
             run(dg, desc, A8, B8, knobs=knobs)
         assert e.value.status == dg.DG_ERR_UNSUPPORTED, (desc, knobs)
@@ -174,15 +175,17 @@ def test_special_codes(dg):
     B8[:, 6] = 0x7E
     desc = dict(mma="16x16x128_f8f6f4", tile_k=128)
     want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
-    for knobs in (dict(kernel=13, tile_m=256), dict(kernel=13, tile_m=128), dict(kernel=1)):
+    for knobs in (dict(kernel=13, tile_m=256, tile_n=256), dict(kernel=13, tile_m=256, tile_n=128),
+                  dict(kernel=13, tile_m=128), dict(kernel=1)):
         got = run(dg, desc, A8, B8, knobs=knobs)
         assert_bits_equal(got, want, str(knobs))
     assert np.isnan(want[3]).all() and np.isnan(want[:, 5]).all()
     assert np.isfinite(np.delete(np.delete(want, 3, 0), 5, 1)).all()
 
 
-@pytest.mark.parametrize("knobs", [dict(kernel=13, tile_m=256), dict(kernel=13, tile_m=128), dict(kernel=1)],
-                         ids=["k13-256", "k13-128", "k1"])
+@pytest.mark.parametrize("knobs", [dict(kernel=13, tile_m=256, tile_n=256), dict(kernel=13, tile_m=256, tile_n=128),
+                                   dict(kernel=13, tile_m=128), dict(kernel=1)],
+                         ids=["k13-256", "k13-256x128", "k13-128", "k1"])
 def test_mlp_shape_sampled(dg, knobs):
     """2048 x 14336 x 4096 with the fused bias + SiLU and bf16 output (the
     bench's fp8 MLP launch: kernel 13 on 256 x 256 blocks; also its 128 x 128
