@@ -338,7 +338,10 @@ typedef struct {
                       multiple of 16, A, B, C and bias 16-byte aligned;
                       otherwise DG_ERR_UNSUPPORTED, and kernel 0 runs the
                       generic kernel 1).  e4m3 x e4m3 is not taken by
-                      dg_gemm_packed */
+                      dg_gemm_packed.  14 bf16 operands on kernel 13's
+                      pipeline (256 x 128 blocks, two per CU, 32x32x16
+                      instructions; the tiled layout's conditions; no
+                      other knob) */
   int32_t tile_m;  /* tiled kernels' rows per workgroup: 0, 16, 32, 64, 128, 256
                       (kernel 3: no 256 x 256 block) */
   int32_t tile_n;  /* tiled kernels' columns per workgroup: 0, 64, 128, 256 */

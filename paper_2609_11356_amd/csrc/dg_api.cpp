@@ -305,7 +305,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   int order = knobs ? knobs->order : 0, occ = knobs ? knobs->occupancy : 0;
   int depth = knobs ? knobs->depth : 0, slab_k = knobs ? knobs->slab_k : 0;
   int64_t split_n = knobs ? knobs->split_n : 0;
-  if (!in(kern, 0, 13) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
+  if (!in(kern, 0, 14) || !in(order, 0, 3) || !in(occ, 0, 2)) return DG_ERR_UNSUPPORTED;
   // packed B runs on kernel 11 only, and kernel 11 runs nothing else
   if (packed ? (kern != 0 && kern != 11) : kern == 11) return DG_ERR_UNSUPPORTED;
   if (packed) kern = 11;
@@ -325,6 +325,9 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   const bool f8 = p.in_dtype == DG_IN_E4M3;
   if (f8 && (packed || !(kern == 0 || kern == 1 || kern == 13))) return DG_ERR_UNSUPPORTED;
   if (!f8 && kern == 13) return DG_ERR_UNSUPPORTED;
+  // kernel 14: bf16 operands only, no knob
+  if (kern == 14 && (p.in_dtype != DG_IN_BF16 || tm || tn || order || occ || depth || slab_k || split_n))
+    return DG_ERR_UNSUPPORTED;
   // kernel 13 blocks: 128 x 128, 256 x 256 or 256 x 128 (tile_m, tile_n)
   if (kern == 13 && (order || occ || depth || slab_k || split_n ||
                      !((tm == 0 && tn == 0) || (tm == 128 && (tn == 0 || tn == 128)) ||
@@ -491,6 +494,7 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   if (kern == 12 && !tc_ok) return DG_ERR_UNSUPPORTED;
   if (kern == 0 && !tiled_ok && tc_ok) kern = 12;
   if (kern >= 2 && kern != 9 && kern != 11 && kern != 12 && kern != 13 && !tiled_ok) return DG_ERR_UNSUPPORTED;
+  if (kern == 14 && !(M * K < 0x3fffffff && K * N < 0x3fffffff)) return DG_ERR_UNSUPPORTED;
   if (strided && kern == 0) {
     const int tmc = M <= 16 ? 16 : M <= 32 ? 32 : 64;
     const int tnc = (a.S * ((N + 63) / 64) >= 256) ? 64 : 32;
@@ -533,6 +537,10 @@ static dg_status gemm_impl(const dg_desc* d, const void* A, const void* B, const
   hipError_t e;
   if (kern == 11) {
     e = dg::launch_gemm_panel(a, panel_tms, panel_depth, panel_avec, st);
+  } else if (kern == 14) {
+    if (((M + 255) / 256) * ((N + 127) / 128) > INT32_MAX) return DG_ERR_SHAPE;
+    a.order = 1;
+    e = dg::launch_gemm_b16n(a, st);
   } else if (kern == 13) {
     if (((M + tm - 1) / tm) * ((N + tn - 1) / tn) > INT32_MAX) return DG_ERR_SHAPE;
     a.order = 1;

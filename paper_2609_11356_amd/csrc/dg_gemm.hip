@@ -1807,13 +1807,18 @@ __device__ __forceinline__ uint8_t* f8w_bslot() {
   }
 }
 
-// BN 256: four slots; BN 128 (waves of 128 x 64): three slots.
-template <int BN>
+// BN 256: four slots; BN 128 (waves of 128 x 64): three slots.  EB is the
+// operand's bytes: 1 (e4m3, 64-k slabs, the block-scaled 32x32x64) or 2
+// (bf16, 32-k slabs of the same bytes, two 32x32x16 bf16 instructions per
+// slab in k order -- the bf16 chain of 8-k chunks; 256 x 128 blocks only).
+template <int BN, int EB = 1>
 __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t j0) {
   constexpr int NS = BN == 256 ? 4 : 3, D = NS;
-  constexpr int BM = 256, BK = 64, CPR = BK / 16, BROW = BN / 16;
+  constexpr int EPC = 16 / EB;                                  // elements per 16-byte chunk
+  constexpr int BM = 256, BK = 64 / EB, CPR = 4, BROW = BN * EB / 16;
   constexpr int WTM = 128, WTN = BN / 2, TM = WTM / 32, TN = WTN / 32;
-  constexpr int A_BYTES = BM * BK, B_BYTES = BK * BN;
+  constexpr int A_BYTES = BM * BK * EB, B_BYTES = BK * BN * EB;
+  static_assert(EB == 1 || BN == 128, "bf16: 256 x 128 blocks");
   constexpr int NIA = A_BYTES / 1024 / 4, NIB = B_BYTES / 1024 / 4, NI = NIA + NIB;   // per wave
   constexpr int BRUN = 1024 / (16 * BROW);                                            // B rows per 1 KB run
   static_assert((BN == 256 || BN == 128) && TN <= TM && A_BYTES == 16384, "block shapes");
@@ -1824,9 +1829,15 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   const int64_t k0 = a.cuts[s], k1 = a.cuts[s + 1];
   const int nslab = (int)((k1 - k0 + BK - 1) / BK);
   auto ldsA = [](int row, int c) { return row * CPR + (c ^ swz_a<CPR>(row)); };
-  // 128-byte B rows: two rows span the 64 banks, so c ^ (k & 7) already
-  // spreads a transposing read's 8 rows and two groups over them
-  auto ldsB = [](int k, int c) { return k * BROW + (c ^ (k & 7) ^ (BROW == 16 ? (c & 1) << 3 : 0)); };
+  // e4m3, 128-byte B rows: two rows span the 64 banks, so c ^ (k & 7)
+  // already spreads a transposing read's 8 rows and two groups over them.
+  // bf16 (256-byte rows, 4-row transposing reads of 32 bytes per 16-lane
+  // group): c ^ 4 (k & 3) gives the 4 rows of both groups of a pass 16
+  // different chunks.
+  auto ldsB = [](int k, int c) {
+    if constexpr (EB == 2) return k * BROW + (c ^ ((k & 3) << 2));
+    else return k * BROW + (c ^ (k & 7) ^ (BROW == 16 ? (c & 1) << 3 : 0));
+  };
 
   // load t of the wave: A run r = NIA wave + t (rows 16r..), B run
   // r = NIB wave + (t - NIA) (k rows BRUN r..); each lane fetches the chunk
@@ -1838,23 +1849,24 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   for (int t = 0; t < NIA; ++t) {
     const int row = (NIA * wave + t) * 16 + lane / 4, pc = lane % 4;
     const int c = pc ^ swz_a<CPR>(row);
-    off[t] = (i0 + row < a.M) ? (uint32_t)(row * a.K + 16 * c) : OOB;
-    kc[t] = 16 * c;
+    off[t] = (i0 + row < a.M) ? (uint32_t)(row * a.K * EB + 16 * c) : OOB;
+    kc[t] = EPC * c;
   }
 #pragma unroll
   for (int u = 0; u < NIB; ++u) {
     const int kr = (NIB * wave + u) * BRUN + lane / BROW, pc = lane % BROW;
-    const int c = pc ^ (kr & 7) ^ (BROW == 16 ? ((pc ^ kr) & 1) << 3 : 0);   // the chunk stored at position pc
-    off[NIA + u] = (j0 + 16 * c < a.N) ? (uint32_t)(kr * a.N + j0 + 16 * c) : OOB;
+    // the chunk stored at position pc
+    const int c = EB == 2 ? pc ^ ((kr & 3) << 2) : pc ^ (kr & 7) ^ (BROW == 16 ? ((pc ^ kr) & 1) << 3 : 0);
+    off[NIA + u] = (j0 + EPC * c < a.N) ? (uint32_t)((kr * a.N + j0 + EPC * c) * EB) : OOB;
     kc[NIA + u] = kr;
   }
   const uint8_t* A8 = (const uint8_t*)a.A;
   const uint8_t* B8 = (const uint8_t*)a.B;
-  const int64_t recA = (a.M - i0) * a.K, recB = (a.K - k0) * a.N;   // below 2^31 (host check)
-  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void*)(A8 + i0 * a.K), (short)0, (int)recA,
-                                                                      0x00020000);
-  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc((void*)(B8 + k0 * a.N), (short)0, (int)recB,
-                                                                      0x00020000);
+  const int64_t recA = (a.M - i0) * a.K * EB, recB = (a.K - k0) * a.N * EB;   // below 2^31 (host check)
+  const __amdgpu_buffer_rsrc_t rA = __builtin_amdgcn_make_buffer_rsrc((void*)(A8 + i0 * a.K * EB), (short)0,
+                                                                      (int)recA, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rB = __builtin_amdgcn_make_buffer_rsrc((void*)(B8 + k0 * a.N * EB), (short)0,
+                                                                      (int)recB, 0x00020000);
   auto dma1 = [&](int sl_in, auto SL, auto T) {
     constexpr int t = decltype(T)::value;
     const bool past = sl_in >= nslab;
@@ -1863,10 +1875,10 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
     constexpr int sl_ = decltype(SL)::value;
     if constexpr (t < NIA)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rA, (lds_void)(f8w_aslot<sl_>() + (NIA * wave + t) * 1024), 16,
-                                               kc[t] < lim ? off[t] : OOB, (int)ks, 0, 0);
+                                               kc[t] < lim ? off[t] : OOB, (int)(ks * EB), 0, 0);
     else
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rB, (lds_void)(f8w_bslot<BN, sl_>() + (NIB * wave + t - NIA) * 1024), 16,
-                                               kc[t] < lim ? off[t] : OOB, (int)((ks - k0) * a.N), 0, 0);
+                                               kc[t] < lim ? off[t] : OOB, (int)((ks - k0) * a.N * EB), 0, 0);
   };
 
   floatx16 acc[TM][TN];
@@ -1876,7 +1888,10 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
     for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[mi][ni][r] = 0.f;
-  intx8 fa[2][TM], fb[2][TN];
+  // bf16 keeps one set of A fragments (a row's next fragment is read once
+  // that row's MFMAs are issued), so that the block fits two waves per SIMD
+  constexpr int FA = EB == 2 ? 1 : 2;
+  intx8 fa[FA][TM], fb[2][TN];
   auto rdA = [&](auto SL, int mi, intx8& f) {
     const uint8_t* As = f8w_aslot<decltype(SL)::value>();
     const int row = wm * WTM + 32 * mi + (lane & 31), h = lane >> 5;
@@ -1887,12 +1902,25 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
   auto rdB = [&](auto SL, int ni, intx8& f) {
     const uint8_t* Bs = f8w_bslot<BN, decltype(SL)::value>();
     const int q = lane >> 4, i = lane & 15, h = q >> 1;
-    const int c = (wn * WTN + 32 * ni + 16 * (q & 1)) / 16;
     intx2 v[4];
+    if constexpr (EB == 1) {
+      const int c = (wn * WTN + 32 * ni + 16 * (q & 1)) / 16;
 #pragma unroll
-    for (int p = 0; p < 4; ++p) {
-      const int kr = (p < 2 ? 16 * h + 8 * p : 32 + 16 * h + 8 * (p - 2)) + (i >> 1);
-      v[p] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i2)(&Bs[16 * ldsB(kr, c) + 8 * (i & 1)]));
+      for (int p = 0; p < 4; ++p) {
+        const int kr = (p < 2 ? 16 * h + 8 * p : 32 + 16 * h + 8 * (p - 2)) + (i >> 1);
+        v[p] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i2)(&Bs[16 * ldsB(kr, c) + 8 * (i & 1)]));
+      }
+    } else {
+      // ds_read_b64_tr_b16: lane i of a 16-lane group addresses row i/4,
+      // columns 4 (i%4).. of a 4 x 16 block and receives column i; two
+      // reads per 8 k (rows 8h.. and 8h + 4..), k 16.. for the second MFMA
+      const int n = wn * WTN + 32 * ni + 16 * (q & 1) + 4 * (i & 3);
+#pragma unroll
+      for (int p = 0; p < 4; ++p) {
+        const int kr = 16 * (p >> 1) + 8 * h + 4 * (p & 1) + (i >> 2);
+        v[p] = __builtin_bit_cast(intx2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                             (lds_s4)(&Bs[16 * ldsB(kr, n / 8) + 2 * (n % 8)])));
+      }
     }
     f = intx8{v[0][0], v[0][1], v[1][0], v[1][1], v[2][0], v[2][1], v[3][0], v[3][1]};
   };
@@ -1917,12 +1945,24 @@ __device__ __forceinline__ void f8w_body(const GemmArgs& a, int64_t i0, int64_t 
     __builtin_amdgcn_sched_barrier(0);
     static_for<0, TM>([&](auto mi) {
 #pragma unroll
-      for (int ni = 0; ni < TN; ++ni)
-        acc[mi][ni] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[cur][mi], fb[cur][ni], acc[mi][ni],
-                                                                      0, 0, 0, 127, 0, 127);
+      for (int ni = 0; ni < TN; ++ni) {
+        if constexpr (EB == 1) {
+          acc[mi][ni] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa[cur][mi], fb[cur][ni], acc[mi][ni],
+                                                                        0, 0, 0, 127, 0, 127);
+        } else {
+          const intx8& x = fa[0][mi];
+          const intx8& y = fb[cur][ni];
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, x, 0, 1, 2, 3)),
+              __builtin_bit_cast(bf16x8, __builtin_shufflevector(y, y, 0, 1, 2, 3)), acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, __builtin_shufflevector(x, x, 4, 5, 6, 7)),
+              __builtin_bit_cast(bf16x8, __builtin_shufflevector(y, y, 4, 5, 6, 7)), acc[mi][ni], 0, 0, 0);
+        }
+      }
       __builtin_amdgcn_sched_barrier(0);
       constexpr int MI = decltype(mi)::value;
-      rdA(rslot, MI, fa[nxt][MI]);
+      rdA(rslot, MI, fa[FA == 1 ? 0 : nxt][MI]);
       if constexpr (MI < TN) rdB(rslot, MI, fb[nxt][MI]);
       // the step's NI loads spread over the TM row groups
       static_for<0, NI>([&](auto t) {
@@ -1996,6 +2036,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
   int ty, tx;
   grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
   f8w_body<128>(a, (int64_t)ty * 256, (int64_t)tx * 128);
+}
+
+// bf16 operands on the same pipeline (256 x 128 blocks, two per CU).
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_b16n(GemmArgs a) {
+  const int tiles_m = (int)((a.M + 255) / 256);
+  int ty, tx;
+  grouped_tile(blockIdx.x, tiles_m, gridDim.x / tiles_m, a.order, &ty, &tx);
+  f8w_body<128, 2>(a, (int64_t)ty * 256, (int64_t)tx * 128);
 }
 
 // Columns [0, n_split) in 256 x 256 blocks, the rest in 256 x 192 blocks.
@@ -2564,6 +2612,12 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t st) 
   if (tm == 256 && tn == 128) return launch_big_t<256, 128, 2, 2>(a, st);
   if (tm == 128 && tn == 256) return launch_big_t<128, 256, 2, 2>(a, st);
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_gemm_b16n(const GemmArgs& a, hipStream_t st) {
+  const int64_t tiles = ((a.M + 255) / 256) * ((a.N + 127) / 128);
+  hipLaunchKernelGGL(gemm_b16n, dim3((unsigned)tiles, 1, (unsigned)a.S), dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_gemm_f8(const GemmArgs& a, int tile, hipStream_t st) {

@@ -113,6 +113,10 @@ hipError_t launch_gemm_tc(const GemmArgs& a, int levels, hipStream_t s);
 // aligned): tile 128, 128 x 128 blocks on 128-k slabs; tile 256, 256 x 256
 // blocks on 64-k slabs loaded direct to LDS (M K and K N below 2^31 bytes)
 hipError_t launch_gemm_f8(const GemmArgs& a, int tile, hipStream_t s);
+// bf16 on the same four-wave ring: 256 x 128 blocks, two per CU, 32-k slabs
+// loaded direct to LDS (the tiled layout's conditions; M K and K N below
+// 2^30 elements)
+hipError_t launch_gemm_b16n(const GemmArgs& a, hipStream_t s);
 hipError_t launch_gemm_wide(const GemmArgs& a, int tile_m, int tile_n, hipStream_t s);
 bool wide_supported(int tile_m, int tile_n);
 bool wide_is_pp(int tile_m, int tile_n);   // the ping-pong kernel (buffer-resource offsets)

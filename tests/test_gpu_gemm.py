@@ -181,7 +181,7 @@ KNOBS = [dict(kernel=1), dict(kernel=2, tile_m=16, tile_n=64), dict(kernel=2, ti
          dict(kernel=5, tile_m=128, tile_n=256, order=2),
          dict(kernel=6), dict(kernel=6, split_n=256), dict(kernel=6, split_n=512, order=3),
          dict(kernel=7), dict(kernel=7, split_n=256), dict(kernel=7, split_n=512, order=3),
-         dict(kernel=10), dict(kernel=10, split_n=256), dict(kernel=10, split_n=512, order=3),
+         dict(kernel=10), dict(kernel=10, split_n=256), dict(kernel=10, split_n=512, order=3), dict(kernel=14),
          dict(kernel=8), dict(kernel=8, tile_m=16, tile_n=32, depth=6, slab_k=256),
          dict(kernel=8, tile_m=32, tile_n=32, depth=4, slab_k=128), dict(kernel=8, tile_m=64, tile_n=32, depth=3, slab_k=128),
          dict(kernel=8, tile_m=16, tile_n=64, depth=6, slab_k=128), None]
