@@ -376,6 +376,8 @@ def test_fp8_descriptors_need_no_gpu(dg):
                dg.dg_knobs(13, 0, 128, 0, 0, 0, 0, 0), dg.dg_knobs(13, 64, 0, 0, 0, 0, 0, 0)):
         assert lib.dg_gemm_knobs(d.handle, 16, 16, None, 16, 16, 64, 512, ctypes.byref(kn), None) == \
             dg.DG_ERR_UNSUPPORTED
+    # the packed entry point takes a bf16 A only
+    assert lib.dg_gemm_packed(d.handle, 16, 16, None, 16, 16, 64, 512, None) == dg.DG_ERR_UNSUPPORTED
     # byte operands need no alignment of their own; kernel 13 needs 16-byte rows
     assert lib.dg_gemm_knobs(d.handle, 17, 16, None, 16, 16, 64, 512, ctypes.byref(k13), None) == \
         dg.DG_ERR_UNSUPPORTED

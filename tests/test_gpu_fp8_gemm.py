@@ -202,3 +202,40 @@ def test_mlp_shape_sampled(dg, knobs):
     jj = np.concatenate([rng.integers(0, N, 500), [N - 1, 0, N - 1]])
     want = inputs.f32_to_bf16_bits(oracle.gemm_at(dict(desc, in_dtype="e4m3"), A8, B8, bias, ii, jj))
     assert_bits_equal(got[ii, jj], want, "fp8 MLP %s" % knobs)
+
+
+def test_other_entry_points(dg):
+    """e4m3 x e4m3 through the entry point that allocates nothing (split-K
+    partials in its fixed scratch: equal to dg_gemm, also on a second,
+    smaller call) and through dg_gemm_colsum (C as dg_gemm writes it, the
+    column sums as the oracle's tree over that C)."""
+    import torch
+    for desc, (M, N, K) in ((dict(mma="16x16x128_f8f6f4", tile_k=128, split_k=4, split_combine="tree"), (300, 272, 2048)),
+                            (dict(mma="16x16x32_fp8", tile_k=32, split_k=3, fma=0, out="bf16"), (40, 96, 1000))):
+        A8, B8 = inputs.e4m3_uniform(M + K, (M, K)), inputs.e4m3_uniform(N + K, (K, N))
+        d = dg.Desc(**dict(desc, in_dtype="e4m3"))
+        out_bf16 = desc.get("out") == "bf16"
+        dt = torch.bfloat16 if out_bf16 else torch.float32
+        for m in (M, M // 2):
+            dA, dB = dev_u8(A8[:m]), dev_u8(B8)
+            C1 = torch.full((m, N), float("nan"), device="cuda", dtype=dt)
+            C2 = torch.full((m, N), float("nan"), device="cuda", dtype=dt)
+            print("fp8 noalloc", desc, (m, N, K), flush=True)
+            dg.dg_gemm(d, dA, dB, None, C1)
+            dg.dg_gemm_noalloc(d, dA, dB, None, C2)
+            torch.cuda.synchronize()
+            assert_bits_equal(host_bits(C2), host_bits(C1), "noalloc %s m=%d" % (desc, m))
+        want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
+        assert_bits_equal(host_bits(C1), want[:M // 2], "dg_gemm %s" % desc)
+    desc = dict(mma="16x16x128_f8f6f4", tile_k=128)
+    M, N, K = 520, 264, 768
+    A8, B8 = inputs.e4m3_weights(61, (M, K)), inputs.e4m3_weights(62, (K, N))
+    d = dg.Desc(**dict(desc, in_dtype="e4m3"))
+    C = torch.full((M, N), float("nan"), device="cuda", dtype=torch.float32)
+    cs = torch.full((N,), float("nan"), device="cuda", dtype=torch.float32)
+    print("fp8 colsum", flush=True)
+    dg.dg_gemm_colsum(d, dev_u8(A8), dev_u8(B8), None, C, cs)
+    torch.cuda.synchronize()
+    want = oracle.gemm(dict(desc, in_dtype="e4m3"), A8, B8)
+    assert_bits_equal(host_bits(C), want, "colsum GEMM")
+    assert_bits_equal(cs.cpu().numpy(), oracle.colsum(want), "column sums")
