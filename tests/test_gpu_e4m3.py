@@ -112,7 +112,12 @@ DESCS = [
 def test_ragged_shapes(dg, di, packed):
     desc = DESCS[di]
     if packed and (desc.get("fma", 1) == 0 or desc.get("tile_combine", "carry") != "carry"):
-        pytest.skip("the packed kernel takes a carried accumulator only")
+        # the packed kernel takes a carried, fused accumulator only: refused
+        A, B8 = inputs.normal_bf16(7, (5, 256)), inputs.e4m3_uniform(8, (256, 16))
+        with pytest.raises(dg.DgError) as ei:
+            run(dg, desc, A, B8, packed=True)
+        assert ei.value.status == dg.DG_ERR_UNSUPPORTED
+        return
     for (M, N, K), draw in [((1, 37, 1000), "uniform"), ((7, 160, 256), "weights"), ((33, 50, 512), "uniform"),
                             ((64, 21, 320), "weights"), ((5, 16, 100), "uniform")]:
         if packed and K % 8:

@@ -88,7 +88,15 @@ def test_matches_oracle(dg, di, shape):
     desc = DESCS[di]
     M, N, K = shape
     if any(ln == 0 for ln in parts(desc, K)):
-        pytest.skip("the span rule leaves a part empty at this K (refused on both sides elsewhere)")
+        # the span rule leaves a part empty: the oracle and the library both refuse
+        A, B = inputs.normal_bf16(7, (M, K)), inputs.normal_bf16(8, (K, N))
+        bias = inputs.normal_bf16(9, (N,)) if desc.get("epilogue", "none") != "none" else None
+        with pytest.raises(oracle.OracleError, match="status 3"):
+            oracle.gemm(desc, A, B, bias)
+        with pytest.raises(dg.DgError) as ei:
+            run(dg, desc, A, B, bias)
+        assert ei.value.status == dg.DG_ERR_SHAPE
+        return
     seed = 1000 + 37 * di + M + K
     bias = inputs.normal_bf16(seed + 2, (N,), 0.5) if desc.get("epilogue", "none") != "none" else None
     tiled = takes_tiled_path(desc, K, N)
