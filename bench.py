@@ -623,8 +623,8 @@ def main():
             row["frac_fp8_peak"] = round(fl8 / (t8 * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4)
             f8mlp[name] = row
             f8mlp_out[name] = (dd, C_)
-        f8mlp["what"] = ("2048 x 14336 x 4096, A and B OCP e4m3, fp8 16-k chunk order (kernel 13: 256 x 256 "
-                         "blocks, block-scaled 32x32x64 at unit scales), bf16 out, with and without the fused "
+        f8mlp["what"] = ("2048 x 14336 x 4096, A and B OCP e4m3, fp8 16-k chunk order (kernel 13: 256 x 128 "
+                         "blocks, two per CU, block-scaled 32x32x64 at unit scales), bf16 out, with and without the fused "
                          "bias + SiLU; FLOP 2MNK against the 5.0 PFLOP/s dense fp8 peak; the reference is "
                          "torch._scaled_mm (hipBLASLt fp8, free order, no epilogue)")
     except Exception as exc:  # reported, never hidden
