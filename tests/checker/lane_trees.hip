@@ -1,0 +1,114 @@
+// Wave-level sums of x[0..63] (one wave of 64 lanes) written several ways,
+// for the static order checker: the lane steps of the library (dg_lanes.h)
+// and hand-written alternatives.  Compiled to gfx950 assembly only; never
+// launched.
+#include <hip/hip_runtime.h>
+
+#include "../../paper_2609_11356_amd/csrc/dg_lanes.h"
+
+#define KERNEL extern "C" __global__ void __launch_bounds__(64)
+
+// the count-up tree as the library lowers it (DPP, ds_swizzle, ds_bpermute)
+KERNEL up_library(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  y[l] = dg::tree_sum_lanes<6>(x[l]);
+}
+
+// the same tree with every step a __shfl_xor
+KERNEL up_shfl(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  for (int m = 1; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
+  y[l] = v;
+}
+
+// four consecutive elements per lane (pairwise in the lane), 16 lanes
+KERNEL up_four(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  if (l < 16) {
+    const float a = x[4 * l], b = x[4 * l + 1], c = x[4 * l + 2], d = x[4 * l + 3];
+    const float v = dg::tree_sum_lanes<4>((a + b) + (c + d));
+    if (l == 0) y[0] = v;
+  }
+}
+
+// two consecutive elements per lane, 32 lanes
+KERNEL up_two(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  if (l < 32) {
+    const float v = dg::tree_sum_lanes<5>(x[2 * l] + x[2 * l + 1]);
+    if (l == 0) y[0] = v;
+  }
+}
+
+// lanes read the elements in reverse order: every node's operands swap,
+// which addition's commutativity allows
+KERNEL up_reversed(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  const float v = dg::tree_sum_lanes<6>(x[63 - l]);
+  if (l == 0) y[0] = v;
+}
+
+// the count-down fold (lanes 32 apart first), the library's xor partners
+KERNEL down_library(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  v = v + dg::xor_partner<32>(v);
+  v = v + dg::xor_partner<16>(v);
+  v = v + dg::xor_partner<8>(v);
+  v = v + dg::xor_partner<4>(v);
+  v = v + dg::xor_partner<2>(v);
+  v = v + dg::xor_partner<1>(v);
+  y[l] = v;
+}
+
+// the count-down fold with every step a __shfl_xor
+KERNEL down_shfl(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  for (int m = 32; m >= 1; m >>= 1) v = v + __shfl_xor(v, m, 64);
+  y[l] = v;
+}
+
+// a plausible slip: the first two steps swapped (lanes 2 apart, then 1)
+KERNEL up_steps_swapped(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  v = v + __shfl_xor(v, 2, 64);
+  v = v + __shfl_xor(v, 1, 64);
+  for (int m = 4; m < 64; m <<= 1) v = v + __shfl_xor(v, m, 64);
+  y[l] = v;
+}
+
+// a left fold in one lane
+KERNEL chain(const float* __restrict__ x, float* __restrict__ y) {
+  if (threadIdx.x == 0) {
+    float v = x[0];
+#pragma unroll
+    for (int i = 1; i < 64; ++i) v = v + x[i];
+    y[0] = v;
+  }
+}
+
+// groups of 16 lanes: four sums, one per group (the row sums of a 16-lane
+// row group, as in the attention kernel's block row sum)
+KERNEL groups16(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  const float v = dg::tree_sum_lanes<4>(x[l]);
+  if ((l & 15) == 0) y[l >> 4] = v;
+}
+
+// an instruction the walk does not model (the hardware reciprocal): an
+// uninterpreted function of its operand, so each lane's leaf stays distinct
+KERNEL rcp_then_up(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  y[l] = dg::tree_sum_lanes<6>(__builtin_amdgcn_rcpf(x[l]));
+}
+
+// control flow that depends on the data: the walk refuses it
+KERNEL branch_on_data(const float* __restrict__ x, float* __restrict__ y) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  if (v > 0.f) v = dg::tree_sum_lanes<6>(v);
+  y[l] = v;
+}

@@ -1,0 +1,166 @@
+"""The static order checker (Sec. 6) on gfx950 assembly built here: the
+wave-level sums of tests/checker/lane_trees.hip, compiled with hipcc to
+assembly (no GPU), walked, and compared with trees written from their
+definitions; kernels that share a signature give the same bits, and kernels
+in different classes differ on some input (checked by evaluating the walked
+trees in binary32 on the CPU)."""
+import os
+import shutil
+
+import numpy as np
+import pytest
+
+from paper_2609_11356_amd import order_check as oc
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SRC = os.path.join(HERE, "checker", "lane_trees.hip")
+Y0 = [(8, 0)]                       # y[0]: the second pointer argument, byte 0
+
+
+@pytest.fixture(scope="module")
+def asm():
+    if not os.path.exists(oc.HIPCC) and shutil.which("hipcc") is None:
+        pytest.skip("no hipcc")
+    return oc.compile_asm(SRC)
+
+
+def leaf(i):
+    """The leaf of x[i] (x the first pointer argument, 4-byte elements)."""
+    return oc.Node("load", leaf=repr(oc.Aff(4 * i, {"arg0": 1})))
+
+
+def add(a, b):
+    return oc.Node("add", [a, b])
+
+
+def butterfly(steps, n=64):
+    """Every lane's value after the butterfly steps (lane i adds lane i ^ m),
+    from the definition of the count-up and count-down trees."""
+    v = [leaf(i) for i in range(n)]
+    for m in steps:
+        v = [add(v[i], v[i ^ m]) for i in range(n)]
+    return v
+
+
+def root(asm, name, outputs=Y0):
+    w = oc.Walk(asm, name)
+    r = w.roots(outputs)
+    assert len(r) == len(outputs), (name, r)
+    return r
+
+
+def test_functions_found(asm):
+    fns = set(oc.functions(asm))
+    assert {"up_library", "up_shfl", "up_four", "up_two", "up_reversed", "down_library", "down_shfl",
+            "up_steps_swapped", "chain", "groups16", "rcp_then_up", "branch_on_data"} <= fns
+
+
+def test_count_up_read_off_the_assembly_is_the_perfect_tree(asm):
+    """The library's lane steps (DPP quad_perm, half-row and row mirrors,
+    ds_swizzle, ds_bpermute) give every lane the perfect tree over x[0..63]
+    in element order."""
+    want = oc.canon(butterfly([1, 2, 4, 8, 16, 32])[0])
+    w = oc.Walk(asm, "up_library")
+    assert len(w.stores) == 64 and not w.opaque
+    assert all(t == want for _, t in w.roots())
+
+
+def test_count_down_and_chain_match_their_definitions(asm):
+    assert root(asm, "down_library")[0][1] == oc.canon(butterfly([32, 16, 8, 4, 2, 1])[0])
+    v = leaf(0)
+    for i in range(1, 64):
+        v = add(v, leaf(i))
+    assert root(asm, "chain")[0][1] == oc.canon(v)
+
+
+def test_groups_of_sixteen(asm):
+    """tree_sum_lanes<4>: four roots, each the perfect tree over its group."""
+    r = root(asm, "groups16", [(8, 4 * g) for g in range(4)])
+    for g in range(4):
+        v = [leaf(16 * g + i) for i in range(16)]
+        for m in (1, 2, 4, 8):
+            v = [add(v[i], v[i ^ m]) for i in range(16)]
+        assert r[g][1] == oc.canon(v[0])
+
+
+def test_layouts_of_one_tree_share_a_signature(asm):
+    """One element per lane over 64 lanes (DPP steps or shuffles), two or four
+    consecutive elements per lane folded in the lane first, or the lanes
+    reading the elements in reverse: one logical tree, one signature."""
+    sigs = {k: oc.Walk(asm, k).signature(Y0) for k in ("up_library", "up_shfl", "up_two", "up_four", "up_reversed")}
+    assert len(set(sigs.values())) == 1, sigs
+
+
+def test_classes(asm):
+    names = ["up_library", "up_shfl", "up_four", "up_two", "up_reversed", "down_library", "down_shfl",
+             "up_steps_swapped", "chain"]
+    got = oc.classes({k: oc.Walk(asm, k).signature(Y0) for k in names})
+    assert got == [["chain"], ["down_library", "down_shfl"], ["up_library", "up_shfl", "up_four", "up_two", "up_reversed"],
+                   ["up_steps_swapped"]]
+
+
+def evaluate(n, x, memo):
+    """A walked tree in binary32 (numpy, one rounding per add)."""
+    k = id(n)
+    if k not in memo:
+        if n.op == "load":
+            memo[k] = x[int(n.leaf.split("+")[-1]) // 4]
+        elif n.op == "add":
+            memo[k] = np.float32(evaluate(n.kids[0], x, memo) + evaluate(n.kids[1], x, memo))
+        else:
+            raise AssertionError(n.op)
+    return memo[k]
+
+
+def test_the_classes_are_real(asm):
+    """Trees in one class give equal bits on every draw; every pair of classes
+    differs on some draw of exponent-spread binary32 inputs."""
+    reps = {"up": "up_library", "down": "down_library", "swapped": "up_steps_swapped", "chain": "chain"}
+    trees = {}
+    for k, name in list(reps.items()) + [("up_four", "up_four"), ("up_reversed", "up_reversed")]:
+        w = oc.Walk(asm, name)
+        trees[k] = [n for a, n in sorted(w.stores.values(), key=lambda an: an[0].key()) if a.key() == oc.Aff(0, {"arg8": 1}).key()][0]
+    rng = np.random.default_rng(3)
+    differ = set()
+    for _ in range(200):
+        x = (rng.standard_normal(64) * np.exp2(rng.integers(-20, 20, 64))).astype(np.float32)
+        out = {k: evaluate(t, x, {}) for k, t in trees.items()}
+        assert out["up"].view(np.uint32) == out["up_four"].view(np.uint32) == out["up_reversed"].view(np.uint32)
+        for a in reps:
+            for b in reps:
+                if a < b and out[a].view(np.uint32) != out[b].view(np.uint32):
+                    differ.add((a, b))
+    assert differ == {(a, b) for a in reps for b in reps if a < b}
+
+
+def test_unmodelled_instruction_is_a_function_of_its_operands(asm):
+    """v_rcp_f32 is not modelled: it becomes an uninterpreted node over each
+    lane's own leaf, so the 64 leaves stay distinct and the tree keeps its
+    shape."""
+    w = oc.Walk(asm, "rcp_then_up")
+    assert any("v_rcp_f32" in t for t in w.opaque)
+    r = w.roots(Y0)[0][1]
+    assert r.count("opaque[v_rcp_f32") == 64 and len({r.find("L(%r)" % repr(oc.Aff(4 * i, {"arg0": 1}))) for i in range(64)}) == 64
+    assert oc.Walk(asm, "rcp_then_up").signature(Y0) != oc.Walk(asm, "up_library").signature(Y0)
+
+
+def test_data_dependent_control_flow_is_refused(asm):
+    with pytest.raises(oc.Unsupported):
+        oc.Walk(asm, "branch_on_data")
+
+
+def test_parser_pieces():
+    assert oc.parse_line("\tv_add_f32_dpp v1, v1, v1 quad_perm:[1,0,3,2] row_mask:0xf bank_mask:0xf bound_ctrl:1") == \
+        ("v_add_f32_dpp", ["v1", "v1", "v1"], ["quad_perm:[1,0,3,2]", "row_mask:0xf", "bank_mask:0xf", "bound_ctrl:1"])
+    assert oc.parse_line("\tglobal_load_dword v1, v[2:3], off offset:252") == \
+        ("global_load_dword", ["v1", "v[2:3]", "off"], ["offset:252"])
+    assert oc.parse_line(".LBB2_3:") is None and oc.parse_line("\t; comment") is None
+    # DPP and swizzle lane maps against their definitions
+    assert [oc._dpp_src(["quad_perm:[1,0,3,2]"], l) for l in range(4)] == [1, 0, 3, 2]
+    assert [oc._dpp_src(["row_mirror"], l) for l in (0, 5, 16, 31)] == [15, 10, 31, 16]
+    assert [oc._dpp_src(["row_half_mirror"], l) for l in (0, 7, 8, 15)] == [7, 0, 15, 8]
+    assert [oc._dpp_src(["row_ror:8"], l) for l in (0, 8, 17)] == [8, 0, 25]
+    assert oc._dpp_src(["row_shr:1"], 16) is None and oc._dpp_src(["row_shr:1"], 17) == 16
+    assert [oc._swizzle_src(["offset:swizzle(SWAP,16)"], l) for l in (0, 16, 33, 63)] == [16, 0, 49, 47]
+    assert [oc._swizzle_src(["offset:0x401f"], l) for l in (0, 16, 33)] == [16, 0, 49]   # bit mode, xor 16
+    assert [oc._swizzle_src(["offset:0x101f"], l) for l in (0, 4, 35)] == [4, 0, 39]     # bit mode, xor 4
