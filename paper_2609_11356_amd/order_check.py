@@ -287,28 +287,37 @@ class Walk:
             raise KeyError(name)
         self.name, self.lines = name, fns[name]
         self.meta = _kernel_meta(asm, name)
-        self.V, self.S = {}, {}
-        self.exec = (1 << WAVE) - 1
-        self.vcc = 0
-        self.scc = 0
         self.stores = {}              # address key -> (Aff, Node)
+        self.lds = {}                 # LDS byte address (4-byte words) -> value
         self._leaves = {}
         self.opaque = []
         nthreads = block[0] * block[1] * block[2]
-        if nthreads < WAVE:
-            self.exec = (1 << nthreads) - 1
-        # v0: work-item ids (x in bits 0-9, y and z above when present)
-        self.V[0] = [Aff((l % block[0]) | ((l // block[0] % block[1]) << 10) | ((l // (block[0] * block[1])) << 20))
-                     for l in range(WAVE)]
-        # s[0:1]: the kernel-argument pointer; after the user SGPRs, the workgroup ids
-        self.S[0] = ("kernarg", 0)
-        nu = self.meta.get("amdhsa_user_sgpr_count", 2)
-        k = nu
-        for d in "xyz":
-            if self.meta.get("amdhsa_system_sgpr_workgroup_id_" + d, 1 if d == "x" else 0):
-                self.S[k] = Aff(0, {"wg_" + d: 1})
-                k += 1
+        # one state per wave of the workgroup: registers, exec, vcc, scc
+        self.waves = []
+        for w in range((nthreads + WAVE - 1) // WAVE):
+            t0 = WAVE * w
+            n = min(WAVE, nthreads - t0)
+            # v0: work-item ids (x in bits 0-9, y and z above when present)
+            tid = [t0 + l for l in range(WAVE)]
+            V = {0: [Aff((t % block[0]) | ((t // block[0] % block[1]) << 10) | ((t // (block[0] * block[1])) << 20))
+                     for t in tid]}
+            # s[0:1]: the kernel-argument pointer; after the user SGPRs, the workgroup ids
+            S = {0: ("kernarg", 0)}
+            k = self.meta.get("amdhsa_user_sgpr_count", 2)
+            for d in "xyz":
+                if self.meta.get("amdhsa_system_sgpr_workgroup_id_" + d, 1 if d == "x" else 0):
+                    S[k] = Aff(0, {"wg_" + d: 1})
+                    k += 1
+            self.waves.append(dict(V=V, S=S, exec=(1 << n) - 1, vcc=0, scc=0, pc=0, done=False))
         self._run()
+
+    def _enter(self, w):
+        st = self.waves[w]
+        self.V, self.S, self.exec, self.vcc, self.scc = st["V"], st["S"], st["exec"], st["vcc"], st["scc"]
+
+    def _leave(self, w):
+        st = self.waves[w]
+        st["V"], st["S"], st["exec"], st["vcc"], st["scc"] = self.V, self.S, self.exec, self.vcc, self.scc
 
     # --- registers
     def v(self, tok, lane):
@@ -407,23 +416,39 @@ class Walk:
             p = parse_line(line)
             if p:
                 prog.append((p, s))
-        pc, steps = 0, 0
-        while pc < len(prog):
-            steps += 1
-            if steps > MAX_STEPS:
-                raise Unsupported("step limit")
-            (op, ops, mods), text = prog[pc]
-            pc += 1
-            if op == "s_endpgm":
-                return
-            jump = self._branch(op, ops)
-            if jump is not None:
-                if jump is True:
-                    if ops[0] not in labels:
-                        raise Unsupported("branch target " + ops[0])
-                    pc = labels[ops[0]]
-                continue
-            self._step(op, ops, mods, text)
+        # each wave runs to its next barrier (or its end), then the next wave:
+        # an order every barrier-synchronised program allows
+        steps = 0
+        while not all(st["done"] for st in self.waves):
+            for w, st in enumerate(self.waves):
+                if st["done"]:
+                    continue
+                self._enter(w)
+                pc = st["pc"]
+                while True:
+                    if pc >= len(prog):
+                        st["done"] = True
+                        break
+                    steps += 1
+                    if steps > MAX_STEPS:
+                        raise Unsupported("step limit")
+                    (op, ops, mods), text = prog[pc]
+                    pc += 1
+                    if op == "s_endpgm":
+                        st["done"] = True
+                        break
+                    if op == "s_barrier":
+                        break
+                    jump = self._branch(op, ops)
+                    if jump is not None:
+                        if jump is True:
+                            if ops[0] not in labels:
+                                raise Unsupported("branch target " + ops[0])
+                            pc = labels[ops[0]]
+                        continue
+                    self._step(op, ops, mods, text)
+                st["pc"] = pc
+                self._leave(w)
 
     def _branch(self, op, ops):
         if not op.startswith("s_branch") and not op.startswith("s_cbranch"):
@@ -446,7 +471,7 @@ class Walk:
 
     def _step(self, op, ops, mods, text):
         base = re.sub(r"_e(32|64)$", "", op)
-        if op.startswith("s_waitcnt") or op in ("s_nop", "s_barrier", "s_setprio", "s_sleep") or \
+        if op.startswith("s_waitcnt") or op in ("s_nop", "s_setprio", "s_sleep") or \
                 op.startswith("s_sched") or op == "s_setreg_imm32_b32" or op == "s_denorm_mode":
             return
         # scalar: argument loads, exec and mask logic
@@ -559,6 +584,9 @@ class Walk:
             for l, x in vals.items():
                 self.setv(ops[0], l, x)
             return
+        if op.startswith("ds_write") or op.startswith("ds_read"):
+            self._lds(op, ops, mods)
+            return
         if op.startswith("global_load_dword"):
             n = {"global_load_dword": 1, "global_load_dwordx2": 2, "global_load_dwordx3": 3,
                  "global_load_dwordx4": 4}[op]
@@ -594,6 +622,46 @@ class Walk:
             elif r and r[0] == "s":
                 for k in range(r[2]):
                     self.S[r[1] + k] = ("opaque", text)
+
+    def _lds(self, op, ops, mods):
+        """LDS words move values between the waves of the workgroup (Sec. 6:
+        a store to shared memory, a barrier and a load are one cross-wave
+        exchange that combines nothing)."""
+        g = re.fullmatch(r"ds_(read|write)(2?)(st64)?_b(32|64|128)", op)
+        if not g:
+            raise Unsupported(op)
+        rd, two, st64, bits = g.group(1) == "read", g.group(2) == "2", g.group(3) is not None, int(g.group(4))
+        words = bits // 32
+        opt = {}
+        for m in mods:
+            k, _, v = m.partition(":")
+            opt[k] = int(v, 0)
+        if two:
+            unit = (bits // 8) * (64 if st64 else 1)
+            offs = [opt.get("offset0", 0) * unit, opt.get("offset1", 0) * unit]
+        else:
+            offs = [opt.get("offset", 0)]
+        addr_tok = ops[1] if rd else ops[0]
+        data = [ops[0]] if rd else ops[1:]
+        vals = {}
+        for l in self.lanes():
+            a = self.v(addr_tok, l)
+            if not isinstance(a, Aff) or not a.concrete():
+                raise Unsupported("LDS address not lane-derived")
+            for j, off in enumerate(offs):
+                for k in range(words):
+                    byte = (a.c + off) & 0xFFFFFFFF
+                    if rd:
+                        vals[(l, j * words + k)] = self.lds.get(byte + 4 * k, Node("const", leaf="lds-uninit"))
+                    else:
+                        r = _reg(data[j] if two else data[0])
+                        if not r or r[0] not in "va":
+                            raise Unsupported("LDS store of " + str(data))
+                        base = r[1] if r[0] == "v" else 1000 + r[1]
+                        self.lds[byte + 4 * k] = self.V.get(base + k, [None] * WAVE)[l]
+        if rd:
+            for (l, k), x in vals.items():
+                self.setv(ops[0], l, x, k)
 
     def _as_node(self, tok, l):
         try:

@@ -112,3 +112,38 @@ KERNEL branch_on_data(const float* __restrict__ x, float* __restrict__ y) {
   if (v > 0.f) v = dg::tree_sum_lanes<6>(v);
   y[l] = v;
 }
+
+// a workgroup's sum of x[0..255]: each wave's tree over its 64 elements, the
+// four wave sums through LDS, then a tree over them in wave order
+extern "C" __global__ void __launch_bounds__(256) block_256(const float* __restrict__ x, float* __restrict__ y) {
+  __shared__ float part[4];
+  const int t = threadIdx.x, l = t & 63, w = t >> 6;
+  const float v = dg::tree_sum_lanes<6>(x[t]);
+  if (l == 0) part[w] = v;
+  __syncthreads();
+  if (t < 4) {
+    const float s = dg::tree_sum_lanes<2>(part[t]);
+    if (t == 0) y[0] = s;
+  }
+}
+
+// the same tree from 128 threads holding two consecutive elements each (the
+// cut between in-thread, in-wave and cross-wave levels moves)
+extern "C" __global__ void __launch_bounds__(128) block_128x2(const float* __restrict__ x, float* __restrict__ y) {
+  __shared__ float part[2];
+  const int t = threadIdx.x, l = t & 63, w = t >> 6;
+  const float v = dg::tree_sum_lanes<6>(x[2 * t] + x[2 * t + 1]);
+  if (l == 0) part[w] = v;
+  __syncthreads();
+  if (t == 0) y[0] = part[0] + part[1];
+}
+
+// the wave sums chained in wave order
+extern "C" __global__ void __launch_bounds__(256) block_256_chain(const float* __restrict__ x, float* __restrict__ y) {
+  __shared__ float part[4];
+  const int t = threadIdx.x, l = t & 63, w = t >> 6;
+  const float v = dg::tree_sum_lanes<6>(x[t]);
+  if (l == 0) part[w] = v;
+  __syncthreads();
+  if (t == 0) y[0] = ((part[0] + part[1]) + part[2]) + part[3];
+}

@@ -164,3 +164,33 @@ def test_parser_pieces():
     assert [oc._swizzle_src(["offset:swizzle(SWAP,16)"], l) for l in (0, 16, 33, 63)] == [16, 0, 49, 47]
     assert [oc._swizzle_src(["offset:0x401f"], l) for l in (0, 16, 33)] == [16, 0, 49]   # bit mode, xor 16
     assert [oc._swizzle_src(["offset:0x101f"], l) for l in (0, 4, 35)] == [4, 0, 39]     # bit mode, xor 4
+
+
+def perfect(lo, n):
+    """The perfect tree over x[lo .. lo + n) in element order."""
+    v = [leaf(lo + i) for i in range(n)]
+    while len(v) > 1:
+        v = [add(v[2 * i], v[2 * i + 1]) for i in range(len(v) // 2)]
+    return v[0]
+
+
+def test_cross_wave_exchange_through_lds(asm):
+    """Waves of one workgroup meet through LDS (a store, a barrier, a load:
+    one exchange that combines nothing).  256 threads with one element each
+    and 128 threads with two consecutive elements each reach the perfect tree
+    over x[0..255] and share its signature; chaining the four wave sums is
+    another tree."""
+    a = oc.Walk(asm, "block_256", block=(256, 1, 1))
+    b = oc.Walk(asm, "block_128x2", block=(128, 1, 1))
+    c = oc.Walk(asm, "block_256_chain", block=(256, 1, 1))
+    assert a.roots(Y0)[0][1] == oc.canon(perfect(0, 256))
+    assert a.signature(Y0) == b.signature(Y0)
+    chained = add(add(add(perfect(0, 64), perfect(64, 64)), perfect(128, 64)), perfect(192, 64))
+    assert c.roots(Y0)[0][1] == oc.canon(chained)
+    assert c.signature(Y0) != a.signature(Y0)
+    # the two classes are real: some draw separates them
+    y0 = oc.Aff(0, {"arg8": 1}).key()
+    ta, tc = a.stores[y0][1], c.stores[y0][1]
+    rng = np.random.default_rng(4)
+    x = (rng.standard_normal((50, 256)) * np.exp2(rng.integers(-20, 20, (50, 256)))).astype(np.float32)
+    assert any(evaluate(ta, r, {}).view(np.uint32) != evaluate(tc, r, {}).view(np.uint32) for r in x)
