@@ -281,7 +281,11 @@ def _swizzle_src(mods, lane):
 class Walk:
     """One entry function walked over one wave."""
 
-    def __init__(self, asm: str, name: str, block=(64, 1, 1)):
+    def __init__(self, asm: str, name: str, block=(64, 1, 1), args=None):
+        """block: the workgroup shape; args: {kernel-argument byte offset:
+        value} for 32-bit integer arguments bound to a configuration (loops
+        whose trip count they fix are then walked exactly)."""
+        self.args = dict(args or {})
         fns = functions(asm)
         if name not in fns:
             raise KeyError(name)
@@ -374,6 +378,11 @@ class Walk:
             m = self.S.get(r[1])
             if isinstance(m, tuple) and m[0] == "mask":
                 return m[1]
+            h = self.S.get(r[1] + 1)
+            if isinstance(m, Aff) and m.concrete() and isinstance(h, Aff) and h.concrete():
+                return ((m.c & 0xFFFFFFFF) | ((h.c & 0xFFFFFFFF) << 32)) & ((1 << WAVE) - 1)
+        if _imm(tok) is not None:
+            return _imm(tok) & ((1 << WAVE) - 1)
         raise Unsupported("mask operand " + tok)
 
     def setmask(self, tok, m):
@@ -394,7 +403,8 @@ class Walk:
         p = self.S.get(r[1])
         if isinstance(p, tuple) and p[0] == "arg":
             return Aff(0, {"arg%d" % p[1]: 1})
-        if isinstance(p, Aff):
+        if isinstance(p, Aff) and (isinstance(self.S.get(r[1] + 1), tuple) and self.S.get(r[1] + 1)[0] == "arghi"
+                                   or isinstance(self.S.get(r[1] + 1), HiWord)):
             return p
         raise Unsupported("address base " + tok)
 
@@ -485,11 +495,16 @@ class Walk:
             if src == ("kernarg", 0):
                 for k in range(n):
                     o = off + 4 * k
-                    self.S[d + k] = ("arg", o) if o % 8 == 0 else ("arghi", o - 4)
+                    if o in self.args:
+                        self.S[d + k] = Aff(self.args[o])
+                    else:
+                        self.S[d + k] = ("arg", o) if o % 8 == 0 else ("arghi", o - 4)
                 return
             base = self._ptr(ops[1])              # data: one leaf per dword
             for k in range(n):
                 self.S[d + k] = self.leaf(base + Aff(off + 4 * k))
+            return
+        if self._salu(op, ops):
             return
         if op in ("s_and_saveexec_b64", "s_or_saveexec_b64"):
             old = self.exec
@@ -584,6 +599,19 @@ class Walk:
             for l, x in vals.items():
                 self.setv(ops[0], l, x)
             return
+        if op == "v_lshl_add_u64":
+            # 64-bit (a << shift) + b on register pairs: the low word carries the
+            # affine value, the high word marks a pointer (or is a concrete 0)
+            for l in self.lanes():
+                (alo, ahi), sh, (blo, bhi) = self._pair(ops[1], l), self.v(ops[2], l), self._pair(ops[3], l)
+                if not (isinstance(sh, Aff) and sh.concrete()):
+                    raise Unsupported("v_lshl_add_u64 shift")
+                aptr, bptr = isinstance(ahi, HiWord), isinstance(bhi, HiWord)
+                if (aptr and sh.c) or (aptr and bptr):
+                    raise Unsupported("v_lshl_add_u64 on two pointers or a shifted pointer")
+                self.setv(ops[0], l, alo.scale(1 << sh.c) + blo, 0)
+                self.setv(ops[0], l, HiWord() if (aptr or bptr) else Aff(0), 1)
+            return
         if op.startswith("ds_write") or op.startswith("ds_read"):
             self._lds(op, ops, mods)
             return
@@ -622,6 +650,109 @@ class Walk:
             elif r and r[0] == "s":
                 for k in range(r[2]):
                     self.S[r[1] + k] = ("opaque", text)
+
+    def _pair(self, tok, l):
+        """A 64-bit operand as (low word value, high word value)."""
+        r = _reg(tok)
+        if r and r[2] == 2:
+            if r[0] == "s":
+                lo, hi = self.v("s%d" % r[1], l), self.v("s%d" % (r[1] + 1), l)
+            else:
+                lo, hi = self.v("v%d" % r[1], l), self.v("v%d" % (r[1] + 1), l)
+            if isinstance(lo, Aff) and (isinstance(hi, HiWord) or (isinstance(hi, Aff) and hi.concrete() and hi.c == 0)):
+                return lo, hi
+            raise Unsupported("64-bit operand " + tok)
+        i = _imm(tok)
+        if i is not None:
+            return Aff(i), Aff(0)
+        raise Unsupported("64-bit operand " + tok)
+
+    def _sval(self, tok):
+        x = self.v(tok, 0) if _reg(tok) is None or _reg(tok)[0] == "s" else None
+        return x
+
+    def _salu(self, op, ops):
+        """Scalar integer work on concrete values and affine addresses; False
+        if op is not one of these."""
+        b32 = {"s_add_i32", "s_add_u32", "s_sub_i32", "s_sub_u32", "s_mul_i32", "s_lshl_b32", "s_lshr_b32",
+               "s_ashr_i32", "s_and_b32", "s_or_b32", "s_xor_b32", "s_min_i32", "s_min_u32", "s_max_i32",
+               "s_max_u32", "s_mov_b32", "s_cselect_b32", "s_addc_u32", "s_subb_u32", "s_lshl1_add_u32",
+               "s_lshl2_add_u32", "s_lshl3_add_u32", "s_lshl4_add_u32", "s_bfe_u32", "s_mul_hi_u32"}
+        if op.startswith("s_cmp_"):
+            g = re.fullmatch(r"s_cmp_(eq|lg|lt|le|gt|ge)_(i32|u32|u64)", op)
+            if not g:
+                raise Unsupported(op)
+            a, b = self._sval(ops[0]), self._sval(ops[1])
+            if not (isinstance(a, Aff) and isinstance(b, Aff)):
+                raise Unsupported("scalar compare on " + str(ops))
+            d = a + b.neg()
+            if not d.concrete():
+                if g.group(1) in ("eq", "lg") and a.t and b.t and a.t == b.t:
+                    pass
+                else:
+                    raise Unsupported("scalar compare on symbolic values")
+            if a.concrete() and b.concrete():
+                x, y = a.c, b.c
+                if g.group(2) == "i32":
+                    x, y = [(z & 0xFFFFFFFF) - (1 << 32) if (z & 0xFFFFFFFF) >> 31 else z & 0xFFFFFFFF for z in (x, y)]
+                elif g.group(2) == "u32":
+                    x, y = x & 0xFFFFFFFF, y & 0xFFFFFFFF
+            else:
+                x, y = d.c, 0
+            self.scc = int({"eq": x == y, "lg": x != y, "lt": x < y, "le": x <= y, "gt": x > y, "ge": x >= y}[g.group(1)])
+            return True
+        if op == "s_mov_b64" and ops[0] not in ("exec", "vcc"):
+            r, q = _reg(ops[0]), _reg(ops[1])
+            if r and q and r[0] == q[0] == "s":
+                self.S[r[1]], self.S[r[1] + 1] = self.S.get(q[1]), self.S.get(q[1] + 1)
+                return True
+            if r and q is None and _imm(ops[1]) is not None:
+                self.S[r[1]], self.S[r[1] + 1] = Aff(_imm(ops[1])), Aff(0)
+                return True
+            return False
+        if op not in b32:
+            return False
+        d = _reg(ops[0])
+        if op in ("s_addc_u32", "s_subb_u32"):
+            self.S[d[1]] = ("arghi", -1)                 # the high word of a 64-bit address
+            return True
+        if op == "s_mov_b32":
+            x = self.S.get(_reg(ops[1])[1]) if _reg(ops[1]) else Aff(_imm(ops[1]) or 0)
+            self.S[d[1]] = x
+            return True
+        if op == "s_cselect_b32":
+            self.S[d[1]] = self._sval(ops[1]) if self.scc else self._sval(ops[2])
+            return True
+        a = [self._sval(t) for t in ops[1:]]
+        if not all(isinstance(x, Aff) for x in a):
+            raise Unsupported("scalar op %s on %s" % (op, ops))
+        if op in ("s_add_i32", "s_add_u32"):
+            r = a[0] + a[1]
+        elif op in ("s_sub_i32", "s_sub_u32"):
+            r = a[0] + a[1].neg()
+        elif op == "s_mul_i32" and (a[0].concrete() or a[1].concrete()):
+            r = a[1].scale(a[0].c) if a[0].concrete() else a[0].scale(a[1].c)
+        elif op == "s_lshl_b32" and a[1].concrete():
+            r = a[0].scale(1 << (a[1].c & 31))
+        elif op.startswith("s_lshl") and op.endswith("_add_u32"):
+            r = a[0].scale(1 << int(op[6])) + a[1]
+        elif all(x.concrete() for x in a):
+            c = [x.c & 0xFFFFFFFF for x in a]
+            sg = [(z - (1 << 32)) if z >> 31 else z for z in c]
+            f = {"s_lshr_b32": lambda: c[0] >> (c[1] & 31), "s_ashr_i32": lambda: sg[0] >> (c[1] & 31),
+                 "s_and_b32": lambda: c[0] & c[1], "s_or_b32": lambda: c[0] | c[1], "s_xor_b32": lambda: c[0] ^ c[1],
+                 "s_min_i32": lambda: min(sg), "s_max_i32": lambda: max(sg), "s_min_u32": lambda: min(c),
+                 "s_max_u32": lambda: max(c), "s_mul_i32": lambda: c[0] * c[1],
+                 "s_bfe_u32": lambda: (c[0] >> (c[1] & 31)) & ((1 << ((c[1] >> 16) & 0x7F)) - 1),
+                 "s_mul_hi_u32": lambda: (c[0] * c[1]) >> 32}
+            if op not in f:
+                raise Unsupported(op)
+            r = Aff(f[op]() & 0xFFFFFFFF)
+        else:
+            raise Unsupported("scalar op %s on symbolic values" % op)
+        self.S[d[1]] = r
+        self.scc = int(r.concrete() and (r.c & 0xFFFFFFFF) != 0) if op not in ("s_add_u32", "s_sub_u32") else 0
+        return True
 
     def _lds(self, op, ops, mods):
         """LDS words move values between the waves of the workgroup (Sec. 6:

@@ -147,3 +147,41 @@ extern "C" __global__ void __launch_bounds__(256) block_256_chain(const float* _
   __syncthreads();
   if (t == 0) y[0] = ((part[0] + part[1]) + part[2]) + part[3];
 }
+
+// loops over n (bound to a configuration by the caller): lane l folds
+// x[l], x[l + 64], x[l + 128], ... in order, then the count-up tree
+KERNEL strided_fold(const float* __restrict__ x, float* __restrict__ y, int n) {
+  const int l = threadIdx.x;
+  float v = x[l];
+#pragma nounroll
+  for (int k = l + 64; k < n; k += 64) v = v + x[k];
+  y[l] = dg::tree_sum_lanes<6>(v);
+}
+
+// the same chain unrolled by two (one accumulator): the same tree
+KERNEL strided_fold_unroll2(const float* __restrict__ x, float* __restrict__ y, int n) {
+  const int l = threadIdx.x;
+  float v = x[l];
+  int k = l + 64;
+#pragma nounroll
+  for (; k + 64 < n; k += 128) {
+    v = v + x[k];
+    v = v + x[k + 64];
+  }
+  if (k < n) v = v + x[k];
+  y[l] = dg::tree_sum_lanes<6>(v);
+}
+
+// two accumulators (even and odd steps) joined at the end: re-chunking a
+// sequential fold regroups the sum
+KERNEL strided_fold_two_acc(const float* __restrict__ x, float* __restrict__ y, int n) {
+  const int l = threadIdx.x;
+  float v0 = x[l], v1 = x[l + 64];
+  int k = l + 128;
+#pragma nounroll
+  for (; k + 64 < n; k += 128) {
+    v0 = v0 + x[k];
+    v1 = v1 + x[k + 64];
+  }
+  y[l] = dg::tree_sum_lanes<6>(v0 + v1);
+}

@@ -194,3 +194,32 @@ def test_cross_wave_exchange_through_lds(asm):
     rng = np.random.default_rng(4)
     x = (rng.standard_normal((50, 256)) * np.exp2(rng.integers(-20, 20, (50, 256)))).astype(np.float32)
     assert any(evaluate(ta, r, {}).view(np.uint32) != evaluate(tc, r, {}).view(np.uint32) for r in x)
+
+
+@pytest.mark.parametrize("n", [512, 448])
+def test_loops_walked_for_a_bound_configuration(asm, n):
+    """With n bound (the third argument, byte 16) the loops are walked
+    exactly: lane l's chain x[l], x[l + 64], ... then the count-up tree.
+    Unrolling the chain by two with one accumulator keeps the tree; two
+    accumulators (even and odd steps) regroup it.  Unbound, the trip count
+    is data and the walk refuses."""
+    fold = oc.Walk(asm, "strided_fold", args={16: n})
+    lanes = []
+    for l in range(64):
+        v = leaf(l)
+        for k in range(l + 64, n, 64):
+            v = add(v, leaf(k))
+        lanes.append(v)
+    for m in (1, 2, 4, 8, 16, 32):
+        lanes = [add(lanes[i], lanes[i ^ m]) for i in range(64)]
+    assert fold.roots(Y0)[0][1] == oc.canon(lanes[0])
+    assert oc.Walk(asm, "strided_fold_unroll2", args={16: n}).signature(Y0) == fold.signature(Y0)
+    two = oc.Walk(asm, "strided_fold_two_acc", args={16: n})
+    assert two.signature(Y0) != fold.signature(Y0)
+    y0 = oc.Aff(0, {"arg8": 1}).key()
+    rng = np.random.default_rng(5)
+    x = (rng.standard_normal((50, n)) * np.exp2(rng.integers(-20, 20, (50, n)))).astype(np.float32)
+    assert any(evaluate(fold.stores[y0][1], r, {}).view(np.uint32) != evaluate(two.stores[y0][1], r, {}).view(np.uint32)
+               for r in x)
+    with pytest.raises(oc.Unsupported):
+        oc.Walk(asm, "strided_fold")
