@@ -197,10 +197,10 @@ def profile_only(args, torch, dg, inputs, d_bf16):
                 dg.dg_gemm(D, dA, dBs[it[0] % len(dBs)], None, C, stream=sptr)
                 it[0] += 1
     else:
-        src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)   # 1 GiB
+        src = torch.ones(args.copy_mib << 19, dtype=torch.bfloat16, device=dev)   # copy_mib MiB
         dst = torch.empty_like(src)
         run = lambda: dst.copy_(src)
-        what = "device copy of 1 GiB (reads 1 GiB, writes 1 GiB)"
+        what = "device copy of %d MiB (reads and writes %d MiB)" % (args.copy_mib, args.copy_mib)
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
@@ -233,6 +233,8 @@ def main():
                          "GEMM (M=128, 1024, 4096), the M=1024 sweep GEMM under a tile-tree or fma=0 "
                          "descriptor, or a plain 1 GiB device copy (the calibration "
                          "kernel for HBM byte counters)")
+    ap.add_argument("--copy-mib", type=int, default=1024,
+                    help="with --only copy: the size of the copied buffer in MiB (default 1 GiB)")
     ap.add_argument("--block-order", type=int, choices=(0, 1, 2, 3), default=0,
                     help="with --only mlp: run the mixed-width kernel with this block order (1 row-major, "
                          "2 groups of eight block rows, 3 the same with each XCD given a contiguous range)")
