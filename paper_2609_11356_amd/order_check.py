@@ -968,3 +968,11 @@ def classes(signatures: dict) -> list[list]:
     for k, s in signatures.items():
         by.setdefault(s, []).append(k)
     return sorted(by.values(), key=lambda g: str(g[0]))
+
+
+def prune(signatures: dict, reference) -> list:
+    """The configurations bitwise equivalent to the reference (Sec. 6: a
+    search that benchmarks only these keeps the reference's bits); reference
+    is a key of signatures or a signature."""
+    ref = signatures.get(reference, reference)
+    return [k for k, s in signatures.items() if s == ref]

@@ -223,3 +223,14 @@ def test_loops_walked_for_a_bound_configuration(asm, n):
                for r in x)
     with pytest.raises(oc.Unsupported):
         oc.Walk(asm, "strided_fold")
+
+
+def test_pruning_predicate(asm):
+    """A search over ways of summing 512 elements keeps the configurations
+    with the reference's signature: the one-accumulator chain and its unroll
+    by two, not the two-accumulator variant or a count-down lane fold."""
+    space = {"fold": ("strided_fold", {16: 512}), "fold_unroll2": ("strided_fold_unroll2", {16: 512}),
+             "fold_two_acc": ("strided_fold_two_acc", {16: 512}), "up_library": ("up_library", None)}
+    sigs = {k: oc.Walk(asm, name, args=args).signature(Y0) for k, (name, args) in space.items()}
+    assert oc.prune(sigs, "fold") == ["fold", "fold_unroll2"]
+    assert oc.prune(sigs, sigs["up_library"]) == ["up_library"]
