@@ -234,3 +234,30 @@ def test_pruning_predicate(asm):
     sigs = {k: oc.Walk(asm, name, args=args).signature(Y0) for k, (name, args) in space.items()}
     assert oc.prune(sigs, "fold") == ["fold", "fold_unroll2"]
     assert oc.prune(sigs, sigs["up_library"]) == ["up_library"]
+
+
+@pytest.mark.parametrize("mutant", ["no_commutative_sort", "leaf_by_lane", "lds_store_lost", "swizzle_xor_ignored"])
+def test_planted_checker_mistakes_change_an_answer(asm, monkeypatch, mutant):
+    """Each plausible slip in the walk changes a result the tests above pin:
+    the one-class answer for the count-up layouts, or a tree against its
+    definition."""
+    if mutant == "no_commutative_sort":
+        monkeypatch.setattr(oc, "COMMUTATIVE", set())
+    elif mutant == "leaf_by_lane":
+        real = oc.Walk.leaf
+        monkeypatch.setattr(oc.Walk, "leaf", lambda self, addr: real(self, oc.Aff(addr.c % 256, addr.t)))
+    elif mutant == "lds_store_lost":
+        monkeypatch.setattr(oc.Walk, "_lds", lambda self, op, ops, mods: None)
+    else:
+        real_src = oc._swizzle_src
+        monkeypatch.setattr(oc, "_swizzle_src", lambda mods, lane: lane if "SWAP" in " ".join(mods) else real_src(mods, lane))
+    ok = True
+    try:
+        sigs = {k: oc.Walk(asm, k).signature(Y0) for k in ("up_library", "up_four", "up_reversed")}
+        ok &= len(set(sigs.values())) == 1
+        ok &= root(asm, "up_library")[0][1] == oc.canon(butterfly([1, 2, 4, 8, 16, 32])[0])
+        a = oc.Walk(asm, "block_256", block=(256, 1, 1))
+        ok &= a.roots(Y0)[0][1] == oc.canon(perfect(0, 256))
+    except (oc.Unsupported, AssertionError, KeyError):
+        ok = False
+    assert not ok, mutant
