@@ -6,6 +6,7 @@ import subprocess
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB = os.path.join(HERE, "libmfma_probe.so")
 MATH_LIB = os.path.join(HERE, "libmath_probe.so")
+CHECK_LIB = os.path.join(os.path.dirname(HERE), "checker", "libcheck_fixtures.so")
 
 
 def _hipcc(src, lib, extra=()):
@@ -23,4 +24,7 @@ def _hipcc(src, lib, extra=()):
 def build():
     # the math probe is compiled as the library is (no contraction, no fast math)
     _hipcc("math_probe.hip", MATH_LIB, ("-O3", "-ffp-contract=off", "-fno-fast-math"))
+    # the order checker's fixtures, with the flags the checker compiles them with
+    _hipcc(os.path.join("..", "checker", "launch.hip"), CHECK_LIB, ("-O3", "-std=c++17", "-ffp-contract=off",
+                                                                     "-fno-fast-math"))
     return _hipcc("mfma_probe.hip", LIB)
