@@ -1073,3 +1073,33 @@ def prune(signatures: dict, reference) -> list:
     is a key of signatures or a signature."""
     ref = signatures.get(reference, reference)
     return [k for k, s in signatures.items() if s == ref]
+
+
+def main(argv=None) -> int:
+    """python -m paper_2609_11356_amd.order_check SOURCE.hip [KERNEL ...]
+    [--block N] [--arg OFFSET=VALUE ...] [-I DIR ...]: the classes of the
+    named kernels (every entry function of SOURCE when none is named)."""
+    import argparse
+    ap = argparse.ArgumentParser(prog="order_check", description=main.__doc__)
+    ap.add_argument("source")
+    ap.add_argument("kernels", nargs="*")
+    ap.add_argument("--block", type=int, default=64, help="threads per workgroup (x only)")
+    ap.add_argument("--arg", action="append", default=[], help="bind a 32-bit argument: byte offset=value")
+    ap.add_argument("-I", dest="include", action="append", default=[])
+    a = ap.parse_args(argv)
+    asm = compile_asm(a.source, a.include)
+    names = a.kernels or sorted(functions(asm))
+    args = {int(k, 0): int(v, 0) for k, v in (x.split("=") for x in a.arg)}
+    sigs = {}
+    for n in names:
+        try:
+            sigs[n] = Walk(asm, n, block=(a.block, 1, 1), args=args).signature()
+        except Unsupported as e:
+            print("%s: not walked (%s)" % (n, e))
+    for c in classes(sigs):
+        print("%s  %s" % (sigs[c[0]][:16], " ".join(c)))
+    return 0
+
+
+if __name__ == "__main__":
+    raise SystemExit(main())

@@ -302,3 +302,12 @@ def test_mfma_k_loops(mma_asm, K):
         sigs = {k: oc.Walk(mma_asm, k).signature() for k in ("mma_unrolled", "mma_two_acc", "mma_reversed")}
         assert sigs["mma_unrolled"] == loop32.signature()
         assert len(set(sigs.values())) == 3
+
+
+def test_command_line(asm, capsys):
+    """python -m paper_2609_11356_amd.order_check: one line per class."""
+    assert oc.main([SRC, "up_library", "up_shfl", "down_library", "strided_fold", "--arg", "16=512"]) == 0
+    lines = capsys.readouterr().out.strip().splitlines()
+    assert sorted(l.split()[1:] for l in lines) == [["down_library"], ["strided_fold"], ["up_library", "up_shfl"]]
+    assert oc.main([SRC, "branch_on_data"]) == 0
+    assert "not walked" in capsys.readouterr().out
